@@ -1,0 +1,233 @@
+"""CPU oracle of the DeRF renderer -- test infrastructure only.
+
+Loads ``liboracle.so`` (plain C, built from ``derf_oracle.c`` by ``build()``)
+through ctypes.  Only the tests, the smoke check and the benchmark's CPU
+baseline use this package; the GPU library never imports or links it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "derf_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (OpenMP over rays, no fp contraction)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-std=gnu11", "-fPIC", "-shared", "-fopenmp",
+               "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wno-unused-function",
+               _SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Arch(ctypes.Structure):
+    _fields_ = [("pos_freqs", ctypes.c_int), ("dir_freqs", ctypes.c_int),
+                ("depth", ctypes.c_int), ("width", ctypes.c_int),
+                ("skip_layer", ctypes.c_int), ("rgb_hidden", ctypes.c_int)]
+
+
+_P = ctypes.c_void_p
+
+
+def _lib_handle():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        lib = ctypes.CDLL(_LIB)
+        render_sig = [ctypes.c_int, _P, ctypes.POINTER(_Arch), _P, ctypes.c_longlong, _P, _P, _P,
+                      ctypes.c_float, ctypes.c_float, ctypes.c_int, ctypes.c_int,
+                      ctypes.c_uint64, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_int]
+        for name in ("oracle_render", "oracle_render_direct", "oracle_render_back_to_front",
+                     "oracle_render_plain"):
+            f = getattr(lib, name)
+            f.argtypes = render_sig
+            f.restype = ctypes.c_int
+        lib.oracle_render_soft.argtypes = render_sig + [ctypes.c_double]
+        lib.oracle_render_soft.restype = ctypes.c_int
+        lib.oracle_philox4x32_10.argtypes = [_P, _P, _P]
+        lib.oracle_philox4x32_10.restype = None
+        lib.oracle_jitter.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint32,
+                                      ctypes.c_uint32]
+        lib.oracle_jitter.restype = ctypes.c_float
+        lib.oracle_sample_depths.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_float,
+                                             ctypes.c_float, ctypes.c_int, ctypes.c_int, _P]
+        lib.oracle_sample_depths.restype = None
+        lib.oracle_nearest_site.argtypes = [ctypes.c_int, _P, _P]
+        lib.oracle_nearest_site.restype = ctypes.c_int
+        lib.oracle_bisector_margin.argtypes = [ctypes.c_int, _P, _P, ctypes.c_int]
+        lib.oracle_bisector_margin.restype = ctypes.c_double
+        lib.oracle_posenc.argtypes = [ctypes.c_int, _P, _P]
+        lib.oracle_posenc.restype = None
+        lib.oracle_weights_count.argtypes = [ctypes.POINTER(_Arch)]
+        lib.oracle_weights_count.restype = ctypes.c_longlong
+        lib.oracle_head_eval.argtypes = [ctypes.POINTER(_Arch), _P, _P, _P, _P, _P, _P]
+        lib.oracle_head_eval.restype = None
+        lib.oracle_composite.argtypes = [ctypes.c_int, ctypes.c_int, _P, _P, _P, _P,
+                                         ctypes.c_float, ctypes.c_float, _P, _P, _P, _P]
+        lib.oracle_composite.restype = None
+        lib.oracle_fine_depths.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int,
+                                           ctypes.c_int, ctypes.c_int, _P, ctypes.c_float,
+                                           ctypes.c_float, _P, _P]
+        lib.oracle_fine_depths.restype = None
+        lib.oracle_max_threads.argtypes = []
+        lib.oracle_max_threads.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _arch(arch) -> _Arch:
+    t = arch.as_tuple() if hasattr(arch, "as_tuple") else tuple(arch)
+    return _Arch(*t)
+
+
+def max_threads() -> int:
+    return _lib_handle().oracle_max_threads()
+
+
+def philox4x32_10(counter, key) -> np.ndarray:
+    c = np.ascontiguousarray(counter, np.uint32)
+    k = np.ascontiguousarray(key, np.uint32)
+    out = np.zeros(4, np.uint32)
+    _lib_handle().oracle_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def jitter(seed: int, ray: int, i: int, stream: int) -> float:
+    return _lib_handle().oracle_jitter(seed, ray, i, stream)
+
+
+def sample_depths(seed: int, ray: int, near: float, far: float, n: int, perturb: bool = True):
+    t = np.zeros(n, np.float32)
+    _lib_handle().oracle_sample_depths(seed, ray, near, far, n, int(perturb), _ptr(t))
+    return t
+
+
+def nearest_site(sites: np.ndarray, x) -> int:
+    s = np.ascontiguousarray(sites, np.float32)
+    xx = np.ascontiguousarray(x, np.float32)
+    return _lib_handle().oracle_nearest_site(s.shape[0], _ptr(s), _ptr(xx))
+
+
+def bisector_margin(sites: np.ndarray, x, a: int) -> float:
+    s = np.ascontiguousarray(sites, np.float32)
+    xx = np.ascontiguousarray(x, np.float32)
+    return _lib_handle().oracle_bisector_margin(s.shape[0], _ptr(s), _ptr(xx), a)
+
+
+def posenc(L: int, p) -> np.ndarray:
+    pp = np.ascontiguousarray(p, np.float64)
+    out = np.zeros(3 + 6 * L, np.float64)
+    _lib_handle().oracle_posenc(L, _ptr(pp), _ptr(out))
+    return out
+
+
+def weights_count(arch) -> int:
+    a = _arch(arch)
+    return _lib_handle().oracle_weights_count(ctypes.byref(a))
+
+
+def head_eval(arch, weights: np.ndarray, gx: np.ndarray, gd: np.ndarray):
+    """(sigma, rgb[3]) of one head at encoded inputs gx, gd (float64)."""
+    a = _arch(arch)
+    w = np.ascontiguousarray(weights, np.float32)
+    gx = np.ascontiguousarray(gx, np.float64)
+    gd = np.ascontiguousarray(gd, np.float64)
+    sigma = np.zeros(1, np.float64)
+    rgb = np.zeros(3, np.float64)
+    scratch = np.zeros(4 * (gx.size + a.width + gd.size + a.rgb_hidden + 8), np.float64)
+    _lib_handle().oracle_head_eval(ctypes.byref(a), _ptr(w), _ptr(gx), _ptr(gd), _ptr(sigma),
+                                   _ptr(rgb), _ptr(scratch))
+    return float(sigma[0]), rgb
+
+
+_MODES = {"segments": 0, "direct": 3, "back": 4}
+
+
+def composite(cell, t, sigma, rgb, near: float, far: float, mode: str = "segments"):
+    """Composite given per-sample fields of one ray -> (rgb[3], depth, opacity, weights)."""
+    n = len(t)
+    cell = np.ascontiguousarray(cell, np.int32)
+    t = np.ascontiguousarray(t, np.float32)
+    sigma = np.ascontiguousarray(sigma, np.float64)
+    rgb = np.ascontiguousarray(rgb, np.float64).reshape(n, 3)
+    out = np.zeros(3, np.float64)
+    dep = np.zeros(1, np.float64)
+    op = np.zeros(1, np.float64)
+    w = np.zeros(max(n, 1), np.float64)
+    _lib_handle().oracle_composite(_MODES[mode], n, _ptr(cell), _ptr(t), _ptr(sigma), _ptr(rgb),
+                                   near, far, _ptr(out), _ptr(dep), _ptr(op), _ptr(w))
+    return out, float(dep[0]), float(op[0]), w[:n]
+
+
+def fine_depths(seed: int, ray: int, perturb: bool, tc: np.ndarray, near: float, far: float,
+                w: np.ndarray, n_fine: int) -> np.ndarray:
+    tc = np.ascontiguousarray(tc, np.float32)
+    w = np.ascontiguousarray(w, np.float64)
+    tf = np.zeros(n_fine, np.float32)
+    _lib_handle().oracle_fine_depths(seed, ray, int(perturb), tc.size, n_fine, _ptr(tc), near,
+                                     far, _ptr(w), _ptr(tf))
+    return tf
+
+
+class RenderResult:
+    """Outputs of an oracle render (double) plus optional per-sample arrays."""
+
+    def __init__(self, rgb, depth, opacity, t=None, cell=None, sigma=None, srgb=None,
+                 margin=None):
+        self.rgb, self.depth, self.opacity = rgb, depth, opacity
+        self.t, self.cell, self.sigma, self.srgb, self.margin = t, cell, sigma, srgb, margin
+
+
+def render(sites, arch, weights, rays_o, rays_d, near: float, far: float, n_coarse: int,
+           n_fine: int = 0, seed: int = 0, perturb: bool = True, ray_ids=None,
+           per_sample: bool = False, mode: str = "derf", beta: float = 0.0,
+           nthreads: int = 0) -> RenderResult:
+    """Render rays on the CPU.  mode: derf | direct | back | plain | soft."""
+    lib = _lib_handle()
+    sites = np.ascontiguousarray(sites, np.float32).reshape(-1, 3)
+    weights = np.ascontiguousarray(weights, np.float32)
+    o = np.ascontiguousarray(rays_o, np.float32).reshape(-1, 3)
+    d = np.ascontiguousarray(rays_d, np.float32).reshape(-1, 3)
+    R = o.shape[0]
+    N = n_coarse + n_fine
+    ids = None if ray_ids is None else np.ascontiguousarray(ray_ids, np.int64)
+    rgb = np.zeros((R, 3), np.float64)
+    dep = np.zeros(R, np.float64)
+    op = np.zeros(R, np.float64)
+    if per_sample:
+        t = np.zeros((R, N), np.float32)
+        cell = np.zeros((R, N), np.int32)
+        sig = np.zeros((R, N), np.float64)
+        srgb = np.zeros((R, N, 3), np.float64)
+        margin = np.zeros((R, N), np.float64)
+    else:
+        t = cell = sig = srgb = margin = None
+    a = _arch(arch)
+    args = [sites.shape[0], _ptr(sites), ctypes.byref(a), _ptr(weights), R, _ptr(o), _ptr(d),
+            _ptr(ids), near, far, n_coarse, n_fine, seed, int(perturb), _ptr(rgb), _ptr(dep),
+            _ptr(op), _ptr(t), _ptr(cell), _ptr(sig), _ptr(srgb), _ptr(margin), nthreads]
+    fn = {"derf": lib.oracle_render, "direct": lib.oracle_render_direct,
+          "back": lib.oracle_render_back_to_front, "plain": lib.oracle_render_plain}
+    if mode == "soft":
+        rc = lib.oracle_render_soft(*args, beta)
+    else:
+        rc = fn[mode](*args)
+    if rc != 0:
+        raise RuntimeError("oracle render failed (%d)" % rc)
+    return RenderResult(rgb, dep, op, t, cell, sig, srgb, margin)

@@ -1,0 +1,724 @@
+/*
+ * DeRF reference oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, single-file CPU implementation of the inference path of
+ * "DeRF: Decomposed Radiance Fields" (Rebain, Jiang, Yazdani, Li, Yi,
+ * Tagliasacchi): render rays through a radiance field split into Voronoi
+ * cells, each cell owned by its own small NeRF head.
+ *
+ * Only the test-suite, the smoke check and the benchmark's CPU baseline may
+ * load this library.  It shares no code with the GPU library.
+ *
+ * Precision.  The paper does not fix one, so everything that produces a
+ * real-valued result (positional encoding, the head networks, quadrature and
+ * compositing) is computed in double.  The values that decide an integer --
+ * the sample depths t and positions x, which decide the owning Voronoi cell
+ * -- are computed in float32, with explicit fused multiply-adds, because the
+ * GPU path takes the same decisions in float32: both sides must reach the
+ * same cell for the same sample.
+ *
+ * Steps (the paper's order):
+ *   Sec. 3.1, Eq. 1-2   stratified samples on [near, far], quadrature of the
+ *                       volume-rendering integral (midpoint tiling of the
+ *                       interval so that the quadrature weights cover it);
+ *   Sec. 3.2            one head per point: the decomposition weights are
+ *                       one-hot, so only the owning head is evaluated;
+ *   Sec. 3.3, Eq. 8     the owning head is the nearest site (the limit of
+ *                       the soft Voronoi weights as the temperature grows);
+ *   Sec. 3.3 Painter's  each cell's contiguous ray segment is integrated on
+ *                       its own, then the segments are composited in order
+ *                       along the ray (front to back; "over" is associative,
+ *                       so this equals the back-to-front Painter's order).
+ *
+ * Self-test helpers (not on the method's path): a plain single-network NeRF
+ * render, a soft-Voronoi render at finite temperature (Eq. 4-5 with Eq. 8),
+ * direct (unsegmented) and back-to-front compositing.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* ------------------------------------------------------------------ RNG --
+ * Philox4x32-10 counter-based generator, written from its definition in
+ * Salmon, Moraes, Dror, Shaw, "Parallel Random Numbers: As Easy as 1, 2, 3"
+ * (SC 2011): ten rounds of two 32x32->64 multiplies, with a Weyl sequence on
+ * the 2-word key between rounds.
+ */
+#define PHILOX_M0 0xD2511F53u
+#define PHILOX_M1 0xCD9E8D57u
+#define PHILOX_W0 0x9E3779B9u
+#define PHILOX_W1 0xBB67AE85u
+
+void oracle_philox4x32_10(const uint32_t ctr_in[4], const uint32_t key_in[2], uint32_t out[4])
+{
+    uint32_t c0 = ctr_in[0], c1 = ctr_in[1], c2 = ctr_in[2], c3 = ctr_in[3];
+    uint32_t k0 = key_in[0], k1 = key_in[1];
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) {
+            k0 += PHILOX_W0;
+            k1 += PHILOX_W1;
+        }
+        uint64_t p0 = (uint64_t)PHILOX_M0 * (uint64_t)c0;
+        uint64_t p1 = (uint64_t)PHILOX_M1 * (uint64_t)c2;
+        uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        uint32_t n0 = hi1 ^ c1 ^ k0;
+        uint32_t n1 = lo1;
+        uint32_t n2 = hi0 ^ c3 ^ k1;
+        uint32_t n3 = lo0;
+        c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* Jitter xi in [0, 1) for sample i of ray r.  Counter (i / 4, ray low word,
+ * ray high word, stream), key = seed words; word i % 4 of the block; the top
+ * 24 bits scaled by 2^-24 (exact in float32).  Stream 0 jitters the coarse
+ * strata, stream 1 the inverse-CDF draws of hierarchical sampling. */
+float oracle_jitter(uint64_t seed, uint64_t ray, uint32_t i, uint32_t stream)
+{
+    uint32_t ctr[4] = { i >> 2, (uint32_t)ray, (uint32_t)(ray >> 32), stream };
+    uint32_t key[2] = { (uint32_t)seed, (uint32_t)(seed >> 32) };
+    uint32_t out[4];
+    oracle_philox4x32_10(ctr, key, out);
+    return (float)(out[i & 3u] >> 8) * 0x1.0p-24f;
+}
+
+/* ------------------------------------------------------------- sampling --
+ * Stratified sampling of [near, far] into n equal strata (Eq. 1 bounds):
+ * t_i = near + (i + xi_i) * (far - near) / n, in float32 with one fma.
+ * perturb == 0 puts every sample at its stratum midpoint (xi = 1/2). */
+void oracle_sample_depths(uint64_t seed, uint64_t ray, float near_t, float far_t, int n,
+                          int perturb, float *t)
+{
+    float step = (far_t - near_t) / (float)n;
+    for (int i = 0; i < n; ++i) {
+        float xi = perturb ? oracle_jitter(seed, ray, (uint32_t)i, 0u) : 0.5f;
+        t[i] = fmaf(step, (float)i + xi, near_t);
+    }
+}
+
+/* x = o + t d per component, float32, one fma each. */
+static void sample_point(const float o[3], const float d[3], float t, float x[3])
+{
+    x[0] = fmaf(t, d[0], o[0]);
+    x[1] = fmaf(t, d[1], o[1]);
+    x[2] = fmaf(t, d[2], o[2]);
+}
+
+/* ----------------------------------------------------------- assignment --
+ * The owning head of x is its nearest Voronoi site (Sec. 3.3: the soft
+ * Voronoi weights of Eq. 8 become a partition as the temperature grows).
+ * Squared distance in float32: one rounding per coordinate difference, then
+ * ((e_x*e_x) + e_y^2) + e_z^2 with fmas.  Exact ties go to the lowest index. */
+int oracle_nearest_site(int K, const float *sites, const float x[3])
+{
+    int best_k = 0;
+    float best = INFINITY;
+    for (int k = 0; k < K; ++k) {
+        float ex = x[0] - sites[3 * k + 0];
+        float ey = x[1] - sites[3 * k + 1];
+        float ez = x[2] - sites[3 * k + 2];
+        float d2 = fmaf(ez, ez, fmaf(ey, ey, ex * ex));
+        if (d2 < best) {
+            best = d2;
+            best_k = k;
+        }
+    }
+    return best_k;
+}
+
+/* Distance (double) from x to the boundary of the cell of site a: the cell is
+ * the intersection of the half-spaces closer to a than to each b, so the
+ * distance is the smallest signed distance to a bisector plane. */
+double oracle_bisector_margin(int K, const float *sites, const float x[3], int a)
+{
+    double m = INFINITY;
+    double xa = x[0], ya = x[1], za = x[2];
+    for (int b = 0; b < K; ++b) {
+        if (b == a)
+            continue;
+        double pax = sites[3 * a], pay = sites[3 * a + 1], paz = sites[3 * a + 2];
+        double pbx = sites[3 * b], pby = sites[3 * b + 1], pbz = sites[3 * b + 2];
+        double da = (xa - pax) * (xa - pax) + (ya - pay) * (ya - pay) + (za - paz) * (za - paz);
+        double db = (xa - pbx) * (xa - pbx) + (ya - pby) * (ya - pby) + (za - pbz) * (za - pbz);
+        double sep = sqrt((pax - pbx) * (pax - pbx) + (pay - pby) * (pay - pby) +
+                          (paz - pbz) * (paz - pbz));
+        double dist = sep > 0.0 ? (db - da) / (2.0 * sep) : INFINITY;
+        if (dist < m)
+            m = dist;
+    }
+    return m;
+}
+
+/* ------------------------------------------------------------- encoding --
+ * Positional encoding of NeRF, used by every head (Sec. 4.1 keeps NeRF's
+ * settings): gamma_L(p) = (p, sin(pi 2^0 p), cos(pi 2^0 p), ...,
+ * sin(pi 2^{L-1} p), cos(pi 2^{L-1} p)), where p is a 3-vector and each
+ * sin/cos block lists x, y, z.  3 + 6L entries.
+ * sin(pi y) is evaluated after the exact reduction r = y - 2 rint(y / 2),
+ * so large 2^l p lose no accuracy. */
+static double sinpi_d(double y)
+{
+    double r = y - 2.0 * rint(0.5 * y);
+    return sin(M_PI * r);
+}
+
+static double cospi_d(double y)
+{
+    double r = y - 2.0 * rint(0.5 * y);
+    return cos(M_PI * r);
+}
+
+void oracle_posenc(int L, const double p[3], double *out)
+{
+    out[0] = p[0];
+    out[1] = p[1];
+    out[2] = p[2];
+    for (int l = 0; l < L; ++l) {
+        double s = ldexp(1.0, l);
+        for (int c = 0; c < 3; ++c) {
+            out[3 + 6 * l + c] = sinpi_d(s * p[c]);
+            out[3 + 6 * l + 3 + c] = cospi_d(s * p[c]);
+        }
+    }
+}
+
+/* ---------------------------------------------------------- head network --
+ * One head is a NeRF MLP (Sec. 4.1, settings of NeRF): `depth` ReLU layers
+ * of `width` units on gamma(x), the skip layer taking [gamma(x); h]; a ReLU
+ * density output from h; a colour branch on [h; gamma(d)] (an optional ReLU
+ * hidden layer) ending in a sigmoid.
+ *
+ * Packed weights of one head, float32, in this order: for each hidden layer
+ * W [width][in] row-major then b [width]; w_sigma [width], b_sigma [1];
+ * then either W_v [rgb_hidden][width + dir_dim], b_v, W_c [3][rgb_hidden],
+ * b_c [3], or (rgb_hidden == 0) W_c [3][width + dir_dim], b_c [3]. */
+typedef struct {
+    int pos_freqs;
+    int dir_freqs;
+    int depth;
+    int width;
+    int skip_layer;
+    int rgb_hidden;
+} oracle_arch;
+
+static int pos_dim(const oracle_arch *a) { return 3 + 6 * a->pos_freqs; }
+static int dir_dim(const oracle_arch *a) { return 3 + 6 * a->dir_freqs; }
+
+static int layer_in(const oracle_arch *a, int l)
+{
+    if (l == 0)
+        return pos_dim(a);
+    if (l == a->skip_layer)
+        return pos_dim(a) + a->width;
+    return a->width;
+}
+
+long long oracle_weights_count(const oracle_arch *a)
+{
+    long long n = 0;
+    for (int l = 0; l < a->depth; ++l)
+        n += (long long)a->width * layer_in(a, l) + a->width;
+    n += a->width + 1;
+    if (a->rgb_hidden > 0) {
+        n += (long long)a->rgb_hidden * (a->width + dir_dim(a)) + a->rgb_hidden;
+        n += 3LL * a->rgb_hidden + 3;
+    } else {
+        n += 3LL * (a->width + dir_dim(a)) + 3;
+    }
+    return n;
+}
+
+/* y[o] = sum_i W[o][i] in[i] + b[o], summed in index order. */
+static void dense(const float *W, const float *b, int n_out, int n_in, const double *in, double *y)
+{
+    for (int o = 0; o < n_out; ++o) {
+        double acc = 0.0;
+        const float *row = W + (size_t)o * n_in;
+        for (int i = 0; i < n_in; ++i)
+            acc += (double)row[i] * in[i];
+        y[o] = acc + (double)b[o];
+    }
+}
+
+static double relu(double v) { return v > 0.0 ? v : 0.0; }
+
+/* Evaluate one head at encoded position gx (pos_dim) and encoded direction gd
+ * (dir_dim).  scratch must hold 4 * (pos_dim + width + dir_dim + rgb_hidden). */
+void oracle_head_eval(const oracle_arch *a, const float *w, const double *gx, const double *gd,
+                      double *sigma, double rgb[3], double *scratch)
+{
+    int W = a->width, P = pos_dim(a), Dd = dir_dim(a);
+    double *h = scratch;                 /* width            */
+    double *in = h + W;                  /* P + W + Dd       */
+    double *g = in + P + W + Dd;         /* rgb_hidden       */
+    const float *p = w;
+    for (int l = 0; l < a->depth; ++l) {
+        int n_in = layer_in(a, l);
+        if (l == 0) {
+            memcpy(in, gx, sizeof(double) * P);
+        } else if (l == a->skip_layer) {
+            memcpy(in, gx, sizeof(double) * P);
+            memcpy(in + P, h, sizeof(double) * W);
+        } else {
+            memcpy(in, h, sizeof(double) * W);
+        }
+        dense(p, p + (size_t)W * n_in, W, n_in, in, h);
+        for (int o = 0; o < W; ++o)
+            h[o] = relu(h[o]);
+        p += (size_t)W * n_in + W;
+    }
+    double s;
+    dense(p, p + W, 1, W, h, &s);
+    *sigma = relu(s);
+    p += W + 1;
+    memcpy(in, h, sizeof(double) * W);
+    memcpy(in + W, gd, sizeof(double) * Dd);
+    double logit[3];
+    if (a->rgb_hidden > 0) {
+        int Hc = a->rgb_hidden;
+        dense(p, p + (size_t)Hc * (W + Dd), Hc, W + Dd, in, g);
+        for (int o = 0; o < Hc; ++o)
+            g[o] = relu(g[o]);
+        p += (size_t)Hc * (W + Dd) + Hc;
+        dense(p, p + 3 * Hc, 3, Hc, g, logit);
+    } else {
+        dense(p, p + 3 * (W + Dd), 3, W + Dd, in, logit);
+    }
+    for (int c = 0; c < 3; ++c)
+        rgb[c] = 1.0 / (1.0 + exp(-logit[c]));
+}
+
+/* --------------------------------------------------------- quadrature -----
+ * The integral of Eq. 1 is discretised on intervals that tile [near, far]:
+ * boundaries b_0 = near, b_i = (t_{i-1} + t_i) / 2, b_n = far; sample i
+ * stands for [b_i, b_{i+1}) of length delta_i.  Per sample the opacity is
+ * alpha = 1 - exp(-sigma delta) and the transmittance factor tau = exp(-sigma
+ * delta) (Eq. 2 on one interval). */
+static void intervals(const float *t, int n, float near_t, float far_t, double *delta)
+{
+    double prev = near_t;
+    for (int i = 0; i < n; ++i) {
+        double next = (i + 1 < n) ? 0.5 * ((double)t[i] + (double)t[i + 1]) : (double)far_t;
+        delta[i] = next - prev;
+        prev = next;
+    }
+}
+
+/* Per-segment integration and Painter's merge (Sec. 3.3).  A segment is a
+ * maximal run of samples with the same cell; by the convexity of Voronoi
+ * cells each cell contributes at most one run per ray.  Within a segment the
+ * local transmittance starts at 1 and the segment yields (C_s, D_s, T_s); the
+ * segments are then composited front to back: C += T C_s, D += T D_s,
+ * T *= T_s.  Returns rgb = C, depth = D, opacity = 1 - T.
+ * If w_out is given it receives the per-sample compositing weights T_i alpha_i
+ * with T_i the transmittance accumulated over all earlier samples. */
+static void composite_segments(int n, const int *cell, const float *t, const double *sigma,
+                               const double *rgb, const double *delta, double out_rgb[3],
+                               double *out_depth, double *out_opacity, double *w_out)
+{
+    double C[3] = {0.0, 0.0, 0.0}, D = 0.0, T = 1.0;
+    int i = 0;
+    while (i < n) {
+        int j = i;
+        double Cs[3] = {0.0, 0.0, 0.0}, Ds = 0.0, Tloc = 1.0;
+        while (j < n && cell[j] == cell[i]) {
+            double x = sigma[j] * delta[j];
+            double alpha = -expm1(-x);
+            double tau = exp(-x);
+            double w = Tloc * alpha;
+            if (w_out)
+                w_out[j] = T * w;
+            Cs[0] += w * rgb[3 * j + 0];
+            Cs[1] += w * rgb[3 * j + 1];
+            Cs[2] += w * rgb[3 * j + 2];
+            Ds += w * (double)t[j];
+            Tloc *= tau;
+            ++j;
+        }
+        C[0] += T * Cs[0];
+        C[1] += T * Cs[1];
+        C[2] += T * Cs[2];
+        D += T * Ds;
+        T *= Tloc;
+        i = j;
+    }
+    out_rgb[0] = C[0];
+    out_rgb[1] = C[1];
+    out_rgb[2] = C[2];
+    *out_depth = D;
+    *out_opacity = 1.0 - T;
+}
+
+/* Direct front-to-back compositing of all samples, ignoring cells. */
+static void composite_direct(int n, const float *t, const double *sigma, const double *rgb,
+                             const double *delta, double out_rgb[3], double *out_depth,
+                             double *out_opacity)
+{
+    double C[3] = {0.0, 0.0, 0.0}, D = 0.0, T = 1.0;
+    for (int j = 0; j < n; ++j) {
+        double x = sigma[j] * delta[j];
+        double w = T * -expm1(-x);
+        C[0] += w * rgb[3 * j + 0];
+        C[1] += w * rgb[3 * j + 1];
+        C[2] += w * rgb[3 * j + 2];
+        D += w * (double)t[j];
+        T *= exp(-x);
+    }
+    out_rgb[0] = C[0];
+    out_rgb[1] = C[1];
+    out_rgb[2] = C[2];
+    *out_depth = D;
+    *out_opacity = 1.0 - T;
+}
+
+/* Back-to-front compositing (the Painter's Algorithm as the paper states it):
+ * walking from the far end, C = C_i alpha_i + (1 - alpha_i) C; the depth and
+ * the transmittance use the same recurrence. */
+static void composite_back_to_front(int n, const float *t, const double *sigma,
+                                    const double *rgb, const double *delta, double out_rgb[3],
+                                    double *out_depth, double *out_opacity)
+{
+    double C[3] = {0.0, 0.0, 0.0}, D = 0.0, T = 1.0;
+    for (int j = n - 1; j >= 0; --j) {
+        double x = sigma[j] * delta[j];
+        double alpha = -expm1(-x);
+        double tau = exp(-x);
+        C[0] = alpha * rgb[3 * j + 0] + tau * C[0];
+        C[1] = alpha * rgb[3 * j + 1] + tau * C[1];
+        C[2] = alpha * rgb[3 * j + 2] + tau * C[2];
+        D = alpha * (double)t[j] + tau * D;
+        T = tau * T;
+    }
+    out_rgb[0] = C[0];
+    out_rgb[1] = C[1];
+    out_rgb[2] = C[2];
+    *out_depth = D;
+    *out_opacity = 1.0 - T;
+}
+
+/* ------------------------------------------------- hierarchical sampling --
+ * NeRF's coarse-to-fine sampling (the paper keeps NeRF's settings): the
+ * coarse compositing weights w_i define a piecewise-constant density over
+ * the coarse intervals [b_i, b_{i+1}), with a floor of 1e-5 per interval;
+ * n_fine draws u_j = (j + xi_j) / n_fine (stream 1) are mapped through its
+ * inverse CDF.  The fine depths are rounded to float32 (they decide cells)
+ * and merged with the coarse ones in sorted order (coarse first on ties). */
+static void fine_depths(uint64_t seed, uint64_t ray, int perturb, int nc, int nf, const float *tc,
+                        float near_t, float far_t, const double *w, double *cdf, float *tf)
+{
+    double total = 0.0;
+    cdf[0] = 0.0;
+    for (int i = 0; i < nc; ++i) {
+        total += w[i] + 1e-5;
+        cdf[i + 1] = total;
+    }
+    for (int i = 0; i <= nc; ++i)
+        cdf[i] /= total;
+    cdf[nc] = 1.0;
+    for (int j = 0; j < nf; ++j) {
+        double xi = perturb ? (double)oracle_jitter(seed, ray, (uint32_t)j, 1u) : 0.5;
+        double u = ((double)j + xi) / (double)nf;
+        /* largest i with cdf[i] <= u, i in [0, nc-1] */
+        int i = 0;
+        while (i + 1 < nc && cdf[i + 1] <= u)
+            ++i;
+        double b0 = (i == 0) ? (double)near_t : 0.5 * ((double)tc[i - 1] + (double)tc[i]);
+        double b1 = (i + 1 == nc) ? (double)far_t : 0.5 * ((double)tc[i] + (double)tc[i + 1]);
+        double span = cdf[i + 1] - cdf[i];
+        double frac = span > 0.0 ? (u - cdf[i]) / span : 0.0;
+        if (frac < 0.0)
+            frac = 0.0;
+        if (frac > 1.0)
+            frac = 1.0;
+        tf[j] = (float)(b0 + frac * (b1 - b0));
+    }
+}
+
+static void merge_sorted(const float *a, int na, const float *b, int nb, float *out)
+{
+    int i = 0, j = 0, k = 0;
+    while (i < na || j < nb) {
+        if (j >= nb || (i < na && a[i] <= b[j]))
+            out[k++] = a[i++];
+        else
+            out[k++] = b[j++];
+    }
+}
+
+/* ----------------------------------------------------------- rendering --- */
+
+typedef struct {
+    int K;
+    const float *sites;
+    const oracle_arch *arch;
+    const float *weights; /* K x weights_count, head-major */
+    float near_t, far_t;
+    int n_coarse, n_fine;
+    uint64_t seed;
+    int perturb;
+} render_args;
+
+enum { MODE_DERF = 0, MODE_PLAIN = 1, MODE_SOFT = 2, MODE_DIRECT = 3, MODE_BACK = 4 };
+
+/* Evaluate the field at every sample of one ray: cell, sigma, rgb. */
+static void eval_samples(const render_args *A, int mode, double beta, const float o[3],
+                         const float d[3], const double *gd, int n, const float *t, int *cell,
+                         double *sigma, double *rgb, double *gx, double *scratch)
+{
+    const oracle_arch *a = A->arch;
+    long long wc = oracle_weights_count(a);
+    for (int i = 0; i < n; ++i) {
+        float x[3];
+        sample_point(o, d, t[i], x);
+        double xd[3] = { x[0], x[1], x[2] };
+        oracle_posenc(a->pos_freqs, xd, gx);
+        if (mode == MODE_PLAIN) {
+            cell[i] = 0;
+            oracle_head_eval(a, A->weights, gx, gd, &sigma[i], &rgb[3 * i], scratch);
+        } else if (mode == MODE_SOFT) {
+            /* Eq. 4-5 with the soft Voronoi weights of Eq. 8 */
+            double dist_min = INFINITY;
+            for (int k = 0; k < A->K; ++k) {
+                double ex = xd[0] - A->sites[3 * k], ey = xd[1] - A->sites[3 * k + 1],
+                       ez = xd[2] - A->sites[3 * k + 2];
+                double dk = sqrt(ex * ex + ey * ey + ez * ez);
+                if (dk < dist_min)
+                    dist_min = dk;
+            }
+            double z = 0.0, s = 0.0, c[3] = {0.0, 0.0, 0.0};
+            for (int k = 0; k < A->K; ++k) {
+                double ex = xd[0] - A->sites[3 * k], ey = xd[1] - A->sites[3 * k + 1],
+                       ez = xd[2] - A->sites[3 * k + 2];
+                double dk = sqrt(ex * ex + ey * ey + ez * ez);
+                double wk = exp(-beta * (dk - dist_min));
+                z += wk;
+                if (wk == 0.0)
+                    continue;
+                double sk, ck[3];
+                oracle_head_eval(a, A->weights + (size_t)k * wc, gx, gd, &sk, ck, scratch);
+                s += wk * sk;
+                c[0] += wk * ck[0];
+                c[1] += wk * ck[1];
+                c[2] += wk * ck[2];
+            }
+            sigma[i] = s / z;
+            rgb[3 * i + 0] = c[0] / z;
+            rgb[3 * i + 1] = c[1] / z;
+            rgb[3 * i + 2] = c[2] / z;
+            cell[i] = 0;
+        } else {
+            cell[i] = oracle_nearest_site(A->K, A->sites, x);
+            oracle_head_eval(a, A->weights + (size_t)cell[i] * wc, gx, gd, &sigma[i], &rgb[3 * i],
+                             scratch);
+        }
+    }
+}
+
+static void finish(int mode, int n, const int *cell, const float *t, const double *sigma,
+                   const double *rgb, const double *delta, double *o_rgb, double *o_depth,
+                   double *o_opac, double *w_out)
+{
+    if (mode == MODE_DERF)
+        composite_segments(n, cell, t, sigma, rgb, delta, o_rgb, o_depth, o_opac, w_out);
+    else if (mode == MODE_BACK)
+        composite_back_to_front(n, t, sigma, rgb, delta, o_rgb, o_depth, o_opac);
+    else
+        composite_direct(n, t, sigma, rgb, delta, o_rgb, o_depth, o_opac);
+}
+
+/* Render rays [0, R).  Outputs are double; the optional per-sample arrays
+ * (any may be NULL) hold the final sample list of every ray (N = n_coarse +
+ * n_fine entries): depth t, owning cell, sigma, rgb (3 per sample) and the
+ * distance of the sample to its cell boundary.  ray_ids (optional) gives the
+ * global ray index of each row, used as the RNG counter. */
+static int render_impl(const render_args *A, int mode, double beta, long long R,
+                       const float *rays_o, const float *rays_d, const long long *ray_ids,
+                       double *out_rgb, double *out_depth, double *out_opacity, float *dbg_t,
+                       int *dbg_cell, double *dbg_sigma, double *dbg_rgb, double *dbg_margin,
+                       int nthreads)
+{
+    const oracle_arch *a = A->arch;
+    int nc = A->n_coarse, nf = A->n_fine, N = nc + nf;
+    if (nc < 1 || nf < 0 || (nf > 0 && nc < 2) || R < 0)
+        return -1;
+    int P = 3 + 6 * a->pos_freqs, Dd = 3 + 6 * a->dir_freqs;
+    size_t scratch_len = 4 * (size_t)(P + a->width + Dd + a->rgb_hidden + 8);
+#ifdef _OPENMP
+    if (nthreads > 0)
+        omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+    int failed = 0;
+#pragma omp parallel
+    {
+        float *tc = malloc(sizeof(float) * (size_t)N);
+        float *tf = malloc(sizeof(float) * (size_t)N);
+        float *tm = malloc(sizeof(float) * (size_t)N);
+        int *cell = malloc(sizeof(int) * (size_t)N);
+        double *sigma = malloc(sizeof(double) * (size_t)N);
+        double *rgb = malloc(sizeof(double) * 3 * (size_t)N);
+        double *delta = malloc(sizeof(double) * (size_t)N);
+        double *w = malloc(sizeof(double) * (size_t)N);
+        double *cdf = malloc(sizeof(double) * (size_t)(N + 1));
+        double *gx = malloc(sizeof(double) * (size_t)P);
+        double *gd = malloc(sizeof(double) * (size_t)Dd);
+        double *scratch = malloc(sizeof(double) * scratch_len);
+        if (!tc || !tf || !tm || !cell || !sigma || !rgb || !delta || !w || !cdf || !gx || !gd ||
+            !scratch) {
+#pragma omp atomic write
+            failed = 1;
+        } else {
+#pragma omp for schedule(dynamic, 16)
+            for (long long r = 0; r < R; ++r) {
+                const float *o = rays_o + 3 * r, *d = rays_d + 3 * r;
+                uint64_t rid = ray_ids ? (uint64_t)ray_ids[r] : (uint64_t)r;
+                /* encoded unit view direction, Sec. 3.1: c depends on d */
+                double dn = sqrt((double)d[0] * d[0] + (double)d[1] * d[1] + (double)d[2] * d[2]);
+                double dh[3] = { d[0] / dn, d[1] / dn, d[2] / dn };
+                oracle_posenc(a->dir_freqs, dh, gd);
+
+                oracle_sample_depths(A->seed, rid, A->near_t, A->far_t, nc, A->perturb, tc);
+                const float *tt = tc;
+                int n = nc;
+                eval_samples(A, mode, beta, o, d, gd, nc, tc, cell, sigma, rgb, gx, scratch);
+                intervals(tc, nc, A->near_t, A->far_t, delta);
+                double c3[3], dep, op;
+                finish(mode, nc, cell, tc, sigma, rgb, delta, c3, &dep, &op, w);
+                if (nf > 0) {
+                    if (mode != MODE_DERF)
+                        composite_segments(nc, cell, tc, sigma, rgb, delta, c3, &dep, &op, w);
+                    fine_depths(A->seed, rid, A->perturb, nc, nf, tc, A->near_t, A->far_t, w, cdf,
+                                tf);
+                    merge_sorted(tc, nc, tf, nf, tm);
+                    tt = tm;
+                    n = N;
+                    eval_samples(A, mode, beta, o, d, gd, N, tm, cell, sigma, rgb, gx, scratch);
+                    intervals(tm, N, A->near_t, A->far_t, delta);
+                    finish(mode, N, cell, tm, sigma, rgb, delta, c3, &dep, &op, NULL);
+                }
+                out_rgb[3 * r + 0] = c3[0];
+                out_rgb[3 * r + 1] = c3[1];
+                out_rgb[3 * r + 2] = c3[2];
+                out_depth[r] = dep;
+                out_opacity[r] = op;
+                for (int i = 0; i < n; ++i) {
+                    size_t s = (size_t)r * N + i;
+                    if (dbg_t)
+                        dbg_t[s] = tt[i];
+                    if (dbg_cell)
+                        dbg_cell[s] = cell[i];
+                    if (dbg_sigma)
+                        dbg_sigma[s] = sigma[i];
+                    if (dbg_rgb) {
+                        dbg_rgb[3 * s + 0] = rgb[3 * i + 0];
+                        dbg_rgb[3 * s + 1] = rgb[3 * i + 1];
+                        dbg_rgb[3 * s + 2] = rgb[3 * i + 2];
+                    }
+                    if (dbg_margin) {
+                        float x[3];
+                        sample_point(o, d, tt[i], x);
+                        dbg_margin[s] = (mode == MODE_PLAIN || mode == MODE_SOFT || A->K == 1)
+                                            ? INFINITY
+                                            : oracle_bisector_margin(A->K, A->sites, x, cell[i]);
+                    }
+                }
+            }
+        }
+        free(tc); free(tf); free(tm); free(cell); free(sigma); free(rgb); free(delta);
+        free(w); free(cdf); free(gx); free(gd); free(scratch);
+    }
+    return failed ? -3 : 0;
+}
+
+#define ORACLE_RENDER_ARGS                                                                    \
+    int K, const float *sites, const oracle_arch *arch, const float *weights, long long R,     \
+        const float *rays_o, const float *rays_d, const long long *ray_ids, float near_t,      \
+        float far_t, int n_coarse, int n_fine, uint64_t seed, int perturb, double *out_rgb,    \
+        double *out_depth, double *out_opacity, float *dbg_t, int *dbg_cell, double *dbg_sigma, \
+        double *dbg_rgb, double *dbg_margin, int nthreads
+
+#define ORACLE_FILL_ARGS                                                                       \
+    render_args A = { K, sites, arch, weights, near_t, far_t, n_coarse, n_fine, seed, perturb };
+
+/* DeRF render: nearest-site heads, per-segment integration, Painter's merge. */
+int oracle_render(ORACLE_RENDER_ARGS)
+{
+    ORACLE_FILL_ARGS
+    return render_impl(&A, MODE_DERF, 0.0, R, rays_o, rays_d, ray_ids, out_rgb, out_depth,
+                       out_opacity, dbg_t, dbg_cell, dbg_sigma, dbg_rgb, dbg_margin, nthreads);
+}
+
+/* Same heads, direct front-to-back compositing over all samples (no segments). */
+int oracle_render_direct(ORACLE_RENDER_ARGS)
+{
+    ORACLE_FILL_ARGS
+    return render_impl(&A, MODE_DIRECT, 0.0, R, rays_o, rays_d, ray_ids, out_rgb, out_depth,
+                       out_opacity, dbg_t, dbg_cell, dbg_sigma, dbg_rgb, dbg_margin, nthreads);
+}
+
+/* Same heads, back-to-front compositing (Painter's order as the paper states it). */
+int oracle_render_back_to_front(ORACLE_RENDER_ARGS)
+{
+    ORACLE_FILL_ARGS
+    return render_impl(&A, MODE_BACK, 0.0, R, rays_o, rays_d, ray_ids, out_rgb, out_depth,
+                       out_opacity, dbg_t, dbg_cell, dbg_sigma, dbg_rgb, dbg_margin, nthreads);
+}
+
+/* Plain NeRF: head 0 everywhere, direct compositing, no decomposition. */
+int oracle_render_plain(ORACLE_RENDER_ARGS)
+{
+    ORACLE_FILL_ARGS
+    return render_impl(&A, MODE_PLAIN, 0.0, R, rays_o, rays_d, ray_ids, out_rgb, out_depth,
+                       out_opacity, dbg_t, dbg_cell, dbg_sigma, dbg_rgb, dbg_margin, nthreads);
+}
+
+/* Soft Voronoi at temperature beta: every head evaluated, blended by Eq. 8. */
+int oracle_render_soft(ORACLE_RENDER_ARGS, double beta)
+{
+    ORACLE_FILL_ARGS
+    return render_impl(&A, MODE_SOFT, beta, R, rays_o, rays_d, ray_ids, out_rgb, out_depth,
+                       out_opacity, dbg_t, dbg_cell, dbg_sigma, dbg_rgb, dbg_margin, nthreads);
+}
+
+/* Composite given per-sample fields (pins of the quadrature and of the
+ * Painter's merge on hand-made inputs).  mode: 0 segments, 3 direct, 4 back. */
+void oracle_composite(int mode, int n, const int *cell, const float *t, const double *sigma,
+                      const double *rgb, float near_t, float far_t, double out_rgb[3],
+                      double *out_depth, double *out_opacity, double *w_out)
+{
+    double *delta = malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
+    intervals(t, n, near_t, far_t, delta);
+    if (mode == MODE_DERF)
+        composite_segments(n, cell, t, sigma, rgb, delta, out_rgb, out_depth, out_opacity, w_out);
+    else if (mode == MODE_BACK)
+        composite_back_to_front(n, t, sigma, rgb, delta, out_rgb, out_depth, out_opacity);
+    else
+        composite_direct(n, t, sigma, rgb, delta, out_rgb, out_depth, out_opacity);
+    free(delta);
+}
+
+/* Inverse-CDF fine depths of one ray from given coarse weights (pins). */
+void oracle_fine_depths(uint64_t seed, uint64_t ray, int perturb, int nc, int nf, const float *tc,
+                        float near_t, float far_t, const double *w, float *tf)
+{
+    double *cdf = malloc(sizeof(double) * (size_t)(nc + 1));
+    fine_depths(seed, ray, perturb, nc, nf, tc, near_t, far_t, w, cdf, tf);
+    free(cdf);
+}
+
+int oracle_max_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

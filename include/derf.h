@@ -1,0 +1,173 @@
+/*
+ * derf.h -- C ABI of the MI355X (gfx950) DeRF renderer.
+ *
+ * DeRF ("Decomposed Radiance Fields", Rebain et al.) splits a NeRF radiance
+ * field into the cells of a Voronoi diagram and gives every cell its own
+ * small network head (Sec. 3.2, Eq. 4-5).  At inference the decomposition is
+ * a hard partition -- each point is owned by its nearest site, the limit of
+ * the soft Voronoi weights of Eq. 8 -- so every ray sample is evaluated by
+ * exactly one head.  A ray crosses each convex cell in one contiguous
+ * segment; each segment is volume-integrated on its own (Eq. 1-2) and the
+ * segments are composited front to back in the order the Painter's argument
+ * of Sec. 3.3 fixes.
+ *
+ * Calls:
+ *   derf_create   upload sites and per-head weights            (Sec. 3.2-3.3)
+ *   derf_render   render rays: sample, encode, assign, bucket,
+ *                 per-head MLP, segment integration, merge      (Sec. 3.1, 3.3)
+ *   derf_render_debug  the same, also returning per-sample data
+ *
+ * All functions return a derf_status (0 on success, negative on error),
+ * never abort and never print.  derf_last_error() returns a thread-local
+ * text describing the last failure of the calling thread.
+ */
+#ifndef DERF_H
+#define DERF_H
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct derf_handle derf_handle;
+
+typedef enum {
+    DERF_OK = 0,
+    DERF_ERR_INVALID_ARG = -1, /* a null pointer, an out-of-range size or value     */
+    DERF_ERR_UNSUPPORTED = -2, /* a head architecture with no compiled kernel      */
+    DERF_ERR_OOM = -3,         /* device or host allocation failed                  */
+    DERF_ERR_HIP = -4          /* a HIP runtime call or kernel launch failed        */
+} derf_status;
+
+typedef enum {
+    DERF_PREC_FP32 = 0, /* fp32 operands, fp32 MFMA accumulate                      */
+    DERF_PREC_BF16 = 1  /* bf16 operands (round to nearest even), fp32 accumulate   */
+} derf_precision;
+
+/* Architecture shared by every head (the paper's heads are homogeneous; the
+ * head network keeps NeRF's layout, Sec. 4.1).
+ *   pos_freqs  L of the positional encoding gamma(x): 3 + 6L inputs
+ *   dir_freqs  L of the direction encoding gamma(d / |d|): 3 + 6L inputs
+ *   depth      number of hidden ReLU layers
+ *   width      units per hidden layer
+ *   skip_layer 0-based hidden layer whose input is [gamma(x); h], -1 = none
+ *   rgb_hidden width of the ReLU hidden layer of the colour branch on
+ *              [h; gamma(d)]; 0 = the colour logits read [h; gamma(d)] directly
+ * The compiled kernels cover (pos, dir, depth, width, skip, rgb_hidden) =
+ * (6,4,4,64,-1,0), (10,4,8,256,5,128), (10,4,8,128,5,64), (10,4,6,64,-1,32);
+ * any other architecture is DERF_ERR_UNSUPPORTED. */
+typedef struct {
+    int pos_freqs;
+    int dir_freqs;
+    int depth;
+    int width;
+    int skip_layer;
+    int rgb_hidden;
+} derf_head_arch;
+
+/* Sampling of each ray on [near, far] (Sec. 3.1 Eq. 1 bounds).
+ *   n_coarse  stratified samples per ray (>= 1, n_coarse + n_fine <= 1024)
+ *   n_fine    inverse-CDF samples per ray drawn from the coarse weights; 0 =
+ *             single pass.  (Hierarchical sampling is not built yet: any
+ *             n_fine > 0 returns DERF_ERR_UNSUPPORTED.)
+ *   seed      key of the Philox4x32-10 generator of the stratum jitter
+ *   perturb   1: t_i = near + (i + xi) (far - near) / n with xi from Philox;
+ *             0: xi = 1/2 (stratum midpoints)
+ *   ray_offset  frame index of the first ray of the call: the jitter of sample
+ *             i of ray r is word i % 4 of Philox4x32-10 at counter
+ *             (i / 4, low and high words of ray_offset + r, 0), key = the
+ *             seed's low and high words, mapped as (word >> 8) * 2^-24; so a
+ *             frame split over several calls renders exactly as one call */
+typedef struct {
+    int n_coarse;
+    int n_fine;
+    unsigned long long seed;
+    int perturb;
+    unsigned long long ray_offset;
+} derf_sampling;
+
+/* Number of floats of one head's packed weights for this architecture, or
+ * -1 for invalid values.  Per head, in this order: for each hidden layer l,
+ * W_l [width][in_l] row-major (out x in) then b_l [width], with in_0 =
+ * 3 + 6 pos_freqs and in_skip = (3 + 6 pos_freqs) + width (input order
+ * [gamma(x); h]); then w_sigma [width], b_sigma [1]; then, if rgb_hidden > 0,
+ * W_v [rgb_hidden][width + 3 + 6 dir_freqs], b_v [rgb_hidden], W_c
+ * [3][rgb_hidden], b_c [3], else W_c [3][width + 3 + 6 dir_freqs], b_c [3]
+ * (input order [h; gamma(d)]).  Density is ReLU(w_sigma . h + b_sigma),
+ * colour is sigmoid of the logits. */
+long long derf_weights_count(const derf_head_arch *arch);
+
+/* Create a renderer on the current HIP device.
+ *   out        receives the handle (set to NULL on failure)
+ *   num_sites  K, number of Voronoi sites = number of heads, 1 <= K <= 256
+ *   sites_xyz  host float [K][3]: the sites phi (Sec. 3.3)
+ *   arch       head architecture (see above)
+ *   weights    host float [K][derf_weights_count(arch)]: head k's packed
+ *              weights at weights + k * derf_weights_count(arch)
+ *   precision  a derf_precision
+ * The host arrays are copied (converted and re-laid-out for the kernels) and
+ * may be freed on return.  The call synchronises the device. */
+int derf_create(derf_handle **out, int num_sites, const float *sites_xyz,
+                const derf_head_arch *arch, const float *weights, int precision);
+
+/* Render num_rays rays.  All array arguments are device pointers:
+ *   rays_o, rays_d   float [R][3] origins and directions (directions need
+ *                    not be unit length: samples are o + t d, the colour
+ *                    head sees gamma(d / |d|))
+ *   out_rgb          float [R][3] composited colour (black background)
+ *   out_depth        float [R] expected depth sum_i w_i t_i
+ *   out_opacity      float [R] 1 - transmittance after the last sample
+ * near_t < far_t; samp as above; hip_stream is a hipStream_t (NULL: the
+ * default stream).  The work is enqueued on hip_stream and the call returns
+ * without waiting for it; the inputs must stay valid and the outputs
+ * untouched until it completes.  Kernel faults surface at the caller's next
+ * synchronisation.  num_rays == 0 is a no-op.  R * n_coarse must stay below
+ * 2^32; larger frames are rendered in several calls.  Calls on one handle
+ * must not run concurrently (they share the handle's workspace, which grows
+ * as needed and is reused). */
+int derf_render(derf_handle *h, const float *rays_o, const float *rays_d, long long num_rays,
+                float near_t, float far_t, const derf_sampling *samp, float *out_rgb,
+                float *out_depth, float *out_opacity, void *hip_stream);
+
+/* Optional per-sample outputs of derf_render_debug: device pointers, any may
+ * be NULL.  N = samples per ray; sample i of ray r is at index r * N + i. */
+typedef struct {
+    int *cell;    /* [R][N] owning site of each sample                       */
+    float *t;     /* [R][N] sample depth                                     */
+    float *sigma; /* [R][N] density from the owning head                     */
+    float *rgb;   /* [R][N][3] colour from the owning head                   */
+} derf_debug_out;
+
+int derf_render_debug(derf_handle *h, const float *rays_o, const float *rays_d,
+                      long long num_rays, float near_t, float far_t, const derf_sampling *samp,
+                      float *out_rgb, float *out_depth, float *out_opacity,
+                      const derf_debug_out *dbg, void *hip_stream);
+
+/* Per-stage GPU time, recorded with HIP events on the render's stream when
+ * timing is on (derf_set_timing); accumulated over renders since the last
+ * derf_reset_stats.  Stages: 0 sample+encode+assign, 1 bucket scan,
+ * 2 bucket scatter, 3 per-head MLP, 4 segment compositing. */
+#define DERF_NUM_STAGES 5
+typedef struct {
+    long long renders;                  /* renders since reset              */
+    long long samples;                  /* samples since reset              */
+    double stage_ms[DERF_NUM_STAGES];   /* summed event time per stage      */
+    long long stage_launches[DERF_NUM_STAGES];
+    long long head_samples[256];        /* samples per head of the last render */
+} derf_stats;
+
+int derf_set_timing(derf_handle *h, int on);
+/* Waits for the last render's stream, then fills *out. */
+int derf_get_stats(derf_handle *h, derf_stats *out);
+int derf_reset_stats(derf_handle *h);
+
+/* Waits for the handle's last stream, then frees everything.  NULL is a no-op. */
+void derf_destroy(derf_handle *h);
+
+const char *derf_status_string(int status);
+const char *derf_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DERF_H */

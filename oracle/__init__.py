@@ -81,6 +81,11 @@ def _lib_handle():
                                            ctypes.c_int, ctypes.c_int, _P, ctypes.c_float,
                                            ctypes.c_float, _P, _P]
         lib.oracle_fine_depths.restype = None
+        lib.oracle_sample_assign.argtypes = [ctypes.c_int, _P, ctypes.c_longlong, _P, _P,
+                                             ctypes.c_uint64, ctypes.c_float, ctypes.c_float,
+                                             ctypes.c_int, ctypes.c_uint64, ctypes.c_int, _P, _P,
+                                             _P, ctypes.c_int]
+        lib.oracle_sample_assign.restype = ctypes.c_int
         lib.oracle_max_threads.argtypes = []
         lib.oracle_max_threads.restype = ctypes.c_int
         _lib = lib
@@ -183,6 +188,26 @@ def fine_depths(seed: int, ray: int, perturb: bool, tc: np.ndarray, near: float,
     _lib_handle().oracle_fine_depths(seed, ray, int(perturb), tc.size, n_fine, _ptr(tc), near,
                                      far, _ptr(w), _ptr(tf))
     return tf
+
+
+def sample_assign(sites, rays_o, rays_d, near: float, far: float, n: int, seed: int,
+                  perturb: bool = True, ray_offset: int = 0, margin: bool = False,
+                  nthreads: int = 0):
+    """Sample depths t [R, n] (float32), owning cells [R, n] and optionally each
+    sample's distance to its cell boundary, for every sample of the rays."""
+    sites = np.ascontiguousarray(sites, np.float32).reshape(-1, 3)
+    o = np.ascontiguousarray(rays_o, np.float32).reshape(-1, 3)
+    d = np.ascontiguousarray(rays_d, np.float32).reshape(-1, 3)
+    R = o.shape[0]
+    t = np.zeros((R, n), np.float32)
+    cell = np.zeros((R, n), np.int32)
+    m = np.zeros((R, n), np.float64) if margin else None
+    rc = _lib_handle().oracle_sample_assign(sites.shape[0], _ptr(sites), R, _ptr(o), _ptr(d),
+                                            ray_offset, near, far, n, seed, int(perturb), _ptr(t),
+                                            _ptr(cell), _ptr(m), nthreads)
+    if rc != 0:
+        raise RuntimeError("oracle sample_assign failed (%d)" % rc)
+    return t, cell, m
 
 
 class RenderResult:

@@ -688,6 +688,40 @@ int oracle_render_soft(ORACLE_RENDER_ARGS, double beta)
                        out_opacity, dbg_t, dbg_cell, dbg_sigma, dbg_rgb, dbg_margin, nthreads);
 }
 
+/* Sample depths and owning cells of every sample of rays [0, R) (no network):
+ * the full-frame check of the assignment.  Ray r uses RNG ray index
+ * ray_offset + r.  margin (optional) receives each sample's distance to its
+ * cell boundary. */
+int oracle_sample_assign(int K, const float *sites, long long R, const float *rays_o,
+                         const float *rays_d, uint64_t ray_offset, float near_t, float far_t, int n,
+                         uint64_t seed, int perturb, float *t_out, int *cell_out,
+                         double *margin_out, int nthreads)
+{
+    if (n < 1 || R < 0 || K < 1)
+        return -1;
+#ifdef _OPENMP
+    if (nthreads > 0)
+        omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+#pragma omp parallel for schedule(static)
+    for (long long r = 0; r < R; ++r) {
+        float *t = t_out + (size_t)r * n;
+        oracle_sample_depths(seed, ray_offset + (uint64_t)r, near_t, far_t, n, perturb, t);
+        for (int i = 0; i < n; ++i) {
+            float x[3];
+            sample_point(rays_o + 3 * r, rays_d + 3 * r, t[i], x);
+            int c = oracle_nearest_site(K, sites, x);
+            cell_out[(size_t)r * n + i] = c;
+            if (margin_out)
+                margin_out[(size_t)r * n + i] =
+                    K > 1 ? oracle_bisector_margin(K, sites, x, c) : INFINITY;
+        }
+    }
+    return 0;
+}
+
 /* Composite given per-sample fields (pins of the quadrature and of the
  * Painter's merge on hand-made inputs).  mode: 0 segments, 3 direct, 4 back. */
 void oracle_composite(int mode, int n, const int *cell, const float *t, const double *sigma,

@@ -1,0 +1,454 @@
+// Host side of the C ABI declared in include/derf.h: argument checking,
+// weight layout at creation, workspace management and the stream-ordered
+// launch sequence of a render.
+#include "derf.h"
+
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "derf_internal.h"
+
+using namespace derf;
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int fail(int status, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int status, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int hip_fail(hipError_t e, const char *what)
+{
+    return fail(DERF_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, what)                  \
+    do {                                     \
+        hipError_t e_ = (expr);              \
+        if (e_ != hipSuccess)                \
+            return hip_fail(e_, what);       \
+    } while (0)
+
+long long weights_count(const derf_head_arch *a)
+{
+    const long long P = 3 + 6LL * a->pos_freqs, Dd = 3 + 6LL * a->dir_freqs, W = a->width;
+    long long n = 0;
+    for (int l = 0; l < a->depth; ++l) {
+        const long long in = l == 0 ? P : (l == a->skip_layer ? P + W : W);
+        n += W * in + W;
+    }
+    n += W + 1;
+    if (a->rgb_hidden > 0)
+        n += (long long)a->rgb_hidden * (W + Dd) + a->rgb_hidden + 3LL * a->rgb_hidden + 3;
+    else
+        n += 3 * (W + Dd) + 3;
+    return n;
+}
+
+bool arch_values_valid(const derf_head_arch *a)
+{
+    return a->pos_freqs >= 0 && a->pos_freqs <= 16 && a->dir_freqs >= 0 && a->dir_freqs <= 16 &&
+           a->depth >= 1 && a->depth <= 64 && a->width >= 1 && a->width <= 4096 &&
+           (a->skip_layer == -1 || (a->skip_layer >= 1 && a->skip_layer < a->depth)) &&
+           a->rgb_hidden >= 0 && a->rgb_hidden <= 4096;
+}
+
+struct Workspace {
+    void *mem = nullptr;
+    size_t bytes = 0;
+};
+
+}  // namespace
+
+struct derf_handle {
+    int device = 0;
+    int num_sites = 0;
+    int site_bits = 0;
+    bool bf16 = false;
+    derf_head_arch arch{};
+    const MlpVariant *mlp = nullptr;
+    int mlp_grid = 0;
+    float4 *sites = nullptr;
+    unsigned char *streams = nullptr;
+    float *blocks = nullptr;
+    Workspace ws;
+    hipStream_t last_stream = nullptr;
+    bool timing = false;
+    hipEvent_t ev[2 * DERF_NUM_STAGES] = {};
+    bool ev_pending = false;
+    derf_stats stats{};
+    unsigned *totals = nullptr;  // device pointer into the workspace of the last render
+};
+
+namespace {
+
+template <class T>
+T *carve(char *&p, size_t count)
+{
+    T *r = reinterpret_cast<T *>(p);
+    p += ((count * sizeof(T) + 255) / 256) * 256;
+    return r;
+}
+
+struct Buffers {
+    float *t;
+    uint8_t *cell;
+    float4 *sr;
+    unsigned *bucket;
+    void *dirbuf;
+    unsigned *counts;
+    unsigned *totals;
+};
+
+size_t layout(char *base, unsigned S, unsigned R, unsigned nblk, int K, bool bf16, Buffers *b)
+{
+    char *p = base;
+    Buffers x;
+    x.t = carve<float>(p, S);
+    x.cell = carve<uint8_t>(p, (size_t)S + 16);
+    x.sr = carve<float4>(p, S);
+    x.bucket = carve<unsigned>(p, S);
+    x.dirbuf = carve<char>(p, (size_t)R * kDirPad * (bf16 ? 2 : 4));
+    x.counts = carve<unsigned>(p, (size_t)nblk * K);
+    x.totals = carve<unsigned>(p, K);
+    if (b)
+        *b = x;
+    return (size_t)(p - base);
+}
+
+void accumulate_timing(derf_handle *h)
+{
+    if (!h->ev_pending)
+        return;
+    for (int s = 0; s < DERF_NUM_STAGES; ++s) {
+        float ms = 0.0f;
+        if (hipEventElapsedTime(&ms, h->ev[2 * s], h->ev[2 * s + 1]) == hipSuccess) {
+            h->stats.stage_ms[s] += ms;
+            h->stats.stage_launches[s] += 1;
+        }
+    }
+    h->ev_pending = false;
+}
+
+int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long long num_rays,
+                float near_t, float far_t, const derf_sampling *samp, float *out_rgb,
+                float *out_depth, float *out_opacity, const derf_debug_out *dbg, void *stream)
+{
+    if (!h)
+        return fail(DERF_ERR_INVALID_ARG, "null handle");
+    if (!samp)
+        return fail(DERF_ERR_INVALID_ARG, "null sampling descriptor");
+    if (num_rays < 0)
+        return fail(DERF_ERR_INVALID_ARG, "num_rays < 0");
+    if (!(near_t < far_t) || !isfinite(near_t) || !isfinite(far_t))
+        return fail(DERF_ERR_INVALID_ARG, "need finite near < far");
+    if (samp->n_coarse < 1 || samp->n_fine < 0 || samp->n_coarse + samp->n_fine > 1024)
+        return fail(DERF_ERR_INVALID_ARG, "need 1 <= n_coarse, 0 <= n_fine, total <= 1024");
+    if (samp->n_fine > 0 && samp->n_coarse < 2)
+        return fail(DERF_ERR_INVALID_ARG, "hierarchical sampling needs n_coarse >= 2");
+    if (samp->n_fine > 0)
+        return fail(DERF_ERR_UNSUPPORTED, "hierarchical (n_fine > 0) sampling is not built");
+    if (num_rays == 0)
+        return DERF_OK;
+    if (!rays_o || !rays_d || !out_rgb || !out_depth || !out_opacity)
+        return fail(DERF_ERR_INVALID_ARG, "null ray or output pointer");
+    const unsigned long long S64 = (unsigned long long)num_rays * (unsigned)samp->n_coarse;
+    if (S64 >= (1ull << 32))
+        return fail(DERF_ERR_INVALID_ARG, "num_rays * samples must be < 2^32 per call");
+
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    HIP_TRY(hipSetDevice(h->device), "hipSetDevice");
+    const unsigned R = (unsigned)num_rays, N = (unsigned)samp->n_coarse, S = (unsigned)S64;
+    const unsigned nblk = (S + kBucketBlock - 1) / kBucketBlock;
+    const size_t need = layout(nullptr, S, R, nblk, h->num_sites, h->bf16, nullptr);
+    if (need > h->ws.bytes) {
+        // the old workspace may still be in use by work on the previous stream
+        if (h->last_stream || h->ws.mem)
+            HIP_TRY(hipStreamSynchronize(h->last_stream), "hipStreamSynchronize");
+        if (h->ws.mem)
+            HIP_TRY(hipFree(h->ws.mem), "hipFree");
+        h->ws.mem = nullptr;
+        h->ws.bytes = 0;
+        const size_t grow = need + need / 8;
+        if (hipMalloc(&h->ws.mem, grow) != hipSuccess) {
+            (void)hipGetLastError();
+            h->ws.mem = nullptr;
+            return fail(DERF_ERR_OOM, "workspace of %zu bytes", grow);
+        }
+        h->ws.bytes = grow;
+    }
+    if (h->timing && h->ev_pending) {
+        HIP_TRY(hipEventSynchronize(h->ev[2 * DERF_NUM_STAGES - 1]), "hipEventSynchronize");
+        accumulate_timing(h);
+    }
+    Buffers b;
+    layout(reinterpret_cast<char *>(h->ws.mem), S, R, nblk, h->num_sites, h->bf16, &b);
+
+    RenderGeometry g;
+    g.rays_o = rays_o;
+    g.rays_d = rays_d;
+    g.num_rays = R;
+    g.n = N;
+    g.num_samples = S;
+    g.inv_n = 1.0 / (double)N;
+    g.near_t = near_t;
+    g.far_t = far_t;
+    g.step = (far_t - near_t) / (float)N;
+    g.seed = samp->seed;
+    g.ray_offset = samp->ray_offset;
+    g.perturb = samp->perturb ? 1 : 0;
+
+    auto mark = [&](int idx) -> hipError_t {
+        return h->timing ? hipEventRecord(h->ev[idx], s) : hipSuccess;
+    };
+
+    HIP_TRY(mark(0), "hipEventRecord");
+    HIP_TRY(launch_ray_encode(g, b.dirbuf, h->bf16, s), "ray_encode launch");
+    HIP_TRY(launch_sample_assign(g, h->sites, h->num_sites, h->site_bits, b.t, b.cell, b.counts,
+                                 nblk, s),
+            "sample_assign launch");
+    HIP_TRY(mark(1), "hipEventRecord");
+    HIP_TRY(mark(2), "hipEventRecord");
+    HIP_TRY(launch_bucket_scan(b.counts, nblk, h->num_sites, b.totals, s), "bucket_scan launch");
+    HIP_TRY(mark(3), "hipEventRecord");
+    HIP_TRY(mark(4), "hipEventRecord");
+    HIP_TRY(launch_bucket_scatter(b.cell, b.counts, b.totals, S, nblk, h->num_sites, h->site_bits,
+                                  b.bucket, s),
+            "bucket_scatter launch");
+    HIP_TRY(mark(5), "hipEventRecord");
+    HIP_TRY(mark(6), "hipEventRecord");
+    HIP_TRY(h->mlp->launch(b.bucket, b.totals, h->num_sites, g, b.t, b.dirbuf, h->streams,
+                           h->blocks, b.sr, h->mlp_grid, s),
+            "mlp launch");
+    HIP_TRY(mark(7), "hipEventRecord");
+    HIP_TRY(mark(8), "hipEventRecord");
+    HIP_TRY(launch_composite(g, b.t, b.cell, b.sr, out_rgb, out_depth, out_opacity, s),
+            "composite launch");
+    HIP_TRY(mark(9), "hipEventRecord");
+    if (dbg && (dbg->cell || dbg->t || dbg->sigma || dbg->rgb))
+        HIP_TRY(launch_debug_expand(S, b.t, b.cell, b.sr, dbg->cell, dbg->t, dbg->sigma, dbg->rgb,
+                                    s),
+                "debug_expand launch");
+    h->ev_pending = h->timing;
+    h->last_stream = s;
+    h->totals = b.totals;
+    h->stats.renders += 1;
+    h->stats.samples += S;
+    return DERF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+long long derf_weights_count(const derf_head_arch *arch)
+{
+    if (!arch || !arch_values_valid(arch))
+        return -1;
+    return weights_count(arch);
+}
+
+int derf_create(derf_handle **out, int num_sites, const float *sites_xyz,
+                const derf_head_arch *arch, const float *weights, int precision)
+{
+    if (!out)
+        return fail(DERF_ERR_INVALID_ARG, "null output handle pointer");
+    *out = nullptr;
+    if (!sites_xyz || !arch || !weights)
+        return fail(DERF_ERR_INVALID_ARG, "null sites, arch or weights");
+    if (num_sites < 1 || num_sites > kMaxSites)
+        return fail(DERF_ERR_INVALID_ARG, "num_sites must be in [1, 256]");
+    if (precision != DERF_PREC_FP32 && precision != DERF_PREC_BF16)
+        return fail(DERF_ERR_INVALID_ARG, "unknown precision %d", precision);
+    if (!arch_values_valid(arch))
+        return fail(DERF_ERR_INVALID_ARG, "head architecture values out of range");
+    for (int i = 0; i < 3 * num_sites; ++i)
+        if (!isfinite(sites_xyz[i]))
+            return fail(DERF_ERR_INVALID_ARG, "non-finite site coordinate");
+    HeadArch ha{arch->pos_freqs, arch->dir_freqs, arch->depth, arch->width, arch->skip_layer,
+                arch->rgb_hidden};
+    const bool bf16 = precision == DERF_PREC_BF16;
+    const MlpVariant *v = find_mlp_variant(ha, bf16);
+    if (!v)
+        return fail(DERF_ERR_UNSUPPORTED, "no %s kernel for arch (%d,%d,%d,%d,%d,%d)",
+                    bf16 ? "bf16" : "fp32", arch->pos_freqs, arch->dir_freqs, arch->depth,
+                    arch->width, arch->skip_layer, arch->rgb_hidden);
+
+    derf_handle *h = new (std::nothrow) derf_handle();
+    if (!h)
+        return fail(DERF_ERR_OOM, "handle");
+    auto cleanup = [&](int status) {
+        derf_destroy(h);
+        return status;
+    };
+    hipError_t e = hipGetDevice(&h->device);
+    if (e != hipSuccess)
+        return cleanup(hip_fail(e, "hipGetDevice"));
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device);
+    if (e != hipSuccess)
+        return cleanup(hip_fail(e, "hipDeviceGetAttribute"));
+    h->num_sites = num_sites;
+    h->site_bits = 0;
+    while ((1 << h->site_bits) < num_sites)
+        ++h->site_bits;
+    h->bf16 = bf16;
+    h->arch = *arch;
+    h->mlp = v;
+    h->mlp_grid = cus;
+
+    // sites as float4 (xyz, 0)
+    std::vector<float4> sites(num_sites);
+    for (int k = 0; k < num_sites; ++k)
+        sites[k] = make_float4(sites_xyz[3 * k], sites_xyz[3 * k + 1], sites_xyz[3 * k + 2], 0.f);
+    // per-head kernel layout
+    const long long wc = weights_count(arch);
+    std::vector<unsigned char> streams;
+    std::vector<float> blocks;
+    try {
+        streams.resize(v->stream_bytes * num_sites);
+        blocks.resize(v->block_bytes / 4 * num_sites);
+    } catch (...) {
+        return cleanup(fail(DERF_ERR_OOM, "host staging"));
+    }
+    for (int k = 0; k < num_sites; ++k) {
+        const float *wk = weights + (size_t)k * wc;
+        for (long long i = 0; i < wc; ++i)
+            if (!isfinite(wk[i]))
+                return cleanup(fail(DERF_ERR_INVALID_ARG, "non-finite weight (head %d)", k));
+        v->pack(wk, streams.data() + v->stream_bytes * k, blocks.data() + v->block_bytes / 4 * k);
+    }
+    if (hipMalloc(&h->sites, sizeof(float4) * num_sites) != hipSuccess ||
+        hipMalloc(&h->streams, streams.size()) != hipSuccess ||
+        hipMalloc(&h->blocks, blocks.size() * 4) != hipSuccess) {
+        (void)hipGetLastError();
+        return cleanup(fail(DERF_ERR_OOM, "device weights"));
+    }
+    e = hipMemcpy(h->sites, sites.data(), sizeof(float4) * num_sites, hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+        e = hipMemcpy(h->streams, streams.data(), streams.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+        e = hipMemcpy(h->blocks, blocks.data(), blocks.size() * 4, hipMemcpyHostToDevice);
+    if (e != hipSuccess)
+        return cleanup(hip_fail(e, "hipMemcpy"));
+    for (int i = 0; i < 2 * DERF_NUM_STAGES; ++i) {
+        e = hipEventCreate(&h->ev[i]);
+        if (e != hipSuccess)
+            return cleanup(hip_fail(e, "hipEventCreate"));
+    }
+    e = hipDeviceSynchronize();
+    if (e != hipSuccess)
+        return cleanup(hip_fail(e, "hipDeviceSynchronize"));
+    *out = h;
+    return DERF_OK;
+}
+
+int derf_render(derf_handle *h, const float *rays_o, const float *rays_d, long long num_rays,
+                float near_t, float far_t, const derf_sampling *samp, float *out_rgb,
+                float *out_depth, float *out_opacity, void *hip_stream)
+{
+    return render_impl(h, rays_o, rays_d, num_rays, near_t, far_t, samp, out_rgb, out_depth,
+                       out_opacity, nullptr, hip_stream);
+}
+
+int derf_render_debug(derf_handle *h, const float *rays_o, const float *rays_d,
+                      long long num_rays, float near_t, float far_t, const derf_sampling *samp,
+                      float *out_rgb, float *out_depth, float *out_opacity,
+                      const derf_debug_out *dbg, void *hip_stream)
+{
+    return render_impl(h, rays_o, rays_d, num_rays, near_t, far_t, samp, out_rgb, out_depth,
+                       out_opacity, dbg, hip_stream);
+}
+
+int derf_set_timing(derf_handle *h, int on)
+{
+    if (!h)
+        return fail(DERF_ERR_INVALID_ARG, "null handle");
+    h->timing = on != 0;
+    return DERF_OK;
+}
+
+int derf_get_stats(derf_handle *h, derf_stats *out)
+{
+    if (!h || !out)
+        return fail(DERF_ERR_INVALID_ARG, "null handle or output");
+    if (h->last_stream || h->totals) {
+        HIP_TRY(hipSetDevice(h->device), "hipSetDevice");
+        HIP_TRY(hipStreamSynchronize(h->last_stream), "hipStreamSynchronize");
+    }
+    accumulate_timing(h);
+    memset(h->stats.head_samples, 0, sizeof(h->stats.head_samples));
+    if (h->totals) {
+        std::vector<unsigned> tot(h->num_sites);
+        HIP_TRY(hipMemcpy(tot.data(), h->totals, sizeof(unsigned) * h->num_sites,
+                          hipMemcpyDeviceToHost),
+                "hipMemcpy");
+        for (int k = 0; k < h->num_sites; ++k)
+            h->stats.head_samples[k] = tot[k];
+    }
+    *out = h->stats;
+    return DERF_OK;
+}
+
+int derf_reset_stats(derf_handle *h)
+{
+    if (!h)
+        return fail(DERF_ERR_INVALID_ARG, "null handle");
+    if (h->ev_pending) {
+        HIP_TRY(hipEventSynchronize(h->ev[2 * DERF_NUM_STAGES - 1]), "hipEventSynchronize");
+        h->ev_pending = false;
+    }
+    memset(&h->stats, 0, sizeof(h->stats));
+    return DERF_OK;
+}
+
+void derf_destroy(derf_handle *h)
+{
+    if (!h)
+        return;
+    (void)hipSetDevice(h->device);
+    if (h->last_stream || h->ws.mem)
+        (void)hipStreamSynchronize(h->last_stream);
+    if (h->ws.mem)
+        (void)hipFree(h->ws.mem);
+    if (h->sites)
+        (void)hipFree(h->sites);
+    if (h->streams)
+        (void)hipFree(h->streams);
+    if (h->blocks)
+        (void)hipFree(h->blocks);
+    for (int i = 0; i < 2 * DERF_NUM_STAGES; ++i)
+        if (h->ev[i])
+            (void)hipEventDestroy(h->ev[i]);
+    delete h;
+}
+
+const char *derf_status_string(int status)
+{
+    switch (status) {
+    case DERF_OK: return "ok";
+    case DERF_ERR_INVALID_ARG: return "invalid argument";
+    case DERF_ERR_UNSUPPORTED: return "unsupported";
+    case DERF_ERR_OOM: return "out of memory";
+    case DERF_ERR_HIP: return "HIP error";
+    default: return "unknown status";
+    }
+}
+
+const char *derf_last_error(void) { return g_last_error; }
+
+}  // extern "C"

@@ -1,0 +1,69 @@
+// Internal interfaces between the host API (derf_api.cpp) and the HIP kernel
+// sources.  Nothing here is part of the public C ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace derf {
+
+// Samples covered by one bucketing block: the counting pass and the scatter
+// pass must agree on this partition of the sample range.
+constexpr int kBucketBlock = 4096;
+// Padded length of the per-ray direction feature vector gamma(d / |d|).
+constexpr int kDirPad = 32;
+constexpr int kMaxSites = 256;
+
+struct RenderGeometry {
+    const float *rays_o;
+    const float *rays_d;
+    unsigned num_rays;
+    unsigned n;          // samples per ray
+    unsigned num_samples;
+    double inv_n;        // 1.0 / n, for the sample -> (ray, index) split
+    float near_t, far_t, step;
+    uint64_t seed;
+    uint64_t ray_offset;
+    int perturb;
+};
+
+// ---- sampling, assignment and bucketing (kernels_sample.hip) -------------
+hipError_t launch_ray_encode(const RenderGeometry &g, void *dirbuf, bool bf16, hipStream_t s);
+hipError_t launch_sample_assign(const RenderGeometry &g, const float4 *sites, int num_sites,
+                                int site_bits, float *t, uint8_t *cell, unsigned *counts,
+                                unsigned num_blocks, hipStream_t s);
+hipError_t launch_bucket_scan(unsigned *counts, unsigned num_blocks, int num_sites,
+                              unsigned *totals, hipStream_t s);
+hipError_t launch_bucket_scatter(const uint8_t *cell, const unsigned *counts,
+                                 const unsigned *totals, unsigned num_samples,
+                                 unsigned num_blocks, int num_sites, int site_bits,
+                                 unsigned *bucket, hipStream_t s);
+hipError_t launch_composite(const RenderGeometry &g, const float *t, const uint8_t *cell,
+                            const float4 *sr, float *rgb, float *depth, float *opacity,
+                            hipStream_t s);
+hipError_t launch_debug_expand(unsigned num_samples, const float *t, const uint8_t *cell,
+                               const float4 *sr, int *dcell, float *dt, float *dsigma,
+                               float *drgb, hipStream_t s);
+
+// ---- grouped per-head MLP (kernels_mlp.hip) ------------------------------
+struct HeadArch {
+    int pos_freqs, dir_freqs, depth, width, skip_layer, rgb_hidden;
+};
+
+struct MlpVariant {
+    // bytes of one head's fragment stream and of its resident block
+    size_t stream_bytes;
+    size_t block_bytes;
+    int tile;            // samples per tile
+    // Lay out one head's fp32 weights (packed order of derf.h) for the kernel.
+    void (*pack)(const float *w, unsigned char *stream, float *block);
+    hipError_t (*launch)(const unsigned *bucket, const unsigned *totals, int num_sites,
+                         const RenderGeometry &g, const float *t, const void *dirbuf,
+                         const unsigned char *streams, const float *blocks, float4 *sr,
+                         int grid, hipStream_t s);
+};
+
+// Returns nullptr when no kernel is compiled for this architecture/precision.
+const MlpVariant *find_mlp_variant(const HeadArch &a, bool bf16);
+
+}  // namespace derf

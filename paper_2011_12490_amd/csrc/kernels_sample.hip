@@ -1,0 +1,486 @@
+// Ray sampling, nearest-site assignment, per-head bucketing and segment
+// compositing for gfx950.
+//
+// The sample depths and positions decide which Voronoi cell owns a sample,
+// so they are computed with explicit fused multiply-adds and no other
+// contraction (the pragma below), giving the same float32 values on every
+// run and in every reference.
+#pragma clang fp contract(off)
+
+#include "derf_internal.h"
+
+namespace derf {
+namespace {
+
+constexpr int kThreads = 256;
+
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC 2011): ten rounds of two
+// 32x32->64-bit products, Weyl-sequence key schedule between rounds.
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint2 k)
+{
+#pragma unroll
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) {
+            k.x += 0x9E3779B9u;
+            k.y += 0xBB67AE85u;
+        }
+        const unsigned lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
+        const unsigned lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
+        c = make_uint4(hi1 ^ c.y ^ k.x, lo1, hi0 ^ c.w ^ k.y, lo0);
+    }
+    return c;
+}
+
+__device__ __forceinline__ unsigned word(uint4 v, unsigned i)
+{
+    return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
+}
+
+// sample index s -> (ray, index within the ray); s < 2^32, n <= 1024.  The
+// float64 quotient is at most one below the true one (at exact multiples).
+__device__ __forceinline__ void split_sample(unsigned s, unsigned n, double inv_n, unsigned &r,
+                                             unsigned &i)
+{
+    r = (unsigned)((double)s * inv_n);
+    i = s - r * n;
+    if (i >= n) {
+        ++r;
+        i -= n;
+    }
+}
+
+// sin(pi y) and cos(pi y) for y = 2^l p: v_sin/v_cos take revolutions, so the
+// argument is 2^(l-1) p, reduced exactly to [0, 1) first.
+__device__ __forceinline__ void sincos_pi_pow2(float p, int l, float &s, float &c)
+{
+    const float u = __builtin_amdgcn_fractf(ldexpf(p, l - 1));
+    s = __builtin_amdgcn_sinf(u);
+    c = __builtin_amdgcn_cosf(u);
+}
+
+// ---------------------------------------------------------------------------
+// Per-ray direction features: f = [gamma_4(d / |d|) (27 values), 0 x 5],
+// stored as bf16 (round to nearest even) or float.
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void ray_encode_kernel(const float *__restrict__ rays_d,
+                                                              unsigned num_rays, void *dirbuf)
+{
+    const unsigned r = blockIdx.x * kThreads + threadIdx.x;
+    if (r >= num_rays)
+        return;
+    const float dx = rays_d[3 * r], dy = rays_d[3 * r + 1], dz = rays_d[3 * r + 2];
+    const float inv = 1.0f / sqrtf(dx * dx + dy * dy + dz * dz);
+    const float p[3] = {dx * inv, dy * inv, dz * inv};
+    float f[kDirPad];
+#pragma unroll
+    for (int j = 0; j < kDirPad; ++j)
+        f[j] = 0.0f;
+    f[0] = p[0];
+    f[1] = p[1];
+    f[2] = p[2];
+#pragma unroll
+    for (int l = 0; l < 4; ++l) {
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+            float s, co;
+            sincos_pi_pow2(p[c], l, s, co);
+            f[3 + 6 * l + c] = s;
+            f[3 + 6 * l + 3 + c] = co;
+        }
+    }
+    if constexpr (BF16) {
+        typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+        bf16x8 *out = reinterpret_cast<bf16x8 *>(dirbuf) + (size_t)r * (kDirPad / 8);
+#pragma unroll
+        for (int q = 0; q < kDirPad / 8; ++q) {
+            bf16x8 v;
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                v[j] = (__bf16)f[8 * q + j];
+            out[q] = v;
+        }
+    } else {
+        float4 *out = reinterpret_cast<float4 *>(dirbuf) + (size_t)r * (kDirPad / 4);
+#pragma unroll
+        for (int q = 0; q < kDirPad / 4; ++q)
+            out[q] = make_float4(f[4 * q], f[4 * q + 1], f[4 * q + 2], f[4 * q + 3]);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Lanes of this wave whose value equals mine, among the lanes in `valid`:
+// one ballot per bit of the value.
+__device__ __forceinline__ uint64_t match_peers(unsigned v, int bits, uint64_t valid)
+{
+    uint64_t peers = valid;
+    for (int b = 0; b < bits; ++b) {
+        const bool bit = (v >> b) & 1u;
+        const uint64_t m = __ballot(bit);
+        peers &= bit ? m : ~m;
+    }
+    return peers;
+}
+
+// Stratified depths t, owning cell (nearest site, ties to the lowest index)
+// and per-block head histograms.  Block b covers samples
+// [b * kBucketBlock, (b + 1) * kBucketBlock); each thread takes 4 consecutive
+// samples per round, so one Philox block serves 4 samples of a ray.
+__global__ __launch_bounds__(kThreads) void sample_assign_kernel(
+    RenderGeometry g, const float4 *__restrict__ sites, int num_sites, int site_bits,
+    float *__restrict__ t_out, uint8_t *__restrict__ cell_out, unsigned *__restrict__ counts,
+    unsigned num_blocks)
+{
+    __shared__ float4 s_sites[kMaxSites];
+    __shared__ unsigned s_hist[kMaxSites];
+    for (int k = threadIdx.x; k < num_sites; k += kThreads) {
+        s_sites[k] = sites[k];
+        s_hist[k] = 0;
+    }
+    __syncthreads();
+
+    const uint2 key = make_uint2((unsigned)g.seed, (unsigned)(g.seed >> 32));
+    const unsigned block_base = blockIdx.x * (unsigned)kBucketBlock;
+    const uint64_t lane_bit = 1ull << (threadIdx.x & 63);
+    for (int round = 0; round < kBucketBlock / (4 * kThreads); ++round) {
+        const unsigned s0 = block_base + round * (4 * kThreads) + 4 * threadIdx.x;
+        unsigned r, i;
+        split_sample(s0 < g.num_samples ? s0 : 0, g.n, g.inv_n, r, i);
+        float tv[4];
+        unsigned cv[4];
+        uint4 blk = make_uint4(0, 0, 0, 0);
+        float ox = 0, oy = 0, oz = 0, dx = 0, dy = 0, dz = 0;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const unsigned s = s0 + v;
+            cv[v] = 0xFFFFFFFFu;
+            tv[v] = 0.0f;
+            if (s < g.num_samples) {
+                if (v == 0 || i == 0) {
+                    ox = g.rays_o[3 * r];
+                    oy = g.rays_o[3 * r + 1];
+                    oz = g.rays_o[3 * r + 2];
+                    dx = g.rays_d[3 * r];
+                    dy = g.rays_d[3 * r + 1];
+                    dz = g.rays_d[3 * r + 2];
+                }
+                if (v == 0 || (i & 3u) == 0) {
+                    const uint64_t rg = g.ray_offset + r;
+                    blk = philox4x32_10(make_uint4(i >> 2, (unsigned)rg, (unsigned)(rg >> 32), 0u), key);
+                }
+                const float xi =
+                    g.perturb ? (float)(word(blk, i & 3u) >> 8) * 0x1.0p-24f : 0.5f;
+                const float t = fmaf(g.step, (float)i + xi, g.near_t);
+                const float x = fmaf(t, dx, ox), y = fmaf(t, dy, oy), z = fmaf(t, dz, oz);
+                float best = INFINITY;
+                unsigned bk = 0;
+                for (int k = 0; k < num_sites; ++k) {
+                    const float4 p = s_sites[k];
+                    const float ex = x - p.x, ey = y - p.y, ez = z - p.z;
+                    const float d2 = fmaf(ez, ez, fmaf(ey, ey, ex * ex));
+                    if (d2 < best) {
+                        best = d2;
+                        bk = k;
+                    }
+                }
+                tv[v] = t;
+                cv[v] = bk;
+            }
+            // next sample of the same thread
+            if (++i == g.n) {
+                i = 0;
+                ++r;
+            }
+        }
+        if (s0 + 3 < g.num_samples) {
+            *reinterpret_cast<float4 *>(t_out + s0) = make_float4(tv[0], tv[1], tv[2], tv[3]);
+            *reinterpret_cast<unsigned *>(cell_out + s0) =
+                cv[0] | (cv[1] << 8) | (cv[2] << 16) | (cv[3] << 24);
+        } else {
+            for (int v = 0; v < 4; ++v)
+                if (s0 + v < g.num_samples) {
+                    t_out[s0 + v] = tv[v];
+                    cell_out[s0 + v] = (uint8_t)cv[v];
+                }
+        }
+        // histogram: the lowest lane of each group of equal cells adds the group size
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const bool ok = s0 + v < g.num_samples;
+            const uint64_t valid = __ballot(ok);
+            const uint64_t peers = match_peers(cv[v], site_bits, valid);
+            if (ok && (peers & (lane_bit - 1)) == 0)
+                atomicAdd(&s_hist[cv[v]], (unsigned)__popcll(peers));
+        }
+    }
+    __syncthreads();
+    for (int k = threadIdx.x; k < num_sites; k += kThreads)
+        counts[(size_t)k * num_blocks + blockIdx.x] = s_hist[k];
+}
+
+// ---------------------------------------------------------------------------
+// Exclusive prefix over blocks of each head's counts (one block per head),
+// in place; the head's total goes to totals[head].
+__global__ __launch_bounds__(1024) void bucket_scan_kernel(unsigned *__restrict__ counts,
+                                                           unsigned num_blocks,
+                                                           unsigned *__restrict__ totals)
+{
+    __shared__ unsigned s_wave[16];
+    __shared__ unsigned s_carry;
+    unsigned *col = counts + (size_t)blockIdx.x * num_blocks;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    if (threadIdx.x == 0)
+        s_carry = 0;
+    __syncthreads();
+    for (unsigned base = 0; base < num_blocks; base += 1024) {
+        const unsigned idx = base + threadIdx.x;
+        const unsigned v = idx < num_blocks ? col[idx] : 0u;
+        // inclusive scan within the wave
+        unsigned x = v;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const unsigned y = __shfl_up(x, off);
+            if (lane >= off)
+                x += y;
+        }
+        if (lane == 63)
+            s_wave[w] = x;
+        __syncthreads();
+        if (w == 0) {
+            unsigned ws = lane < 16 ? s_wave[lane] : 0u;
+#pragma unroll
+            for (int off = 1; off < 16; off <<= 1) {
+                const unsigned y = __shfl_up(ws, off);
+                if (lane >= off)
+                    ws += y;
+            }
+            if (lane < 16)
+                s_wave[lane] = ws;  // inclusive over waves
+        }
+        __syncthreads();
+        const unsigned carry = s_carry;
+        const unsigned before = (w > 0 ? s_wave[w - 1] : 0u) + x - v;
+        if (idx < num_blocks)
+            col[idx] = carry + before;
+        __syncthreads();
+        if (threadIdx.x == 0)
+            s_carry = carry + s_wave[15];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0)
+        totals[blockIdx.x] = s_carry;
+}
+
+// Stable scatter of sample ids into per-head buckets.  Bucket k occupies
+// [offset_k, offset_k + total_k) with offset_k = sum of totals below k;
+// within it samples keep increasing sample-id order, so each ray's run
+// through cell k stays contiguous.  Each round covers 256 consecutive
+// samples (4 waves x 64 lanes); ranks come from per-wave equal-cell ballots
+// plus per-head counters of the earlier waves and rounds.
+__global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
+    const uint8_t *__restrict__ cell, const unsigned *__restrict__ prefix,
+    const unsigned *__restrict__ totals, unsigned num_samples, unsigned num_blocks,
+    int num_sites, int site_bits, unsigned *__restrict__ bucket)
+{
+    __shared__ unsigned s_base[kMaxSites];
+    __shared__ unsigned s_wave[4][kMaxSites];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    if (threadIdx.x == 0) {
+        unsigned acc = 0;
+        for (int k = 0; k < num_sites; ++k) {
+            s_base[k] = acc + prefix[(size_t)k * num_blocks + blockIdx.x];
+            acc += totals[k];
+        }
+    }
+    for (int k = threadIdx.x; k < num_sites; k += kThreads)
+        s_wave[0][k] = s_wave[1][k] = s_wave[2][k] = s_wave[3][k] = 0;
+    __syncthreads();
+    const uint64_t lane_bit = 1ull << lane;
+    const unsigned block_base = blockIdx.x * (unsigned)kBucketBlock;
+    for (int round = 0; round < kBucketBlock / kThreads; ++round) {
+        const unsigned s = block_base + round * kThreads + threadIdx.x;
+        const bool ok = s < num_samples;
+        const unsigned c = ok ? cell[s] : 0u;
+        const uint64_t valid = __ballot(ok);
+        const uint64_t peers = match_peers(c, site_bits, valid);
+        const unsigned rank = (unsigned)__popcll(peers & (lane_bit - 1));
+        if (ok && rank == 0)
+            s_wave[w][c] = (unsigned)__popcll(peers);
+        __syncthreads();
+        if (ok) {
+            unsigned pos = s_base[c] + rank;
+            for (int v = 0; v < w; ++v)
+                pos += s_wave[v][c];
+            if (pos < num_samples)  // always true when the counts are consistent
+                bucket[pos] = s;
+        }
+        __syncthreads();
+        for (int k = threadIdx.x; k < num_sites; k += kThreads) {
+            s_base[k] += s_wave[0][k] + s_wave[1][k] + s_wave[2][k] + s_wave[3][k];
+            s_wave[0][k] = s_wave[1][k] = s_wave[2][k] = s_wave[3][k] = 0;
+        }
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Segment integration and Painter's merge, one wave per ray.  Lane j takes
+// the contiguous samples [j c, j c + c) with c = ceil(n / 64).  Within a
+// lane, each maximal run of one cell is integrated with its own local
+// transmittance, and the runs are merged front to back; the 64 lane results
+// are then merged in lane order.  Merging is the associative "over":
+// (C, D, T) then (C', D', T') gives (C + T C', D + T D', T T').
+struct Over {
+    float r, g, b, d, t;
+};
+
+__device__ __forceinline__ Over over(const Over &a, const Over &b)
+{
+    return Over{fmaf(a.t, b.r, a.r), fmaf(a.t, b.g, a.g), fmaf(a.t, b.b, a.b),
+                fmaf(a.t, b.d, a.d), a.t * b.t};
+}
+
+__global__ __launch_bounds__(kThreads) void composite_kernel(
+    const float *__restrict__ t, const uint8_t *__restrict__ cell, const float4 *__restrict__ sr,
+    unsigned n, unsigned num_rays, float near_t, float far_t, float *__restrict__ out_rgb,
+    float *__restrict__ out_depth, float *__restrict__ out_opacity)
+{
+    const unsigned ray = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (ray >= num_rays)
+        return;
+    const unsigned c = (n + 63) / 64;
+    const unsigned i0 = lane * c;
+    const unsigned i1 = min(i0 + c, n);
+    const size_t base = (size_t)ray * n;
+    Over acc{0.f, 0.f, 0.f, 0.f, 1.f};   // merged runs of this lane
+    Over seg{0.f, 0.f, 0.f, 0.f, 1.f};   // current run, local transmittance
+    unsigned cur = 0xFFFFFFFFu;
+    float t_prev = (i0 > 0 && i0 < n) ? t[base + i0 - 1] : 0.0f;
+    float t_cur = i0 < n ? t[base + i0] : 0.0f;
+    for (unsigned i = i0; i < i1; ++i) {
+        const float t_next = (i + 1 < n) ? t[base + i + 1] : 0.0f;
+        const float lo = (i == 0) ? near_t : 0.5f * (t_prev + t_cur);
+        const float hi = (i + 1 == n) ? far_t : 0.5f * (t_cur + t_next);
+        const unsigned ci = cell[base + i];
+        const float4 v = sr[base + i];
+        const float tau = __expf(-v.x * (hi - lo));
+        const float alpha = 1.0f - tau;
+        if (ci != cur) {
+            acc = over(acc, seg);
+            seg = Over{0.f, 0.f, 0.f, 0.f, 1.f};
+            cur = ci;
+        }
+        const float w = seg.t * alpha;
+        seg.r = fmaf(w, v.y, seg.r);
+        seg.g = fmaf(w, v.z, seg.g);
+        seg.b = fmaf(w, v.w, seg.b);
+        seg.d = fmaf(w, t_cur, seg.d);
+        seg.t *= tau;
+        t_prev = t_cur;
+        t_cur = t_next;
+    }
+    acc = over(acc, seg);
+    // ordered tree merge across the wave: lane j absorbs lane j + off
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        Over o;
+        o.r = __shfl_down(acc.r, off);
+        o.g = __shfl_down(acc.g, off);
+        o.b = __shfl_down(acc.b, off);
+        o.d = __shfl_down(acc.d, off);
+        o.t = __shfl_down(acc.t, off);
+        if ((lane & (2 * off - 1)) == 0)
+            acc = over(acc, o);
+    }
+    if (lane == 0) {
+        out_rgb[3 * ray] = acc.r;
+        out_rgb[3 * ray + 1] = acc.g;
+        out_rgb[3 * ray + 2] = acc.b;
+        out_depth[ray] = acc.d;
+        out_opacity[ray] = 1.0f - acc.t;
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void debug_expand_kernel(
+    unsigned num_samples, const float *__restrict__ t, const uint8_t *__restrict__ cell,
+    const float4 *__restrict__ sr, int *dcell, float *dt, float *dsigma, float *drgb)
+{
+    const unsigned s = blockIdx.x * kThreads + threadIdx.x;
+    if (s >= num_samples)
+        return;
+    if (dcell)
+        dcell[s] = cell[s];
+    if (dt)
+        dt[s] = t[s];
+    if (dsigma || drgb) {
+        const float4 v = sr[s];
+        if (dsigma)
+            dsigma[s] = v.x;
+        if (drgb) {
+            drgb[3 * (size_t)s] = v.y;
+            drgb[3 * (size_t)s + 1] = v.z;
+            drgb[3 * (size_t)s + 2] = v.w;
+        }
+    }
+}
+
+inline unsigned blocks_for(unsigned items, unsigned per) { return (items + per - 1) / per; }
+
+}  // namespace
+
+hipError_t launch_ray_encode(const RenderGeometry &g, void *dirbuf, bool bf16, hipStream_t s)
+{
+    const unsigned grid = blocks_for(g.num_rays, kThreads);
+    if (bf16)
+        ray_encode_kernel<true><<<grid, kThreads, 0, s>>>(g.rays_d, g.num_rays, dirbuf);
+    else
+        ray_encode_kernel<false><<<grid, kThreads, 0, s>>>(g.rays_d, g.num_rays, dirbuf);
+    return hipGetLastError();
+}
+
+hipError_t launch_sample_assign(const RenderGeometry &g, const float4 *sites, int num_sites,
+                                int site_bits, float *t, uint8_t *cell, unsigned *counts,
+                                unsigned num_blocks, hipStream_t s)
+{
+    sample_assign_kernel<<<num_blocks, kThreads, 0, s>>>(g, sites, num_sites, site_bits, t, cell,
+                                                         counts, num_blocks);
+    return hipGetLastError();
+}
+
+hipError_t launch_bucket_scan(unsigned *counts, unsigned num_blocks, int num_sites,
+                              unsigned *totals, hipStream_t s)
+{
+    bucket_scan_kernel<<<num_sites, 1024, 0, s>>>(counts, num_blocks, totals);
+    return hipGetLastError();
+}
+
+hipError_t launch_bucket_scatter(const uint8_t *cell, const unsigned *counts,
+                                 const unsigned *totals, unsigned num_samples,
+                                 unsigned num_blocks, int num_sites, int site_bits,
+                                 unsigned *bucket, hipStream_t s)
+{
+    bucket_scatter_kernel<<<num_blocks, kThreads, 0, s>>>(cell, counts, totals, num_samples,
+                                                          num_blocks, num_sites, site_bits, bucket);
+    return hipGetLastError();
+}
+
+hipError_t launch_composite(const RenderGeometry &g, const float *t, const uint8_t *cell,
+                            const float4 *sr, float *rgb, float *depth, float *opacity,
+                            hipStream_t s)
+{
+    const unsigned grid = blocks_for(g.num_rays, kThreads / 64);
+    composite_kernel<<<grid, kThreads, 0, s>>>(t, cell, sr, g.n, g.num_rays, g.near_t, g.far_t,
+                                               rgb, depth, opacity);
+    return hipGetLastError();
+}
+
+hipError_t launch_debug_expand(unsigned num_samples, const float *t, const uint8_t *cell,
+                               const float4 *sr, int *dcell, float *dt, float *dsigma,
+                               float *drgb, hipStream_t s)
+{
+    debug_expand_kernel<<<blocks_for(num_samples, kThreads), kThreads, 0, s>>>(
+        num_samples, t, cell, sr, dcell, dt, dsigma, drgb);
+    return hipGetLastError();
+}
+
+}  // namespace derf

@@ -1,0 +1,222 @@
+"""ctypes binding of libderf.so (include/derf.h).
+
+Argument marshalling only: every step of a render runs in the HIP library.
+torch supplies device memory and streams; it is imported before the library
+is loaded so that both share one HIP runtime.  If libderf.so has not been
+built this module raises -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch  # noqa: F401  (loads the HIP runtime the library binds to)
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libderf.so")
+
+DERF_OK = 0
+DERF_ERR_INVALID_ARG = -1
+DERF_ERR_UNSUPPORTED = -2
+DERF_ERR_OOM = -3
+DERF_ERR_HIP = -4
+DERF_PREC_FP32 = 0
+DERF_PREC_BF16 = 1
+DERF_NUM_STAGES = 5
+STAGE_NAMES = ("sample_assign", "bucket_scan", "bucket_scatter", "mlp", "composite")
+
+
+class derf_head_arch(ctypes.Structure):
+    _fields_ = [("pos_freqs", ctypes.c_int), ("dir_freqs", ctypes.c_int),
+                ("depth", ctypes.c_int), ("width", ctypes.c_int),
+                ("skip_layer", ctypes.c_int), ("rgb_hidden", ctypes.c_int)]
+
+
+class derf_sampling(ctypes.Structure):
+    _fields_ = [("n_coarse", ctypes.c_int), ("n_fine", ctypes.c_int),
+                ("seed", ctypes.c_ulonglong), ("perturb", ctypes.c_int),
+                ("ray_offset", ctypes.c_ulonglong)]
+
+
+class derf_debug_out(ctypes.Structure):
+    _fields_ = [("cell", ctypes.c_void_p), ("t", ctypes.c_void_p),
+                ("sigma", ctypes.c_void_p), ("rgb", ctypes.c_void_p)]
+
+
+class derf_stats(ctypes.Structure):
+    _fields_ = [("renders", ctypes.c_longlong), ("samples", ctypes.c_longlong),
+                ("stage_ms", ctypes.c_double * DERF_NUM_STAGES),
+                ("stage_launches", ctypes.c_longlong * DERF_NUM_STAGES),
+                ("head_samples", ctypes.c_longlong * 256)]
+
+
+EXPORTS = ("derf_weights_count", "derf_create", "derf_render", "derf_render_debug",
+           "derf_set_timing", "derf_get_stats", "derf_reset_stats", "derf_destroy",
+           "derf_status_string", "derf_last_error")
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+class DerfError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__("%s failed: %s (%d): %s" % (what, lib().derf_status_string(status).decode(),
+                                                    status, lib().derf_last_error().decode()))
+
+
+def lib() -> ctypes.CDLL:
+    """Load libderf.so (raises if it is not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libderf.so is not built (%s); run __graft_entry__.build()" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.c_void_p
+        L.derf_weights_count.argtypes = [ctypes.POINTER(derf_head_arch)]
+        L.derf_weights_count.restype = ctypes.c_longlong
+        L.derf_create.argtypes = [ctypes.POINTER(P), ctypes.c_int, P,
+                                  ctypes.POINTER(derf_head_arch), P, ctypes.c_int]
+        L.derf_create.restype = ctypes.c_int
+        render_args = [P, P, P, ctypes.c_longlong, ctypes.c_float, ctypes.c_float,
+                       ctypes.POINTER(derf_sampling), P, P, P]
+        L.derf_render.argtypes = render_args + [P]
+        L.derf_render.restype = ctypes.c_int
+        L.derf_render_debug.argtypes = render_args + [ctypes.POINTER(derf_debug_out), P]
+        L.derf_render_debug.restype = ctypes.c_int
+        L.derf_set_timing.argtypes = [P, ctypes.c_int]
+        L.derf_set_timing.restype = ctypes.c_int
+        L.derf_get_stats.argtypes = [P, ctypes.POINTER(derf_stats)]
+        L.derf_get_stats.restype = ctypes.c_int
+        L.derf_reset_stats.argtypes = [P]
+        L.derf_reset_stats.restype = ctypes.c_int
+        L.derf_destroy.argtypes = [P]
+        L.derf_destroy.restype = None
+        L.derf_status_string.argtypes = [ctypes.c_int]
+        L.derf_status_string.restype = ctypes.c_char_p
+        L.derf_last_error.argtypes = []
+        L.derf_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(status: int, what: str):
+    if status != DERF_OK:
+        raise DerfError(status, what)
+
+
+def _arch(arch) -> derf_head_arch:
+    t = arch.as_tuple() if hasattr(arch, "as_tuple") else tuple(arch)
+    return derf_head_arch(*t)
+
+
+def _dptr(x: Optional[torch.Tensor]):
+    return None if x is None else ctypes.c_void_p(x.data_ptr())
+
+
+# ---- thin wrappers with the C names -------------------------------------------
+
+def derf_weights_count(arch) -> int:
+    a = _arch(arch)
+    return lib().derf_weights_count(ctypes.byref(a))
+
+
+def derf_create(sites, arch, weights, precision: int) -> ctypes.c_void_p:
+    """sites: host float32 [K, 3]; weights: host float32 [K, derf_weights_count]."""
+    import numpy as np
+    s = np.ascontiguousarray(sites, np.float32).reshape(-1, 3)
+    w = np.ascontiguousarray(weights, np.float32)
+    a = _arch(arch)
+    h = ctypes.c_void_p()
+    _check(lib().derf_create(ctypes.byref(h), s.shape[0], s.ctypes.data_as(ctypes.c_void_p),
+                             ctypes.byref(a), w.ctypes.data_as(ctypes.c_void_p), precision),
+           "derf_create")
+    return h
+
+
+def derf_render(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far: float,
+                samp: derf_sampling, out_rgb: torch.Tensor, out_depth: torch.Tensor,
+                out_opacity: torch.Tensor, stream=None, debug: Optional[derf_debug_out] = None):
+    """Enqueue a render on `stream` (default: torch's current stream)."""
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    R = rays_o.shape[0]
+    args = [h, _dptr(rays_o), _dptr(rays_d), R, near, far, ctypes.byref(samp), _dptr(out_rgb),
+            _dptr(out_depth), _dptr(out_opacity)]
+    if debug is None:
+        _check(lib().derf_render(*args, sp), "derf_render")
+    else:
+        _check(lib().derf_render_debug(*args, ctypes.byref(debug), sp), "derf_render_debug")
+
+
+def derf_set_timing(h, on: bool):
+    _check(lib().derf_set_timing(h, int(on)), "derf_set_timing")
+
+
+def derf_get_stats(h) -> derf_stats:
+    st = derf_stats()
+    _check(lib().derf_get_stats(h, ctypes.byref(st)), "derf_get_stats")
+    return st
+
+
+def derf_reset_stats(h):
+    _check(lib().derf_reset_stats(h), "derf_reset_stats")
+
+
+def derf_destroy(h):
+    lib().derf_destroy(h)
+
+
+# ---- convenience ----------------------------------------------------------------
+
+class Renderer:
+    """A renderer handle bound to the current device."""
+
+    def __init__(self, sites, arch, weights, precision: str = "bf16"):
+        self.arch = arch
+        self.precision = precision
+        prec = DERF_PREC_BF16 if precision == "bf16" else DERF_PREC_FP32
+        self.handle = derf_create(sites, arch, weights, prec)
+
+    def close(self):
+        if self.handle is not None and self.handle.value:
+            derf_destroy(self.handle)
+        self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def render(self, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far: float,
+               n_coarse: int, n_fine: int = 0, seed: int = 0, perturb: bool = True,
+               out=None, debug: bool = False, stream=None, ray_offset: int = 0):
+        """Render device rays; returns (rgb [R,3], depth [R], opacity [R]) and, with
+        debug=True, a dict of per-sample cell/t/sigma/rgb."""
+        assert rays_o.is_cuda and rays_o.dtype == torch.float32 and rays_o.is_contiguous()
+        assert rays_d.is_cuda and rays_d.dtype == torch.float32 and rays_d.is_contiguous()
+        R = rays_o.shape[0]
+        dev = rays_o.device
+        if out is None:
+            rgb = torch.empty((R, 3), dtype=torch.float32, device=dev)
+            depth = torch.empty((R,), dtype=torch.float32, device=dev)
+            opac = torch.empty((R,), dtype=torch.float32, device=dev)
+        else:
+            rgb, depth, opac = out
+        samp = derf_sampling(n_coarse, n_fine, seed, int(perturb), ray_offset)
+        dbg = None
+        extra = None
+        if debug:
+            N = n_coarse + n_fine
+            extra = {"cell": torch.empty((R, N), dtype=torch.int32, device=dev),
+                     "t": torch.empty((R, N), dtype=torch.float32, device=dev),
+                     "sigma": torch.empty((R, N), dtype=torch.float32, device=dev),
+                     "rgb": torch.empty((R, N, 3), dtype=torch.float32, device=dev)}
+            dbg = derf_debug_out(_dptr(extra["cell"]), _dptr(extra["t"]),
+                                 _dptr(extra["sigma"]), _dptr(extra["rgb"]))
+        derf_render(self.handle, rays_o, rays_d, near, far, samp, rgb, depth, opac, stream, dbg)
+        if debug:
+            return rgb, depth, opac, extra
+        return rgb, depth, opac

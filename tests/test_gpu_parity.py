@@ -1,0 +1,280 @@
+"""GPU parity: the HIP path, called through the C ABI, against the CPU oracle on
+the same seeded inputs.
+
+Bars: sample depths bit-exact; cells bit-exact except samples within 1e-5 of
+a bisector (counted and printed); pixels (rgb, depth, opacity) within max-abs
+1e-4 on the fp32 path and 2e-2 on the bf16 path.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2011_12490_amd import scenes
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TOL = {"fp32": 1e-4, "bf16": 2e-2}
+NTHREADS = min(16, os.cpu_count() or 1)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    oracle.build(force=False)
+    torch.cuda.set_device(0)
+
+
+def _derf():
+    from paper_2011_12490_amd import derf
+    return derf
+
+
+def _render(sc, precision, rays=None, debug=False, n=None, seed=scenes.SEED_RENDER,
+            perturb=True, ray_offset=0):
+    derf = _derf()
+    cfg = sc.cfg
+    o = torch.from_numpy(sc.rays_o if rays is None else rays[0]).cuda()
+    d = torch.from_numpy(sc.rays_d if rays is None else rays[1]).cuda()
+    r = derf.Renderer(sc.sites, cfg.arch, sc.weights, precision)
+    out = r.render(o, d, cfg.near, cfg.far, n or cfg.n_coarse, 0, seed, perturb, debug=debug,
+                   ray_offset=ray_offset)
+    torch.cuda.synchronize()
+    r.close()
+    return [x.cpu().numpy() if torch.is_tensor(x) else
+            {k: v.cpu().numpy() for k, v in x.items()} for x in out]
+
+
+def _oracle(sc, ids, n=None, per_sample=False, seed=scenes.SEED_RENDER, perturb=True):
+    cfg = sc.cfg
+    return oracle.render(sc.sites, cfg.arch, sc.weights, sc.rays_o[ids], sc.rays_d[ids],
+                         cfg.near, cfg.far, n or cfg.n_coarse, 0, seed=seed, perturb=perturb,
+                         ray_ids=ids, per_sample=per_sample, nthreads=NTHREADS)
+
+
+def _check_pixels(gpu, ref, ids, tol, label):
+    rgb, depth, opac = gpu[0][ids], gpu[1][ids], gpu[2][ids]
+    e_rgb = np.abs(rgb - ref.rgb).max()
+    e_dep = np.abs(depth - ref.depth).max()
+    e_op = np.abs(opac - ref.opacity).max()
+    print("%s: rays=%d max|d rgb|=%.3g max|d depth|=%.3g max|d opacity|=%.3g (tol %.0e)"
+          % (label, len(ids), e_rgb, e_dep, e_op, tol), flush=True)
+    assert e_rgb <= tol and e_dep <= tol and e_op <= tol
+
+
+def _check_cells(sc, t_gpu, cell_gpu, n, label, ray_offset=0, perturb=True):
+    cfg = sc.cfg
+    t_ref, cell_ref, _ = oracle.sample_assign(sc.sites, sc.rays_o, sc.rays_d, cfg.near, cfg.far,
+                                              n, scenes.SEED_RENDER, perturb=perturb,
+                                              ray_offset=ray_offset, nthreads=NTHREADS)
+    assert np.array_equal(t_gpu, t_ref), "sample depths differ"
+    diff = np.argwhere(cell_gpu != cell_ref)
+    near = 0
+    for r, i in diff:
+        x = np.float32(sc.rays_o[r]) + np.float32(t_ref[r, i]) * sc.rays_d[r]
+        m = oracle.bisector_margin(sc.sites, x.astype(np.float32), int(cell_ref[r, i]))
+        assert m < 1e-5, (r, i, cell_gpu[r, i], cell_ref[r, i], m)
+        near += 1
+    print("%s: samples=%d cell mismatches=%d (all within 1e-5 of a bisector)"
+          % (label, cell_gpu.size, near), flush=True)
+
+
+# ------------------------------------------------------------- tiny scene ----
+
+@pytest.mark.parametrize("precision", ["fp32", "bf16"])
+@pytest.mark.parametrize("sigma_bias", [0.0, 3.0])
+def test_tiny_full_frame(precision, sigma_bias):
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], sigma_bias=sigma_bias)
+    sc = scenes.make_scene(cfg)
+    gpu = _render(sc, precision, debug=True)
+    dbg = gpu[3]
+    ids = np.arange(cfg.num_rays)
+    ref = _oracle(sc, ids, per_sample=True)
+    _check_cells(sc, dbg["t"], dbg["cell"], cfg.n_coarse, "tiny %s" % precision)
+    ok = ref.cell == dbg["cell"]
+    e_sig = np.abs(dbg["sigma"] - ref.sigma)[ok].max()
+    e_rgb = np.abs(dbg["rgb"] - ref.srgb)[ok].max()
+    print("tiny %s per-sample max|d sigma|=%.3g max|d rgb|=%.3g" % (precision, e_sig, e_rgb))
+    if precision == "fp32":
+        assert e_sig <= 1e-4 * max(1.0, np.abs(ref.sigma).max()) and e_rgb <= 1e-4
+    _check_pixels(gpu, ref, ids, TOL[precision], "tiny %s bias %.0f" % (precision, sigma_bias))
+
+
+# ------------------------------------------------------- paper workloads ----
+
+def _subset_parity(name, precision, n_rays, sigma_bias=None, check_cells=True):
+    cfg = scenes.CONFIGS[name]
+    if sigma_bias is not None:
+        cfg = scenes.with_changes(cfg, sigma_bias=sigma_bias)
+    sc = scenes.make_scene(cfg)
+    gpu = _render(sc, precision, debug=check_cells)
+    if check_cells:
+        _check_cells(sc, gpu[3]["t"], gpu[3]["cell"], cfg.n_coarse, "%s %s" % (name, precision))
+    ids = scenes.ray_subset(n_rays, cfg.num_rays)
+    # also one full image row (contiguous rays)
+    row = cfg.height // 2
+    ids = np.unique(np.concatenate([ids, np.arange(row * cfg.width, (row + 1) * cfg.width)]))
+    ref = _oracle(sc, ids)
+    _check_pixels(gpu, ref, ids, TOL[precision], "%s %s" % (name, precision))
+    assert np.all(np.isfinite(gpu[0])) and np.all(np.isfinite(gpu[1]))
+
+
+@pytest.mark.parametrize("precision", ["bf16", "fp32"])
+def test_derf_k16_headline_frame(precision):
+    """504x378 forward-facing frame, 192 samples, 16 heads of 8x128."""
+    _subset_parity("derf_k16", precision, 1024)
+
+
+def test_derf_k16_dense_bf16():
+    """Same frame with a density bias so compositing is far from transparent."""
+    _subset_parity("derf_k16", "bf16", 512, sigma_bias=4.0, check_cells=False)
+
+
+def test_nerf_k1_bf16():
+    """Single 8x256 head (the NeRF-equivalent configuration)."""
+    _subset_parity("nerf_k1", "bf16", 256, check_cells=False)
+
+
+@pytest.mark.parametrize("precision", ["bf16", "fp32"])
+def test_skew_k64(precision):
+    """1024x1024, 256 samples, 64 skewed heads of 6x64, density bias +2."""
+    _subset_parity("skew_k64", precision, 1024, check_cells=False)
+
+
+def test_skew_k64_cells_slice():
+    """Cells of a contiguous slice of the skewed frame (ray_offset keeps the jitter)."""
+    cfg = scenes.CONFIGS["skew_k64"]
+    sc = scenes.make_scene(cfg)
+    a, b = 300_000, 300_000 + 65_536
+    sub = scenes.Scene(cfg, sc.sites, sc.weights, sc.rays_o[a:b], sc.rays_d[a:b])
+    gpu = _render(sub, "bf16", debug=True, ray_offset=a)
+    _check_cells(sub, gpu[3]["t"], gpu[3]["cell"], cfg.n_coarse, "skew_k64 slice",
+                 ray_offset=a)
+
+
+# ------------------------------------------------------------ edge cases ----
+
+@pytest.mark.parametrize("n", [1, 3, 7, 33, 200])
+def test_ragged_sample_counts(n):
+    cfg = scenes.CONFIGS["tiny"]
+    sc = scenes.make_scene(scenes.with_changes(cfg, sigma_bias=2.0))
+    R = 333
+    rays = (sc.rays_o[:R].copy(), sc.rays_d[:R].copy())
+    sub = scenes.Scene(sc.cfg, sc.sites, sc.weights, rays[0], rays[1])
+    gpu = _render(sub, "fp32", debug=True, n=n)
+    _check_cells(sub, gpu[3]["t"], gpu[3]["cell"], n, "tiny n=%d" % n)
+    ref = _oracle(sub, np.arange(R), n=n)
+    _check_pixels(gpu, ref, np.arange(R), TOL["fp32"], "tiny n=%d" % n)
+
+
+def test_single_ray_and_single_head():
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], num_sites=1, sigma_bias=1.0)
+    sc = scenes.make_scene(cfg)
+    sub = scenes.Scene(cfg, sc.sites, sc.weights, sc.rays_o[5:6].copy(), sc.rays_d[5:6].copy())
+    gpu = _render(sub, "fp32")
+    ref = _oracle(sub, np.array([0]))
+    _check_pixels(gpu, ref, np.array([0]), TOL["fp32"], "one ray, K=1")
+
+
+def test_many_sites_and_empty_heads():
+    """K = 256 (the maximum): most heads own no sample at all."""
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], num_sites=256, sigma_bias=2.0)
+    sc = scenes.make_scene(cfg)
+    gpu = _render(sc, "fp32", debug=True)
+    _check_cells(sc, gpu[3]["t"], gpu[3]["cell"], cfg.n_coarse, "tiny K=256")
+    ids = np.arange(0, cfg.num_rays, 3)
+    ref = _oracle(sc, ids)
+    _check_pixels(gpu, ref, ids, TOL["fp32"], "tiny K=256")
+
+
+def test_far_sites_leave_heads_empty():
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], sigma_bias=2.0)
+    sc = scenes.make_scene(cfg)
+    sites = sc.sites.copy()
+    sites[1] = [50.0, 50.0, 50.0]
+    sites[3] = [-40.0, 60.0, 10.0]
+    sc2 = scenes.Scene(cfg, sites, sc.weights, sc.rays_o, sc.rays_d)
+    gpu = _render(sc2, "bf16", debug=True)
+    assert not np.any(np.isin(gpu[3]["cell"], [1, 3]))
+    ref = _oracle(sc2, np.arange(cfg.num_rays))
+    _check_pixels(gpu, ref, np.arange(cfg.num_rays), TOL["bf16"], "tiny 2 empty heads")
+
+
+def test_unperturbed_midpoints():
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], sigma_bias=1.0)
+    sc = scenes.make_scene(cfg)
+    gpu = _render(sc, "fp32", debug=True, perturb=False)
+    _check_cells(sc, gpu[3]["t"], gpu[3]["cell"], cfg.n_coarse, "tiny midpoints",
+                 perturb=False)
+    ref = _oracle(sc, np.arange(cfg.num_rays), perturb=False)
+    _check_pixels(gpu, ref, np.arange(cfg.num_rays), TOL["fp32"], "tiny midpoints")
+
+
+def test_zero_rays_is_a_noop_and_fine_sampling_is_refused():
+    derf = _derf()
+    cfg = scenes.CONFIGS["tiny"]
+    sc = scenes.make_scene(cfg)
+    r = derf.Renderer(sc.sites, cfg.arch, sc.weights, "fp32")
+    o = torch.zeros((0, 3), device="cuda")
+    out = r.render(o, o, 2.0, 6.0, 32)
+    assert out[0].shape == (0, 3)
+    o1 = torch.from_numpy(sc.rays_o[:4]).cuda()
+    d1 = torch.from_numpy(sc.rays_d[:4]).cuda()
+    with pytest.raises(derf.DerfError) as e:
+        r.render(o1, d1, 2.0, 6.0, 16, 32)
+    assert e.value.status == derf.DERF_ERR_UNSUPPORTED
+    with pytest.raises(derf.DerfError) as e:
+        r.render(o1, d1, 6.0, 2.0, 16)
+    assert e.value.status == derf.DERF_ERR_INVALID_ARG
+    r.close()
+
+
+# ------------------------------------------------------------ invariants ----
+
+def test_determinism_and_batch_invariance():
+    derf = _derf()
+    cfg = scenes.CONFIGS["derf_k16"]
+    sc = scenes.make_scene(cfg)
+    o = torch.from_numpy(sc.rays_o).cuda()
+    d = torch.from_numpy(sc.rays_d).cuda()
+    r = derf.Renderer(sc.sites, cfg.arch, sc.weights, "bf16")
+    a = [x.clone() for x in r.render(o, d, cfg.near, cfg.far, 192, 0, 7)]
+    b = [x.clone() for x in r.render(o, d, cfg.near, cfg.far, 192, 0, 7)]
+    lo, hi = 12345, 12345 + 4000
+    c = r.render(o[lo:hi].contiguous(), d[lo:hi].contiguous(), cfg.near, cfg.far, 192, 0, 7,
+                 ray_offset=lo)
+    torch.cuda.synchronize()
+    for x, y, z in zip(a, b, c):
+        assert torch.equal(x, y)
+        assert torch.equal(x[lo:hi], z)
+    r.close()
+
+
+def test_cells_contiguous_and_ordered_on_gpu_output():
+    """Sec. 3.3 on the GPU's own cells over the full headline frame: each ray
+    meets each cell in one run, in increasing distance of the sites from the
+    ray origin (rays with a sample within 1e-5 of a bisector excepted)."""
+    cfg = scenes.CONFIGS["derf_k16"]
+    sc = scenes.make_scene(cfg)
+    gpu = _render(sc, "bf16", debug=True)
+    cell = gpu[3]["cell"]
+    t_ref, cell_ref, m = oracle.sample_assign(sc.sites, sc.rays_o, sc.rays_d, cfg.near, cfg.far,
+                                              cfg.n_coarse, scenes.SEED_RENDER, margin=True,
+                                              nthreads=NTHREADS)
+    assert np.array_equal(gpu[3]["t"], t_ref)
+    near = np.any(m < 1e-5, axis=1)
+    change = np.concatenate([np.ones((cell.shape[0], 1), bool), cell[:, 1:] != cell[:, :-1]], 1)
+    runs_per_ray = change.sum(1)
+    srt = np.sort(cell, axis=1)
+    distinct = 1 + (srt[:, 1:] != srt[:, :-1]).sum(1)
+    bad = (runs_per_ray != distinct) & ~near
+    print("rays=%d multi-cell rays=%d near-bisector rays=%d non-contiguous=%d"
+          % (cell.shape[0], int((distinct > 1).sum()), int(near.sum()), int(bad.sum())))
+    assert not np.any(bad)
+    for r in np.nonzero(~near & (distinct > 1))[0][::37]:
+        runs = cell[r][change[r]]
+        dist = np.linalg.norm(sc.sites[runs].astype(np.float64) - sc.rays_o[r], axis=1)
+        assert np.all(np.diff(dist) > 0), (r, runs, dist)

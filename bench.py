@@ -1,0 +1,189 @@
+#!/usr/bin/env python3
+"""Throughput of the DeRF render path on one MI355X.
+
+A step is one full render of a frame through the whole path -- sample and
+encode, nearest-site assignment, per-head bucketing, grouped per-head MLP,
+segment integration and Painter's merge -- with the rays already resident in
+HBM.  The default workload is the paper-shaped headline frame: 504x378
+forward-facing rays, 192 stratified samples per ray, 16 Voronoi heads of
+8x128 (bf16 operands, fp32 accumulate).
+
+Prints one JSON line (the last line on stdout).  `value` is rays/s over the
+timed steps.  `roofline` rates the dominant kernel (the grouped MLP) with
+algorithmic FLOPs (no padding) over its average duration, measured with HIP
+events on the render's stream inside the timed region.  `cpu_baseline` times
+the CPU oracle on a bounded ray sample of the same frame.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}  # MI355X dense matrix peaks
+PEAK_HBM_GBPS = 8000.0
+METRIC = "rays/sec on 1 MI355X (504x378, 192 spp, K=16); MFMA util % of bf16 peak"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def workload_text(cfg, precision):
+    a = cfg.arch
+    rgb = ("%d->%d->3" % (a.width + a.dir_dim, a.rgb_hidden)) if a.rgb_hidden else (
+        "%d->3" % (a.width + a.dir_dim))
+    return ("%s: %dx%d %s rays, %d stratified samples/ray on [%g,%g], K=%d Voronoi heads of "
+            "%dx%d (posenc L=%d, skip@%d, rgb %s), %s"
+            % (cfg.name, cfg.width, cfg.height,
+               "forward-facing NDC" if cfg.camera == "forward" else "object-centric",
+               cfg.n_coarse, cfg.near, cfg.far, cfg.num_sites, a.depth, a.width, a.pos_freqs,
+               a.skip_layer, rgb, precision))
+
+
+def cpu_baseline(sc, n_rays, nthreads):
+    import numpy as np
+    import oracle
+    from paper_2011_12490_amd import scenes
+    cfg = sc.cfg
+    ids = scenes.ray_subset(n_rays, cfg.num_rays)
+    t0 = time.perf_counter()
+    oracle.render(sc.sites, cfg.arch, sc.weights, sc.rays_o[ids], sc.rays_d[ids], cfg.near,
+                  cfg.far, cfg.n_coarse, 0, seed=scenes.SEED_RENDER, ray_ids=ids,
+                  nthreads=nthreads)
+    dt = time.perf_counter() - t0
+    return {"value": len(ids) / dt, "unit": "rays/s", "cores": nthreads, "kind": "oracle",
+            "sample": "%d seeded rays of the same frame (%d samples, fp64 heads), %.1f s"
+                      % (len(ids), len(ids) * cfg.n_coarse, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="derf_k16")
+    ap.add_argument("--precision", default=None, choices=[None, "bf16", "fp32"])
+    ap.add_argument("--sites", type=int, default=None, help="override the number of heads")
+    ap.add_argument("--cpu-rays", type=int, default=6144)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB device copy (to scale HBM counters)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py renders on one GPU only: the frame is not sharded across GPUs "
+              "(rays are independent; see the sharding notes). Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2011_12490_amd import derf, scenes
+
+    cfg = scenes.CONFIGS[args.workload]
+    if args.sites is not None:
+        cfg = scenes.with_changes(cfg, num_sites=args.sites)
+    precision = args.precision or cfg.precision
+    log("bench: building scene %s (%d rays x %d samples, K=%d, %s)"
+        % (cfg.name, cfg.num_rays, cfg.n_coarse, cfg.num_sites, precision))
+    sc = scenes.make_scene(cfg)
+    torch.cuda.set_device(0)
+    o = torch.from_numpy(sc.rays_o).cuda()
+    d = torch.from_numpy(sc.rays_d).cuda()
+    R = cfg.num_rays
+    S = R * cfg.n_coarse
+    out = (torch.empty((R, 3), device="cuda"), torch.empty((R,), device="cuda"),
+           torch.empty((R,), device="cuda"))
+    r = derf.Renderer(sc.sites, cfg.arch, sc.weights, precision)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        r.render(o, d, cfg.near, cfg.far, cfg.n_coarse, 0, scenes.SEED_RENDER, out=out,
+                 stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("bench: warmup done (%d steps)" % args.warmup)
+
+    if args.copy_calibration:
+        # a plain copy of known size: its FETCH_SIZE / WRITE_SIZE scale the
+        # counters of the render kernels (1 GiB read + 1 GiB written)
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    derf.derf_reset_stats(r.handle)
+    derf.derf_set_timing(r.handle, True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    st = derf.derf_get_stats(r.handle)
+    derf.derf_set_timing(r.handle, False)
+    log("bench: timed %d steps in %.3f s" % (args.steps, elapsed))
+
+    ms_per_step = 1e3 * elapsed / args.steps
+    stage_ms = {name: st.stage_ms[i] / max(1, st.stage_launches[i])
+                for i, name in enumerate(derf.STAGE_NAMES)}
+    mlp_ms = stage_ms["mlp"]
+    mlp_flop = 2.0 * cfg.arch.macs_per_sample() * S
+    achieved = mlp_flop / (mlp_ms * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[precision]
+    comp_bytes = 21.0 * S + 20.0 * R      # t + cell + sigma/rgb per sample, outputs per ray
+    comp_gbps = comp_bytes / (stage_ms["composite"] * 1e-3) / 1e9
+    heads = np.array(st.head_samples[:cfg.num_sites], dtype=np.int64)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        nthreads = min(16, len(os.sched_getaffinity(0)))
+        log("bench: timing the CPU oracle on %d rays with %d threads" % (args.cpu_rays, nthreads))
+        cpu = cpu_baseline(sc, args.cpu_rays, nthreads)
+
+    res = {
+        "metric": METRIC,
+        "value": R / (ms_per_step * 1e-3),
+        "unit": "rays/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": precision,
+        "data": "synthetic (seeded scene, Glorot-uniform random heads)",
+        "config": {"workload": workload_text(cfg, precision), "rays": R,
+                   "samples_per_ray": cfg.n_coarse, "heads": cfg.num_sites,
+                   "samples": S},
+        "roofline": {"bound": "mfma", "kernel": "mlp_kernel (grouped per-head MLP)",
+                     "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None,
+                     "flop_per_launch": mlp_flop, "avg_launch_ms": mlp_ms},
+        "cpu_baseline": cpu,
+        "samples_per_s": S / (ms_per_step * 1e-3),
+        "stage_ms": stage_ms,
+        "composite": {"bound": "hbm", "achieved": comp_gbps, "peak": PEAK_HBM_GBPS,
+                      "unit": "GB/s", "frac": comp_gbps / PEAK_HBM_GBPS,
+                      "bytes_per_launch": comp_bytes},
+        "head_samples": {"min": int(heads.min()), "median": float(np.median(heads)),
+                         "max": int(heads.max())},
+    }
+    r.close()
+    print(json.dumps(res))
+
+
+if __name__ == "__main__":
+    main()

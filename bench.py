@@ -46,6 +46,23 @@ def workload_text(cfg, precision):
                a.skip_layer, rgb, precision))
 
 
+def measured_traffic():
+    """HBM bytes per MLP launch from the committed counter summary, or None
+    when the kernel source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "mlp_kernel_derf_k16_hbm_counters.md")
+    try:
+        line = [l for l in open(path) if l.startswith("traffic-json:")][0]
+        rec = json.loads(line.split(":", 1)[1])
+        src = b"".join(open(os.path.join(ROOT, "paper_2011_12490_amd", "csrc", f), "rb").read()
+                       for f in ("kernels_mlp.hip", "derf_internal.h"))
+        if hashlib.sha256(src).hexdigest()[:16] != rec["source_sha256_16"]:
+            return None
+        return rec["traffic_bytes"]
+    except (OSError, IndexError, ValueError, KeyError):
+        return None
+
+
 def cpu_baseline(sc, n_rays, nthreads):
     import numpy as np
     import oracle
@@ -70,7 +87,7 @@ def main():
     ap.add_argument("--workload", default="derf_k16")
     ap.add_argument("--precision", default=None, choices=[None, "bf16", "fp32"])
     ap.add_argument("--sites", type=int, default=None, help="override the number of heads")
-    ap.add_argument("--cpu-rays", type=int, default=6144)
+    ap.add_argument("--cpu-rays", type=int, default=24576)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (to scale HBM counters)")
@@ -170,7 +187,9 @@ def main():
                    "samples": S},
         "roofline": {"bound": "mfma", "kernel": "mlp_kernel (grouped per-head MLP)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                     "frac": achieved / peak, "traffic": None,
+                     "frac": achieved / peak,
+                     "traffic": measured_traffic() if cfg.name == "derf_k16" and precision == "bf16"
+                     else None,
                      "flop_per_launch": mlp_flop, "avg_launch_ms": mlp_ms},
         "cpu_baseline": cpu,
         "samples_per_s": S / (ms_per_step * 1e-3),

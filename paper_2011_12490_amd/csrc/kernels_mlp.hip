@@ -117,8 +117,14 @@ struct Cfg {
     static constexpr int B_BC = B_WCD + (RH > 0 ? 0 : 3 * 2 * ED);    // [4]
     static constexpr int BLOCK_FLOATS = (B_BC + 4 + 255) / 256 * 256;
     static constexpr int BLOCK_UNITS = BLOCK_FLOATS / 256;
-    static constexpr int LDS_BYTES = 2 * SMAX * 1024 + BLOCK_FLOATS * 4;
-    static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
+    // bf16 path: gamma(x) and gamma(d) chunks wait in LDS, not registers
+    static constexpr bool XLDS = BF16;
+    static constexpr int GX_UNITS = NB * EX / 8;
+    static constexpr int GD_UNITS = NB * 2;
+    static constexpr int G_WAVE_BYTES = XLDS ? (GX_UNITS + GD_UNITS) * 1024 : 0;
+    static constexpr int G_OFF = 2 * SMAX * 1024 + BLOCK_FLOATS * 4;
+    static constexpr int LDS_BYTES = G_OFF + WAVES * G_WAVE_BYTES;
+    static_assert(LDS_BYTES + 4 * 1024 <= 160 * 1024, "LDS budget");
 };
 
 // Input column (in the packed layer's input order) of lane-entry e of lane
@@ -275,29 +281,45 @@ __device__ __forceinline__ f32x16 mfma(float a, float b, const f32x16 &c)
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
 }
 
+// One wave copies 64 x 16 bytes global -> LDS: lane l reads src_lane and the
+// data lands at lds_base + 16 l (lds_base must be the same for the wave).
+__device__ __forceinline__ void load_lds16(const void *src_lane, unsigned char *lds_base)
+{
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src_lane,
+                                     (__attribute__((address_space(3))) void *)lds_base, 16, 0, 0);
+}
 __device__ __forceinline__ void load_unit_async(const unsigned char *src, unsigned char *lds_unit, int lane)
 {
-    __builtin_amdgcn_global_load_lds(
-        (const __attribute__((address_space(1))) void *)(src + lane * 16),
-        (__attribute__((address_space(3))) void *)lds_unit, 16, 0, 0);
+    load_lds16(src + lane * 16, lds_unit);
 }
 
-// ReLU then round to bf16 (RNE), 8 accumulator values -> one B chunk.
-__device__ __forceinline__ bf16x8 relu_bf16(const f32x16 &a, int h)
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Round 8 floats to bf16 (nearest even) into one B chunk.
+__device__ __forceinline__ bf16x8 to_bf16x8(const float *f)
 {
-    bf16x8 r;
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-        r[j] = (__bf16)a[8 * h + j];
-    // negative bf16 values are negative as int16: max with 0 is the ReLU
-    i16x2 *p = reinterpret_cast<i16x2 *>(&r);
+    unsigned w[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-        p[j] = __builtin_elementwise_max(p[j], i16x2{0, 0});
-    return r;
+        w[j] = __builtin_bit_cast(unsigned, __builtin_convertvector(f32x2{f[2 * j], f[2 * j + 1]}, bf16x2));
+    return __builtin_bit_cast(bf16x8, w);
 }
 
-__device__ __forceinline__ float sigmoid(float x) { return 1.0f / (1.0f + __expf(-x)); }
+// ReLU then round to bf16: accumulator registers 8h .. 8h+7 -> one B chunk.
+// A negative bf16 is a negative int16, so the ReLU is a packed int16 max with 0.
+__device__ __forceinline__ bf16x8 relu_bf16(const f32x16 &a, int h)
+{
+    i16x2 p[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const bf16x2 v = __builtin_convertvector(f32x2{a[8 * h + 2 * j], a[8 * h + 2 * j + 1]}, bf16x2);
+        p[j] = __builtin_elementwise_max(__builtin_bit_cast(i16x2, v), i16x2{0, 0});
+    }
+    return __builtin_bit_cast(bf16x8, p);
+}
+
+__device__ __forceinline__ float sigmoid(float x) { return __builtin_amdgcn_rcpf(1.0f + __expf(-x)); }
 
 // sin(pi 2^l p), cos(pi 2^l p): v_sin/v_cos take revolutions; 2^(l-1) p is
 // exact and its fractional part is an exact reduction.
@@ -311,6 +333,9 @@ __device__ __forceinline__ void sincos_pi_pow2(float p, int l, float &s, float &
 template <class C>
 using Chunk = std::conditional_t<C::BF16, bf16x8, float>;
 
+// Number of A-fragment reads kept in flight ahead of the MFMA that uses them.
+constexpr int kPrefetch = 3;
+
 template <class C>
 __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
     const unsigned *__restrict__ bucket, const unsigned *__restrict__ totals, int num_sites,
@@ -320,6 +345,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
 {
     using CT = Chunk<C>;
     constexpr int NB = C::NB, E = C::E;
+    constexpr int EXC = C::EX / E, EHC = C::EH / E, EDC = C::ED / E;  // chunks
     extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
     unsigned char *buf0 = lds;
     unsigned char *buf1 = lds + C::SMAX * 1024;
@@ -329,6 +355,10 @@ __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int n = lane & 31, g = lane >> 5;
+    // this wave's staging of gamma(x) and gamma(d) (bf16 path): chunk c of
+    // column block nb at ((nb * chunks + c) * 64 + lane) * 16
+    unsigned char *gxl = lds + C::G_OFF + wave * C::G_WAVE_BYTES;
+    unsigned char *gdl = gxl + C::GX_UNITS * 1024;
 
     if (tid == 0) {
         unsigned off = 0, tl = 0;
@@ -355,15 +385,17 @@ __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
     for (unsigned tile = t_begin; tile < t_end; ++tile) {
         while (s_tile[head + 1] <= tile)
             ++head;
-        const unsigned row0 = s_off[head] + (tile - s_tile[head]) * C::TILE;
+        // tile bookkeeping is uniform across the workgroup: keep it scalar
+        head = __builtin_amdgcn_readfirstlane(head);
+        const unsigned row0 = __builtin_amdgcn_readfirstlane(s_off[head] + (tile - s_tile[head]) * C::TILE);
         // rows never pass the sample count when the bucket counts are
         // consistent; the clamps keep every access in bounds regardless
-        const unsigned row_end = min(s_off[head + 1], geo.num_samples);
+        const unsigned row_end = __builtin_amdgcn_readfirstlane(min(s_off[head + 1], geo.num_samples));
         if (row0 >= row_end)
             continue;
         const unsigned char *stream = streams + (size_t)head * C::STREAM_UNITS * 1024;
 
-        __syncthreads();  // previous tile is done with both buffers and the head block
+        __syncthreads();  // previous tile is done with the buffers, the head block and staging
         if (head != loaded_head) {
             const unsigned char *src = reinterpret_cast<const unsigned char *>(blocks + (size_t)head * C::BLOCK_FLOATS);
             for (int u = wave; u < C::BLOCK_UNITS; u += C::WAVES)
@@ -374,8 +406,8 @@ __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
             load_unit_async(stream + (size_t)(C::st_offset(0) + u) * 1024, buf0 + u * 1024, lane);
 
         // ---- gather the wave's samples and encode them ----------------------
-        CT gx[NB][C::EX / E];
-        CT gd[NB][C::ED / E];
+        CT gx[C::XLDS ? 1 : NB][EXC];
+        CT gd[C::XLDS ? 1 : NB][EDC];
         unsigned sid[NB];
         bool valid[NB];
 #pragma unroll
@@ -402,15 +434,14 @@ __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
 #pragma unroll
             for (int e = 2 + 2 * C::P0; e < C::EX; ++e)
                 f[e] = 0.0f;
-            if constexpr (C::BF16) {
+            if constexpr (C::XLDS) {
 #pragma unroll
-                for (int ch = 0; ch < C::EX / 8; ++ch)
-#pragma unroll
-                    for (int j = 0; j < 8; ++j)
-                        gx[nb][ch][j] = (__bf16)f[8 * ch + j];
-                const bf16x8 *dp = reinterpret_cast<const bf16x8 *>(dirbuf) + (size_t)r * (kDirPad / 8);
-                gd[nb][0] = dp[g];
-                gd[nb][1] = dp[2 + g];
+                for (int ch = 0; ch < EXC; ++ch)
+                    *reinterpret_cast<bf16x8 *>(gxl + ((nb * EXC + ch) * 64 + lane) * 16) = to_bf16x8(f + 8 * ch);
+                // gamma(d) chunks f[8g..8g+7] and f[16+8g..16+8g+7] straight to LDS
+                const unsigned char *dp = reinterpret_cast<const unsigned char *>(dirbuf) + (size_t)r * (kDirPad * 2);
+                load_lds16(dp + g * 16, gdl + (nb * 2 + 0) * 1024);
+                load_lds16(dp + 32 + g * 16, gdl + (nb * 2 + 1) * 1024);
             } else {
 #pragma unroll
                 for (int e = 0; e < C::EX; ++e)
@@ -427,8 +458,8 @@ __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
             }
         }
 
-        CT act[NB][C::EH / E];
-        CT nact[NB][C::EH / E];
+        CT act[NB][EHC];
+        CT nact[NB][EHC];
         float sig[NB], rgb[3][NB];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
@@ -442,6 +473,11 @@ __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
             constexpr int kind = C::st_kind(s), layer = C::st_layer(s);
             constexpr int tile0 = C::st_tile0(s), ntiles = C::st_ntiles(s);
             constexpr int chunks = C::st_chunks(s);
+            constexpr int UPT = chunks / C::CPU;   // LDS units per output tile
+            constexpr int NF = ntiles * UPT;       // fragment reads of this stage
+            // chunks of this stage's input that come from gamma(x) / gamma(d)
+            constexpr bool uses_gx = kind == 0 && (layer == 0 || layer == C::SKIP);
+            constexpr bool uses_gd = kind == 1;
             unsigned char *cur = (s % 2 == 0) ? buf0 : buf1;
             unsigned char *nxt = (s % 2 == 0) ? buf1 : buf0;
 
@@ -451,6 +487,58 @@ __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
                 for (int u = wave; u < C::st_units(s + 1); u += C::WAVES)
                     load_unit_async(stream + (size_t)(C::st_offset(s + 1) + u) * 1024, nxt + u * 1024, lane);
             }
+
+            // A fragments of this stage, read kPrefetch ahead of their use
+            using AT = std::conditional_t<C::BF16, bf16x8, f32x4>;
+            auto frag = [&](int j) -> AT {
+                const int t = j % ntiles, u = j / ntiles;
+                return *reinterpret_cast<const AT *>(cur + ((t * UPT + u) * 64 + lane) * 16);
+            };
+            AT fr[kPrefetch];
+            static_for<0, (kPrefetch < NF ? kPrefetch : NF)>([&](auto ic0) {
+                constexpr int i = decltype(ic0)::value;
+                fr[i] = frag(i);
+            });
+
+            // staged encodings needed by this stage (bf16 path)
+            CT xin[NB][(C::XLDS && uses_gx) ? EXC : 1];
+            CT din[NB][(C::XLDS && uses_gd) ? 2 : 1];
+            if constexpr (C::XLDS && uses_gx) {
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                    for (int ch = 0; ch < EXC; ++ch)
+                        xin[nb][ch] = *reinterpret_cast<const bf16x8 *>(gxl + ((nb * EXC + ch) * 64 + lane) * 16);
+            }
+            if constexpr (C::XLDS && uses_gd) {
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                    for (int ch = 0; ch < 2; ++ch)
+                        din[nb][ch] = *reinterpret_cast<const bf16x8 *>(gdl + ((nb * 2 + ch) * 64 + lane) * 16);
+            }
+
+            // B operand chunk c of this stage's input for column block nb
+            auto in_chunk = [&](auto cc, int nb) -> CT {
+                constexpr int c = decltype(cc)::value;
+                if constexpr (kind == 1) {
+                    if constexpr (c < EHC) return act[nb][c];
+                    else if constexpr (C::XLDS) return din[nb][c - EHC];
+                    else return gd[nb][c - EHC];
+                } else if constexpr (layer == 0) {
+                    if constexpr (C::XLDS) return xin[nb][c];
+                    else return gx[nb][c];
+                } else if constexpr (layer == C::SKIP) {
+                    if constexpr (c < EXC) {
+                        if constexpr (C::XLDS) return xin[nb][c];
+                        else return gx[nb][c];
+                    } else {
+                        return act[nb][c - EXC];
+                    }
+                } else {
+                    return act[nb][c];
+                }
+            };
 
             f32x16 acc[C::TPS][NB];
 #pragma unroll
@@ -469,41 +557,23 @@ __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
                     acc[t][nb] = b;
             }
 
-            // B operand chunk c of this stage's input for column block nb
-            auto in_chunk = [&](auto cc, int nb) -> CT {
-                constexpr int c = decltype(cc)::value;
-                if constexpr (kind == 1) {
-                    if constexpr (c < C::EH / E) return act[nb][c];
-                    else return gd[nb][c - C::EH / E];
-                } else if constexpr (layer == 0) {
-                    return gx[nb][c];
-                } else if constexpr (layer == C::SKIP) {
-                    if constexpr (c < C::EX / E) return gx[nb][c];
-                    else return act[nb][c - C::EX / E];
-                } else {
-                    return act[nb][c];
-                }
-            };
-
-            static_for<0, chunks / C::CPU>([&](auto uc) {
-                constexpr int u = decltype(uc)::value;
+            static_for<0, NF>([&](auto jc) {
+                constexpr int j = decltype(jc)::value;
+                constexpr int t = j % ntiles, u = j / ntiles;
+                const AT a = fr[j % kPrefetch];
+                if constexpr (j + kPrefetch < NF)
+                    fr[j % kPrefetch] = frag(j + kPrefetch);
+                if constexpr (C::BF16) {
 #pragma unroll
-                for (int t = 0; t < ntiles; ++t) {
-                    const unsigned char *src = cur + ((t * (chunks / C::CPU) + u) * 64 + lane) * 16;
-                    if constexpr (C::BF16) {
-                        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(src);
+                    for (int nb = 0; nb < NB; ++nb)
+                        acc[t][nb] = mfma(a, in_chunk(ic<u>{}, nb), acc[t][nb]);
+                } else {
+                    static_for<0, 4>([&](auto jj) {
+                        constexpr int q = decltype(jj)::value;
 #pragma unroll
                         for (int nb = 0; nb < NB; ++nb)
-                            acc[t][nb] = mfma(a, in_chunk(ic<u>{}, nb), acc[t][nb]);
-                    } else {
-                        const f32x4 a = *reinterpret_cast<const f32x4 *>(src);
-                        static_for<0, 4>([&](auto jc) {
-                            constexpr int j = decltype(jc)::value;
-#pragma unroll
-                            for (int nb = 0; nb < NB; ++nb)
-                                acc[t][nb] = mfma(a[j], in_chunk(ic<4 * u + j>{}, nb), acc[t][nb]);
-                        });
-                    }
+                            acc[t][nb] = mfma(a[q], in_chunk(ic<4 * u + q>{}, nb), acc[t][nb]);
+                    });
                 }
             });
 
@@ -513,10 +583,6 @@ __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
                 const int mt = tile0 + t;
 #pragma unroll
                 for (int nb = 0; nb < NB; ++nb) {
-                    f32x16 v = acc[t][nb];
-#pragma unroll
-                    for (int i = 0; i < 16; ++i)
-                        v[i] = v[i] > 0.0f ? v[i] : 0.0f;
                     if constexpr (kind == 0) {
                         if constexpr (C::BF16) {
                             nact[nb][2 * mt] = relu_bf16(acc[t][nb], 0);
@@ -524,20 +590,20 @@ __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
                         } else {
 #pragma unroll
                             for (int i = 0; i < 16; ++i)
-                                nact[nb][16 * mt + i] = v[i];
+                                nact[nb][16 * mt + i] = fmaxf(acc[t][nb][i], 0.0f);
                         }
                         if constexpr (layer == C::D - 1) {
                             const float *ws = hb + C::B_WSIG + g * C::EH + 16 * mt;
 #pragma unroll
                             for (int i = 0; i < 16; ++i)
-                                sig[nb] = fmaf(ws[i], v[i], sig[nb]);
+                                sig[nb] = fmaf(ws[i], fmaxf(acc[t][nb][i], 0.0f), sig[nb]);
                             if constexpr (C::RH == 0) {
 #pragma unroll
                                 for (int c3 = 0; c3 < 3; ++c3) {
                                     const float *wc = hb + C::B_WC + (c3 * 2 + g) * C::EH + 16 * mt;
 #pragma unroll
                                     for (int i = 0; i < 16; ++i)
-                                        rgb[c3][nb] = fmaf(wc[i], v[i], rgb[c3][nb]);
+                                        rgb[c3][nb] = fmaf(wc[i], fmaxf(acc[t][nb][i], 0.0f), rgb[c3][nb]);
                                 }
                             }
                         }
@@ -547,7 +613,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
                             const float *wc = hb + C::B_WC + (c3 * 2 + g) * C::ERH + 16 * mt;
 #pragma unroll
                             for (int i = 0; i < 16; ++i)
-                                rgb[c3][nb] = fmaf(wc[i], v[i], rgb[c3][nb]);
+                                rgb[c3][nb] = fmaf(wc[i], fmaxf(acc[t][nb][i], 0.0f), rgb[c3][nb]);
                         }
                     }
                 }
@@ -557,7 +623,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
 #pragma unroll
                 for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-                    for (int c = 0; c < C::EH / E; ++c)
+                    for (int c = 0; c < EHC; ++c)
                         act[nb][c] = nact[nb][c];
             }
         });
@@ -573,8 +639,10 @@ __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
 #pragma unroll
                     for (int e = 0; e < C::ED; ++e) {
                         float dv;
-                        if constexpr (C::BF16) dv = (float)gd[nb][e / 8][e % 8];
-                        else dv = gd[nb][e];
+                        if constexpr (C::XLDS)
+                            dv = (float)reinterpret_cast<const __bf16 *>(gdl + ((nb * 2 + e / 8) * 64 + lane) * 16)[e % 8];
+                        else
+                            dv = gd[nb][e];
                         rgb[c3][nb] = fmaf(wd[e], dv, rgb[c3][nb]);
                     }
                 }

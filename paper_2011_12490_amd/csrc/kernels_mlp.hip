@@ -3,19 +3,34 @@
 // Every ray sample is evaluated by the single head that owns it (Sec. 3.2:
 // the decomposition weights are one-hot, so only that head contributes).
 // After bucketing, the samples of head k are one contiguous range, so the
-// head network becomes a chain of dense products with M = (samples of k):
-// one workgroup takes a tile of a head's samples and runs it through every
-// layer with the activations held in registers, while the head's weights
-// stream through LDS, one stage (two 32-row output tiles of one layer) at a
-// time, double-buffered with direct global->LDS loads.
+// head network becomes a chain of dense products with M = (samples of k).
+//
+// Work split.  A workgroup of 4 waves (one per SIMD) takes a tile of one
+// head's samples, NB x 32 per wave, and runs it through the whole network
+// with the activations held in registers.  Two workgroups share a CU (one for
+// width 256); they do not synchronise with each other, so one's barriers and
+// gathers are covered by the other's matrix work.  Workgroups are persistent
+// and walk contiguous tile ranges, mapped so that each XCD (which has its own
+// L2) works on a contiguous stretch of heads.
 //
 // Operand layout (v_mfma_f32_32x32x16_bf16 / v_mfma_f32_32x32x2_f32):
 // weights are the A operand (32 output rows x k), samples the B operand
-// (k x 32 samples), so a wave owns NB x 32 samples.  Lane l = n + 32 g holds
-// sample n; a 32x32 result leaves in lane l the 16 rows
-// 8 (i / 4) + 4 g + (i % 4), i = 0..15.  The next layer consumes those
-// registers directly as its B operand; the k-order this implies is folded
-// into the weight layout at creation time, so no data moves between layers.
+// (k x 32 samples).  Lane l = n + 32 g holds sample n; a 32x32 result leaves
+// in lane l the 16 rows 8 (i / 4) + 4 g + (i % 4), i = 0..15, and the next
+// layer consumes those registers directly as its B operand.  The k-order this
+// implies is folded into the weight layout at creation time, so layers chain
+// with no data movement.
+//
+// Weight streaming.  A head's weights are cut into stages -- one 32-row
+// output tile and at most 8 KB of its input chunks -- laid out as 1 KB units
+// that are exactly one wave's A-operand registers.  Stages stream
+// global -> LDS (global_load_lds_dwordx4) through a 4-slot ring, issued three
+// stages ahead (across tile boundaries too) and waited for two stages ahead,
+// so one barrier per stage orders slot reuse; each wave also reads the first
+// fragments of the next stage before that stage begins.  A tile's ReLU and
+// bf16 rounding run during the next tile's matrix work.  Density and colour
+// come out of one extra 32-row output tile (row 0 density, rows 1-3 colour
+// logits), so the network tail needs no cross-lane reduction.
 #include <type_traits>
 #include <vector>
 
@@ -24,8 +39,10 @@
 namespace derf {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef short i16x2 __attribute__((ext_vector_type(2)));
 
 template <int N>
@@ -45,15 +62,22 @@ __host__ __device__ constexpr int c_row(int g, int i) { return 8 * (i / 4) + 4 *
 
 // ---------------------------------------------------------------------------
 // Compile-time description of one head architecture / precision.
+//
+// Output tiles, in order: hidden layer l, tile mt (l * MT + mt); the colour
+// hidden layer's tiles; the output tile.  Each tile's input is cut into
+// stages of at most UMAX units.
+enum { K_HID = 0, K_RGBH = 1, K_OUT = 2 };
+
 template <bool BF16_, int W_, int D_, int SKIP_, int RH_, int LP_>
 struct Cfg {
     static constexpr bool BF16 = BF16_;
     static constexpr int W = W_, D = D_, SKIP = SKIP_, RH = RH_, LP = LP_;
     static constexpr int E = BF16 ? 8 : 1;     // k-entries per lane per MFMA
-    static constexpr int CPU = BF16 ? 1 : 4;   // MFMA k-chunks per 1 KB LDS unit
+    static constexpr int CPU = BF16 ? 1 : 4;   // MFMA k-chunks per 1 KB unit
     static constexpr int NB = BF16 ? 2 : 1;    // 32-sample column blocks per wave
-    static constexpr int WAVES = (W >= 256) ? 4 : 8;
+    static constexpr int WAVES = 4;
     static constexpr int THREADS = WAVES * 64;
+    static constexpr int WG_PER_CU = W >= 256 ? 1 : 2;
     static constexpr int TILE = WAVES * NB * 32;
     static constexpr int P = 3 + 6 * LP;       // gamma(x) length
     static constexpr int DD = 27;              // gamma(d) length (4 frequencies)
@@ -63,68 +87,98 @@ struct Cfg {
     static constexpr int ED = 16;              // direction entries per lane
     static constexpr int MT = W / 32;          // output tiles per hidden layer
     static constexpr int MTR = (RH + 31) / 32; // output tiles of the colour hidden layer
-    static constexpr int ERH = MTR * 16;
-    static constexpr int TPS = 2;              // output tiles per stage
-    static constexpr int SPL = (MT + TPS - 1) / TPS;
-    static constexpr int SPR = (MTR + TPS - 1) / TPS;
-    static constexpr int NS = D * SPL + SPR;   // stages per tile
+    static constexpr int ERH = MTR * 16;       // colour-hidden entries per lane
+    static constexpr int EXC = EX / E, EHC = EH / E, EDC = ED / E, ERHC = ERH / E;
+    static constexpr int UMAX = 8;             // units per stage
+    static constexpr int CMAX = UMAX * CPU;    // chunks per stage
+    static constexpr int NBUF = 4;             // LDS ring slots
+    static constexpr int NT = D * MT + MTR + 1;
     static_assert(LP % 2 == 0, "pos_freqs must be even");
-    static_assert(W % 64 == 0 || W == 32, "width");
+    static_assert(W % 64 == 0, "width");
 
-    // stage s: kind (0 hidden, 1 colour hidden), layer, first tile, tiles, input entries
-    static constexpr int st_kind(int s) { return s < D * SPL ? 0 : 1; }
-    static constexpr int st_layer(int s) { return s < D * SPL ? s / SPL : D; }
-    static constexpr int st_tile0(int s) { return s < D * SPL ? (s % SPL) * TPS : (s - D * SPL) * TPS; }
-    static constexpr int st_ntiles(int s)
+    static constexpr int t_kind(int T) { return T < D * MT ? K_HID : (T < D * MT + MTR ? K_RGBH : K_OUT); }
+    static constexpr int t_layer(int T) { return T < D * MT ? T / MT : -1; }
+    static constexpr int t_mt(int T) { return T < D * MT ? T % MT : (T < D * MT + MTR ? T - D * MT : 0); }
+    static constexpr int t_entries(int T)
     {
-        return st_kind(s) == 0 ? (MT - st_tile0(s) < TPS ? MT - st_tile0(s) : TPS)
-                               : (MTR - st_tile0(s) < TPS ? MTR - st_tile0(s) : TPS);
+        return t_kind(T) == K_RGBH ? EH + ED
+               : t_kind(T) == K_OUT ? EH + (RH > 0 ? ERH : ED)
+               : t_layer(T) == 0    ? EX
+               : t_layer(T) == SKIP ? EX + EH
+                                    : EH;
     }
-    static constexpr int st_entries(int s)
+    static constexpr int t_chunks(int T) { return t_entries(T) / E; }
+    static constexpr int t_splits(int T) { return (t_chunks(T) + CMAX - 1) / CMAX; }
+
+    static constexpr int count_stages()
     {
-        return st_kind(s) == 1 ? EH + ED
-               : st_layer(s) == 0 ? EX
-               : st_layer(s) == SKIP ? EX + EH
-                                     : EH;
+        int n = 0;
+        for (int T = 0; T < NT; ++T)
+            n += t_splits(T);
+        return n;
     }
-    static constexpr int st_chunks(int s) { return st_entries(s) / E; }
-    static constexpr int st_units(int s) { return st_ntiles(s) * st_chunks(s) / CPU; }
+    static constexpr int NS = count_stages();
+    static constexpr int st_tile(int s)
+    {
+        for (int T = 0; T < NT; ++T) {
+            if (s < t_splits(T))
+                return T;
+            s -= t_splits(T);
+        }
+        return -1;
+    }
+    static constexpr int st_split(int s)
+    {
+        for (int T = 0; T < NT; ++T) {
+            if (s < t_splits(T))
+                return s;
+            s -= t_splits(T);
+        }
+        return -1;
+    }
+    static constexpr int st_c0(int s) { return st_split(s) * CMAX; }
+    static constexpr int st_c1(int s)
+    {
+        return (st_split(s) + 1) * CMAX < t_chunks(st_tile(s)) ? (st_split(s) + 1) * CMAX : t_chunks(st_tile(s));
+    }
+    static constexpr bool st_first(int s) { return st_split(s) == 0; }
+    static constexpr int st_units(int s) { return (st_c1(s) - st_c0(s)) / CPU; }
+    static constexpr int st_lpw(int s) { return (st_units(s) + WAVES - 1) / WAVES; }  // loads per wave
+    static constexpr int st_units_pad(int s) { return st_lpw(s) * WAVES; }
     static constexpr int st_offset(int s)  // in units
     {
         int o = 0;
         for (int q = 0; q < s; ++q)
-            o += st_units(q);
+            o += st_units_pad(q);
         return o;
     }
-    static constexpr int max_units()
-    {
-        int m = 0;
-        for (int q = 0; q < NS; ++q)
-            m = st_units(q) > m ? st_units(q) : m;
-        return m;
-    }
     static constexpr int STREAM_UNITS = st_offset(NS);
-    static constexpr int SMAX = max_units();
 
-    // resident per-head block (floats): biases in accumulator layout, the
-    // density row and the colour output rows in lane-entry order
-    static constexpr int B_HID = 0;                           // [D][MT][2][16]
-    static constexpr int B_RGBH = B_HID + D * MT * 32;        // [MTR][2][16]
-    static constexpr int B_WSIG = B_RGBH + MTR * 32;          // [2][EH]
-    static constexpr int B_BSIG = B_WSIG + 2 * EH;            // [4]
-    static constexpr int B_WC = B_BSIG + 4;                   // [3][2][ERH] or [3][2][EH]
-    static constexpr int B_WCD = B_WC + 3 * 2 * (RH > 0 ? ERH : EH);  // [3][2][ED]
-    static constexpr int B_BC = B_WCD + (RH > 0 ? 0 : 3 * 2 * ED);    // [4]
-    static constexpr int BLOCK_FLOATS = (B_BC + 4 + 255) / 256 * 256;
+    static constexpr int first_stage_of_tile(int T)
+    {
+        int s = 0;
+        for (int q = 0; q < T; ++q)
+            s += t_splits(q);
+        return s;
+    }
+    // stage that first reads gamma(x) again (skip layer), stage that first
+    // reads gamma(d), and the stage that issues the gamma(d) loads
+    static constexpr int S_SKIP = SKIP >= 0 ? first_stage_of_tile(SKIP * MT) : -1;
+    static constexpr int S_GDUSE = first_stage_of_tile(RH > 0 ? D * MT : D * MT + MTR);
+    static constexpr int S_GD = S_GDUSE >= 3 ? S_GDUSE - 3 : 0;
+    static constexpr int NGD = NB * (BF16 ? 2 : 4);  // gamma(d) loads per lane
+
+    // per-head resident block: bias of every output tile in accumulator layout
+    static constexpr int BLOCK_FLOATS = (NT * 32 + 255) / 256 * 256;
     static constexpr int BLOCK_UNITS = BLOCK_FLOATS / 256;
-    // bf16 path: gamma(x) and gamma(d) chunks wait in LDS, not registers
-    static constexpr bool XLDS = BF16;
-    static constexpr int GX_UNITS = NB * EX / 8;
-    static constexpr int GD_UNITS = NB * 2;
-    static constexpr int G_WAVE_BYTES = XLDS ? (GX_UNITS + GD_UNITS) * 1024 : 0;
-    static constexpr int G_OFF = 2 * SMAX * 1024 + BLOCK_FLOATS * 4;
-    static constexpr int LDS_BYTES = G_OFF + WAVES * G_WAVE_BYTES;
-    static_assert(LDS_BYTES + 4 * 1024 <= 160 * 1024, "LDS budget");
+
+    // LDS: ring | head block | per-wave gamma(x) staging
+    static constexpr int SLOT_BYTES = UMAX * 1024;
+    static constexpr int HB_OFF = NBUF * SLOT_BYTES;
+    static constexpr int GX_OFF = HB_OFF + BLOCK_FLOATS * 4;
+    static constexpr int GX_WAVE_UNITS = NB * EX * (BF16 ? 2 : 4) / 16;
+    static constexpr int LDS_BYTES = GX_OFF + WAVES * GX_WAVE_UNITS * 1024;
+    static_assert(WG_PER_CU * (LDS_BYTES + 3 * 1024) <= 160 * 1024, "LDS budget");
 };
 
 // Input column (in the packed layer's input order) of lane-entry e of lane
@@ -179,22 +233,68 @@ struct Packer {
         }
     }
 
-    // input column of entry e (lane group g) for stage s, or -1
-    static int in_col(int s, int g, int e)
+    // weight of output tile T, row m (0..31 within the tile), lane group g, entry e
+    static float wval(const std::vector<View> &v, int T, int m, int g, int e)
     {
-        if (C::st_kind(s) == 1)
-            return e < C::EH ? h_col(g, e) : (d_col(g, e - C::EH) < C::DD ? C::W + d_col(g, e - C::EH) : -1);
-        const int l = C::st_layer(s);
-        if (l == 0)
-            return x_col<C>(g, e);
-        if (l == C::SKIP) {
-            if (e < C::EX) {
-                const int c = x_col<C>(g, e);
-                return c;
-            }
-            return C::P + h_col(g, e - C::EX);
+        const int kind = C::t_kind(T);
+        if (kind == K_HID) {
+            const int l = C::t_layer(T);
+            const View &L = v[l];
+            const int row = 32 * C::t_mt(T) + m;
+            int col;
+            if (l == 0)
+                col = x_col<C>(g, e);
+            else if (l == C::SKIP)
+                col = e < C::EX ? x_col<C>(g, e) : C::P + h_col(g, e - C::EX);
+            else
+                col = h_col(g, e);
+            return col >= 0 ? L.W[(size_t)row * L.in + col] : 0.0f;
         }
-        return h_col(g, e);
+        if (kind == K_RGBH) {
+            const View &L = v[C::D + 1];
+            const int row = 32 * C::t_mt(T) + m;
+            if (row >= C::RH)
+                return 0.0f;
+            int col;
+            if (e < C::EH)
+                col = h_col(g, e);
+            else
+                col = d_col(g, e - C::EH) < C::DD ? C::W + d_col(g, e - C::EH) : -1;
+            return col >= 0 ? L.W[(size_t)row * L.in + col] : 0.0f;
+        }
+        // output tile: row 0 density (reads h), rows 1..3 colour logits
+        if (m == 0) {
+            const View &S = v[C::D];
+            return e < C::EH ? S.W[h_col(g, e)] : 0.0f;
+        }
+        if (m > 3)
+            return 0.0f;
+        const View &O = v.back();
+        const int c3 = m - 1;
+        if (C::RH > 0) {
+            if (e < C::EH)
+                return 0.0f;
+            const int row = h_col(g, e - C::EH);
+            return row < C::RH ? O.W[(size_t)c3 * O.in + row] : 0.0f;
+        }
+        if (e < C::EH)
+            return O.W[(size_t)c3 * O.in + h_col(g, e)];
+        const int f = d_col(g, e - C::EH);
+        return f < C::DD ? O.W[(size_t)c3 * O.in + C::W + f] : 0.0f;
+    }
+
+    static float bval(const std::vector<View> &v, int T, int row)
+    {
+        const int kind = C::t_kind(T);
+        if (kind == K_HID)
+            return v[C::t_layer(T)].b[32 * C::t_mt(T) + row];
+        if (kind == K_RGBH) {
+            const int r = 32 * C::t_mt(T) + row;
+            return r < C::RH ? v[C::D + 1].b[r] : 0.0f;
+        }
+        if (row == 0)
+            return v[C::D].b[0];
+        return row <= 3 ? v.back().b[row - 1] : 0.0f;
     }
 
     static void pack(const float *w, unsigned char *stream, float *block)
@@ -202,26 +302,21 @@ struct Packer {
         std::vector<View> v;
         views(w, v);
         for (int s = 0; s < C::NS; ++s) {
-            const View &L = C::st_kind(s) == 0 ? v[C::st_layer(s)] : v[C::D + 1];
+            const int T = C::st_tile(s), c0 = C::st_c0(s);
             unsigned char *base = stream + (size_t)C::st_offset(s) * 1024;
-            const int chunks = C::st_chunks(s);
-            for (int t = 0; t < C::st_ntiles(s); ++t) {
-                const int mt = C::st_tile0(s) + t;
-                for (int u = 0; u < chunks / C::CPU; ++u) {
-                    unsigned char *unit = base + (size_t)(t * (chunks / C::CPU) + u) * 1024;
-                    for (int lane = 0; lane < 64; ++lane) {
-                        const int m = 32 * mt + lane % 32, g = lane / 32;
-                        for (int j = 0; j < 8 / (C::BF16 ? 1 : 2); ++j) {
-                            // bf16: 8 k-entries of chunk u; fp32: chunks 4u + j, entry g
-                            const int e = C::BF16 ? 8 * u + j : 4 * u + j;
-                            const int col = in_col(s, g, e);
-                            const float val = (m < L.out && col >= 0) ? L.W[(size_t)m * L.in + col] : 0.0f;
-                            if (C::BF16) {
-                                const __bf16 bv = (__bf16)val;
-                                __builtin_memcpy(unit + lane * 16 + 2 * j, &bv, 2);
-                            } else {
-                                __builtin_memcpy(unit + lane * 16 + 4 * j, &val, 4);
-                            }
+            for (int u = 0; u < C::st_units_pad(s); ++u) {
+                unsigned char *unit = base + (size_t)u * 1024;
+                for (int lane = 0; lane < 64; ++lane) {
+                    const int m = lane % 32, g = lane / 32;
+                    for (int j = 0; j < (C::BF16 ? 8 : 4); ++j) {
+                        // bf16: 8 k-entries of chunk c0 + u; fp32: chunk c0 + 4u + j, one entry
+                        const int e = C::BF16 ? 8 * (c0 + u) + j : c0 + 4 * u + j;
+                        const float val = u < C::st_units(s) ? wval(v, T, m, g, e) : 0.0f;
+                        if (C::BF16) {
+                            const __bf16 bv = (__bf16)val;
+                            __builtin_memcpy(unit + lane * 16 + 2 * j, &bv, 2);
+                        } else {
+                            __builtin_memcpy(unit + lane * 16 + 4 * j, &val, 4);
                         }
                     }
                 }
@@ -229,44 +324,10 @@ struct Packer {
         }
         for (int i = 0; i < C::BLOCK_FLOATS; ++i)
             block[i] = 0.0f;
-        for (int l = 0; l < C::D; ++l)
-            for (int mt = 0; mt < C::MT; ++mt)
-                for (int g = 0; g < 2; ++g)
-                    for (int i = 0; i < 16; ++i)
-                        block[C::B_HID + ((l * C::MT + mt) * 2 + g) * 16 + i] = v[l].b[32 * mt + c_row(g, i)];
-        if (C::RH > 0) {
-            const View &R = v[C::D + 1];
-            for (int mt = 0; mt < C::MTR; ++mt)
-                for (int g = 0; g < 2; ++g)
-                    for (int i = 0; i < 16; ++i) {
-                        const int row = 32 * mt + c_row(g, i);
-                        block[C::B_RGBH + (mt * 2 + g) * 16 + i] = row < C::RH ? R.b[row] : 0.0f;
-                    }
-        }
-        const View &S = v[C::D];
-        for (int g = 0; g < 2; ++g)
-            for (int e = 0; e < C::EH; ++e)
-                block[C::B_WSIG + g * C::EH + e] = S.W[h_col(g, e)];
-        block[C::B_BSIG] = S.b[0];
-        const View &O = v.back();
-        for (int c = 0; c < 3; ++c) {
-            for (int g = 0; g < 2; ++g) {
-                if (C::RH > 0) {
-                    for (int e = 0; e < C::ERH; ++e) {
-                        const int row = h_col(g, e);
-                        block[C::B_WC + (c * 2 + g) * C::ERH + e] = row < C::RH ? O.W[c * O.in + row] : 0.0f;
-                    }
-                } else {
-                    for (int e = 0; e < C::EH; ++e)
-                        block[C::B_WC + (c * 2 + g) * C::EH + e] = O.W[c * O.in + h_col(g, e)];
-                    for (int e = 0; e < C::ED; ++e) {
-                        const int f = d_col(g, e);
-                        block[C::B_WCD + (c * 2 + g) * C::ED + e] = f < C::DD ? O.W[c * O.in + C::W + f] : 0.0f;
-                    }
-                }
-            }
-            block[C::B_BC + c] = O.b[c];
-        }
+        for (int T = 0; T < C::NT; ++T)
+            for (int g = 0; g < 2; ++g)
+                for (int i = 0; i < 16; ++i)
+                    block[(T * 2 + g) * 16 + i] = bval(v, T, c_row(g, i));
     }
 };
 
@@ -288,13 +349,6 @@ __device__ __forceinline__ void load_lds16(const void *src_lane, unsigned char *
     __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src_lane,
                                      (__attribute__((address_space(3))) void *)lds_base, 16, 0, 0);
 }
-__device__ __forceinline__ void load_unit_async(const unsigned char *src, unsigned char *lds_unit, int lane)
-{
-    load_lds16(src + lane * 16, lds_unit);
-}
-
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // Round 8 floats to bf16 (nearest even) into one B chunk.
 __device__ __forceinline__ bf16x8 to_bf16x8(const float *f)
@@ -330,35 +384,49 @@ __device__ __forceinline__ void sincos_pi_pow2(float p, int l, float &s, float &
     c = __builtin_amdgcn_cosf(u);
 }
 
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+// vmcnt low bits [3:0] and high bits [15:14]; expcnt and lgkmcnt left at
+// their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup barrier without the memory fences of __syncthreads(): the waits
+// that make LDS data visible are explicit, so in-flight weight loads for
+// later stages are not drained at every stage.  The memory clobber keeps the
+// compiler from moving LDS accesses across it.
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
 template <class C>
 using Chunk = std::conditional_t<C::BF16, bf16x8, float>;
 
-// Number of A-fragment reads kept in flight ahead of the MFMA that uses them.
+// A-fragment reads kept in flight ahead of the MFMA that uses them.
 constexpr int kPrefetch = 3;
 
 template <class C>
-__global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
+__global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
     const unsigned *__restrict__ bucket, const unsigned *__restrict__ totals, int num_sites,
     RenderGeometry geo, const float *__restrict__ tbuf, const void *__restrict__ dirbuf,
     const unsigned char *__restrict__ streams, const float *__restrict__ blocks,
     float4 *__restrict__ sr)
 {
     using CT = Chunk<C>;
-    constexpr int NB = C::NB, E = C::E;
-    constexpr int EXC = C::EX / E, EHC = C::EH / E, EDC = C::ED / E;  // chunks
+    using AT = std::conditional_t<C::BF16, bf16x8, f32x4>;  // one LDS unit per lane
+    constexpr int NB = C::NB, NS = C::NS;
     extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
-    unsigned char *buf0 = lds;
-    unsigned char *buf1 = lds + C::SMAX * 1024;
-    float *hb = reinterpret_cast<float *>(lds + 2 * C::SMAX * 1024);
+    float *hb = reinterpret_cast<float *>(lds + C::HB_OFF);
     __shared__ unsigned s_off[kMaxSites + 1];   // bucket offset of each head
     __shared__ unsigned s_tile[kMaxSites + 1];  // first tile of each head
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    // wave-uniform by construction; saying so keeps LDS-destination pointers scalar
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int n = lane & 31, g = lane >> 5;
-    // this wave's staging of gamma(x) and gamma(d) (bf16 path): chunk c of
-    // column block nb at ((nb * chunks + c) * 64 + lane) * 16
-    unsigned char *gxl = lds + C::G_OFF + wave * C::G_WAVE_BYTES;
-    unsigned char *gdl = gxl + C::GX_UNITS * 1024;
+    // this wave's gamma(x) staging (read back by the skip layer)
+    unsigned char *gxl = lds + C::GX_OFF + wave * C::GX_WAVE_UNITS * 1024;
 
     if (tid == 0) {
         unsigned off = 0, tl = 0;
@@ -375,49 +443,69 @@ __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
     const unsigned total_tiles = s_tile[num_sites];
     // contiguous tile ranges per workgroup; workgroups are dealt round-robin
     // to the 8 XCDs, so map block b to range (b % 8) * G/8 + b / 8 and each
-    // XCD (with its own L2) walks one contiguous stretch of heads
+    // XCD walks one contiguous stretch of heads
     const unsigned G = gridDim.x;
     const unsigned lb = (G % 8 == 0) ? (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8 : blockIdx.x;
     const unsigned t_begin = (unsigned)(((unsigned long long)total_tiles * lb) / G);
     const unsigned t_end = (unsigned)(((unsigned long long)total_tiles * (lb + 1)) / G);
+    if (t_begin >= t_end)
+        return;
 
-    int head = 0, loaded_head = -1;
+    auto head_of = [&](unsigned tile, int h) {
+        while (s_tile[h + 1] <= tile)
+            ++h;
+        return __builtin_amdgcn_readfirstlane(h);
+    };
+    auto stream_of = [&](int h) { return streams + (size_t)h * C::STREAM_UNITS * 1024; };
+    auto slot = [&](unsigned k) { return lds + (k & (C::NBUF - 1)) * C::SLOT_BYTES; };
+    // issue this wave's share of stage s's units into ring slot k
+    auto issue = [&](auto sc, const unsigned char *src, unsigned k) {
+        constexpr int s = decltype(sc)::value;
+        constexpr int lpw = C::st_lpw(s), off = C::st_offset(s);
+        unsigned char *dst = slot(k);
+#pragma unroll
+        for (int q = 0; q < lpw; ++q) {
+            const int u = wave + q * C::WAVES;
+            load_lds16(src + (size_t)(off + u) * 1024 + lane * 16, dst + u * 1024);
+        }
+    };
+
+    int head = head_of(t_begin, 0);
+    const unsigned char *stream = stream_of(head);
+    unsigned ring = 0;  // ring slot of stage 0 of the current tile (mod NBUF)
+    static_for<0, (NS < 3 ? NS : 3)>([&](auto sc) { issue(sc, stream, ring + decltype(sc)::value); });
+    int loaded_head = -1;
+
     for (unsigned tile = t_begin; tile < t_end; ++tile) {
-        while (s_tile[head + 1] <= tile)
-            ++head;
-        // tile bookkeeping is uniform across the workgroup: keep it scalar
-        head = __builtin_amdgcn_readfirstlane(head);
+        const bool has_next = tile + 1 < t_end;
+        const int nhead = has_next ? head_of(tile + 1, head) : head;
+        const unsigned char *nstream = stream_of(nhead);
         const unsigned row0 = __builtin_amdgcn_readfirstlane(s_off[head] + (tile - s_tile[head]) * C::TILE);
         // rows never pass the sample count when the bucket counts are
         // consistent; the clamps keep every access in bounds regardless
         const unsigned row_end = __builtin_amdgcn_readfirstlane(min(s_off[head + 1], geo.num_samples));
-        if (row0 >= row_end)
-            continue;
-        const unsigned char *stream = streams + (size_t)head * C::STREAM_UNITS * 1024;
 
-        __syncthreads();  // previous tile is done with the buffers, the head block and staging
+        wg_barrier();  // previous tile is done with the head block and the staging
         if (head != loaded_head) {
             const unsigned char *src = reinterpret_cast<const unsigned char *>(blocks + (size_t)head * C::BLOCK_FLOATS);
             for (int u = wave; u < C::BLOCK_UNITS; u += C::WAVES)
-                load_unit_async(src + u * 1024, reinterpret_cast<unsigned char *>(hb) + u * 1024, lane);
+                load_lds16(src + u * 1024 + lane * 16, reinterpret_cast<unsigned char *>(hb) + u * 1024);
             loaded_head = head;
         }
-        for (int u = wave; u < C::st_units(0); u += C::WAVES)
-            load_unit_async(stream + (size_t)(C::st_offset(0) + u) * 1024, buf0 + u * 1024, lane);
 
-        // ---- gather the wave's samples and encode them ----------------------
-        CT gx[C::XLDS ? 1 : NB][EXC];
-        CT gd[C::XLDS ? 1 : NB][EDC];
-        unsigned sid[NB];
+        // ---- gather the wave's samples and encode them ------------------------
+        CT gx[NB][C::EXC];
+        unsigned sid[NB], ray[NB];
         bool valid[NB];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
             const unsigned row = row0 + (wave * NB + nb) * 32 + n;
             valid[nb] = row < row_end;
-            sid[nb] = min(bucket[valid[nb] ? row : row0], geo.num_samples - 1);
+            sid[nb] = min(bucket[min(valid[nb] ? row : row0, geo.num_samples - 1)], geo.num_samples - 1);
             unsigned r = (unsigned)((double)sid[nb] * geo.inv_n);
             if (sid[nb] - r * geo.n >= geo.n)
                 ++r;
+            ray[nb] = r;
             const float t = tbuf[sid[nb]];
             float x[3];
 #pragma unroll
@@ -434,237 +522,231 @@ __global__ __launch_bounds__(C::THREADS, 1) void mlp_kernel(
 #pragma unroll
             for (int e = 2 + 2 * C::P0; e < C::EX; ++e)
                 f[e] = 0.0f;
-            if constexpr (C::XLDS) {
+            if constexpr (C::BF16) {
 #pragma unroll
-                for (int ch = 0; ch < EXC; ++ch)
-                    *reinterpret_cast<bf16x8 *>(gxl + ((nb * EXC + ch) * 64 + lane) * 16) = to_bf16x8(f + 8 * ch);
-                // gamma(d) chunks f[8g..8g+7] and f[16+8g..16+8g+7] straight to LDS
-                const unsigned char *dp = reinterpret_cast<const unsigned char *>(dirbuf) + (size_t)r * (kDirPad * 2);
-                load_lds16(dp + g * 16, gdl + (nb * 2 + 0) * 1024);
-                load_lds16(dp + 32 + g * 16, gdl + (nb * 2 + 1) * 1024);
+                for (int ch = 0; ch < C::EXC; ++ch) {
+                    gx[nb][ch] = to_bf16x8(f + 8 * ch);
+                    *reinterpret_cast<bf16x8 *>(gxl + ((nb * C::EXC + ch) * 64 + lane) * 16) = gx[nb][ch];
+                }
             } else {
 #pragma unroll
                 for (int e = 0; e < C::EX; ++e)
                     gx[nb][e] = f[e];
-                const float4 *dp = reinterpret_cast<const float4 *>(dirbuf) + (size_t)r * (kDirPad / 4);
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const float4 a = dp[4 * h + 2 * g], b = dp[4 * h + 2 * g + 1];
-                    gd[nb][8 * h + 0] = a.x; gd[nb][8 * h + 1] = a.y;
-                    gd[nb][8 * h + 2] = a.z; gd[nb][8 * h + 3] = a.w;
-                    gd[nb][8 * h + 4] = b.x; gd[nb][8 * h + 5] = b.y;
-                    gd[nb][8 * h + 6] = b.z; gd[nb][8 * h + 7] = b.w;
+                for (int q = 0; q < C::EX / 4; ++q)
+                    *reinterpret_cast<f32x4 *>(gxl + ((nb * (C::EX / 4) + q) * 64 + lane) * 16) =
+                        f32x4{f[4 * q], f[4 * q + 1], f[4 * q + 2], f[4 * q + 3]};
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0);  // weight stages 0..2, head block, staging writes
+        wg_barrier();
+
+        CT hbuf[2][NB][C::EHC];                    // hidden outputs, by layer parity
+        CT gbuf[NB][C::ERHC > 0 ? C::ERHC : 1];    // colour hidden outputs
+        CT gxs[NB][C::EXC];                        // gamma(x) again, for the skip layer
+        CT gd[NB][C::EDC];                         // gamma(d)
+        f32x16 acc[2][NB];                         // by output-tile parity
+        AT fr[kPrefetch];
+
+        auto frag = [&](auto sc, int j) -> AT {
+            constexpr int s = decltype(sc)::value;
+            return *reinterpret_cast<const AT *>(slot(ring + s) + (j * 64 + lane) * 16);
+        };
+        auto load_bias = [&](auto tc) {
+            constexpr int T = decltype(tc)::value;
+            const float *b = hb + (T * 2 + g) * 16;
+            f32x16 v;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const f32x4 q = *reinterpret_cast<const f32x4 *>(b + 4 * j);
+                v[4 * j] = q[0]; v[4 * j + 1] = q[1]; v[4 * j + 2] = q[2]; v[4 * j + 3] = q[3];
+            }
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+                acc[T % 2][nb] = v;
+        };
+        // ReLU + conversion of output tile T into the next layer's input chunks
+        auto epilogue = [&](auto tc) {
+            constexpr int T = decltype(tc)::value;
+            constexpr int kind = C::t_kind(T), mt = C::t_mt(T), par = C::t_layer(T) % 2;
+            if constexpr (kind != K_OUT) {
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) {
+                    const f32x16 &a = acc[T % 2][nb];
+                    if constexpr (C::BF16) {
+                        if constexpr (kind == K_HID) {
+                            hbuf[par][nb][2 * mt] = relu_bf16(a, 0);
+                            hbuf[par][nb][2 * mt + 1] = relu_bf16(a, 1);
+                        } else {
+                            gbuf[nb][2 * mt] = relu_bf16(a, 0);
+                            gbuf[nb][2 * mt + 1] = relu_bf16(a, 1);
+                        }
+                    } else {
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            if constexpr (kind == K_HID)
+                                hbuf[par][nb][16 * mt + i] = fmaxf(a[i], 0.0f);
+                            else
+                                gbuf[nb][16 * mt + i] = fmaxf(a[i], 0.0f);
+                        }
+                    }
                 }
             }
-        }
+        };
 
-        CT act[NB][EHC];
-        CT nact[NB][EHC];
-        float sig[NB], rgb[3][NB];
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-            sig[nb] = 0.0f;
-            rgb[0][nb] = rgb[1][nb] = rgb[2][nb] = 0.0f;
-        }
+        // stage 0's bias and first fragments
+        constexpr int NF0 = C::st_units(0);
+        load_bias(ic<0>{});
+        static_for<0, (kPrefetch < NF0 ? kPrefetch : NF0)>([&](auto jc) {
+            fr[decltype(jc)::value] = frag(ic<0>{}, decltype(jc)::value);
+        });
 
-        // ---- stages -----------------------------------------------------------
-        static_for<0, C::NS>([&](auto sc) {
+        // ---- stages ------------------------------------------------------------
+        static_for<0, NS>([&](auto sc) {
             constexpr int s = decltype(sc)::value;
-            constexpr int kind = C::st_kind(s), layer = C::st_layer(s);
-            constexpr int tile0 = C::st_tile0(s), ntiles = C::st_ntiles(s);
-            constexpr int chunks = C::st_chunks(s);
-            constexpr int UPT = chunks / C::CPU;   // LDS units per output tile
-            constexpr int NF = ntiles * UPT;       // fragment reads of this stage
-            // chunks of this stage's input that come from gamma(x) / gamma(d)
-            constexpr bool uses_gx = kind == 0 && (layer == 0 || layer == C::SKIP);
-            constexpr bool uses_gd = kind == 1;
-            unsigned char *cur = (s % 2 == 0) ? buf0 : buf1;
-            unsigned char *nxt = (s % 2 == 0) ? buf1 : buf0;
+            constexpr int T = C::st_tile(s), kind = C::t_kind(T), layer = C::t_layer(T);
+            constexpr int c0 = C::st_c0(s), NF = C::st_units(s);
+            constexpr bool first = C::st_first(s);
+            constexpr bool next_first = s + 1 < NS ? C::st_first(s + 1) : false;
+            constexpr int next_tile = s + 1 < NS ? C::st_tile(s + 1) : 0;
+            constexpr int NF1 = s + 1 < NS ? C::st_units(s + 1) : 0;
+            constexpr int lpw2 = s + 2 < NS ? C::st_lpw(s + 2) : C::st_lpw(s + 2 - NS);
+            constexpr int gd_after = (C::S_GD == s - 1 || C::S_GD == s - 2) ? C::NGD : 0;
 
-            __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of stage s landed
-            __syncthreads();                // ... and everyone else's; stage s-1 is done
-            if constexpr (s + 1 < C::NS) {
-                for (int u = wave; u < C::st_units(s + 1); u += C::WAVES)
-                    load_unit_async(stream + (size_t)(C::st_offset(s + 1) + u) * 1024, nxt + u * 1024, lane);
+            if constexpr (s > 0) {
+                // stage s+1's units must have landed; stage s+2's (and gamma(d)
+                // loads issued after stage s+1's) may still be in flight
+                if constexpr (s + 2 < NS) {
+                    wait_vmcnt<lpw2 + gd_after>();
+                } else {
+                    if (has_next)
+                        wait_vmcnt<lpw2 + gd_after>();
+                    else
+                        wait_vmcnt<gd_after>();
+                }
+                wg_barrier();
             }
-
-            // A fragments of this stage, read kPrefetch ahead of their use
-            using AT = std::conditional_t<C::BF16, bf16x8, f32x4>;
-            auto frag = [&](int j) -> AT {
-                const int t = j % ntiles, u = j / ntiles;
-                return *reinterpret_cast<const AT *>(cur + ((t * UPT + u) * 64 + lane) * 16);
-            };
-            AT fr[kPrefetch];
-            static_for<0, (kPrefetch < NF ? kPrefetch : NF)>([&](auto ic0) {
-                constexpr int i = decltype(ic0)::value;
-                fr[i] = frag(i);
-            });
-
-            // staged encodings needed by this stage (bf16 path)
-            CT xin[NB][(C::XLDS && uses_gx) ? EXC : 1];
-            CT din[NB][(C::XLDS && uses_gd) ? 2 : 1];
-            if constexpr (C::XLDS && uses_gx) {
+            // weights three stages ahead, across the tile boundary
+            if constexpr (s + 3 < NS)
+                issue(ic<s + 3>{}, stream, ring + s + 3);
+            else if (has_next)
+                issue(ic<s + 3 - NS>{}, nstream, ring + s + 3);
+            if constexpr (s == C::S_GD) {
 #pragma unroll
-                for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-                    for (int ch = 0; ch < EXC; ++ch)
-                        xin[nb][ch] = *reinterpret_cast<const bf16x8 *>(gxl + ((nb * EXC + ch) * 64 + lane) * 16);
+                for (int nb = 0; nb < NB; ++nb) {
+                    const unsigned char *dp = reinterpret_cast<const unsigned char *>(dirbuf) +
+                                              (size_t)ray[nb] * (kDirPad * (C::BF16 ? 2 : 4));
+                    if constexpr (C::BF16) {
+                        gd[nb][0] = *reinterpret_cast<const bf16x8 *>(dp + g * 16);
+                        gd[nb][1] = *reinterpret_cast<const bf16x8 *>(dp + 32 + g * 16);
+                    } else {
+                        const f32x4 a0 = *reinterpret_cast<const f32x4 *>(dp + g * 32);
+                        const f32x4 a1 = *reinterpret_cast<const f32x4 *>(dp + g * 32 + 16);
+                        const f32x4 b0 = *reinterpret_cast<const f32x4 *>(dp + 64 + g * 32);
+                        const f32x4 b1 = *reinterpret_cast<const f32x4 *>(dp + 64 + g * 32 + 16);
+                        static_for<0, 4>([&](auto kc) {
+                            constexpr int k = decltype(kc)::value;
+                            gd[nb][k] = a0[k];
+                            gd[nb][4 + k] = a1[k];
+                            gd[nb][8 + k] = b0[k];
+                            gd[nb][12 + k] = b1[k];
+                        });
+                    }
+                }
             }
-            if constexpr (C::XLDS && uses_gd) {
+            if constexpr (s == C::S_SKIP) {
 #pragma unroll
-                for (int nb = 0; nb < NB; ++nb)
+                for (int nb = 0; nb < NB; ++nb) {
+                    if constexpr (C::BF16) {
 #pragma unroll
-                    for (int ch = 0; ch < 2; ++ch)
-                        din[nb][ch] = *reinterpret_cast<const bf16x8 *>(gdl + ((nb * 2 + ch) * 64 + lane) * 16);
+                        for (int ch = 0; ch < C::EXC; ++ch)
+                            gxs[nb][ch] = *reinterpret_cast<const bf16x8 *>(gxl + ((nb * C::EXC + ch) * 64 + lane) * 16);
+                    } else {
+#pragma unroll
+                        for (int q = 0; q < C::EX / 4; ++q) {
+                            const f32x4 v = *reinterpret_cast<const f32x4 *>(gxl + ((nb * (C::EX / 4) + q) * 64 + lane) * 16);
+                            gxs[nb][4 * q] = v[0];
+                            gxs[nb][4 * q + 1] = v[1];
+                            gxs[nb][4 * q + 2] = v[2];
+                            gxs[nb][4 * q + 3] = v[3];
+                        }
+                    }
+                }
             }
+            // the previous output tile's ReLU / rounding overlaps this stage's MFMAs
+            if constexpr (first && T > 0)
+                epilogue(ic<T - 1>{});
 
-            // B operand chunk c of this stage's input for column block nb
+            // B operand chunk c of this tile's input for column block nb
             auto in_chunk = [&](auto cc, int nb) -> CT {
                 constexpr int c = decltype(cc)::value;
-                if constexpr (kind == 1) {
-                    if constexpr (c < EHC) return act[nb][c];
-                    else if constexpr (C::XLDS) return din[nb][c - EHC];
-                    else return gd[nb][c - EHC];
-                } else if constexpr (layer == 0) {
-                    if constexpr (C::XLDS) return xin[nb][c];
-                    else return gx[nb][c];
-                } else if constexpr (layer == C::SKIP) {
-                    if constexpr (c < EXC) {
-                        if constexpr (C::XLDS) return xin[nb][c];
-                        else return gx[nb][c];
+                if constexpr (kind == K_HID) {
+                    if constexpr (layer == 0) {
+                        return gx[nb][c];
+                    } else if constexpr (layer == C::SKIP) {
+                        if constexpr (c < C::EXC) return gxs[nb][c];
+                        else return hbuf[(layer - 1) % 2][nb][c - C::EXC];
                     } else {
-                        return act[nb][c - EXC];
+                        return hbuf[(layer - 1) % 2][nb][c];
                     }
+                } else if constexpr (kind == K_RGBH) {
+                    if constexpr (c < C::EHC) return hbuf[(C::D - 1) % 2][nb][c];
+                    else return gd[nb][c - C::EHC];
                 } else {
-                    return act[nb][c];
+                    if constexpr (c < C::EHC) return hbuf[(C::D - 1) % 2][nb][c];
+                    else if constexpr (C::RH > 0) return gbuf[nb][c - C::EHC];
+                    else return gd[nb][c - C::EHC];
                 }
             };
-
-            f32x16 acc[C::TPS][NB];
-#pragma unroll
-            for (int t = 0; t < ntiles; ++t) {
-                const float *bsrc = (kind == 0)
-                    ? hb + C::B_HID + ((layer * C::MT + tile0 + t) * 2 + g) * 16
-                    : hb + C::B_RGBH + ((tile0 + t) * 2 + g) * 16;
-                f32x16 b;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const f32x4 v = *reinterpret_cast<const f32x4 *>(bsrc + 4 * j);
-                    b[4 * j] = v[0]; b[4 * j + 1] = v[1]; b[4 * j + 2] = v[2]; b[4 * j + 3] = v[3];
-                }
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb)
-                    acc[t][nb] = b;
-            }
 
             static_for<0, NF>([&](auto jc) {
                 constexpr int j = decltype(jc)::value;
-                constexpr int t = j % ntiles, u = j / ntiles;
                 const AT a = fr[j % kPrefetch];
                 if constexpr (j + kPrefetch < NF)
-                    fr[j % kPrefetch] = frag(j + kPrefetch);
+                    fr[j % kPrefetch] = frag(sc, j + kPrefetch);
                 if constexpr (C::BF16) {
 #pragma unroll
                     for (int nb = 0; nb < NB; ++nb)
-                        acc[t][nb] = mfma(a, in_chunk(ic<u>{}, nb), acc[t][nb]);
+                        acc[T % 2][nb] = mfma(a, in_chunk(ic<c0 + j>{}, nb), acc[T % 2][nb]);
                 } else {
-                    static_for<0, 4>([&](auto jj) {
-                        constexpr int q = decltype(jj)::value;
+                    static_for<0, 4>([&](auto qc) {
+                        constexpr int q = decltype(qc)::value;
 #pragma unroll
                         for (int nb = 0; nb < NB; ++nb)
-                            acc[t][nb] = mfma(a[q], in_chunk(ic<4 * u + q>{}, nb), acc[t][nb]);
+                            acc[T % 2][nb] = mfma(a[q], in_chunk(ic<c0 + 4 * j + q>{}, nb), acc[T % 2][nb]);
                     });
                 }
             });
 
-            // ---- epilogue -------------------------------------------------------
-#pragma unroll
-            for (int t = 0; t < ntiles; ++t) {
-                const int mt = tile0 + t;
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb) {
-                    if constexpr (kind == 0) {
-                        if constexpr (C::BF16) {
-                            nact[nb][2 * mt] = relu_bf16(acc[t][nb], 0);
-                            nact[nb][2 * mt + 1] = relu_bf16(acc[t][nb], 1);
-                        } else {
-#pragma unroll
-                            for (int i = 0; i < 16; ++i)
-                                nact[nb][16 * mt + i] = fmaxf(acc[t][nb][i], 0.0f);
-                        }
-                        if constexpr (layer == C::D - 1) {
-                            const float *ws = hb + C::B_WSIG + g * C::EH + 16 * mt;
-#pragma unroll
-                            for (int i = 0; i < 16; ++i)
-                                sig[nb] = fmaf(ws[i], fmaxf(acc[t][nb][i], 0.0f), sig[nb]);
-                            if constexpr (C::RH == 0) {
-#pragma unroll
-                                for (int c3 = 0; c3 < 3; ++c3) {
-                                    const float *wc = hb + C::B_WC + (c3 * 2 + g) * C::EH + 16 * mt;
-#pragma unroll
-                                    for (int i = 0; i < 16; ++i)
-                                        rgb[c3][nb] = fmaf(wc[i], fmaxf(acc[t][nb][i], 0.0f), rgb[c3][nb]);
-                                }
-                            }
-                        }
-                    } else {
-#pragma unroll
-                        for (int c3 = 0; c3 < 3; ++c3) {
-                            const float *wc = hb + C::B_WC + (c3 * 2 + g) * C::ERH + 16 * mt;
-#pragma unroll
-                            for (int i = 0; i < 16; ++i)
-                                rgb[c3][nb] = fmaf(wc[i], fmaxf(acc[t][nb][i], 0.0f), rgb[c3][nb]);
-                        }
-                    }
-                }
-            }
-            if constexpr (kind == 0 && tile0 + ntiles == C::MT) {
-                // layer complete: its output becomes the next input
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-                    for (int c = 0; c < EHC; ++c)
-                        act[nb][c] = nact[nb][c];
+            // prefetch for the next stage: its first fragments and, if it starts
+            // a new output tile, its bias (into the accumulator slot just freed)
+            if constexpr (s + 1 < NS) {
+                static_for<0, (kPrefetch < NF1 ? kPrefetch : NF1)>([&](auto jc) {
+                    fr[decltype(jc)::value] = frag(ic<s + 1>{}, decltype(jc)::value);
+                });
+                if constexpr (next_first)
+                    load_bias(ic<next_tile>{});
             }
         });
 
-        // ---- heads' outputs ----------------------------------------------------
-        if constexpr (C::RH == 0) {
-            // colour logits also read gamma(d) directly
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-                for (int c3 = 0; c3 < 3; ++c3) {
-                    const float *wd = hb + C::B_WCD + (c3 * 2 + g) * C::ED;
-#pragma unroll
-                    for (int e = 0; e < C::ED; ++e) {
-                        float dv;
-                        if constexpr (C::XLDS)
-                            dv = (float)reinterpret_cast<const __bf16 *>(gdl + ((nb * 2 + e / 8) * 64 + lane) * 16)[e % 8];
-                        else
-                            dv = gd[nb][e];
-                        rgb[c3][nb] = fmaf(wd[e], dv, rgb[c3][nb]);
-                    }
-                }
-        }
-        const float bsig = hb[C::B_BSIG];
-        const float bc0 = hb[C::B_BC], bc1 = hb[C::B_BC + 1], bc2 = hb[C::B_BC + 2];
+        // ---- density and colour: rows 0..3 of the output tile, lanes g = 0 ----
+        constexpr int TO = C::NT - 1;
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-            const float s_all = sig[nb] + __shfl_xor(sig[nb], 32) + bsig;
-            const float r0 = rgb[0][nb] + __shfl_xor(rgb[0][nb], 32) + bc0;
-            const float r1 = rgb[1][nb] + __shfl_xor(rgb[1][nb], 32) + bc1;
-            const float r2 = rgb[2][nb] + __shfl_xor(rgb[2][nb], 32) + bc2;
+            const f32x16 &a = acc[TO % 2][nb];
             if (g == 0 && valid[nb])
-                sr[sid[nb]] = make_float4(s_all > 0.0f ? s_all : 0.0f, sigmoid(r0), sigmoid(r1), sigmoid(r2));
+                sr[sid[nb]] = make_float4(fmaxf(a[0], 0.0f), sigmoid(a[1]), sigmoid(a[2]), sigmoid(a[3]));
         }
+        ring += NS;
+        head = nhead;
+        stream = nstream;
     }
 }
 
 template <class C>
 hipError_t launch_mlp(const unsigned *bucket, const unsigned *totals, int num_sites,
                       const RenderGeometry &g, const float *t, const void *dirbuf,
-                      const unsigned char *streams, const float *blocks, float4 *sr, int grid,
+                      const unsigned char *streams, const float *blocks, float4 *sr, int cus,
                       hipStream_t s)
 {
     static bool configured = false;
@@ -677,8 +759,8 @@ hipError_t launch_mlp(const unsigned *bucket, const unsigned *totals, int num_si
             (void)hipGetLastError();
         configured = true;
     }
-    mlp_kernel<C><<<grid, C::THREADS, C::LDS_BYTES, s>>>(bucket, totals, num_sites, g, t, dirbuf,
-                                                        streams, blocks, sr);
+    mlp_kernel<C><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(bucket, totals, num_sites, g, t,
+                                                                       dirbuf, streams, blocks, sr);
     return hipGetLastError();
 }
 

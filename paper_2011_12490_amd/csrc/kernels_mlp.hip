@@ -161,8 +161,8 @@ struct Cfg {
             s += t_splits(q);
         return s;
     }
-    // stage that first reads gamma(x) again (skip layer), stage that first
-    // reads gamma(d), and the stage that issues the gamma(d) loads
+    // first stage of the skip layer (gamma(x) is re-encoded one stage
+    // earlier), first stage reading gamma(d), stage issuing the gamma(d) loads
     static constexpr int S_SKIP = SKIP >= 0 ? first_stage_of_tile(SKIP * MT) : -1;
     static constexpr int S_GDUSE = first_stage_of_tile(RH > 0 ? D * MT : D * MT + MTR);
     static constexpr int S_GD = S_GDUSE >= 3 ? S_GDUSE - 3 : 0;
@@ -172,12 +172,10 @@ struct Cfg {
     static constexpr int BLOCK_FLOATS = (NT * 32 + 255) / 256 * 256;
     static constexpr int BLOCK_UNITS = BLOCK_FLOATS / 256;
 
-    // LDS: ring | head block | per-wave gamma(x) staging
+    // LDS: ring | head block
     static constexpr int SLOT_BYTES = UMAX * 1024;
     static constexpr int HB_OFF = NBUF * SLOT_BYTES;
-    static constexpr int GX_OFF = HB_OFF + BLOCK_FLOATS * 4;
-    static constexpr int GX_WAVE_UNITS = NB * EX * (BF16 ? 2 : 4) / 16;
-    static constexpr int LDS_BYTES = GX_OFF + WAVES * GX_WAVE_UNITS * 1024;
+    static constexpr int LDS_BYTES = HB_OFF + BLOCK_FLOATS * 4;
     static_assert(WG_PER_CU * (LDS_BYTES + 3 * 1024) <= 160 * 1024, "LDS budget");
 };
 
@@ -384,15 +382,49 @@ __device__ __forceinline__ void sincos_pi_pow2(float p, int l, float &s, float &
     c = __builtin_amdgcn_cosf(u);
 }
 
-// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
-// vmcnt low bits [3:0] and high bits [15:14]; expcnt and lgkmcnt left at
-// their maxima).
+// This lane group's gamma(x) entries (see x_col): the lowest level of the
+// group is evaluated directly, each higher level by the double-angle
+// identities sin 2a = 2 sin a cos a, cos 2a = 1 - 2 sin^2 a.  The rounding
+// error at most doubles per level (about 2^-19 after four doublings), far
+// below the tolerance of either precision.
+template <class C>
+__device__ __forceinline__ void encode_x(const float x[3], int g, float *f)
+{
+    constexpr int LV = C::P0 / 3;  // levels per lane group
+    f[0] = g ? x[2] : x[0];
+    f[1] = g ? 0.0f : x[1];
+    float s[3], c[3];
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+        sincos_pi_pow2(x[k], g * LV, s[k], c[k]);
+#pragma unroll
+    for (int lv = 0; lv < LV; ++lv) {
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+            f[2 + 2 * (3 * lv + k)] = s[k];
+            f[3 + 2 * (3 * lv + k)] = c[k];
+            if (lv + 1 < LV) {
+                const float t = s[k] * c[k];
+                c[k] = fmaf(-(s[k] + s[k]), s[k], 1.0f);
+                s[k] = t + t;
+            }
+        }
+    }
+#pragma unroll
+    for (int e = 2 + 2 * C::P0; e < C::EX; ++e)
+        f[e] = 0.0f;
+}
+
+// Wait until at most N vector-memory operations of this wave are in flight.
+// Written as asm with a memory clobber so that the compiler cannot move a
+// memory access across it (the count relies on the issue order).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt()
 {
     static_assert(N >= 0 && N < 64, "vmcnt");
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
+__device__ __forceinline__ void wait_all() { asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory"); }
 
 // Workgroup barrier without the memory fences of __syncthreads(): the waits
 // that make LDS data visible are explicit, so in-flight weight loads for
@@ -425,8 +457,6 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
     // wave-uniform by construction; saying so keeps LDS-destination pointers scalar
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int n = lane & 31, g = lane >> 5;
-    // this wave's gamma(x) staging (read back by the skip layer)
-    unsigned char *gxl = lds + C::GX_OFF + wave * C::GX_WAVE_UNITS * 1024;
 
     if (tid == 0) {
         unsigned off = 0, tl = 0;
@@ -495,6 +525,7 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
 
         // ---- gather the wave's samples and encode them ------------------------
         CT gx[NB][C::EXC];
+        float xs[NB][3];  // sample positions, kept to re-encode for the skip layer
         unsigned sid[NB], ray[NB];
         bool valid[NB];
 #pragma unroll
@@ -511,34 +542,22 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
 #pragma unroll
             for (int c = 0; c < 3; ++c)
                 x[c] = fmaf(t, geo.rays_d[3 * r + c], geo.rays_o[3 * r + c]);
+            xs[nb][0] = x[0];
+            xs[nb][1] = x[1];
+            xs[nb][2] = x[2];
             float f[C::EX];
-            f[0] = g ? x[2] : x[0];
-            f[1] = g ? 0.0f : x[1];
-#pragma unroll
-            for (int q = 0; q < C::P0; ++q) {
-                const int l = q / 3 + g * (C::P0 / 3);
-                sincos_pi_pow2(x[q % 3], l, f[2 + 2 * q], f[3 + 2 * q]);
-            }
-#pragma unroll
-            for (int e = 2 + 2 * C::P0; e < C::EX; ++e)
-                f[e] = 0.0f;
+            encode_x<C>(x, g, f);
             if constexpr (C::BF16) {
 #pragma unroll
-                for (int ch = 0; ch < C::EXC; ++ch) {
+                for (int ch = 0; ch < C::EXC; ++ch)
                     gx[nb][ch] = to_bf16x8(f + 8 * ch);
-                    *reinterpret_cast<bf16x8 *>(gxl + ((nb * C::EXC + ch) * 64 + lane) * 16) = gx[nb][ch];
-                }
             } else {
 #pragma unroll
                 for (int e = 0; e < C::EX; ++e)
                     gx[nb][e] = f[e];
-#pragma unroll
-                for (int q = 0; q < C::EX / 4; ++q)
-                    *reinterpret_cast<f32x4 *>(gxl + ((nb * (C::EX / 4) + q) * 64 + lane) * 16) =
-                        f32x4{f[4 * q], f[4 * q + 1], f[4 * q + 2], f[4 * q + 3]};
             }
         }
-        __builtin_amdgcn_s_waitcnt(0);  // weight stages 0..2, head block, staging writes
+        wait_all();  // weight stages 0..2 and the head block have landed
         wg_barrier();
 
         CT hbuf[2][NB][C::EHC];                    // hidden outputs, by layer parity
@@ -654,22 +673,20 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
                     }
                 }
             }
-            if constexpr (s == C::S_SKIP) {
+            if constexpr (s + 1 == C::S_SKIP) {
+                // gamma(x) again for the skip layer, overlapping this stage's MFMAs
 #pragma unroll
                 for (int nb = 0; nb < NB; ++nb) {
+                    float f[C::EX];
+                    encode_x<C>(xs[nb], g, f);
                     if constexpr (C::BF16) {
 #pragma unroll
                         for (int ch = 0; ch < C::EXC; ++ch)
-                            gxs[nb][ch] = *reinterpret_cast<const bf16x8 *>(gxl + ((nb * C::EXC + ch) * 64 + lane) * 16);
+                            gxs[nb][ch] = to_bf16x8(f + 8 * ch);
                     } else {
 #pragma unroll
-                        for (int q = 0; q < C::EX / 4; ++q) {
-                            const f32x4 v = *reinterpret_cast<const f32x4 *>(gxl + ((nb * (C::EX / 4) + q) * 64 + lane) * 16);
-                            gxs[nb][4 * q] = v[0];
-                            gxs[nb][4 * q + 1] = v[1];
-                            gxs[nb][4 * q + 2] = v[2];
-                            gxs[nb][4 * q + 3] = v[3];
-                        }
+                        for (int e = 0; e < C::EX; ++e)
+                            gxs[nb][e] = f[e];
                     }
                 }
             }

@@ -91,7 +91,9 @@ struct Cfg {
     static constexpr int EXC = EX / E, EHC = EH / E, EDC = ED / E, ERHC = ERH / E;
     static constexpr int UMAX = 8;             // units per stage
     static constexpr int CMAX = UMAX * CPU;    // chunks per stage
-    static constexpr int NBUF = 4;             // LDS ring slots
+    static constexpr int NBUF = 8;             // LDS ring slots (power of two)
+    static constexpr int G = 2;                // stages per barrier
+    static constexpr int LA = 6;               // weight loads issued this many stages ahead
     static constexpr int NT = D * MT + MTR + 1;
     static_assert(LP % 2 == 0, "pos_freqs must be even");
     static_assert(W % 64 == 0, "width");
@@ -165,8 +167,43 @@ struct Cfg {
     // earlier), first stage reading gamma(d), stage issuing the gamma(d) loads
     static constexpr int S_SKIP = SKIP >= 0 ? first_stage_of_tile(SKIP * MT) : -1;
     static constexpr int S_GDUSE = first_stage_of_tile(RH > 0 ? D * MT : D * MT + MTR);
-    static constexpr int S_GD = S_GDUSE >= 3 ? S_GDUSE - 3 : 0;
-    static constexpr int NGD = NB * (BF16 ? 2 : 4);  // gamma(d) loads per lane
+    static constexpr int S_GD = S_GDUSE >= 4 ? (S_GDUSE - 4) / G * G : 0;  // a group start
+    static constexpr int NGD = NB * (BF16 ? 2 : 4);  // gamma(d) load instructions per wave
+
+    // Barrier groups: stages [a, a + G) of a tile share one barrier.  At a
+    // group start a the wave issues the weight loads of stages a + LA ..
+    // (the next tile's stages past the end), then the gamma(d) loads if a ==
+    // S_GD.  Before the barrier of group a, the units of stage need(a) -- the
+    // first stage after the group, whose fragments are read at its end -- must
+    // have landed; vm_allowed(a) counts this wave's memory operations issued
+    // after those loads (every operation before them has landed too: they
+    // complete in issue order).  -1: nothing to wait for (the tile prologue
+    // drained everything issued before stage LA's loads).
+    static_assert(NS >= LA + G, "pipeline deeper than the stage list");
+    static_assert(NBUF >= LA + G, "ring too small for the lookahead");
+    static constexpr int grp_end(int a) { return a + G - 1 < NS ? a + G - 1 : NS - 1; }
+    static constexpr int need(int a) { return grp_end(a) + 1 < NS ? grp_end(a) + 1 : grp_end(a); }
+    static constexpr int vm_allowed(int a, bool has_next)
+    {
+        const int xn = need(a);
+        if (xn < LA)
+            return -1;
+        const int gn = (xn - LA) / G * G;
+        int cnt = 0;
+        for (int g = gn; g < a; g += G) {
+            for (int x = g + LA; x <= grp_end(g) + LA; ++x) {
+                if (g == gn && x <= xn)
+                    continue;
+                if (x < NS)
+                    cnt += st_lpw(x);
+                else if (has_next)
+                    cnt += st_lpw(x - NS);
+            }
+            if (g == S_GD)
+                cnt += NGD;
+        }
+        return cnt;
+    }
 
     // per-head resident block: bias of every output tile in accumulator layout
     static constexpr int BLOCK_FLOATS = (NT * 32 + 255) / 256 * 256;
@@ -498,12 +535,14 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
             const int u = wave + q * C::WAVES;
             load_lds16(src + (size_t)(off + u) * 1024 + lane * 16, dst + u * 1024);
         }
+        // keep the issue order the wait counts assume
+        asm volatile("" ::: "memory");
     };
 
     int head = head_of(t_begin, 0);
     const unsigned char *stream = stream_of(head);
     unsigned ring = 0;  // ring slot of stage 0 of the current tile (mod NBUF)
-    static_for<0, (NS < 3 ? NS : 3)>([&](auto sc) { issue(sc, stream, ring + decltype(sc)::value); });
+    static_for<0, C::LA>([&](auto sc) { issue(sc, stream, ring + decltype(sc)::value); });
     int loaded_head = -1;
 
     for (unsigned tile = t_begin; tile < t_end; ++tile) {
@@ -629,27 +668,30 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
             constexpr bool next_first = s + 1 < NS ? C::st_first(s + 1) : false;
             constexpr int next_tile = s + 1 < NS ? C::st_tile(s + 1) : 0;
             constexpr int NF1 = s + 1 < NS ? C::st_units(s + 1) : 0;
-            constexpr int lpw2 = s + 2 < NS ? C::st_lpw(s + 2) : C::st_lpw(s + 2 - NS);
-            constexpr int gd_after = (C::S_GD == s - 1 || C::S_GD == s - 2) ? C::NGD : 0;
 
-            if constexpr (s > 0) {
-                // stage s+1's units must have landed; stage s+2's (and gamma(d)
-                // loads issued after stage s+1's) may still be in flight
-                if constexpr (s + 2 < NS) {
-                    wait_vmcnt<lpw2 + gd_after>();
-                } else {
-                    if (has_next)
-                        wait_vmcnt<lpw2 + gd_after>();
-                    else
-                        wait_vmcnt<gd_after>();
+            if constexpr (s % C::G == 0) {
+                // group start: wait for the units the group needs, then one barrier
+                constexpr int wa = C::vm_allowed(s, true), wb = C::vm_allowed(s, false);
+                if constexpr (s > 0) {
+                    if constexpr (wa >= 0 && wa == wb) {
+                        wait_vmcnt<wa>();
+                    } else if constexpr (wa >= 0) {
+                        if (has_next)
+                            wait_vmcnt<wa>();
+                        else
+                            wait_vmcnt<(wb >= 0 ? wb : 0)>();
+                    }
+                    wg_barrier();
                 }
-                wg_barrier();
+                // weights LA stages ahead (the next tile's past the end)
+                static_for<s + C::LA, C::grp_end(s) + C::LA + 1>([&](auto xc) {
+                    constexpr int x = decltype(xc)::value;
+                    if constexpr (x < NS)
+                        issue(ic<x>{}, stream, ring + x);
+                    else if (has_next)
+                        issue(ic<x - NS>{}, nstream, ring + x);
+                });
             }
-            // weights three stages ahead, across the tile boundary
-            if constexpr (s + 3 < NS)
-                issue(ic<s + 3>{}, stream, ring + s + 3);
-            else if (has_next)
-                issue(ic<s + 3 - NS>{}, nstream, ring + s + 3);
             if constexpr (s == C::S_GD) {
 #pragma unroll
                 for (int nb = 0; nb < NB; ++nb) {

@@ -120,41 +120,58 @@ struct Cfg {
         return n;
     }
     static constexpr int NS = count_stages();
-    static constexpr int st_tile(int s)
+
+    // per-stage table, built once at compile time
+    struct StageTab {
+        int tile[NS], split[NS], c0[NS], c1[NS], units[NS], lpw[NS], off[NS + 1], foff[NS + 1];
+    };
+    static constexpr StageTab make_tab()
     {
-        for (int T = 0; T < NT; ++T) {
-            if (s < t_splits(T))
-                return T;
-            s -= t_splits(T);
+        StageTab t{};
+        int s = 0;
+        for (int T = 0; T < NT; ++T)
+            for (int k = 0; k < t_splits(T); ++k, ++s) {
+                t.tile[s] = T;
+                t.split[s] = k;
+                t.c0[s] = k * CMAX;
+                t.c1[s] = (k + 1) * CMAX < t_chunks(T) ? (k + 1) * CMAX : t_chunks(T);
+                t.units[s] = (t.c1[s] - t.c0[s]) / CPU;
+                t.lpw[s] = (t.units[s] + WAVES - 1) / WAVES;
+            }
+        t.off[0] = 0;
+        t.foff[0] = 0;
+        for (int q = 0; q < NS; ++q) {
+            t.off[q + 1] = t.off[q] + t.lpw[q] * WAVES;
+            t.foff[q + 1] = t.foff[q] + t.units[q];
         }
-        return -1;
+        return t;
     }
-    static constexpr int st_split(int s)
+    static constexpr StageTab TAB = make_tab();
+
+    static constexpr int st_tile(int s) { return TAB.tile[s]; }
+    static constexpr int st_split(int s) { return TAB.split[s]; }
+    static constexpr int st_c0(int s) { return TAB.c0[s]; }
+    static constexpr int st_c1(int s) { return TAB.c1[s]; }
+    static constexpr bool st_first(int s) { return TAB.split[s] == 0; }
+    static constexpr int st_units(int s) { return TAB.units[s]; }
+    static constexpr int st_lpw(int s) { return TAB.lpw[s]; }  // loads per wave
+    static constexpr int st_units_pad(int s) { return TAB.lpw[s] * WAVES; }
+    static constexpr int st_offset(int s) { return TAB.off[s]; }  // in units
+    static constexpr int STREAM_UNITS = TAB.off[NS];
+
+    // A fragments of a tile's stages, numbered consecutively: stage s's
+    // fragment j is number foff(s) + j.  The register window holds fragment
+    // F in slot F % kPrefetch.
+    static constexpr int foff(int s) { return TAB.foff[s]; }
+    static constexpr int FTOTAL = TAB.foff[NS];
+    static constexpr int f_stage(int F)
     {
-        for (int T = 0; T < NT; ++T) {
-            if (s < t_splits(T))
-                return s;
-            s -= t_splits(T);
-        }
-        return -1;
+        int q = 0;
+        while (q + 1 < NS && TAB.foff[q + 1] <= F)
+            ++q;
+        return q;
     }
-    static constexpr int st_c0(int s) { return st_split(s) * CMAX; }
-    static constexpr int st_c1(int s)
-    {
-        return (st_split(s) + 1) * CMAX < t_chunks(st_tile(s)) ? (st_split(s) + 1) * CMAX : t_chunks(st_tile(s));
-    }
-    static constexpr bool st_first(int s) { return st_split(s) == 0; }
-    static constexpr int st_units(int s) { return (st_c1(s) - st_c0(s)) / CPU; }
-    static constexpr int st_lpw(int s) { return (st_units(s) + WAVES - 1) / WAVES; }  // loads per wave
-    static constexpr int st_units_pad(int s) { return st_lpw(s) * WAVES; }
-    static constexpr int st_offset(int s)  // in units
-    {
-        int o = 0;
-        for (int q = 0; q < s; ++q)
-            o += st_units_pad(q);
-        return o;
-    }
-    static constexpr int STREAM_UNITS = st_offset(NS);
+    static constexpr int f_index(int F) { return F - TAB.foff[f_stage(F)]; }
 
     static constexpr int first_stage_of_tile(int T)
     {
@@ -623,40 +640,40 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
             for (int nb = 0; nb < NB; ++nb)
                 acc[T % 2][nb] = v;
         };
-        // ReLU + conversion of output tile T into the next layer's input chunks
-        auto epilogue = [&](auto tc) {
-            constexpr int T = decltype(tc)::value;
+        // ReLU + conversion of output tile T into the next layer's input chunks,
+        // in pieces so that it can be spread over the next tile's MFMAs:
+        // bf16 piece p converts half p / NB of column block p % NB, fp32 piece
+        // p a quarter of it
+        auto epilogue_piece = [&](auto tc, auto pc) {
+            constexpr int T = decltype(tc)::value, p = decltype(pc)::value;
             constexpr int kind = C::t_kind(T), mt = C::t_mt(T), par = C::t_layer(T) % 2;
+            constexpr int nb = p % NB, h = p / NB;
+            const f32x16 &a = acc[T % 2][nb];
             if constexpr (kind != K_OUT) {
+                if constexpr (C::BF16) {
+                    if constexpr (kind == K_HID)
+                        hbuf[par][nb][2 * mt + h] = relu_bf16(a, h);
+                    else
+                        gbuf[nb][2 * mt + h] = relu_bf16(a, h);
+                } else {
 #pragma unroll
-                for (int nb = 0; nb < NB; ++nb) {
-                    const f32x16 &a = acc[T % 2][nb];
-                    if constexpr (C::BF16) {
-                        if constexpr (kind == K_HID) {
-                            hbuf[par][nb][2 * mt] = relu_bf16(a, 0);
-                            hbuf[par][nb][2 * mt + 1] = relu_bf16(a, 1);
-                        } else {
-                            gbuf[nb][2 * mt] = relu_bf16(a, 0);
-                            gbuf[nb][2 * mt + 1] = relu_bf16(a, 1);
-                        }
-                    } else {
-#pragma unroll
-                        for (int i = 0; i < 16; ++i) {
-                            if constexpr (kind == K_HID)
-                                hbuf[par][nb][16 * mt + i] = fmaxf(a[i], 0.0f);
-                            else
-                                gbuf[nb][16 * mt + i] = fmaxf(a[i], 0.0f);
-                        }
+                    for (int i = 4 * h; i < 4 * h + 4; ++i) {
+                        if constexpr (kind == K_HID)
+                            hbuf[par][nb][16 * mt + i] = fmaxf(a[i], 0.0f);
+                        else
+                            gbuf[nb][16 * mt + i] = fmaxf(a[i], 0.0f);
                     }
                 }
             }
         };
+        constexpr int NPIECE = C::BF16 ? 2 * NB : 4 * NB;
 
-        // stage 0's bias and first fragments
-        constexpr int NF0 = C::st_units(0);
+        // stage 0's bias and the first fragments of the window
         load_bias(ic<0>{});
-        static_for<0, (kPrefetch < NF0 ? kPrefetch : NF0)>([&](auto jc) {
-            fr[decltype(jc)::value] = frag(ic<0>{}, decltype(jc)::value);
+        static_for<0, (kPrefetch < C::FTOTAL ? kPrefetch : C::FTOTAL)>([&](auto fc) {
+            constexpr int F = decltype(fc)::value;
+            constexpr int fs = C::f_stage(F), fi = C::f_index(F);
+            fr[F % kPrefetch] = frag(ic<fs>{}, fi);
         });
 
         // ---- stages ------------------------------------------------------------
@@ -667,7 +684,6 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
             constexpr bool first = C::st_first(s);
             constexpr bool next_first = s + 1 < NS ? C::st_first(s + 1) : false;
             constexpr int next_tile = s + 1 < NS ? C::st_tile(s + 1) : 0;
-            constexpr int NF1 = s + 1 < NS ? C::st_units(s + 1) : 0;
 
             if constexpr (s % C::G == 0) {
                 // group start: wait for the units the group needs, then one barrier
@@ -732,9 +748,6 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
                     }
                 }
             }
-            // the previous output tile's ReLU / rounding overlaps this stage's MFMAs
-            if constexpr (first && T > 0)
-                epilogue(ic<T - 1>{});
 
             // B operand chunk c of this tile's input for column block nb
             auto in_chunk = [&](auto cc, int nb) -> CT {
@@ -758,11 +771,33 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
                 }
             };
 
+            // Schedule of one step j: a piece of the previous tile's epilogue
+            // (first stage of a tile), the read of the fragment kPrefetch
+            // ahead (possibly the next stage's), the next tile's bias (late in
+            // its last stage), then this step's MFMAs; sched_barrier keeps the
+            // order, so LDS latency hides behind the MFMAs in between.
+            constexpr bool EPI = first && T > 0;
+            constexpr int ESTEPS = EPI ? (NF < NPIECE ? NF : NPIECE) : 0;
+            constexpr int JB0 = NF >= 2 ? NF - 2 : 0;
+            constexpr int JB = next_first ? (JB0 > ESTEPS ? JB0 : ESTEPS) : NF;  // bias step
             static_for<0, NF>([&](auto jc) {
                 constexpr int j = decltype(jc)::value;
-                const AT a = fr[j % kPrefetch];
-                if constexpr (j + kPrefetch < NF)
-                    fr[j % kPrefetch] = frag(sc, j + kPrefetch);
+                constexpr int F = C::foff(s) + j;
+                if constexpr (EPI && j < ESTEPS) {
+                    // pieces p with p * ESTEPS / NPIECE == j
+                    static_for<0, NPIECE>([&](auto pc) {
+                        constexpr int pp = decltype(pc)::value;
+                        if constexpr (pp * ESTEPS / NPIECE == j)
+                            epilogue_piece(ic<T - 1>{}, pc);
+                    });
+                }
+                const AT a = fr[F % kPrefetch];
+                if constexpr (F + kPrefetch < C::FTOTAL) {
+                    constexpr int fs = C::f_stage(F + kPrefetch), fi = C::f_index(F + kPrefetch);
+                    fr[F % kPrefetch] = frag(ic<fs>{}, fi);
+                }
+                if constexpr (j == JB && next_first)
+                    load_bias(ic<next_tile>{});
                 if constexpr (C::BF16) {
 #pragma unroll
                     for (int nb = 0; nb < NB; ++nb)
@@ -775,17 +810,10 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
                             acc[T % 2][nb] = mfma(a[q], in_chunk(ic<c0 + 4 * j + q>{}, nb), acc[T % 2][nb]);
                     });
                 }
+                __builtin_amdgcn_sched_barrier(0);
             });
-
-            // prefetch for the next stage: its first fragments and, if it starts
-            // a new output tile, its bias (into the accumulator slot just freed)
-            if constexpr (s + 1 < NS) {
-                static_for<0, (kPrefetch < NF1 ? kPrefetch : NF1)>([&](auto jc) {
-                    fr[decltype(jc)::value] = frag(ic<s + 1>{}, decltype(jc)::value);
-                });
-                if constexpr (next_first)
-                    load_bias(ic<next_tile>{});
-            }
+            if constexpr (JB >= NF && next_first)
+                load_bias(ic<next_tile>{});
         });
 
         // ---- density and colour: rows 0..3 of the output tile, lanes g = 0 ----

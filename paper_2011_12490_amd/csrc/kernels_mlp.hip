@@ -394,12 +394,20 @@ __device__ __forceinline__ f32x16 mfma(float a, float b, const f32x16 &c)
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
 }
 
-// One wave copies 64 x 16 bytes global -> LDS: lane l reads src_lane and the
-// data lands at lds_base + 16 l (lds_base must be the same for the wave).
-__device__ __forceinline__ void load_lds16(const void *src_lane, unsigned char *lds_base)
+// One wave copies 64 x 16 bytes global -> LDS: lane l reads base + voff and
+// the data lands at lds_base + 16 l (base and lds_base are wave-uniform).
+// Issued as asm so that the compiler does not track it: its completion is
+// awaited explicitly with vmcnt (where it is counted), and the compiler's own
+// LDS wait bookkeeping stays exact for the ds_reads around it (it would
+// otherwise wait for every outstanding LDS read whenever one of these is in
+// flight).  M0 carries the LDS address; nothing else in these kernels uses M0.
+__device__ __forceinline__ void load_lds16(const unsigned char *base, unsigned voff,
+                                           unsigned char *lds_base)
 {
-    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src_lane,
-                                     (__attribute__((address_space(3))) void *)lds_base, 16, 0, 0);
+    const unsigned l = (unsigned)(unsigned long)(__attribute__((address_space(3))) unsigned char *)lds_base;
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :: "s"(__builtin_amdgcn_readfirstlane(l)), "v"(voff), "s"(base)
+                 : "memory");
 }
 
 // Round 8 floats to bf16 (nearest even) into one B chunk.
@@ -550,7 +558,7 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
 #pragma unroll
         for (int q = 0; q < lpw; ++q) {
             const int u = wave + q * C::WAVES;
-            load_lds16(src + (size_t)(off + u) * 1024 + lane * 16, dst + u * 1024);
+            load_lds16(src + (size_t)(off + u) * 1024, lane * 16, dst + u * 1024);
         }
         // keep the issue order the wait counts assume
         asm volatile("" ::: "memory");
@@ -575,7 +583,7 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
         if (head != loaded_head) {
             const unsigned char *src = reinterpret_cast<const unsigned char *>(blocks + (size_t)head * C::BLOCK_FLOATS);
             for (int u = wave; u < C::BLOCK_UNITS; u += C::WAVES)
-                load_lds16(src + u * 1024 + lane * 16, reinterpret_cast<unsigned char *>(hb) + u * 1024);
+                load_lds16(src + u * 1024, lane * 16, reinterpret_cast<unsigned char *>(hb) + u * 1024);
             loaded_head = head;
         }
 

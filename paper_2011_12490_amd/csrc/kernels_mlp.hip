@@ -548,18 +548,25 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
             ++h;
         return __builtin_amdgcn_readfirstlane(h);
     };
-    auto stream_of = [&](int h) { return streams + (size_t)h * C::STREAM_UNITS * 1024; };
+    // This wave's first unit of head h's stream.  The base is made opaque so
+    // that each unit's address is formed from it with a compile-time offset,
+    // instead of the compiler hoisting one wave-dependent offset per unit out
+    // of the tile loop (more scalar registers than there are).
+    auto stream_of = [&](int h) {
+        const unsigned char *p = streams + ((size_t)h * C::STREAM_UNITS + wave) * 1024;
+        asm volatile("" : "+s"(p));
+        return p;
+    };
     auto slot = [&](unsigned k) { return lds + (k & (C::NBUF - 1)) * C::SLOT_BYTES; };
+    unsigned char *const lds_wave = lds + wave * 1024;
     // issue this wave's share of stage s's units into ring slot k
     auto issue = [&](auto sc, const unsigned char *src, unsigned k) {
         constexpr int s = decltype(sc)::value;
         constexpr int lpw = C::st_lpw(s), off = C::st_offset(s);
-        unsigned char *dst = slot(k);
+        unsigned char *dst = lds_wave + (k & (C::NBUF - 1)) * C::SLOT_BYTES;
 #pragma unroll
-        for (int q = 0; q < lpw; ++q) {
-            const int u = wave + q * C::WAVES;
-            load_lds16(src + (size_t)(off + u) * 1024, lane * 16, dst + u * 1024);
-        }
+        for (int q = 0; q < lpw; ++q)
+            load_lds16(src + (size_t)(off + q * C::WAVES) * 1024, lane * 16, dst + q * C::WAVES * 1024);
         // keep the issue order the wait counts assume
         asm volatile("" ::: "memory");
     };

@@ -86,6 +86,9 @@ def _lib_handle():
                                              ctypes.c_int, ctypes.c_uint64, ctypes.c_int, _P, _P,
                                              _P, ctypes.c_int]
         lib.oracle_sample_assign.restype = ctypes.c_int
+        lib.oracle_assign_depths.argtypes = [ctypes.c_int, _P, ctypes.c_longlong, _P, _P,
+                                             ctypes.c_int, _P, _P, _P, ctypes.c_int]
+        lib.oracle_assign_depths.restype = ctypes.c_int
         lib.oracle_max_threads.argtypes = []
         lib.oracle_max_threads.restype = ctypes.c_int
         _lib = lib
@@ -208,6 +211,25 @@ def sample_assign(sites, rays_o, rays_d, near: float, far: float, n: int, seed: 
     if rc != 0:
         raise RuntimeError("oracle sample_assign failed (%d)" % rc)
     return t, cell, m
+
+
+def assign_depths(sites, rays_o, rays_d, t, margin: bool = False, nthreads: int = 0):
+    """Owning cells [R, n] of the given sample depths t [R, n] (and optionally
+    each sample's distance to its cell boundary)."""
+    sites = np.ascontiguousarray(sites, np.float32).reshape(-1, 3)
+    o = np.ascontiguousarray(rays_o, np.float32).reshape(-1, 3)
+    d = np.ascontiguousarray(rays_d, np.float32).reshape(-1, 3)
+    t = np.ascontiguousarray(t, np.float32)
+    R, n = t.shape
+    if o.shape[0] != R or d.shape[0] != R:
+        raise ValueError("rays and depths disagree on the ray count")
+    cell = np.zeros((R, n), np.int32)
+    m = np.zeros((R, n), np.float64) if margin else None
+    rc = _lib_handle().oracle_assign_depths(sites.shape[0], _ptr(sites), R, _ptr(o), _ptr(d), n,
+                                            _ptr(t), _ptr(cell), _ptr(m), nthreads)
+    if rc != 0:
+        raise RuntimeError("oracle assign_depths failed (%d)" % rc)
+    return cell, m
 
 
 class RenderResult:

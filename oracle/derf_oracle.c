@@ -722,6 +722,37 @@ int oracle_sample_assign(int K, const float *sites, long long R, const float *ra
     return 0;
 }
 
+/* Owning cells of given sample depths t [R][n] (Sec. 3.3 nearest site, at
+ * x = o + t d in float32 with one fma per component): the check of the
+ * assignment of samples whose depths come from elsewhere, such as the
+ * inverse-CDF draws of hierarchical sampling.  margin as above. */
+int oracle_assign_depths(int K, const float *sites, long long R, const float *rays_o,
+                         const float *rays_d, int n, const float *t, int *cell_out,
+                         double *margin_out, int nthreads)
+{
+    if (n < 1 || R < 0 || K < 1)
+        return -1;
+#ifdef _OPENMP
+    if (nthreads > 0)
+        omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+#pragma omp parallel for schedule(static)
+    for (long long r = 0; r < R; ++r) {
+        for (int i = 0; i < n; ++i) {
+            float x[3];
+            sample_point(rays_o + 3 * r, rays_d + 3 * r, t[(size_t)r * n + i], x);
+            int c = oracle_nearest_site(K, sites, x);
+            cell_out[(size_t)r * n + i] = c;
+            if (margin_out)
+                margin_out[(size_t)r * n + i] =
+                    K > 1 ? oracle_bisector_margin(K, sites, x, c) : INFINITY;
+        }
+    }
+    return 0;
+}
+
 /* Composite given per-sample fields (pins of the quadrature and of the
  * Painter's merge on hand-made inputs).  mode: 0 segments, 3 direct, 4 back. */
 void oracle_composite(int mode, int n, const int *cell, const float *t, const double *sigma,

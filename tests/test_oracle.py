@@ -117,6 +117,27 @@ def test_nearest_site_matches_kdtree_away_from_bisectors():
         assert n_close < 5
 
 
+def test_assign_depths_matches_brute_force_and_sample_assign():
+    rng = np.random.default_rng(11)
+    K, R, n = 16, 64, 40
+    sites = rng.uniform(-1, 1, size=(K, 3)).astype(np.float32)
+    o = rng.uniform(-0.5, 0.5, size=(R, 3)).astype(np.float32)
+    d = rng.standard_normal((R, 3)).astype(np.float32)
+    # arbitrary (unsorted) depths: float64 brute force away from bisectors
+    t = rng.uniform(0.0, 2.0, size=(R, n)).astype(np.float32)
+    cell, m = oracle.assign_depths(sites, o, d, t, margin=True)
+    x = o[:, None, :].astype(np.float64) + t[..., None].astype(np.float64) * d[:, None, :]
+    d2 = ((x[:, :, None, :] - sites[None, None].astype(np.float64)) ** 2).sum(-1)
+    ref = d2.argmin(-1)
+    far = m >= 1e-5
+    assert far.mean() > 0.99
+    np.testing.assert_array_equal(cell[far], ref[far])
+    # on stratified depths it reproduces the sampling pass's cells exactly
+    ts, cs, _ = oracle.sample_assign(sites, o, d, 0.0, 2.0, n, seed=5, ray_offset=7)
+    c2, _ = oracle.assign_depths(sites, o, d, ts)
+    np.testing.assert_array_equal(c2, cs)
+
+
 def test_nearest_site_ties_go_to_lowest_index():
     sites = np.array([[1, 0, 0], [-1, 0, 0], [1, 0, 0]], np.float32)
     assert oracle.nearest_site(sites, [0, 0, 0]) == 0
@@ -456,6 +477,32 @@ def test_fine_depths_concentrate_on_one_interval():
         inside = np.sum((tf >= lo - 1e-6) & (tf <= hi + 1e-6))
         assert inside >= nf - 1
         assert np.all(np.diff(tf) >= 0)
+
+
+def test_fine_depths_follow_the_piecewise_constant_pdf():
+    """Pooled over many rays, inverse-CDF draws follow the piecewise-uniform
+    density that puts mass (w_i + 1e-5) / sum on the i-th quadrature interval."""
+    rng = np.random.default_rng(8)
+    nc, nf, near, far = 16, 64, 2.0, 6.0
+    tc = oracle.sample_depths(4, 0, near, far, nc, True)
+    w = rng.exponential(size=nc) * (rng.uniform(size=nc) < 0.5)
+    b = np.concatenate([[near], 0.5 * (tc[:-1].astype(np.float64) + tc[1:]), [far]])
+    p = (w + 1e-5) / (w + 1e-5).sum()
+    F = np.concatenate([[0.0], np.cumsum(p)])
+
+    def cdf(x):
+        i = np.clip(np.searchsorted(b, x, side="right") - 1, 0, nc - 1)
+        return F[i] + (x - b[i]) / (b[i + 1] - b[i]) * p[i]
+
+    pooled = np.concatenate([oracle.fine_depths(4, ray, True, tc, near, far, w, nf)
+                             for ray in range(300)])
+    assert stats.kstest(pooled, cdf).pvalue > 1e-3
+    # an interval index off by one moves mass between neighbours: the
+    # per-interval counts follow p within a few standard deviations
+    counts = np.bincount(np.clip(np.searchsorted(b, pooled, side="right") - 1, 0, nc - 1),
+                         minlength=nc)
+    expect = p * pooled.size
+    assert np.all(np.abs(counts - expect) <= 5 * np.sqrt(expect) + 2)
 
 
 def test_hierarchical_render_merges_sorted_lists():

@@ -38,12 +38,13 @@ def workload_text(cfg, precision):
     a = cfg.arch
     rgb = ("%d->%d->3" % (a.width + a.dir_dim, a.rgb_hidden)) if a.rgb_hidden else (
         "%d->3" % (a.width + a.dir_dim))
-    return ("%s: %dx%d %s rays, %d stratified samples/ray on [%g,%g], K=%d Voronoi heads of "
+    fine = (" + %d inverse-CDF fine (coarse outputs reused)" % cfg.n_fine) if cfg.n_fine else ""
+    return ("%s: %dx%d %s rays, %d stratified%s samples/ray on [%g,%g], K=%d Voronoi heads of "
             "%dx%d (posenc L=%d, skip@%d, rgb %s), %s"
             % (cfg.name, cfg.width, cfg.height,
                "forward-facing NDC" if cfg.camera == "forward" else "object-centric",
-               cfg.n_coarse, cfg.near, cfg.far, cfg.num_sites, a.depth, a.width, a.pos_freqs,
-               a.skip_layer, rgb, precision))
+               cfg.n_coarse, fine, cfg.near, cfg.far, cfg.num_sites, a.depth, a.width,
+               a.pos_freqs, a.skip_layer, rgb, precision))
 
 
 def measured_traffic():
@@ -71,12 +72,12 @@ def cpu_baseline(sc, n_rays, nthreads):
     ids = scenes.ray_subset(n_rays, cfg.num_rays)
     t0 = time.perf_counter()
     oracle.render(sc.sites, cfg.arch, sc.weights, sc.rays_o[ids], sc.rays_d[ids], cfg.near,
-                  cfg.far, cfg.n_coarse, 0, seed=scenes.SEED_RENDER, ray_ids=ids,
+                  cfg.far, cfg.n_coarse, cfg.n_fine, seed=scenes.SEED_RENDER, ray_ids=ids,
                   nthreads=nthreads)
     dt = time.perf_counter() - t0
     return {"value": len(ids) / dt, "unit": "rays/s", "cores": nthreads, "kind": "oracle",
-            "sample": "%d seeded rays of the same frame (%d samples, fp64 heads), %.1f s"
-                      % (len(ids), len(ids) * cfg.n_coarse, dt)}
+            "sample": "%d seeded rays of the same frame (%d head evaluations, fp64 heads), %.1f s"
+                      % (len(ids), len(ids) * (cfg.n_coarse + cfg.n_fine), dt)}
 
 
 def main():
@@ -116,14 +117,14 @@ def main():
     o = torch.from_numpy(sc.rays_o).cuda()
     d = torch.from_numpy(sc.rays_d).cuda()
     R = cfg.num_rays
-    S = R * cfg.n_coarse
+    S = R * (cfg.n_coarse + cfg.n_fine)   # head evaluations (both passes when hierarchical)
     out = (torch.empty((R, 3), device="cuda"), torch.empty((R,), device="cuda"),
            torch.empty((R,), device="cuda"))
     r = derf.Renderer(sc.sites, cfg.arch, sc.weights, precision)
     stream = torch.cuda.current_stream()
 
     def step():
-        r.render(o, d, cfg.near, cfg.far, cfg.n_coarse, 0, scenes.SEED_RENDER, out=out,
+        r.render(o, d, cfg.near, cfg.far, cfg.n_coarse, cfg.n_fine, scenes.SEED_RENDER, out=out,
                  stream=stream)
 
     for _ in range(args.warmup):
@@ -159,7 +160,8 @@ def main():
     mlp_flop = 2.0 * cfg.arch.macs_per_sample() * S
     achieved = mlp_flop / (mlp_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[precision]
-    comp_bytes = 21.0 * S + 20.0 * R      # t + cell + sigma/rgb per sample, outputs per ray
+    # t + cell + sigma/rgb per sample (coarse and fine lists when hierarchical), outputs per ray
+    comp_bytes = 21.0 * S + 20.0 * R
     comp_gbps = comp_bytes / (stage_ms["composite"] * 1e-3) / 1e9
     heads = np.array(st.head_samples[:cfg.num_sites], dtype=np.int64)
 
@@ -183,7 +185,7 @@ def main():
         "dtype": precision,
         "data": "synthetic (seeded scene, Glorot-uniform random heads)",
         "config": {"workload": workload_text(cfg, precision), "rays": R,
-                   "samples_per_ray": cfg.n_coarse, "heads": cfg.num_sites,
+                   "samples_per_ray": cfg.n_coarse + cfg.n_fine, "heads": cfg.num_sites,
                    "samples": S},
         "roofline": {"bound": "mfma", "kernel": "mlp_kernel (grouped per-head MLP)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",

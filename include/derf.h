@@ -66,9 +66,17 @@ typedef struct {
 
 /* Sampling of each ray on [near, far] (Sec. 3.1 Eq. 1 bounds).
  *   n_coarse  stratified samples per ray (>= 1, n_coarse + n_fine <= 1024)
- *   n_fine    inverse-CDF samples per ray drawn from the coarse weights; 0 =
- *             single pass.  (Hierarchical sampling is not built yet: any
- *             n_fine > 0 returns DERF_ERR_UNSUPPORTED.)
+ *   n_fine    0: one pass over the n_coarse samples.  > 0 (needs n_coarse
+ *             >= 2): hierarchical sampling as in NeRF, which the paper keeps
+ *             for its heads (Sec. 4): the coarse pass's quadrature weights
+ *             w_i = T_i alpha_i plus 1e-5 define a piecewise-constant
+ *             density on the coarse midpoint intervals; n_fine draws
+ *             u_j = (j + xi_j) / n_fine (xi_j: stream 1 of the generator
+ *             below) go through its inverse CDF (computed in float64); the
+ *             coarse and fine depths are merged in order (coarse first on
+ *             equal depths), the fine samples are assigned and evaluated,
+ *             the coarse heads' outputs are reused, and the result is the
+ *             composite of all n_coarse + n_fine samples.
  *   seed      key of the Philox4x32-10 generator of the stratum jitter
  *   perturb   1: t_i = near + (i + xi) (far - near) / n with xi from Philox;
  *             0: xi = 1/2 (stratum midpoints)
@@ -120,8 +128,8 @@ int derf_create(derf_handle **out, int num_sites, const float *sites_xyz,
  * default stream).  The work is enqueued on hip_stream and the call returns
  * without waiting for it; the inputs must stay valid and the outputs
  * untouched until it completes.  Kernel faults surface at the caller's next
- * synchronisation.  num_rays == 0 is a no-op.  R * n_coarse must stay below
- * 2^32; larger frames are rendered in several calls.  Calls on one handle
+ * synchronisation.  num_rays == 0 is a no-op.  R * (n_coarse + n_fine) must
+ * stay below 2^32; larger frames are rendered in several calls.  Calls on one handle
  * must not run concurrently (they share the handle's workspace, which grows
  * as needed and is reused). */
 int derf_render(derf_handle *h, const float *rays_o, const float *rays_d, long long num_rays,
@@ -129,7 +137,9 @@ int derf_render(derf_handle *h, const float *rays_o, const float *rays_d, long l
                 float *out_depth, float *out_opacity, void *hip_stream);
 
 /* Optional per-sample outputs of derf_render_debug: device pointers, any may
- * be NULL.  N = samples per ray; sample i of ray r is at index r * N + i. */
+ * be NULL.  N = n_coarse + n_fine samples per ray, in depth order (with
+ * hierarchical sampling: the merged coarse and fine samples); sample i of
+ * ray r is at index r * N + i. */
 typedef struct {
     int *cell;    /* [R][N] owning site of each sample                       */
     float *t;     /* [R][N] sample depth                                     */
@@ -144,9 +154,18 @@ int derf_render_debug(derf_handle *h, const float *rays_o, const float *rays_d,
 
 /* Per-stage GPU time, recorded with HIP events on the render's stream when
  * timing is on (derf_set_timing); accumulated over renders since the last
- * derf_reset_stats.  Stages: 0 sample+encode+assign, 1 bucket scan,
- * 2 bucket scatter, 3 per-head MLP, 4 segment compositing. */
-#define DERF_NUM_STAGES 5
+ * derf_reset_stats.  With hierarchical sampling a stage's time is the sum of
+ * its coarse and fine passes; stage_launches counts the renders that ran the
+ * stage.  head_samples counts head evaluations of both passes. */
+enum {
+    DERF_STAGE_SAMPLE = 0,         /* sample + encode + assign (given depths: assign) */
+    DERF_STAGE_BUCKET_SCAN = 1,    /* per-head counts -> offsets                     */
+    DERF_STAGE_BUCKET_SCATTER = 2, /* sample ids into per-head buckets               */
+    DERF_STAGE_MLP = 3,            /* grouped per-head MLP                           */
+    DERF_STAGE_COMPOSITE = 4,      /* segment integration + Painter's merge          */
+    DERF_STAGE_FINE = 5            /* coarse weights -> inverse-CDF fine depths      */
+};
+#define DERF_NUM_STAGES 6
 typedef struct {
     long long renders;                  /* renders since reset              */
     long long samples;                  /* samples since reset              */

@@ -89,6 +89,11 @@ def _lib_handle():
         lib.oracle_assign_depths.argtypes = [ctypes.c_int, _P, ctypes.c_longlong, _P, _P,
                                              ctypes.c_int, _P, _P, _P, ctypes.c_int]
         lib.oracle_assign_depths.restype = ctypes.c_int
+        lib.oracle_render_depths.argtypes = [ctypes.c_int, _P, ctypes.POINTER(_Arch), _P,
+                                             ctypes.c_longlong, _P, _P, ctypes.c_float,
+                                             ctypes.c_float, ctypes.c_int, _P, _P, _P, _P, _P, _P,
+                                             _P, ctypes.c_int]
+        lib.oracle_render_depths.restype = ctypes.c_int
         lib.oracle_max_threads.argtypes = []
         lib.oracle_max_threads.restype = ctypes.c_int
         _lib = lib
@@ -230,6 +235,34 @@ def assign_depths(sites, rays_o, rays_d, t, margin: bool = False, nthreads: int 
     if rc != 0:
         raise RuntimeError("oracle assign_depths failed (%d)" % rc)
     return cell, m
+
+
+def render_depths(sites, arch, weights, rays_o, rays_d, near: float, far: float, t,
+                  per_sample: bool = False, nthreads: int = 0):
+    """DeRF render at given sorted sample depths t [R, n]: heads of the owning
+    cells, quadrature, segments and Painter's merge (no sampling)."""
+    sites = np.ascontiguousarray(sites, np.float32).reshape(-1, 3)
+    weights = np.ascontiguousarray(weights, np.float32)
+    o = np.ascontiguousarray(rays_o, np.float32).reshape(-1, 3)
+    d = np.ascontiguousarray(rays_d, np.float32).reshape(-1, 3)
+    t = np.ascontiguousarray(t, np.float32)
+    R, n = t.shape
+    if o.shape[0] != R or d.shape[0] != R:
+        raise ValueError("rays and depths disagree on the ray count")
+    rgb = np.zeros((R, 3), np.float64)
+    dep = np.zeros(R, np.float64)
+    op = np.zeros(R, np.float64)
+    cell = np.zeros((R, n), np.int32) if per_sample else None
+    sig = np.zeros((R, n), np.float64) if per_sample else None
+    srgb = np.zeros((R, n, 3), np.float64) if per_sample else None
+    a = _arch(arch)
+    rc = _lib_handle().oracle_render_depths(sites.shape[0], _ptr(sites), ctypes.byref(a),
+                                            _ptr(weights), R, _ptr(o), _ptr(d), near, far, n,
+                                            _ptr(t), _ptr(rgb), _ptr(dep), _ptr(op), _ptr(cell),
+                                            _ptr(sig), _ptr(srgb), nthreads)
+    if rc != 0:
+        raise RuntimeError("oracle render_depths failed (%d)" % rc)
+    return RenderResult(rgb, dep, op, t, cell, sig, srgb)
 
 
 class RenderResult:

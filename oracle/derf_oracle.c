@@ -722,6 +722,73 @@ int oracle_sample_assign(int K, const float *sites, long long R, const float *ra
     return 0;
 }
 
+/* DeRF render of rays [0, R) at given sample depths t [R][n] (sorted per
+ * ray, inside [near, far]): each sample's nearest-site head (Sec. 3.2-3.3),
+ * midpoint quadrature on [near, far] and the per-segment integration with
+ * the Painter's merge (Sec. 3.3) -- the steps that follow sampling, applied
+ * to depths that come from elsewhere (e.g. the fine depths of hierarchical
+ * sampling).  Per-sample outputs are optional (NULL). */
+int oracle_render_depths(int K, const float *sites, const oracle_arch *arch, const float *weights,
+                         long long R, const float *rays_o, const float *rays_d, float near_t,
+                         float far_t, int n, const float *t, double *out_rgb, double *out_depth,
+                         double *out_opacity, int *dbg_cell, double *dbg_sigma, double *dbg_rgb,
+                         int nthreads)
+{
+    if (n < 1 || R < 0 || K < 1)
+        return -1;
+    render_args A = { K, sites, arch, weights, near_t, far_t, n, 0, 0, 0 };
+    int P = 3 + 6 * arch->pos_freqs, Dd = 3 + 6 * arch->dir_freqs;
+    size_t scratch_len = 4 * (size_t)(P + arch->width + Dd + arch->rgb_hidden + 8);
+#ifdef _OPENMP
+    if (nthreads > 0)
+        omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+    int failed = 0;
+#pragma omp parallel
+    {
+        int *cell = malloc(sizeof(int) * (size_t)n);
+        double *sigma = malloc(sizeof(double) * (size_t)n);
+        double *rgb = malloc(sizeof(double) * 3 * (size_t)n);
+        double *delta = malloc(sizeof(double) * (size_t)n);
+        double *gx = malloc(sizeof(double) * (size_t)P);
+        double *gd = malloc(sizeof(double) * (size_t)Dd);
+        double *scratch = malloc(sizeof(double) * scratch_len);
+        if (!cell || !sigma || !rgb || !delta || !gx || !gd || !scratch) {
+#pragma omp atomic write
+            failed = 1;
+        } else {
+#pragma omp for schedule(dynamic, 16)
+            for (long long r = 0; r < R; ++r) {
+                const float *o = rays_o + 3 * r, *d = rays_d + 3 * r;
+                const float *tr = t + (size_t)r * n;
+                double dn = sqrt((double)d[0] * d[0] + (double)d[1] * d[1] + (double)d[2] * d[2]);
+                double dh[3] = { d[0] / dn, d[1] / dn, d[2] / dn };
+                oracle_posenc(arch->dir_freqs, dh, gd);
+                eval_samples(&A, MODE_DERF, 0.0, o, d, gd, n, tr, cell, sigma, rgb, gx, scratch);
+                intervals(tr, n, near_t, far_t, delta);
+                composite_segments(n, cell, tr, sigma, rgb, delta, out_rgb + 3 * r, out_depth + r,
+                                   out_opacity + r, NULL);
+                for (int i = 0; i < n; ++i) {
+                    size_t s = (size_t)r * n + i;
+                    if (dbg_cell)
+                        dbg_cell[s] = cell[i];
+                    if (dbg_sigma)
+                        dbg_sigma[s] = sigma[i];
+                    if (dbg_rgb) {
+                        dbg_rgb[3 * s + 0] = rgb[3 * i + 0];
+                        dbg_rgb[3 * s + 1] = rgb[3 * i + 1];
+                        dbg_rgb[3 * s + 2] = rgb[3 * i + 2];
+                    }
+                }
+            }
+        }
+        free(cell); free(sigma); free(rgb); free(delta); free(gx); free(gd); free(scratch);
+    }
+    return failed ? -3 : 0;
+}
+
 /* Owning cells of given sample depths t [R][n] (Sec. 3.3 nearest site, at
  * x = o + t d in float32 with one fma per component): the check of the
  * assignment of samples whose depths come from elsewhere, such as the

@@ -17,7 +17,7 @@ LIB = os.path.join(PKG, "libderf.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["kernels_sample.hip", "kernels_mlp.hip", "derf_api.cpp"]
+SOURCES = ["kernels_sample.hip", "kernels_fine.hip", "kernels_mlp.hip", "derf_api.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH,
           "-I" + os.path.join(ROOT, "include"), "-I" + CSRC,

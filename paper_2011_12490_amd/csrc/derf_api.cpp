@@ -72,6 +72,10 @@ struct Workspace {
     size_t bytes = 0;
 };
 
+constexpr int kPasses = 2;
+constexpr int kEvents = 2 * kPasses * DERF_NUM_STAGES;
+inline int ev_index(int pass, int stage, int end) { return 2 * (pass * DERF_NUM_STAGES + stage) + end; }
+
 }  // namespace
 
 struct derf_handle {
@@ -88,10 +92,15 @@ struct derf_handle {
     Workspace ws;
     hipStream_t last_stream = nullptr;
     bool timing = false;
-    hipEvent_t ev[2 * DERF_NUM_STAGES] = {};
+    // one event pair per (pass, stage): pass 0 is the single or coarse pass,
+    // pass 1 the fine pass of hierarchical sampling
+    hipEvent_t ev[kEvents] = {};
+    unsigned ev_mask = 0;      // event pairs recorded by the pending render
     bool ev_pending = false;
     derf_stats stats{};
-    unsigned *totals = nullptr;  // device pointer into the workspace of the last render
+    // per-head counts of the last render (device pointers into the workspace)
+    unsigned *totals = nullptr;
+    unsigned *totals_fine = nullptr;
 };
 
 namespace {
@@ -104,44 +113,75 @@ T *carve(char *&p, size_t count)
     return r;
 }
 
+// Workspace of one render.  S samples of the single (or coarse) pass and Sf
+// of the fine pass (0 without hierarchical sampling); the bucket and the
+// per-block counts are reused by the fine pass.
 struct Buffers {
     float *t;
     uint8_t *cell;
     float4 *sr;
+    float *t_fine;
+    uint8_t *cell_fine;
+    float4 *sr_fine;
     unsigned *bucket;
     void *dirbuf;
     unsigned *counts;
     unsigned *totals;
+    unsigned *totals_fine;
 };
 
-size_t layout(char *base, unsigned S, unsigned R, unsigned nblk, int K, bool bf16, Buffers *b)
+size_t layout(char *base, unsigned S, unsigned Sf, unsigned R, unsigned nblk, int K, bool bf16,
+              Buffers *b)
 {
     char *p = base;
     Buffers x;
     x.t = carve<float>(p, S);
     x.cell = carve<uint8_t>(p, (size_t)S + 16);
     x.sr = carve<float4>(p, S);
-    x.bucket = carve<unsigned>(p, S);
+    x.t_fine = carve<float>(p, Sf);
+    x.cell_fine = carve<uint8_t>(p, Sf ? (size_t)Sf + 16 : 0);
+    x.sr_fine = carve<float4>(p, Sf);
+    x.bucket = carve<unsigned>(p, S > Sf ? S : Sf);
     x.dirbuf = carve<char>(p, (size_t)R * kDirPad * (bf16 ? 2 : 4));
     x.counts = carve<unsigned>(p, (size_t)nblk * K);
     x.totals = carve<unsigned>(p, K);
+    x.totals_fine = carve<unsigned>(p, K);
     if (b)
         *b = x;
     return (size_t)(p - base);
 }
 
+// Adds the pending render's stage times: per stage, the sum over passes;
+// stage_launches counts the renders that ran the stage.
 void accumulate_timing(derf_handle *h)
 {
     if (!h->ev_pending)
         return;
     for (int s = 0; s < DERF_NUM_STAGES; ++s) {
-        float ms = 0.0f;
-        if (hipEventElapsedTime(&ms, h->ev[2 * s], h->ev[2 * s + 1]) == hipSuccess) {
-            h->stats.stage_ms[s] += ms;
-            h->stats.stage_launches[s] += 1;
+        bool ran = false;
+        for (int pass = 0; pass < kPasses; ++pass) {
+            const int k = pass * DERF_NUM_STAGES + s;
+            float ms = 0.0f;
+            if ((h->ev_mask >> k) & 1u &&
+                hipEventElapsedTime(&ms, h->ev[ev_index(pass, s, 0)], h->ev[ev_index(pass, s, 1)]) ==
+                    hipSuccess) {
+                h->stats.stage_ms[s] += ms;
+                ran = true;
+            }
         }
+        if (ran)
+            h->stats.stage_launches[s] += 1;
     }
     h->ev_pending = false;
+}
+
+// the last event the pending render recorded
+hipEvent_t last_event(const derf_handle *h)
+{
+    for (int k = kPasses * DERF_NUM_STAGES - 1; k >= 0; --k)
+        if ((h->ev_mask >> k) & 1u)
+            return h->ev[2 * k + 1];
+    return nullptr;
 }
 
 int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long long num_rays,
@@ -160,21 +200,25 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
         return fail(DERF_ERR_INVALID_ARG, "need 1 <= n_coarse, 0 <= n_fine, total <= 1024");
     if (samp->n_fine > 0 && samp->n_coarse < 2)
         return fail(DERF_ERR_INVALID_ARG, "hierarchical sampling needs n_coarse >= 2");
-    if (samp->n_fine > 0)
-        return fail(DERF_ERR_UNSUPPORTED, "hierarchical (n_fine > 0) sampling is not built");
     if (num_rays == 0)
         return DERF_OK;
     if (!rays_o || !rays_d || !out_rgb || !out_depth || !out_opacity)
         return fail(DERF_ERR_INVALID_ARG, "null ray or output pointer");
-    const unsigned long long S64 = (unsigned long long)num_rays * (unsigned)samp->n_coarse;
+    const unsigned long long S64 =
+        (unsigned long long)num_rays * (unsigned)(samp->n_coarse + samp->n_fine);
     if (S64 >= (1ull << 32))
-        return fail(DERF_ERR_INVALID_ARG, "num_rays * samples must be < 2^32 per call");
+        return fail(DERF_ERR_INVALID_ARG,
+                    "num_rays * (n_coarse + n_fine) must be < 2^32 per call");
 
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     HIP_TRY(hipSetDevice(h->device), "hipSetDevice");
-    const unsigned R = (unsigned)num_rays, N = (unsigned)samp->n_coarse, S = (unsigned)S64;
+    const bool hier = samp->n_fine > 0;
+    const unsigned R = (unsigned)num_rays, N = (unsigned)samp->n_coarse, NF = (unsigned)samp->n_fine;
+    const unsigned S = R * N, Sf = R * NF;
     const unsigned nblk = (S + kBucketBlock - 1) / kBucketBlock;
-    const size_t need = layout(nullptr, S, R, nblk, h->num_sites, h->bf16, nullptr);
+    const unsigned nblk_f = (Sf + kBucketBlock - 1) / kBucketBlock;
+    const unsigned nblk_max = nblk > nblk_f ? nblk : nblk_f;
+    const size_t need = layout(nullptr, S, Sf, R, nblk_max, h->num_sites, h->bf16, nullptr);
     if (need > h->ws.bytes) {
         // the old workspace may still be in use by work on the previous stream
         if (h->last_stream || h->ws.mem)
@@ -192,11 +236,11 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
         h->ws.bytes = grow;
     }
     if (h->timing && h->ev_pending) {
-        HIP_TRY(hipEventSynchronize(h->ev[2 * DERF_NUM_STAGES - 1]), "hipEventSynchronize");
+        HIP_TRY(hipEventSynchronize(last_event(h)), "hipEventSynchronize");
         accumulate_timing(h);
     }
     Buffers b;
-    layout(reinterpret_cast<char *>(h->ws.mem), S, R, nblk, h->num_sites, h->bf16, &b);
+    layout(reinterpret_cast<char *>(h->ws.mem), S, Sf, R, nblk_max, h->num_sites, h->bf16, &b);
 
     RenderGeometry g;
     g.rays_o = rays_o;
@@ -212,42 +256,86 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
     g.ray_offset = samp->ray_offset;
     g.perturb = samp->perturb ? 1 : 0;
 
-    auto mark = [&](int idx) -> hipError_t {
-        return h->timing ? hipEventRecord(h->ev[idx], s) : hipSuccess;
+    h->ev_mask = 0;
+    auto mark = [&](int pass, int stage, int end) -> hipError_t {
+        if (!h->timing)
+            return hipSuccess;
+        h->ev_mask |= 1u << (pass * DERF_NUM_STAGES + stage);
+        return hipEventRecord(h->ev[ev_index(pass, stage, end)], s);
+    };
+    // assignment counts -> bucket -> per-head MLP of one pass
+    auto bucket_and_mlp = [&](int pass, const RenderGeometry &gp, const float *t,
+                              const uint8_t *cell, unsigned nb, unsigned *totals,
+                              float4 *sr) -> int {
+        HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCAN, 0), "hipEventRecord");
+        HIP_TRY(launch_bucket_scan(b.counts, nb, h->num_sites, totals, s), "bucket_scan launch");
+        HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCAN, 1), "hipEventRecord");
+        HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCATTER, 0), "hipEventRecord");
+        HIP_TRY(launch_bucket_scatter(cell, b.counts, totals, gp.num_samples, nb, h->num_sites,
+                                      h->site_bits, b.bucket, s),
+                "bucket_scatter launch");
+        HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCATTER, 1), "hipEventRecord");
+        HIP_TRY(mark(pass, DERF_STAGE_MLP, 0), "hipEventRecord");
+        HIP_TRY(h->mlp->launch(b.bucket, totals, h->num_sites, gp, t, b.dirbuf, h->streams,
+                               h->blocks, sr, h->mlp_grid, s),
+                "mlp launch");
+        HIP_TRY(mark(pass, DERF_STAGE_MLP, 1), "hipEventRecord");
+        return DERF_OK;
     };
 
-    HIP_TRY(mark(0), "hipEventRecord");
+    // ---- single or coarse pass: stratified samples (Sec. 3.1)
+    HIP_TRY(mark(0, DERF_STAGE_SAMPLE, 0), "hipEventRecord");
     HIP_TRY(launch_ray_encode(g, b.dirbuf, h->bf16, s), "ray_encode launch");
     HIP_TRY(launch_sample_assign(g, h->sites, h->num_sites, h->site_bits, b.t, b.cell, b.counts,
                                  nblk, s),
             "sample_assign launch");
-    HIP_TRY(mark(1), "hipEventRecord");
-    HIP_TRY(mark(2), "hipEventRecord");
-    HIP_TRY(launch_bucket_scan(b.counts, nblk, h->num_sites, b.totals, s), "bucket_scan launch");
-    HIP_TRY(mark(3), "hipEventRecord");
-    HIP_TRY(mark(4), "hipEventRecord");
-    HIP_TRY(launch_bucket_scatter(b.cell, b.counts, b.totals, S, nblk, h->num_sites, h->site_bits,
-                                  b.bucket, s),
-            "bucket_scatter launch");
-    HIP_TRY(mark(5), "hipEventRecord");
-    HIP_TRY(mark(6), "hipEventRecord");
-    HIP_TRY(h->mlp->launch(b.bucket, b.totals, h->num_sites, g, b.t, b.dirbuf, h->streams,
-                           h->blocks, b.sr, h->mlp_grid, s),
-            "mlp launch");
-    HIP_TRY(mark(7), "hipEventRecord");
-    HIP_TRY(mark(8), "hipEventRecord");
-    HIP_TRY(launch_composite(g, b.t, b.cell, b.sr, out_rgb, out_depth, out_opacity, s),
-            "composite launch");
-    HIP_TRY(mark(9), "hipEventRecord");
-    if (dbg && (dbg->cell || dbg->t || dbg->sigma || dbg->rgb))
-        HIP_TRY(launch_debug_expand(S, b.t, b.cell, b.sr, dbg->cell, dbg->t, dbg->sigma, dbg->rgb,
-                                    s),
-                "debug_expand launch");
+    HIP_TRY(mark(0, DERF_STAGE_SAMPLE, 1), "hipEventRecord");
+    int rc = bucket_and_mlp(0, g, b.t, b.cell, nblk, b.totals, b.sr);
+    if (rc != DERF_OK)
+        return rc;
+    const bool want_dbg = dbg && (dbg->cell || dbg->t || dbg->sigma || dbg->rgb);
+    if (!hier) {
+        HIP_TRY(mark(0, DERF_STAGE_COMPOSITE, 0), "hipEventRecord");
+        HIP_TRY(launch_composite(g, b.t, b.cell, b.sr, out_rgb, out_depth, out_opacity, s),
+                "composite launch");
+        HIP_TRY(mark(0, DERF_STAGE_COMPOSITE, 1), "hipEventRecord");
+        if (want_dbg)
+            HIP_TRY(launch_debug_expand(S, b.t, b.cell, b.sr, dbg->cell, dbg->t, dbg->sigma,
+                                        dbg->rgb, s),
+                    "debug_expand launch");
+    } else {
+        // ---- fine pass: inverse-CDF depths from the coarse weights, their
+        // cells and heads; the coarse outputs are reused in the composite
+        HIP_TRY(mark(0, DERF_STAGE_FINE, 0), "hipEventRecord");
+        HIP_TRY(launch_fine_sample(g, b.t, b.sr, NF, b.t_fine, s), "fine_sample launch");
+        HIP_TRY(mark(0, DERF_STAGE_FINE, 1), "hipEventRecord");
+        RenderGeometry gf = g;
+        gf.n = NF;
+        gf.num_samples = Sf;
+        gf.inv_n = 1.0 / (double)NF;
+        HIP_TRY(mark(1, DERF_STAGE_SAMPLE, 0), "hipEventRecord");
+        HIP_TRY(launch_assign_given(gf, h->sites, h->num_sites, h->site_bits, b.t_fine,
+                                    b.cell_fine, b.counts, nblk_f, s),
+                "assign launch");
+        HIP_TRY(mark(1, DERF_STAGE_SAMPLE, 1), "hipEventRecord");
+        rc = bucket_and_mlp(1, gf, b.t_fine, b.cell_fine, nblk_f, b.totals_fine, b.sr_fine);
+        if (rc != DERF_OK)
+            return rc;
+        HIP_TRY(mark(1, DERF_STAGE_COMPOSITE, 0), "hipEventRecord");
+        HIP_TRY(launch_merge_composite(g, b.t, b.cell, b.sr, NF, b.t_fine, b.cell_fine, b.sr_fine,
+                                       out_rgb, out_depth, out_opacity,
+                                       want_dbg ? dbg->cell : nullptr, want_dbg ? dbg->t : nullptr,
+                                       want_dbg ? dbg->sigma : nullptr,
+                                       want_dbg ? dbg->rgb : nullptr, s),
+                "merge_composite launch");
+        HIP_TRY(mark(1, DERF_STAGE_COMPOSITE, 1), "hipEventRecord");
+    }
     h->ev_pending = h->timing;
     h->last_stream = s;
     h->totals = b.totals;
+    h->totals_fine = hier ? b.totals_fine : nullptr;
     h->stats.renders += 1;
-    h->stats.samples += S;
+    h->stats.samples += (long long)S + Sf;
     return DERF_OK;
 }
 
@@ -345,7 +433,7 @@ int derf_create(derf_handle **out, int num_sites, const float *sites_xyz,
         e = hipMemcpy(h->blocks, blocks.data(), blocks.size() * 4, hipMemcpyHostToDevice);
     if (e != hipSuccess)
         return cleanup(hip_fail(e, "hipMemcpy"));
-    for (int i = 0; i < 2 * DERF_NUM_STAGES; ++i) {
+    for (int i = 0; i < kEvents; ++i) {
         e = hipEventCreate(&h->ev[i]);
         if (e != hipSuccess)
             return cleanup(hip_fail(e, "hipEventCreate"));
@@ -399,6 +487,13 @@ int derf_get_stats(derf_handle *h, derf_stats *out)
                 "hipMemcpy");
         for (int k = 0; k < h->num_sites; ++k)
             h->stats.head_samples[k] = tot[k];
+        if (h->totals_fine) {
+            HIP_TRY(hipMemcpy(tot.data(), h->totals_fine, sizeof(unsigned) * h->num_sites,
+                              hipMemcpyDeviceToHost),
+                    "hipMemcpy");
+            for (int k = 0; k < h->num_sites; ++k)
+                h->stats.head_samples[k] += tot[k];
+        }
     }
     *out = h->stats;
     return DERF_OK;
@@ -409,7 +504,7 @@ int derf_reset_stats(derf_handle *h)
     if (!h)
         return fail(DERF_ERR_INVALID_ARG, "null handle");
     if (h->ev_pending) {
-        HIP_TRY(hipEventSynchronize(h->ev[2 * DERF_NUM_STAGES - 1]), "hipEventSynchronize");
+        HIP_TRY(hipEventSynchronize(last_event(h)), "hipEventSynchronize");
         h->ev_pending = false;
     }
     memset(&h->stats, 0, sizeof(h->stats));
@@ -431,7 +526,7 @@ void derf_destroy(derf_handle *h)
         (void)hipFree(h->streams);
     if (h->blocks)
         (void)hipFree(h->blocks);
-    for (int i = 0; i < 2 * DERF_NUM_STAGES; ++i)
+    for (int i = 0; i < kEvents; ++i)
         if (h->ev[i])
             (void)hipEventDestroy(h->ev[i]);
     delete h;

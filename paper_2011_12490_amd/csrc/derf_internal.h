@@ -32,6 +32,10 @@ hipError_t launch_ray_encode(const RenderGeometry &g, void *dirbuf, bool bf16, h
 hipError_t launch_sample_assign(const RenderGeometry &g, const float4 *sites, int num_sites,
                                 int site_bits, float *t, uint8_t *cell, unsigned *counts,
                                 unsigned num_blocks, hipStream_t s);
+// same, for given depths t (read only): no sampling
+hipError_t launch_assign_given(const RenderGeometry &g, const float4 *sites, int num_sites,
+                               int site_bits, const float *t, uint8_t *cell, unsigned *counts,
+                               unsigned num_blocks, hipStream_t s);
 hipError_t launch_bucket_scan(unsigned *counts, unsigned num_blocks, int num_sites,
                               unsigned *totals, hipStream_t s);
 hipError_t launch_bucket_scatter(const uint8_t *cell, const unsigned *counts,
@@ -44,6 +48,19 @@ hipError_t launch_composite(const RenderGeometry &g, const float *t, const uint8
 hipError_t launch_debug_expand(unsigned num_samples, const float *t, const uint8_t *cell,
                                const float4 *sr, int *dcell, float *dt, float *dsigma,
                                float *drgb, hipStream_t s);
+
+// ---- hierarchical sampling (kernels_fine.hip) -----------------------------
+// g describes the coarse pass (n = n_coarse).  tf [R][n_fine] receives the
+// sorted inverse-CDF depths drawn from the coarse outputs src.
+hipError_t launch_fine_sample(const RenderGeometry &g, const float *tc, const float4 *src,
+                              unsigned n_fine, float *tf, hipStream_t s);
+// Composite of the depth-ordered merge of the coarse (tc, cc, sc) and fine
+// (tf, cf, sf) samples; the optional debug arrays receive the merged fields.
+hipError_t launch_merge_composite(const RenderGeometry &g, const float *tc, const uint8_t *cc,
+                                  const float4 *sc, unsigned n_fine, const float *tf,
+                                  const uint8_t *cf, const float4 *sf, float *rgb, float *depth,
+                                  float *opacity, int *dcell, float *dt, float *dsigma,
+                                  float *drgb, hipStream_t s);
 
 // ---- grouped per-head MLP (kernels_mlp.hip) ------------------------------
 struct HeadArch {

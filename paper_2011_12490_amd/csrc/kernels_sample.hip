@@ -7,34 +7,13 @@
 // run and in every reference.
 #pragma clang fp contract(off)
 
+#include "derf_device.h"
 #include "derf_internal.h"
 
 namespace derf {
 namespace {
 
 constexpr int kThreads = 256;
-
-// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC 2011): ten rounds of two
-// 32x32->64-bit products, Weyl-sequence key schedule between rounds.
-__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint2 k)
-{
-#pragma unroll
-    for (int round = 0; round < 10; ++round) {
-        if (round > 0) {
-            k.x += 0x9E3779B9u;
-            k.y += 0xBB67AE85u;
-        }
-        const unsigned lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
-        const unsigned lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
-        c = make_uint4(hi1 ^ c.y ^ k.x, lo1, hi0 ^ c.w ^ k.y, lo0);
-    }
-    return c;
-}
-
-__device__ __forceinline__ unsigned word(uint4 v, unsigned i)
-{
-    return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
-}
 
 // sample index s -> (ray, index within the ray); s < 2^32, n <= 1024.  The
 // float64 quotient is at most one below the true one (at exact multiples).
@@ -124,7 +103,10 @@ __device__ __forceinline__ uint64_t match_peers(unsigned v, int bits, uint64_t v
 // Stratified depths t, owning cell (nearest site, ties to the lowest index)
 // and per-block head histograms.  Block b covers samples
 // [b * kBucketBlock, (b + 1) * kBucketBlock); each thread takes 4 consecutive
-// samples per round, so one Philox block serves 4 samples of a ray.
+// samples per round, so one Philox block serves 4 samples of a ray.  With
+// FROM_T the depths are given (t is read, not written): the assignment of
+// the inverse-CDF samples of hierarchical sampling.
+template <bool FROM_T>
 __global__ __launch_bounds__(kThreads) void sample_assign_kernel(
     RenderGeometry g, const float4 *__restrict__ sites, int num_sites, int site_bits,
     float *__restrict__ t_out, uint8_t *__restrict__ cell_out, unsigned *__restrict__ counts,
@@ -148,12 +130,25 @@ __global__ __launch_bounds__(kThreads) void sample_assign_kernel(
         float tv[4];
         unsigned cv[4];
         uint4 blk = make_uint4(0, 0, 0, 0);
+        if constexpr (FROM_T) {
+            if (s0 + 3 < g.num_samples) {
+                const float4 q = *reinterpret_cast<const float4 *>(t_out + s0);
+                tv[0] = q.x;
+                tv[1] = q.y;
+                tv[2] = q.z;
+                tv[3] = q.w;
+            } else {
+                for (int v = 0; v < 4; ++v)
+                    tv[v] = s0 + v < g.num_samples ? t_out[s0 + v] : 0.0f;
+            }
+        }
         float ox = 0, oy = 0, oz = 0, dx = 0, dy = 0, dz = 0;
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
             const unsigned s = s0 + v;
             cv[v] = 0xFFFFFFFFu;
-            tv[v] = 0.0f;
+            if constexpr (!FROM_T)
+                tv[v] = 0.0f;
             if (s < g.num_samples) {
                 if (v == 0 || i == 0) {
                     ox = g.rays_o[3 * r];
@@ -163,13 +158,18 @@ __global__ __launch_bounds__(kThreads) void sample_assign_kernel(
                     dy = g.rays_d[3 * r + 1];
                     dz = g.rays_d[3 * r + 2];
                 }
-                if (v == 0 || (i & 3u) == 0) {
-                    const uint64_t rg = g.ray_offset + r;
-                    blk = philox4x32_10(make_uint4(i >> 2, (unsigned)rg, (unsigned)(rg >> 32), 0u), key);
+                float t;
+                if constexpr (FROM_T) {
+                    t = tv[v];
+                } else {
+                    if (v == 0 || (i & 3u) == 0) {
+                        const uint64_t rg = g.ray_offset + r;
+                        blk = philox4x32_10(make_uint4(i >> 2, (unsigned)rg, (unsigned)(rg >> 32), 0u), key);
+                    }
+                    const float xi =
+                        g.perturb ? (float)(philox_word(blk, i & 3u) >> 8) * 0x1.0p-24f : 0.5f;
+                    t = fmaf(g.step, (float)i + xi, g.near_t);
                 }
-                const float xi =
-                    g.perturb ? (float)(word(blk, i & 3u) >> 8) * 0x1.0p-24f : 0.5f;
-                const float t = fmaf(g.step, (float)i + xi, g.near_t);
                 const float x = fmaf(t, dx, ox), y = fmaf(t, dy, oy), z = fmaf(t, dz, oz);
                 float best = INFINITY;
                 unsigned bk = 0;
@@ -192,13 +192,15 @@ __global__ __launch_bounds__(kThreads) void sample_assign_kernel(
             }
         }
         if (s0 + 3 < g.num_samples) {
-            *reinterpret_cast<float4 *>(t_out + s0) = make_float4(tv[0], tv[1], tv[2], tv[3]);
+            if constexpr (!FROM_T)
+                *reinterpret_cast<float4 *>(t_out + s0) = make_float4(tv[0], tv[1], tv[2], tv[3]);
             *reinterpret_cast<unsigned *>(cell_out + s0) =
                 cv[0] | (cv[1] << 8) | (cv[2] << 16) | (cv[3] << 24);
         } else {
             for (int v = 0; v < 4; ++v)
                 if (s0 + v < g.num_samples) {
-                    t_out[s0 + v] = tv[v];
+                    if constexpr (!FROM_T)
+                        t_out[s0 + v] = tv[v];
                     cell_out[s0 + v] = (uint8_t)cv[v];
                 }
         }
@@ -324,21 +326,8 @@ __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
 
 // ---------------------------------------------------------------------------
 // Segment integration and Painter's merge, one wave per ray.  Lane j takes
-// the contiguous samples [j c, j c + c) with c = ceil(n / 64).  Within a
-// lane, each maximal run of one cell is integrated with its own local
-// transmittance, and the runs are merged front to back; the 64 lane results
-// are then merged in lane order.  Merging is the associative "over":
-// (C, D, T) then (C', D', T') gives (C + T C', D + T D', T T').
-struct Over {
-    float r, g, b, d, t;
-};
-
-__device__ __forceinline__ Over over(const Over &a, const Over &b)
-{
-    return Over{fmaf(a.t, b.r, a.r), fmaf(a.t, b.g, a.g), fmaf(a.t, b.b, a.b),
-                fmaf(a.t, b.d, a.d), a.t * b.t};
-}
-
+// the contiguous samples [j c, j c + c) with c = ceil(n / 64), integrates
+// its runs (integrate_runs) and the 64 lane results are merged in lane order.
 __global__ __launch_bounds__(kThreads) void composite_kernel(
     const float *__restrict__ t, const uint8_t *__restrict__ cell, const float4 *__restrict__ sr,
     unsigned n, unsigned num_rays, float near_t, float far_t, float *__restrict__ out_rgb,
@@ -352,46 +341,10 @@ __global__ __launch_bounds__(kThreads) void composite_kernel(
     const unsigned i0 = lane * c;
     const unsigned i1 = min(i0 + c, n);
     const size_t base = (size_t)ray * n;
-    Over acc{0.f, 0.f, 0.f, 0.f, 1.f};   // merged runs of this lane
-    Over seg{0.f, 0.f, 0.f, 0.f, 1.f};   // current run, local transmittance
-    unsigned cur = 0xFFFFFFFFu;
-    float t_prev = (i0 > 0 && i0 < n) ? t[base + i0 - 1] : 0.0f;
-    float t_cur = i0 < n ? t[base + i0] : 0.0f;
-    for (unsigned i = i0; i < i1; ++i) {
-        const float t_next = (i + 1 < n) ? t[base + i + 1] : 0.0f;
-        const float lo = (i == 0) ? near_t : 0.5f * (t_prev + t_cur);
-        const float hi = (i + 1 == n) ? far_t : 0.5f * (t_cur + t_next);
-        const unsigned ci = cell[base + i];
-        const float4 v = sr[base + i];
-        const float tau = __expf(-v.x * (hi - lo));
-        const float alpha = 1.0f - tau;
-        if (ci != cur) {
-            acc = over(acc, seg);
-            seg = Over{0.f, 0.f, 0.f, 0.f, 1.f};
-            cur = ci;
-        }
-        const float w = seg.t * alpha;
-        seg.r = fmaf(w, v.y, seg.r);
-        seg.g = fmaf(w, v.z, seg.g);
-        seg.b = fmaf(w, v.w, seg.b);
-        seg.d = fmaf(w, t_cur, seg.d);
-        seg.t *= tau;
-        t_prev = t_cur;
-        t_cur = t_next;
-    }
-    acc = over(acc, seg);
-    // ordered tree merge across the wave: lane j absorbs lane j + off
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        Over o;
-        o.r = __shfl_down(acc.r, off);
-        o.g = __shfl_down(acc.g, off);
-        o.b = __shfl_down(acc.b, off);
-        o.d = __shfl_down(acc.d, off);
-        o.t = __shfl_down(acc.t, off);
-        if ((lane & (2 * off - 1)) == 0)
-            acc = over(acc, o);
-    }
+    Over acc = integrate_runs(
+        i0, i1, n, near_t, far_t, [&](unsigned i) { return t[base + i]; },
+        [&](unsigned i) { return (unsigned)cell[base + i]; }, [&](unsigned i) { return sr[base + i]; });
+    acc = wave_over(acc, lane);
     if (lane == 0) {
         out_rgb[3 * ray] = acc.r;
         out_rgb[3 * ray + 1] = acc.g;
@@ -442,8 +395,18 @@ hipError_t launch_sample_assign(const RenderGeometry &g, const float4 *sites, in
                                 int site_bits, float *t, uint8_t *cell, unsigned *counts,
                                 unsigned num_blocks, hipStream_t s)
 {
-    sample_assign_kernel<<<num_blocks, kThreads, 0, s>>>(g, sites, num_sites, site_bits, t, cell,
-                                                         counts, num_blocks);
+    sample_assign_kernel<false><<<num_blocks, kThreads, 0, s>>>(g, sites, num_sites, site_bits, t,
+                                                                cell, counts, num_blocks);
+    return hipGetLastError();
+}
+
+hipError_t launch_assign_given(const RenderGeometry &g, const float4 *sites, int num_sites,
+                               int site_bits, const float *t, uint8_t *cell, unsigned *counts,
+                               unsigned num_blocks, hipStream_t s)
+{
+    // t is only read in this instantiation
+    sample_assign_kernel<true><<<num_blocks, kThreads, 0, s>>>(
+        g, sites, num_sites, site_bits, const_cast<float *>(t), cell, counts, num_blocks);
     return hipGetLastError();
 }
 

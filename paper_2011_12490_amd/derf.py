@@ -23,8 +23,8 @@ DERF_ERR_OOM = -3
 DERF_ERR_HIP = -4
 DERF_PREC_FP32 = 0
 DERF_PREC_BF16 = 1
-DERF_NUM_STAGES = 5
-STAGE_NAMES = ("sample_assign", "bucket_scan", "bucket_scatter", "mlp", "composite")
+DERF_NUM_STAGES = 6
+STAGE_NAMES = ("sample_assign", "bucket_scan", "bucket_scatter", "mlp", "composite", "fine_sample")
 
 
 class derf_head_arch(ctypes.Structure):

@@ -23,6 +23,14 @@ def test_header_declares_the_binding_names():
     assert set(declared_functions()) == set(derf.EXPORTS)
 
 
+def test_stage_count_agrees_with_the_binding():
+    text = open(os.path.join(ROOT, "include", "derf.h")).read()
+    n = int(re.search(r"#define DERF_NUM_STAGES (\d+)", text).group(1))
+    assert n == derf.DERF_NUM_STAGES == len(derf.STAGE_NAMES)
+    stages = re.findall(r"DERF_STAGE_([A-Z_]+) = (\d+)", text)
+    assert sorted(int(v) for _, v in stages) == list(range(n))
+
+
 def test_library_exports_every_declared_symbol():
     L = derf.lib()
     for name in declared_functions():

@@ -213,7 +213,7 @@ def test_unperturbed_midpoints():
     _check_pixels(gpu, ref, np.arange(cfg.num_rays), TOL["fp32"], "tiny midpoints")
 
 
-def test_zero_rays_is_a_noop_and_fine_sampling_is_refused():
+def test_zero_rays_is_a_noop_and_bad_sampling_is_refused():
     derf = _derf()
     cfg = scenes.CONFIGS["tiny"]
     sc = scenes.make_scene(cfg)
@@ -221,14 +221,15 @@ def test_zero_rays_is_a_noop_and_fine_sampling_is_refused():
     o = torch.zeros((0, 3), device="cuda")
     out = r.render(o, o, 2.0, 6.0, 32)
     assert out[0].shape == (0, 3)
+    out = r.render(o, o, 2.0, 6.0, 16, 32)
+    assert out[0].shape == (0, 3)
     o1 = torch.from_numpy(sc.rays_o[:4]).cuda()
     d1 = torch.from_numpy(sc.rays_d[:4]).cuda()
-    with pytest.raises(derf.DerfError) as e:
-        r.render(o1, d1, 2.0, 6.0, 16, 32)
-    assert e.value.status == derf.DERF_ERR_UNSUPPORTED
-    with pytest.raises(derf.DerfError) as e:
-        r.render(o1, d1, 6.0, 2.0, 16)
-    assert e.value.status == derf.DERF_ERR_INVALID_ARG
+    for args in ((6.0, 2.0, 16), (2.0, 6.0, 1, 8), (2.0, 6.0, 16, 1009), (2.0, 6.0, 0),
+                 (2.0, 6.0, 16, -1)):
+        with pytest.raises(derf.DerfError) as e:
+            r.render(o1, d1, *args)
+        assert e.value.status == derf.DERF_ERR_INVALID_ARG, args
     r.close()
 
 

@@ -519,6 +519,24 @@ def test_hierarchical_render_merges_sorted_lists():
     assert np.all(np.isfinite(r.rgb)) and np.all((r.opacity >= 0) & (r.opacity <= 1))
 
 
+def test_render_at_given_depths_reproduces_both_render_paths():
+    """Rendering at the depths a render used (its own stratified samples, or
+    its merged coarse + fine list) reproduces that render bit for bit: the
+    steps after sampling are the same in both."""
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], sigma_bias=2.0)
+    sc = scenes.make_scene(cfg)
+    ids = np.arange(0, cfg.num_rays, 7)
+    o, d = sc.rays_o[ids], sc.rays_d[ids]
+    for nc, nf in ((24, 0), (12, 20)):
+        r = oracle.render(sc.sites, cfg.arch, sc.weights, o, d, cfg.near, cfg.far, nc, nf,
+                          seed=5, ray_ids=ids, per_sample=True)
+        g = oracle.render_depths(sc.sites, cfg.arch, sc.weights, o, d, cfg.near, cfg.far, r.t,
+                                 per_sample=True)
+        assert np.array_equal(g.rgb, r.rgb) and np.array_equal(g.depth, r.depth)
+        assert np.array_equal(g.opacity, r.opacity)
+        assert np.array_equal(g.cell, r.cell) and np.array_equal(g.sigma, r.sigma)
+
+
 def test_oracle_regression_fixture():
     """Stored oracle values (tests/golden/make_golden.py) still reproduce."""
     import json

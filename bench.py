@@ -90,6 +90,8 @@ def main():
     ap.add_argument("--sites", type=int, default=None, help="override the number of heads")
     ap.add_argument("--cpu-rays", type=int, default=24576)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--k-sweep", default=None,
+                    help="comma-separated head counts: the same frame with K k-means sites each")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (to scale HBM counters)")
     args = ap.parse_args()
@@ -110,52 +112,58 @@ def main():
     if args.sites is not None:
         cfg = scenes.with_changes(cfg, num_sites=args.sites)
     precision = args.precision or cfg.precision
-    log("bench: building scene %s (%d rays x %d samples, K=%d, %s)"
-        % (cfg.name, cfg.num_rays, cfg.n_coarse, cfg.num_sites, precision))
-    sc = scenes.make_scene(cfg)
     torch.cuda.set_device(0)
-    o = torch.from_numpy(sc.rays_o).cuda()
-    d = torch.from_numpy(sc.rays_d).cuda()
+
+    def run(cfg, steps, warmup, copy_calibration=False):
+        """Time `steps` renders of the workload; per-stage times from the
+        library's HIP events on the render stream."""
+        log("bench: building scene %s (%d rays x %d samples, K=%d, %s)"
+            % (cfg.name, cfg.num_rays, cfg.n_coarse + cfg.n_fine, cfg.num_sites, precision))
+        sc = scenes.make_scene(cfg)
+        o = torch.from_numpy(sc.rays_o).cuda()
+        d = torch.from_numpy(sc.rays_d).cuda()
+        R = cfg.num_rays
+        out = (torch.empty((R, 3), device="cuda"), torch.empty((R,), device="cuda"),
+               torch.empty((R,), device="cuda"))
+        r = derf.Renderer(sc.sites, cfg.arch, sc.weights, precision)
+        stream = torch.cuda.current_stream()
+
+        def step():
+            r.render(o, d, cfg.near, cfg.far, cfg.n_coarse, cfg.n_fine, scenes.SEED_RENDER,
+                     out=out, stream=stream)
+
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        log("bench: warmup done (%d steps)" % warmup)
+        if copy_calibration:
+            # a plain copy of known size: its FETCH_SIZE / WRITE_SIZE scale the
+            # counters of the render kernels (1 GiB read + 1 GiB written)
+            src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+            dst = torch.empty_like(src)
+            dst.copy_(src)
+            torch.cuda.synchronize()
+            del src, dst
+        derf.derf_reset_stats(r.handle)
+        derf.derf_set_timing(r.handle, True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            step()
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        st = derf.derf_get_stats(r.handle)
+        derf.derf_set_timing(r.handle, False)
+        log("bench: timed %d steps in %.3f s" % (steps, elapsed))
+        stage_ms = {name: st.stage_ms[i] / max(1, st.stage_launches[i])
+                    for i, name in enumerate(derf.STAGE_NAMES)}
+        heads = np.array(st.head_samples[:cfg.num_sites], dtype=np.int64)
+        r.close()
+        return sc, elapsed * 1e3 / steps, stage_ms, heads
+
+    sc, ms_per_step, stage_ms, heads = run(cfg, args.steps, args.warmup, args.copy_calibration)
     R = cfg.num_rays
     S = R * (cfg.n_coarse + cfg.n_fine)   # head evaluations (both passes when hierarchical)
-    out = (torch.empty((R, 3), device="cuda"), torch.empty((R,), device="cuda"),
-           torch.empty((R,), device="cuda"))
-    r = derf.Renderer(sc.sites, cfg.arch, sc.weights, precision)
-    stream = torch.cuda.current_stream()
-
-    def step():
-        r.render(o, d, cfg.near, cfg.far, cfg.n_coarse, cfg.n_fine, scenes.SEED_RENDER, out=out,
-                 stream=stream)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    log("bench: warmup done (%d steps)" % args.warmup)
-
-    if args.copy_calibration:
-        # a plain copy of known size: its FETCH_SIZE / WRITE_SIZE scale the
-        # counters of the render kernels (1 GiB read + 1 GiB written)
-        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
-
-    derf.derf_reset_stats(r.handle)
-    derf.derf_set_timing(r.handle, True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    st = derf.derf_get_stats(r.handle)
-    derf.derf_set_timing(r.handle, False)
-    log("bench: timed %d steps in %.3f s" % (args.steps, elapsed))
-
-    ms_per_step = 1e3 * elapsed / args.steps
-    stage_ms = {name: st.stage_ms[i] / max(1, st.stage_launches[i])
-                for i, name in enumerate(derf.STAGE_NAMES)}
     mlp_ms = stage_ms["mlp"]
     mlp_flop = 2.0 * cfg.arch.macs_per_sample() * S
     achieved = mlp_flop / (mlp_ms * 1e-3) / 1e12
@@ -163,7 +171,19 @@ def main():
     # t + cell + sigma/rgb per sample (coarse and fine lists when hierarchical), outputs per ray
     comp_bytes = 21.0 * S + 20.0 * R
     comp_gbps = comp_bytes / (stage_ms["composite"] * 1e-3) / 1e9
-    heads = np.array(st.head_samples[:cfg.num_sites], dtype=np.int64)
+
+    k_sweep = None
+    if args.k_sweep:
+        k_sweep = []
+        for K in [int(k) for k in args.k_sweep.split(",")]:
+            ck = scenes.with_changes(cfg, num_sites=K)
+            _, ms_k, st_k, heads_k = run(ck, max(3, args.steps // 2), 2)
+            k_sweep.append({"K": K, "rays_per_s": R / (ms_k * 1e-3), "ms_per_step": ms_k,
+                            "mlp_ms": st_k["mlp"],
+                            "mlp_frac": mlp_flop / (st_k["mlp"] * 1e-3) / 1e12 / peak,
+                            "stage_ms": st_k,
+                            "head_samples_min_max": [int(heads_k.min()), int(heads_k.max())]})
+            log("bench: K=%d %.4g rays/s" % (K, k_sweep[-1]["rays_per_s"]))
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -190,9 +210,10 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "mlp_kernel (grouped per-head MLP)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak,
-                     "traffic": measured_traffic() if cfg.name == "derf_k16" and precision == "bf16"
-                     else None,
-                     "flop_per_launch": mlp_flop, "avg_launch_ms": mlp_ms},
+                     "traffic": measured_traffic() if (cfg.name == "derf_k16" and cfg.num_sites == 16
+                                                       and precision == "bf16") else None,
+                     "flop_per_step": mlp_flop, "mlp_ms_per_step": mlp_ms,
+                     "launches_per_step": 2 if cfg.n_fine else 1},
         "cpu_baseline": cpu,
         "samples_per_s": S / (ms_per_step * 1e-3),
         "stage_ms": stage_ms,
@@ -202,7 +223,8 @@ def main():
         "head_samples": {"min": int(heads.min()), "median": float(np.median(heads)),
                          "max": int(heads.max())},
     }
-    r.close()
+    if k_sweep is not None:
+        res["k_sweep"] = k_sweep
     print(json.dumps(res))
 
 

@@ -47,17 +47,27 @@ def workload_text(cfg, precision):
                a.pos_freqs, a.skip_layer, rgb, precision))
 
 
+def kernel_source_hash():
+    """Hash of the MLP kernel's source with comments and whitespace removed:
+    a code change alters it, an edit of comments does not."""
+    import hashlib
+    import re
+    text = "".join(open(os.path.join(ROOT, "paper_2011_12490_amd", "csrc", f)).read()
+                   for f in ("kernels_mlp.hip", "derf_internal.h"))
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    text = re.sub(r"\s+", " ", text)
+    return hashlib.sha256(text.encode()).hexdigest()[:16]
+
+
 def measured_traffic():
     """HBM bytes per MLP launch from the committed counter summary, or None
-    when the kernel source has changed since the counters were taken."""
-    import hashlib
+    when the kernel code has changed since the counters were taken."""
     path = os.path.join(ROOT, "profiles", "mlp_kernel_derf_k16_hbm_counters.md")
     try:
         line = [l for l in open(path) if l.startswith("traffic-json:")][0]
         rec = json.loads(line.split(":", 1)[1])
-        src = b"".join(open(os.path.join(ROOT, "paper_2011_12490_amd", "csrc", f), "rb").read()
-                       for f in ("kernels_mlp.hip", "derf_internal.h"))
-        if hashlib.sha256(src).hexdigest()[:16] != rec["source_sha256_16"]:
+        if kernel_source_hash() != rec["source_code_hash"]:
             return None
         return rec["traffic_bytes"]
     except (OSError, IndexError, ValueError, KeyError):

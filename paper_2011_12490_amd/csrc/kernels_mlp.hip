@@ -24,13 +24,18 @@
 // Weight streaming.  A head's weights are cut into stages -- one 32-row
 // output tile and at most 8 KB of its input chunks -- laid out as 1 KB units
 // that are exactly one wave's A-operand registers.  Stages stream
-// global -> LDS (global_load_lds_dwordx4) through a 4-slot ring, issued three
-// stages ahead (across tile boundaries too) and waited for two stages ahead,
-// so one barrier per stage orders slot reuse; each wave also reads the first
-// fragments of the next stage before that stage begins.  A tile's ReLU and
-// bf16 rounding run during the next tile's matrix work.  Density and colour
-// come out of one extra 32-row output tile (row 0 density, rows 1-3 colour
-// logits), so the network tail needs no cross-lane reduction.
+// global -> LDS (global_load_lds_dwordx4, issued as asm so the compiler's
+// LDS wait bookkeeping stays exact) through an 8-slot ring, six stages ahead
+// (across tile boundaries too).  Stages are consumed in groups of two: before
+// a group, each wave waits with a counted vmcnt for exactly the loads that
+// group needs (the count is simulated at compile time from the issue order)
+// and one fence-free barrier makes every wave's loads visible and orders
+// slot reuse.  The per-step schedule is explicit: A fragments are read from
+// LDS a few steps ahead (a window continuous across stages), and a tile's
+// bias, ReLU and bf16 rounding are spread over the next tile's MFMAs.
+// Density and colour come out of one extra 32-row output tile (row 0
+// density, rows 1-3 colour logits), so the network tail needs no cross-lane
+// reduction.
 #include <type_traits>
 #include <vector>
 

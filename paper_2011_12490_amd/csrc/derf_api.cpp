@@ -128,6 +128,7 @@ struct Buffers {
     unsigned *counts;
     unsigned *totals;
     unsigned *totals_fine;
+    unsigned *mlp_queue;
 };
 
 size_t layout(char *base, unsigned S, unsigned Sf, unsigned R, unsigned nblk, int K, bool bf16,
@@ -146,6 +147,7 @@ size_t layout(char *base, unsigned S, unsigned Sf, unsigned R, unsigned nblk, in
     x.counts = carve<unsigned>(p, (size_t)nblk * K);
     x.totals = carve<unsigned>(p, K);
     x.totals_fine = carve<unsigned>(p, K);
+    x.mlp_queue = carve<unsigned>(p, kMlpQueues);
     if (b)
         *b = x;
     return (size_t)(p - base);
@@ -268,7 +270,8 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
                               const uint8_t *cell, unsigned nb, unsigned *totals,
                               float4 *sr) -> int {
         HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCAN, 0), "hipEventRecord");
-        HIP_TRY(launch_bucket_scan(b.counts, nb, h->num_sites, totals, s), "bucket_scan launch");
+        HIP_TRY(launch_bucket_scan(b.counts, nb, h->num_sites, totals, b.mlp_queue, s),
+                "bucket_scan launch");
         HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCAN, 1), "hipEventRecord");
         HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCATTER, 0), "hipEventRecord");
         HIP_TRY(launch_bucket_scatter(cell, b.counts, totals, gp.num_samples, nb, h->num_sites,
@@ -277,7 +280,7 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
         HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCATTER, 1), "hipEventRecord");
         HIP_TRY(mark(pass, DERF_STAGE_MLP, 0), "hipEventRecord");
         HIP_TRY(h->mlp->launch(b.bucket, totals, h->num_sites, gp, t, b.dirbuf, h->streams,
-                               h->blocks, sr, h->mlp_grid, s),
+                               h->blocks, sr, b.mlp_queue, h->mlp_grid, s),
                 "mlp launch");
         HIP_TRY(mark(pass, DERF_STAGE_MLP, 1), "hipEventRecord");
         return DERF_OK;

@@ -13,6 +13,8 @@ constexpr int kBucketBlock = 4096;
 // Padded length of the per-ray direction feature vector gamma(d / |d|).
 constexpr int kDirPad = 32;
 constexpr int kMaxSites = 256;
+// Tile counters of the MLP's work queues (one per XCD).
+constexpr int kMlpQueues = 8;
 
 struct RenderGeometry {
     const float *rays_o;
@@ -36,8 +38,9 @@ hipError_t launch_sample_assign(const RenderGeometry &g, const float4 *sites, in
 hipError_t launch_assign_given(const RenderGeometry &g, const float4 *sites, int num_sites,
                                int site_bits, const float *t, uint8_t *cell, unsigned *counts,
                                unsigned num_blocks, hipStream_t s);
+// also clears the kMlpQueues tile counters of the MLP launch that follows
 hipError_t launch_bucket_scan(unsigned *counts, unsigned num_blocks, int num_sites,
-                              unsigned *totals, hipStream_t s);
+                              unsigned *totals, unsigned *mlp_queue, hipStream_t s);
 hipError_t launch_bucket_scatter(const uint8_t *cell, const unsigned *counts,
                                  const unsigned *totals, unsigned num_samples,
                                  unsigned num_blocks, int num_sites, int site_bits,
@@ -74,10 +77,11 @@ struct MlpVariant {
     int tile;            // samples per tile
     // Lay out one head's fp32 weights (packed order of derf.h) for the kernel.
     void (*pack)(const float *w, unsigned char *stream, float *block);
+    // queue: kMlpQueues tile counters, zero at launch
     hipError_t (*launch)(const unsigned *bucket, const unsigned *totals, int num_sites,
                          const RenderGeometry &g, const float *t, const void *dirbuf,
                          const unsigned char *streams, const float *blocks, float4 *sr,
-                         int grid, hipStream_t s);
+                         unsigned *queue, int grid, hipStream_t s);
 };
 
 // Returns nullptr when no kernel is compiled for this architecture/precision.

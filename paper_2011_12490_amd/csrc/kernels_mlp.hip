@@ -504,13 +504,15 @@ using Chunk = std::conditional_t<C::BF16, bf16x8, float>;
 
 // A-fragment reads kept in flight ahead of the MFMA that uses them.
 constexpr int kPrefetch = 3;
+// "no tile left" from the work queues
+constexpr unsigned kNoTile = 0xFFFFFFFFu;
 
 template <class C>
 __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
     const unsigned *__restrict__ bucket, const unsigned *__restrict__ totals, int num_sites,
     RenderGeometry geo, const float *__restrict__ tbuf, const void *__restrict__ dirbuf,
     const unsigned char *__restrict__ streams, const float *__restrict__ blocks,
-    float4 *__restrict__ sr)
+    float4 *__restrict__ sr, unsigned *__restrict__ queue)
 {
     using CT = Chunk<C>;
     using AT = std::conditional_t<C::BF16, bf16x8, f32x4>;  // one LDS unit per lane
@@ -519,6 +521,7 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
     float *hb = reinterpret_cast<float *>(lds + C::HB_OFF);
     __shared__ unsigned s_off[kMaxSites + 1];   // bucket offset of each head
     __shared__ unsigned s_tile[kMaxSites + 1];  // first tile of each head
+    __shared__ unsigned s_q[2];                 // tile indices handed out by the queues
 
     const int tid = threadIdx.x, lane = tid & 63;
     // wave-uniform by construction; saying so keeps LDS-destination pointers scalar
@@ -538,20 +541,50 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
     }
     __syncthreads();
     const unsigned total_tiles = s_tile[num_sites];
-    // contiguous tile ranges per workgroup; workgroups are dealt round-robin
-    // to the 8 XCDs, so map block b to range (b % 8) * G/8 + b / 8 and each
-    // XCD walks one contiguous stretch of heads
-    const unsigned G = gridDim.x;
-    const unsigned lb = (G % 8 == 0) ? (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8 : blockIdx.x;
-    const unsigned t_begin = (unsigned)(((unsigned long long)total_tiles * lb) / G);
-    const unsigned t_end = (unsigned)(((unsigned long long)total_tiles * (lb + 1)) / G);
-    if (t_begin >= t_end)
+
+    // Tiles are handed out dynamically.  The tile range is cut into 8
+    // contiguous stretches, one per XCD (each XCD has its own L2, and a
+    // stretch covers few heads); queue[x] counts the tiles taken from
+    // stretch x.  A workgroup takes from its own XCD's stretch, then from the
+    // others.  The two workgroups sharing a CU do not get equal shares of its
+    // matrix pipe, so static ranges would leave one finishing long after the
+    // other.  The counters are zero at launch (the bucket scan clears them).
+    const unsigned xcc = (unsigned)__builtin_amdgcn_s_getreg(20 | (31 << 11)) & 7u;  // XCC_ID
+    auto q_base = [&](unsigned x) { return (unsigned)(((unsigned long long)total_tiles * x) / 8); };
+    // finish a take whose first attempt on the own stretch returned t
+    auto take_rest = [&](unsigned t) -> unsigned {
+        if (t < q_base(xcc + 1) - q_base(xcc))
+            return q_base(xcc) + t;
+        for (unsigned k = 1; k < 8; ++k) {
+            const unsigned x = (xcc + k) & 7u;
+            const unsigned u = atomicAdd(queue + x, 1u);
+            if (u < q_base(x + 1) - q_base(x))
+                return q_base(x) + u;
+        }
+        return kNoTile;
+    };
+    if (tid == 0) {
+        s_q[0] = take_rest(atomicAdd(queue + xcc, 1u));
+        s_q[1] = take_rest(atomicAdd(queue + xcc, 1u));
+    }
+    __syncthreads();
+    unsigned tile = __builtin_amdgcn_readfirstlane(s_q[0]);
+    unsigned next = __builtin_amdgcn_readfirstlane(s_q[1]);
+    if (tile == kNoTile)
         return;
 
-    auto head_of = [&](unsigned tile, int h) {
-        while (s_tile[h + 1] <= tile)
-            ++h;
-        return __builtin_amdgcn_readfirstlane(h);
+    // head owning a tile: the last h with s_tile[h] <= tile (empty heads
+    // have s_tile[h] == s_tile[h + 1] and are skipped)
+    auto head_of = [&](unsigned t) {
+        int lo = 0, hi = num_sites;
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (s_tile[mid] <= t)
+                lo = mid;
+            else
+                hi = mid;
+        }
+        return __builtin_amdgcn_readfirstlane(lo);
     };
     // This wave's first unit of head h's stream.  The base is made opaque so
     // that each unit's address is formed from it with a compile-time offset,
@@ -576,15 +609,15 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
         asm volatile("" ::: "memory");
     };
 
-    int head = head_of(t_begin, 0);
+    int head = head_of(tile);
     const unsigned char *stream = stream_of(head);
     unsigned ring = 0;  // ring slot of stage 0 of the current tile (mod NBUF)
     static_for<0, C::LA>([&](auto sc) { issue(sc, stream, ring + decltype(sc)::value); });
     int loaded_head = -1;
 
-    for (unsigned tile = t_begin; tile < t_end; ++tile) {
-        const bool has_next = tile + 1 < t_end;
-        const int nhead = has_next ? head_of(tile + 1, head) : head;
+    while (tile != kNoTile) {
+        const bool has_next = next != kNoTile;
+        const int nhead = has_next ? head_of(next) : head;
         const unsigned char *nstream = stream_of(nhead);
         const unsigned row0 = __builtin_amdgcn_readfirstlane(s_off[head] + (tile - s_tile[head]) * C::TILE);
         // rows never pass the sample count when the bucket counts are
@@ -592,6 +625,12 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
         const unsigned row_end = __builtin_amdgcn_readfirstlane(min(s_off[head + 1], geo.num_samples));
 
         wg_barrier();  // previous tile is done with the head block and the staging
+        // take the tile after next: the attempt on the own stretch is issued
+        // here and completes under the prologue's full wait below, so it
+        // never disturbs the counted waits of the weight stream
+        unsigned q_first = 0;
+        if (tid == 0)
+            q_first = atomicAdd(queue + xcc, 1u);
         if (head != loaded_head) {
             const unsigned char *src = reinterpret_cast<const unsigned char *>(blocks + (size_t)head * C::BLOCK_FLOATS);
             for (int u = wave; u < C::BLOCK_UNITS; u += C::WAVES)
@@ -634,6 +673,9 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
             }
         }
         wait_all();  // weight stages 0..2 and the head block have landed
+        if (tid == 0)
+            s_q[0] = take_rest(q_first);
+        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");  // the store above
         wg_barrier();
 
         CT hbuf[2][NB][C::EHC];                    // hidden outputs, by layer parity
@@ -847,14 +889,16 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
         ring += NS;
         head = nhead;
         stream = nstream;
+        tile = next;
+        next = __builtin_amdgcn_readfirstlane(s_q[0]);
     }
 }
 
 template <class C>
 hipError_t launch_mlp(const unsigned *bucket, const unsigned *totals, int num_sites,
                       const RenderGeometry &g, const float *t, const void *dirbuf,
-                      const unsigned char *streams, const float *blocks, float4 *sr, int cus,
-                      hipStream_t s)
+                      const unsigned char *streams, const float *blocks, float4 *sr,
+                      unsigned *queue, int cus, hipStream_t s)
 {
     static bool configured = false;
     if (!configured) {
@@ -866,8 +910,8 @@ hipError_t launch_mlp(const unsigned *bucket, const unsigned *totals, int num_si
             (void)hipGetLastError();
         configured = true;
     }
-    mlp_kernel<C><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(bucket, totals, num_sites, g, t,
-                                                                       dirbuf, streams, blocks, sr);
+    mlp_kernel<C><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(
+        bucket, totals, num_sites, g, t, dirbuf, streams, blocks, sr, queue);
     return hipGetLastError();
 }
 

@@ -221,11 +221,15 @@ __global__ __launch_bounds__(kThreads) void sample_assign_kernel(
 
 // ---------------------------------------------------------------------------
 // Exclusive prefix over blocks of each head's counts (one block per head),
-// in place; the head's total goes to totals[head].
+// in place; the head's total goes to totals[head].  Block 0 also clears the
+// tile counters of the MLP launch that follows on the stream.
 __global__ __launch_bounds__(1024) void bucket_scan_kernel(unsigned *__restrict__ counts,
                                                            unsigned num_blocks,
-                                                           unsigned *__restrict__ totals)
+                                                           unsigned *__restrict__ totals,
+                                                           unsigned *__restrict__ mlp_queue)
 {
+    if (blockIdx.x == 0 && threadIdx.x < (unsigned)kMlpQueues)
+        mlp_queue[threadIdx.x] = 0;
     __shared__ unsigned s_wave[16];
     __shared__ unsigned s_carry;
     unsigned *col = counts + (size_t)blockIdx.x * num_blocks;
@@ -411,9 +415,9 @@ hipError_t launch_assign_given(const RenderGeometry &g, const float4 *sites, int
 }
 
 hipError_t launch_bucket_scan(unsigned *counts, unsigned num_blocks, int num_sites,
-                              unsigned *totals, hipStream_t s)
+                              unsigned *totals, unsigned *mlp_queue, hipStream_t s)
 {
-    bucket_scan_kernel<<<num_sites, 1024, 0, s>>>(counts, num_blocks, totals);
+    bucket_scan_kernel<<<num_sites, 1024, 0, s>>>(counts, num_blocks, totals, mlp_queue);
     return hipGetLastError();
 }
 

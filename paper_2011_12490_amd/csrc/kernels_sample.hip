@@ -7,6 +7,8 @@
 // run and in every reference.
 #pragma clang fp contract(off)
 
+#include <type_traits>
+
 #include "derf_device.h"
 #include "derf_internal.h"
 
@@ -219,6 +221,172 @@ __global__ __launch_bounds__(kThreads) void sample_assign_kernel(
         counts[(size_t)k * num_blocks + blockIdx.x] = s_hist[k];
 }
 
+// Wave-wide minimum / maximum, result in every lane, without LDS: DPP
+// within each 16-lane row (quad swaps, half-row and row mirrors), then the
+// row-pair and half swaps.
+template <bool MAX>
+__device__ __forceinline__ float wave_reduce(float v)
+{
+    auto op = [](float a, float b) { return MAX ? fmaxf(a, b) : fminf(a, b); };
+    auto dpp = [](float x, auto ctrl) {
+        return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), decltype(ctrl)::value, 0xF, 0xF, false));
+    };
+    v = op(v, dpp(v, std::integral_constant<int, 0xB1>{}));   // quad_perm [1,0,3,2]
+    v = op(v, dpp(v, std::integral_constant<int, 0x4E>{}));   // quad_perm [2,3,0,1]
+    v = op(v, dpp(v, std::integral_constant<int, 0x141>{}));  // row_half_mirror
+    v = op(v, dpp(v, std::integral_constant<int, 0x140>{}));  // row_mirror
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = op(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return op(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float wave_min(float v) { return wave_reduce<false>(v); }
+__device__ __forceinline__ float wave_max(float v) { return wave_reduce<true>(v); }
+
+// Heads at or above this count use site pruning in the assignment (below it
+// the brute force over all sites costs less than the per-slice bounds).
+constexpr int kPruneSites = 48;
+
+// The same, for many heads: in a round wave w takes 256 consecutive
+// samples, lane l the samples l + 64 v (v = 0..3), so each v is a slice of
+// 64 consecutive samples -- a short piece of one or two rays.  Per slice the
+// wave takes the bounding box of its sample points and
+// keeps only the sites whose smallest squared distance to the box is within
+// a factor 1 + 1e-4 of the smallest largest squared distance of any site to
+// the box.  For every point of the box a dropped site is farther, by more
+// than that relative margin, than the site attaining that bound, and the
+// float32 distances are accurate to a few ulp, so a dropped site can neither
+// win nor tie: the argmin over the kept sites (in ascending index order,
+// same arithmetic) is the argmin over all sites.
+template <bool FROM_T>
+__global__ __launch_bounds__(kThreads) void sample_assign_pruned_kernel(
+    RenderGeometry g, const float4 *__restrict__ sites, int num_sites, int site_bits,
+    float *__restrict__ t_out, uint8_t *__restrict__ cell_out, unsigned *__restrict__ counts,
+    unsigned num_blocks)
+{
+    __shared__ float4 s_sites[kMaxSites];
+    __shared__ unsigned s_hist[kMaxSites];
+    for (int k = threadIdx.x; k < num_sites; k += kThreads) {
+        s_sites[k] = sites[k];
+        s_hist[k] = 0;
+    }
+    __syncthreads();
+
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const uint64_t lane_bit = 1ull << lane;
+    const uint2 key = make_uint2((unsigned)g.seed, (unsigned)(g.seed >> 32));
+    const unsigned block_base = blockIdx.x * (unsigned)kBucketBlock;
+    // with n % 4 == 0 the 4 samples sharing a generator block sit in 4
+    // neighbouring lanes: each lane computes one block and they trade words
+    const bool quad = (g.n & 3u) == 0;
+    for (int round = 0; round < kBucketBlock / (4 * kThreads); ++round) {
+        const unsigned wbase = block_base + round * (4 * kThreads) + wv * 256;
+        uint4 qb = make_uint4(0, 0, 0, 0);
+        if constexpr (!FROM_T) {
+            if (g.perturb && quad) {
+                // lane L: block of samples wbase + 64 (L / 16) + 4 (L % 16) + 0..3
+                const unsigned sq = wbase + 64 * (lane >> 4) + 4 * (lane & 15);
+                unsigned rq, iq;
+                split_sample(sq < g.num_samples ? sq : 0, g.n, g.inv_n, rq, iq);
+                const uint64_t rg = g.ray_offset + rq;
+                qb = philox4x32_10(make_uint4(iq >> 2, (unsigned)rg, (unsigned)(rg >> 32), 0u), key);
+            }
+        }
+        float tv[4];
+        unsigned cv[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const unsigned s = wbase + 64 * v + lane;
+            const bool ok = s < g.num_samples;
+            unsigned r, i;
+            split_sample(ok ? s : 0, g.n, g.inv_n, r, i);
+            float t;
+            if constexpr (FROM_T) {
+                t = ok ? t_out[s] : 0.0f;
+            } else {
+                float xi = 0.5f;
+                if (g.perturb) {
+                    unsigned w;
+                    if (quad) {
+                        const int src = 16 * v + (lane >> 2);
+                        const unsigned w0 = __shfl(qb.x, src), w1 = __shfl(qb.y, src);
+                        const unsigned w2 = __shfl(qb.z, src), w3 = __shfl(qb.w, src);
+                        const unsigned q = lane & 3;
+                        w = q == 0 ? w0 : q == 1 ? w1 : q == 2 ? w2 : w3;
+                    } else {
+                        const uint64_t rg = g.ray_offset + r;
+                        w = philox_word(philox4x32_10(make_uint4(i >> 2, (unsigned)rg, (unsigned)(rg >> 32), 0u), key),
+                                        i & 3u);
+                    }
+                    xi = (float)(w >> 8) * 0x1.0p-24f;
+                }
+                t = fmaf(g.step, (float)i + xi, g.near_t);
+            }
+            const float x = fmaf(t, g.rays_d[3 * r], g.rays_o[3 * r]);
+            const float y = fmaf(t, g.rays_d[3 * r + 1], g.rays_o[3 * r + 1]);
+            const float z = fmaf(t, g.rays_d[3 * r + 2], g.rays_o[3 * r + 2]);
+
+            float best = INFINITY;
+            unsigned bk = 0;
+            const float lx = wave_min(ok ? x : INFINITY), hx = wave_max(ok ? x : -INFINITY);
+            const float ly = wave_min(ok ? y : INFINITY), hy = wave_max(ok ? y : -INFINITY);
+            const float lz = wave_min(ok ? z : INFINITY), hz = wave_max(ok ? z : -INFINITY);
+            // smallest over sites of the largest squared distance to the box
+            float thr = INFINITY;
+            for (int k = lane; k < num_sites; k += 64) {
+                const float4 p = s_sites[k];
+                const float ax = fmaxf(p.x - lx, hx - p.x), ay = fmaxf(p.y - ly, hy - p.y);
+                const float az = fmaxf(p.z - lz, hz - p.z);
+                thr = fminf(thr, fmaf(az, az, fmaf(ay, ay, ax * ax)));
+            }
+            thr = wave_min(thr) * (1.0f + 1e-4f);
+            for (int m = 0; 64 * m < num_sites; ++m) {
+                const int kl = 64 * m + lane;
+                bool keep = false;
+                if (kl < num_sites) {
+                    const float4 p = s_sites[kl];
+                    const float bx = fmaxf(fmaxf(lx - p.x, p.x - hx), 0.0f);
+                    const float by = fmaxf(fmaxf(ly - p.y, p.y - hy), 0.0f);
+                    const float bz = fmaxf(fmaxf(lz - p.z, p.z - hz), 0.0f);
+                    keep = fmaf(bz, bz, fmaf(by, by, bx * bx)) <= thr;
+                }
+                uint64_t mk = __ballot(keep);
+                while (mk) {
+                    const int k = 64 * m + __builtin_ctzll(mk);
+                    mk &= mk - 1;
+                    const float4 p = s_sites[k];
+                    const float ex = x - p.x, ey = y - p.y, ez = z - p.z;
+                    const float d2 = fmaf(ez, ez, fmaf(ey, ey, ex * ex));
+                    if (d2 < best) {
+                        best = d2;
+                        bk = k;
+                    }
+                }
+            }
+            tv[v] = t;
+            cv[v] = ok ? bk : 0xFFFFFFFFu;
+            if (ok) {
+                if constexpr (!FROM_T)
+                    t_out[s] = t;
+                cell_out[s] = (uint8_t)bk;
+            }
+        }
+        // histogram: the lowest lane of each group of equal cells adds the group size
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const bool ok = wbase + 64 * v + lane < g.num_samples;
+            const uint64_t valid = __ballot(ok);
+            const uint64_t peers = match_peers(cv[v], site_bits, valid);
+            if (ok && (peers & (lane_bit - 1)) == 0)
+                atomicAdd(&s_hist[cv[v]], (unsigned)__popcll(peers));
+        }
+        (void)tv;
+    }
+    __syncthreads();
+    for (int k = threadIdx.x; k < num_sites; k += kThreads)
+        counts[(size_t)k * num_blocks + blockIdx.x] = s_hist[k];
+}
+
 // ---------------------------------------------------------------------------
 // Exclusive prefix over blocks of each head's counts (one block per head),
 // in place; the head's total goes to totals[head].  Block 0 also clears the
@@ -399,8 +567,12 @@ hipError_t launch_sample_assign(const RenderGeometry &g, const float4 *sites, in
                                 int site_bits, float *t, uint8_t *cell, unsigned *counts,
                                 unsigned num_blocks, hipStream_t s)
 {
-    sample_assign_kernel<false><<<num_blocks, kThreads, 0, s>>>(g, sites, num_sites, site_bits, t,
-                                                                cell, counts, num_blocks);
+    if (num_sites >= kPruneSites)
+        sample_assign_pruned_kernel<false><<<num_blocks, kThreads, 0, s>>>(
+            g, sites, num_sites, site_bits, t, cell, counts, num_blocks);
+    else
+        sample_assign_kernel<false><<<num_blocks, kThreads, 0, s>>>(
+            g, sites, num_sites, site_bits, t, cell, counts, num_blocks);
     return hipGetLastError();
 }
 
@@ -409,8 +581,12 @@ hipError_t launch_assign_given(const RenderGeometry &g, const float4 *sites, int
                                unsigned num_blocks, hipStream_t s)
 {
     // t is only read in this instantiation
-    sample_assign_kernel<true><<<num_blocks, kThreads, 0, s>>>(
-        g, sites, num_sites, site_bits, const_cast<float *>(t), cell, counts, num_blocks);
+    if (num_sites >= kPruneSites)
+        sample_assign_pruned_kernel<true><<<num_blocks, kThreads, 0, s>>>(
+            g, sites, num_sites, site_bits, const_cast<float *>(t), cell, counts, num_blocks);
+    else
+        sample_assign_kernel<true><<<num_blocks, kThreads, 0, s>>>(
+            g, sites, num_sites, site_bits, const_cast<float *>(t), cell, counts, num_blocks);
     return hipGetLastError();
 }
 

@@ -238,6 +238,19 @@ def test_hier_sample_count_edges(nc, nf, n_rays):
                 ids, rays=rays, end_to_end="all")
 
 
+def test_hier_many_heads_slice():
+    """64 skewed heads of 6x64 (pruned assignment of the given fine depths),
+    32 coarse + 32 fine samples, on a contiguous slice of the 1024x1024 frame."""
+    cfg = scenes.CONFIGS["skew_k64"]
+    sc = scenes.make_scene(cfg)
+    lo, hi = 500_000, 504_096
+    rays = (sc.rays_o[lo:hi].copy(), sc.rays_d[lo:hi].copy())
+    gpu = _render(sc, "fp32", 32, 32, rays=rays, ray_offset=lo)
+    ids = np.arange(0, hi - lo, 4)
+    _check_hier(sc, gpu, 32, 32, "fp32", "hier K=64 slice", ids, ids[::4], ray_offset=lo,
+                rays=rays)
+
+
 def test_hier_unperturbed_and_transparent():
     """perturb = 0 (stratum midpoints, u_j = (j + 1/2) / n_fine) on heads with
     zero density: every weight is exactly 0 on both sides, so the density is

@@ -122,6 +122,19 @@ def _subset_parity(name, precision, n_rays, sigma_bias=None, check_cells=True):
     assert np.all(np.isfinite(gpu[0])) and np.all(np.isfinite(gpu[1]))
 
 
+def test_headline_frame_with_64_heads():
+    """The headline frame and 8x128 heads with K = 64 k-means sites (the top of
+    the K sweep, where the assignment prunes sites per 64-sample slice):
+    full-frame cells bit-exact, pixels on a subset."""
+    cfg = scenes.with_changes(scenes.CONFIGS["derf_k16"], num_sites=64)
+    sc = scenes.make_scene(cfg)
+    gpu = _render(sc, "bf16", debug=True)
+    _check_cells(sc, gpu[3]["t"], gpu[3]["cell"], cfg.n_coarse, "derf frame K=64")
+    ids = scenes.ray_subset(512, cfg.num_rays)
+    ref = _oracle(sc, ids)
+    _check_pixels(gpu, ref, ids, TOL["bf16"], "derf frame K=64")
+
+
 @pytest.mark.parametrize("precision", ["bf16", "fp32"])
 def test_derf_k16_headline_frame(precision):
     """504x378 forward-facing frame, 192 samples, 16 heads of 8x128."""
@@ -157,17 +170,20 @@ def test_skew_k64_cells_slice():
 
 # ------------------------------------------------------------ edge cases ----
 
+@pytest.mark.parametrize("sites", [4, 64])
 @pytest.mark.parametrize("n", [1, 3, 7, 33, 200])
-def test_ragged_sample_counts(n):
+def test_ragged_sample_counts(n, sites):
+    """Sample counts that are not multiples of 4 or of 64, with brute-force
+    (4 heads) and pruned (64 heads) assignment."""
     cfg = scenes.CONFIGS["tiny"]
-    sc = scenes.make_scene(scenes.with_changes(cfg, sigma_bias=2.0))
+    sc = scenes.make_scene(scenes.with_changes(cfg, sigma_bias=2.0, num_sites=sites))
     R = 333
     rays = (sc.rays_o[:R].copy(), sc.rays_d[:R].copy())
     sub = scenes.Scene(sc.cfg, sc.sites, sc.weights, rays[0], rays[1])
     gpu = _render(sub, "fp32", debug=True, n=n)
-    _check_cells(sub, gpu[3]["t"], gpu[3]["cell"], n, "tiny n=%d" % n)
+    _check_cells(sub, gpu[3]["t"], gpu[3]["cell"], n, "tiny n=%d K=%d" % (n, sites))
     ref = _oracle(sub, np.arange(R), n=n)
-    _check_pixels(gpu, ref, np.arange(R), TOL["fp32"], "tiny n=%d" % n)
+    _check_pixels(gpu, ref, np.arange(R), TOL["fp32"], "tiny n=%d K=%d" % (n, sites))
 
 
 def test_single_ray_and_single_head():

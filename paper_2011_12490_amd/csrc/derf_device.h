@@ -94,21 +94,41 @@ __device__ __forceinline__ Over integrate_runs(unsigned i0, unsigned i1, unsigne
     return over(acc, seg);
 }
 
+// Value of lane + OFF (OFF = 1, 2, 4, 8; within the 16-lane row) by DPP
+// row shift; other lanes' results are unused by the merge below.
+template <int OFF>
+__device__ __forceinline__ float from_lane_above(float x)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x100 + OFF, 0xF, 0xF, false));
+}
+// Value of lane + 16 for lanes 0 and 32 (row-pair swap), of lane + 32 for
+// lane 0 (half swap).
+__device__ __forceinline__ float from_row_above(float x)
+{
+    return __uint_as_float(__builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false)[1]);
+}
+__device__ __forceinline__ float from_half_above(float x)
+{
+    return __uint_as_float(__builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false)[1]);
+}
+
 // Ordered merge of the 64 lane results of a wave (lane j's stretch precedes
-// lane j + 1's); the result is valid in lane 0.
+// lane j + 1's): at step k lane j (j a multiple of 2^(k+1)) absorbs lane
+// j + 2^k.  The lane exchanges are DPP row shifts and row/half swaps (no
+// LDS).  The result is valid in lane 0.
 __device__ __forceinline__ Over wave_over(Over acc, int lane)
 {
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        Over o;
-        o.r = __shfl_down(acc.r, off);
-        o.g = __shfl_down(acc.g, off);
-        o.b = __shfl_down(acc.b, off);
-        o.d = __shfl_down(acc.d, off);
-        o.t = __shfl_down(acc.t, off);
+    auto step = [&](auto fetch, int off) {
+        const Over o{fetch(acc.r), fetch(acc.g), fetch(acc.b), fetch(acc.d), fetch(acc.t)};
         if ((lane & (2 * off - 1)) == 0)
             acc = over(acc, o);
-    }
+    };
+    step([](float x) { return from_lane_above<1>(x); }, 1);
+    step([](float x) { return from_lane_above<2>(x); }, 2);
+    step([](float x) { return from_lane_above<4>(x); }, 4);
+    step([](float x) { return from_lane_above<8>(x); }, 8);
+    step([](float x) { return from_row_above(x); }, 16);
+    step([](float x) { return from_half_above(x); }, 32);
     return acc;
 }
 

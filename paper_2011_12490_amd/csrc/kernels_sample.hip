@@ -497,27 +497,52 @@ __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Segment integration and Painter's merge, one wave per ray.  Lane j takes
-// the contiguous samples [j c, j c + c) with c = ceil(n / 64), integrates
-// its runs (integrate_runs) and the 64 lane results are merged in lane order.
+// Segment integration and Painter's merge, one wave per ray.  The ray's
+// samples are staged through LDS in chunks of kChunk with coalesced loads
+// (lane l loads samples l + 64 v); within a chunk lane j takes the
+// contiguous samples [j c, j c + c), c = ceil(chunk / 64), integrates its
+// runs (integrate_runs), and the 64 lane results are merged in lane order;
+// the chunk results are merged in chunk order.  A segment cut by a lane or
+// chunk boundary is integrated in pieces merged by "over", which is exact.
+constexpr int kChunk = 256;
+
 __global__ __launch_bounds__(kThreads) void composite_kernel(
     const float *__restrict__ t, const uint8_t *__restrict__ cell, const float4 *__restrict__ sr,
     unsigned n, unsigned num_rays, float near_t, float far_t, float *__restrict__ out_rgb,
     float *__restrict__ out_depth, float *__restrict__ out_opacity)
 {
-    const unsigned ray = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
-    if (ray >= num_rays)
-        return;
-    const unsigned c = (n + 63) / 64;
-    const unsigned i0 = lane * c;
-    const unsigned i1 = min(i0 + c, n);
-    const size_t base = (size_t)ray * n;
-    Over acc = integrate_runs(
-        i0, i1, n, near_t, far_t, [&](unsigned i) { return t[base + i]; },
-        [&](unsigned i) { return (unsigned)cell[base + i]; }, [&](unsigned i) { return sr[base + i]; });
-    acc = wave_over(acc, lane);
-    if (lane == 0) {
+    __shared__ float4 s_sr[kThreads / 64][kChunk];
+    __shared__ float s_t[kThreads / 64][kChunk + 2];  // [0]: sample before the chunk, [len + 1]: after
+    __shared__ uint8_t s_c[kThreads / 64][kChunk];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const unsigned ray = blockIdx.x * (kThreads / 64) + wv;
+    // every wave runs every barrier; waves past the last ray stage ray 0 and store nothing
+    const bool live = ray < num_rays;
+    const size_t base = (size_t)(live ? ray : 0u) * n;
+    Over acc{0.f, 0.f, 0.f, 0.f, 1.f};
+    for (unsigned c0 = 0; c0 < n; c0 += kChunk) {
+        const unsigned len = min((unsigned)kChunk, n - c0);
+        for (unsigned k = lane; k < len; k += 64) {
+            s_sr[wv][k] = sr[base + c0 + k];
+            s_t[wv][k + 1] = t[base + c0 + k];
+            s_c[wv][k] = cell[base + c0 + k];
+        }
+        if (lane == 0)
+            s_t[wv][0] = c0 > 0 ? t[base + c0 - 1] : 0.0f;
+        if (lane == 1)
+            s_t[wv][len + 1] = c0 + len < n ? t[base + c0 + len] : 0.0f;
+        __syncthreads();
+        const unsigned cl = (len + 63) / 64;
+        const unsigned i0 = min(lane * cl, len), i1 = min(i0 + cl, len);
+        Over part = integrate_runs(
+            c0 + i0, c0 + i1, n, near_t, far_t, [&](unsigned i) { return s_t[wv][i - c0 + 1]; },
+            [&](unsigned i) { return (unsigned)s_c[wv][i - c0]; },
+            [&](unsigned i) { return s_sr[wv][i - c0]; });
+        part = wave_over(part, lane);
+        acc = over(acc, part);  // meaningful in lane 0
+        __syncthreads();
+    }
+    if (live && lane == 0) {
         out_rgb[3 * ray] = acc.r;
         out_rgb[3 * ray + 1] = acc.g;
         out_rgb[3 * ray + 2] = acc.b;

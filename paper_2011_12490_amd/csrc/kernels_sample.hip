@@ -444,55 +444,110 @@ __global__ __launch_bounds__(1024) void bucket_scan_kernel(unsigned *__restrict_
         totals[blockIdx.x] = s_carry;
 }
 
+// First bucket position of each head's part in block b: the heads below k
+// take sum_{j<k} totals_j entries, and within head k the blocks before b
+// take prefix[k][b] (exclusive scan over blocks).  Computed by wave 0, 4
+// heads per lane (K <= 256), all loads in flight at once.
+__device__ __forceinline__ void head_block_base(const unsigned *__restrict__ prefix,
+                                                const unsigned *__restrict__ totals,
+                                                unsigned num_blocks, int num_sites,
+                                                unsigned *s_base)
+{
+    if (threadIdx.x >= 64)
+        return;
+    const int lane = threadIdx.x;
+    unsigned tot[4], pre[4], sum = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int k = 4 * lane + j;
+        tot[j] = k < num_sites ? totals[k] : 0u;
+        pre[j] = k < num_sites ? prefix[(size_t)k * num_blocks + blockIdx.x] : 0u;
+        sum += tot[j];
+    }
+    unsigned incl = sum;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const unsigned y = __shfl_up(incl, off);
+        if (lane >= off)
+            incl += y;
+    }
+    unsigned acc = incl - sum;  // heads below this lane's first
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int k = 4 * lane + j;
+        if (k < num_sites)
+            s_base[k] = acc + pre[j];
+        acc += tot[j];
+    }
+}
+
 // Stable scatter of sample ids into per-head buckets.  Bucket k occupies
 // [offset_k, offset_k + total_k) with offset_k = sum of totals below k;
 // within it samples keep increasing sample-id order, so each ray's run
-// through cell k stays contiguous.  Each round covers 256 consecutive
-// samples (4 waves x 64 lanes); ranks come from per-wave equal-cell ballots
-// plus per-head counters of the earlier waves and rounds.
+// through cell k stays contiguous.  Block b's samples are its 4096 of the
+// counting pass; wave w takes the 1024 consecutive ones from 1024 w, in 16
+// steps of 64 (all 16 cells loaded up front).  Pass 1 counts each wave's
+// samples per head (equal-cell ballots, wave-private counters); after one
+// barrier every wave knows its first position per head (the block's base
+// plus the earlier waves' counts); pass 2 ranks each step's samples of one
+// head by ballot and advances the wave's own counters.
 __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
     const uint8_t *__restrict__ cell, const unsigned *__restrict__ prefix,
     const unsigned *__restrict__ totals, unsigned num_samples, unsigned num_blocks,
     int num_sites, int site_bits, unsigned *__restrict__ bucket)
 {
+    constexpr int kWavesPerBlock = kThreads / 64;
+    constexpr int kSteps = kBucketBlock / kThreads;  // 64-sample steps per wave
     __shared__ unsigned s_base[kMaxSites];
-    __shared__ unsigned s_wave[4][kMaxSites];
+    __shared__ unsigned s_pos[kWavesPerBlock][kMaxSites];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    if (threadIdx.x == 0) {
-        unsigned acc = 0;
-        for (int k = 0; k < num_sites; ++k) {
-            s_base[k] = acc + prefix[(size_t)k * num_blocks + blockIdx.x];
-            acc += totals[k];
+    const uint64_t below = (1ull << lane) - 1;
+    head_block_base(prefix, totals, num_blocks, num_sites, s_base);
+    for (int k = threadIdx.x; k < num_sites; k += kThreads)
+        for (int v = 0; v < kWavesPerBlock; ++v)
+            s_pos[v][k] = 0;
+    const unsigned wbase = blockIdx.x * (unsigned)kBucketBlock + w * (kSteps * 64);
+    unsigned cs[kSteps];
+#pragma unroll
+    for (int step = 0; step < kSteps; ++step) {
+        const unsigned s = wbase + step * 64 + lane;
+        cs[step] = s < num_samples ? cell[s] : 0u;
+    }
+    __syncthreads();
+    // pass 1: this wave's count per head
+#pragma unroll
+    for (int step = 0; step < kSteps; ++step) {
+        const bool ok = wbase + step * 64 + lane < num_samples;
+        const uint64_t peers = match_peers(cs[step], site_bits, __ballot(ok));
+        if (ok && (peers & below) == 0)
+            s_pos[w][cs[step]] += (unsigned)__popcll(peers);
+    }
+    __syncthreads();
+    // counts -> each wave's first position per head
+    for (int k = threadIdx.x; k < num_sites; k += kThreads) {
+        unsigned acc = s_base[k];
+        for (int v = 0; v < kWavesPerBlock; ++v) {
+            const unsigned cnt = s_pos[v][k];
+            s_pos[v][k] = acc;
+            acc += cnt;
         }
     }
-    for (int k = threadIdx.x; k < num_sites; k += kThreads)
-        s_wave[0][k] = s_wave[1][k] = s_wave[2][k] = s_wave[3][k] = 0;
     __syncthreads();
-    const uint64_t lane_bit = 1ull << lane;
-    const unsigned block_base = blockIdx.x * (unsigned)kBucketBlock;
-    for (int round = 0; round < kBucketBlock / kThreads; ++round) {
-        const unsigned s = block_base + round * kThreads + threadIdx.x;
+    // pass 2: scatter, advancing the wave's positions
+#pragma unroll
+    for (int step = 0; step < kSteps; ++step) {
+        const unsigned s = wbase + step * 64 + lane;
         const bool ok = s < num_samples;
-        const unsigned c = ok ? cell[s] : 0u;
-        const uint64_t valid = __ballot(ok);
-        const uint64_t peers = match_peers(c, site_bits, valid);
-        const unsigned rank = (unsigned)__popcll(peers & (lane_bit - 1));
-        if (ok && rank == 0)
-            s_wave[w][c] = (unsigned)__popcll(peers);
-        __syncthreads();
+        const unsigned c = cs[step];
+        const uint64_t peers = match_peers(c, site_bits, __ballot(ok));
+        const unsigned start = ok ? s_pos[w][c] : 0u;
         if (ok) {
-            unsigned pos = s_base[c] + rank;
-            for (int v = 0; v < w; ++v)
-                pos += s_wave[v][c];
+            const unsigned pos = start + (unsigned)__popcll(peers & below);
             if (pos < num_samples)  // always true when the counts are consistent
                 bucket[pos] = s;
+            if ((peers & below) == 0)
+                s_pos[w][c] = start + (unsigned)__popcll(peers);
         }
-        __syncthreads();
-        for (int k = threadIdx.x; k < num_sites; k += kThreads) {
-            s_base[k] += s_wave[0][k] + s_wave[1][k] + s_wave[2][k] + s_wave[3][k];
-            s_wave[0][k] = s_wave[1][k] = s_wave[2][k] = s_wave[3][k] = 0;
-        }
-        __syncthreads();
     }
 }
 

@@ -528,16 +528,42 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int n = lane & 31, g = lane >> 5;
 
-    if (tid == 0) {
-        unsigned off = 0, tl = 0;
-        for (int k = 0; k < num_sites; ++k) {
-            s_off[k] = off;
-            s_tile[k] = tl;
-            off += totals[k];
-            tl += (totals[k] + C::TILE - 1) / C::TILE;
+    // bucket offset and first tile of each head: exclusive scans of the
+    // totals and of their tile counts, by wave 0 with 4 heads per lane
+    if (tid < 64) {
+        unsigned tot[4], nt[4], so = 0, st = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int k = 4 * tid + j;
+            tot[j] = k < num_sites ? totals[k] : 0u;
+            nt[j] = (tot[j] + C::TILE - 1) / C::TILE;
+            so += tot[j];
+            st += nt[j];
         }
-        s_off[num_sites] = off;
-        s_tile[num_sites] = tl;
+        unsigned io = so, it = st;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const unsigned yo = __shfl_up(io, o), yt = __shfl_up(it, o);
+            if (tid >= o) {
+                io += yo;
+                it += yt;
+            }
+        }
+        unsigned off = io - so, tl = it - st;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int k = 4 * tid + j;
+            if (k < num_sites) {
+                s_off[k] = off;
+                s_tile[k] = tl;
+            }
+            off += tot[j];
+            tl += nt[j];
+        }
+        if (tid == 63) {
+            s_off[num_sites] = off;
+            s_tile[num_sites] = tl;
+        }
     }
     __syncthreads();
     const unsigned total_tiles = s_tile[num_sites];

@@ -129,6 +129,8 @@ struct Buffers {
     unsigned *totals;
     unsigned *totals_fine;
     unsigned *mlp_queue;
+    SegRec *walk_seg;            // [R][kMaxSeg] (heads >= kWalkSites)
+    unsigned char *walk_nseg;    // [R]
 };
 
 size_t layout(char *base, unsigned S, unsigned Sf, unsigned R, unsigned nblk, int K, bool bf16,
@@ -148,6 +150,9 @@ size_t layout(char *base, unsigned S, unsigned Sf, unsigned R, unsigned nblk, in
     x.totals = carve<unsigned>(p, K);
     x.totals_fine = carve<unsigned>(p, K);
     x.mlp_queue = carve<unsigned>(p, kMlpQueues);
+    const bool walk = K >= kWalkSites;
+    x.walk_seg = walk ? carve<SegRec>(p, (size_t)R * kMaxSeg) : nullptr;
+    x.walk_nseg = walk ? carve<unsigned char>(p, R) : nullptr;
     if (b)
         *b = x;
     return (size_t)(p - base);
@@ -289,8 +294,12 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
     // ---- single or coarse pass: stratified samples (Sec. 3.1)
     HIP_TRY(mark(0, DERF_STAGE_SAMPLE, 0), "hipEventRecord");
     HIP_TRY(launch_ray_encode(g, b.dirbuf, h->bf16, s), "ray_encode launch");
-    HIP_TRY(launch_sample_assign(g, h->sites, h->num_sites, h->site_bits, b.t, b.cell, b.counts,
-                                 nblk, s),
+    const WalkTable walk{b.walk_seg, b.walk_nseg};
+    if (walk.seg)
+        HIP_TRY(launch_ray_walk(g, h->sites, h->num_sites, b.walk_seg, b.walk_nseg, s),
+                "ray_walk launch");
+    HIP_TRY(launch_sample_assign(g, h->sites, h->num_sites, h->site_bits, walk, b.t, b.cell,
+                                 b.counts, nblk, s),
             "sample_assign launch");
     HIP_TRY(mark(0, DERF_STAGE_SAMPLE, 1), "hipEventRecord");
     int rc = bucket_and_mlp(0, g, b.t, b.cell, nblk, b.totals, b.sr);
@@ -317,7 +326,7 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
         gf.num_samples = Sf;
         gf.inv_n = 1.0 / (double)NF;
         HIP_TRY(mark(1, DERF_STAGE_SAMPLE, 0), "hipEventRecord");
-        HIP_TRY(launch_assign_given(gf, h->sites, h->num_sites, h->site_bits, b.t_fine,
+        HIP_TRY(launch_assign_given(gf, h->sites, h->num_sites, h->site_bits, walk, b.t_fine,
                                     b.cell_fine, b.counts, nblk_f, s),
                 "assign launch");
         HIP_TRY(mark(1, DERF_STAGE_SAMPLE, 1), "hipEventRecord");

@@ -16,6 +16,23 @@ constexpr int kMaxSites = 256;
 // Tile counters of the MLP's work queues (one per XCD).
 constexpr int kMlpQueues = 8;
 
+// Per-ray cell walk (see ray_walk_kernel): at most kMaxSeg segments per ray,
+// each with at most kMaxCand candidate sites.
+constexpr int kMaxSeg = 32;
+constexpr int kMaxCand = 11;
+struct alignas(16) SegRec {
+    float t_end;          // the segment covers depths up to t_end
+    unsigned char ncand;  // candidate sites, ascending
+    unsigned char cand[kMaxCand];
+};
+// Heads from which the assignment uses the walk instead of all sites (below,
+// the search over all sites costs less than the walk and its table lookups).
+constexpr int kWalkSites = 28;
+struct WalkTable {
+    const SegRec *seg;           // [R][kMaxSeg]
+    const unsigned char *nseg;   // [R]; 0: the ray takes the search over all sites
+};
+
 struct RenderGeometry {
     const float *rays_o;
     const float *rays_d;
@@ -31,13 +48,18 @@ struct RenderGeometry {
 
 // ---- sampling, assignment and bucketing (kernels_sample.hip) -------------
 hipError_t launch_ray_encode(const RenderGeometry &g, void *dirbuf, bool bf16, hipStream_t s);
+// Walk every ray of g through the cells on [near, far] (one lane per ray).
+hipError_t launch_ray_walk(const RenderGeometry &g, const float4 *sites, int num_sites,
+                           SegRec *seg, unsigned char *nseg, hipStream_t s);
+// walk: the table of launch_ray_walk for the same rays, or {nullptr, nullptr}
 hipError_t launch_sample_assign(const RenderGeometry &g, const float4 *sites, int num_sites,
-                                int site_bits, float *t, uint8_t *cell, unsigned *counts,
-                                unsigned num_blocks, hipStream_t s);
+                                int site_bits, const WalkTable &walk, float *t, uint8_t *cell,
+                                unsigned *counts, unsigned num_blocks, hipStream_t s);
 // same, for given depths t (read only): no sampling
 hipError_t launch_assign_given(const RenderGeometry &g, const float4 *sites, int num_sites,
-                               int site_bits, const float *t, uint8_t *cell, unsigned *counts,
-                               unsigned num_blocks, hipStream_t s);
+                               int site_bits, const WalkTable &walk, const float *t,
+                               uint8_t *cell, unsigned *counts, unsigned num_blocks,
+                               hipStream_t s);
 // also clears the kMlpQueues tile counters of the MLP launch that follows
 hipError_t launch_bucket_scan(unsigned *counts, unsigned num_blocks, int num_sites,
                               unsigned *totals, unsigned *mlp_queue, hipStream_t s);

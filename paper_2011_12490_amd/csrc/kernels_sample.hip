@@ -102,28 +102,329 @@ __device__ __forceinline__ uint64_t match_peers(unsigned v, int bits, uint64_t v
     return peers;
 }
 
+// ---------------------------------------------------------------------------
+// Cross-lane helpers over the aligned group of L lanes (L = 1, 2, 4, 8, 16)
+// holding this lane: DPP quad permutes (lane ^ 1, lane ^ 2) and the 8- and
+// 16-lane mirrors, each pairing the halves of the next larger group, so
+// every lane of the group ends with the group's result.
+template <int CTRL>
+__device__ __forceinline__ unsigned dpp_u32(unsigned x)
+{
+    return (unsigned)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
+}
+
+template <int L, class Step>
+__device__ __forceinline__ void group_steps(Step step)
+{
+    if constexpr (L >= 2)
+        step(std::integral_constant<int, 0xB1>{});
+    if constexpr (L >= 4)
+        step(std::integral_constant<int, 0x4E>{});
+    if constexpr (L >= 8)
+        step(std::integral_constant<int, 0x141>{});
+    if constexpr (L >= 16)
+        step(std::integral_constant<int, 0x140>{});
+}
+
+// lexicographic minimum of (v, j)
+template <int L>
+__device__ __forceinline__ void group_argmin(double &v, int &j)
+{
+    group_steps<L>([&](auto ctrl) {
+        constexpr int C = decltype(ctrl)::value;
+        const unsigned long long b = (unsigned long long)__double_as_longlong(v);
+        const unsigned lo = dpp_u32<C>((unsigned)b), hi = dpp_u32<C>((unsigned)(b >> 32));
+        const int jo = (int)dpp_u32<C>((unsigned)j);
+        const double vo = __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+        if (vo < v || (vo == v && jo < j)) {
+            v = vo;
+            j = jo;
+        }
+    });
+}
+
+template <int L>
+__device__ __forceinline__ unsigned group_sum(unsigned x)
+{
+    group_steps<L>([&](auto ctrl) { x += dpp_u32<decltype(ctrl)::value>(x); });
+    return x;
+}
+
+template <int L>
+__device__ __forceinline__ unsigned long long group_or(unsigned long long x)
+{
+    group_steps<L>([&](auto ctrl) {
+        constexpr int C = decltype(ctrl)::value;
+        x |= ((unsigned long long)dpp_u32<C>((unsigned)(x >> 32)) << 32) | dpp_u32<C>((unsigned)x);
+    });
+    return x;
+}
+
+// sum of x over the lanes of the group below this one (gl: lane in group)
+template <int L>
+__device__ __forceinline__ unsigned group_exclusive_sum(unsigned x, int gl)
+{
+    unsigned inc = x;
+    auto up = [&](auto ctrl, int n) {  // row_shr:n (within the 16-lane row)
+        const unsigned y = dpp_u32<decltype(ctrl)::value>(inc);
+        if (gl >= n)
+            inc += y;
+    };
+    if constexpr (L >= 2)
+        up(std::integral_constant<int, 0x111>{}, 1);
+    if constexpr (L >= 4)
+        up(std::integral_constant<int, 0x112>{}, 2);
+    if constexpr (L >= 8)
+        up(std::integral_constant<int, 0x114>{}, 4);
+    if constexpr (L >= 16)
+        up(std::integral_constant<int, 0x118>{}, 8);
+    return inc - x;
+}
+
+// Cells along each ray, in float64, by a group of L lanes per ray (lane l
+// holds the sites [l m, (l + 1) m), m = ceil(K / L)).  From t0 = near, c is
+// the nearest site; moving along the ray, site j overtakes c where
+// f_j(t) = |x(t) - phi_j|^2 - |x(t) - phi_c|^2, a linear function of t with
+// slope 2 d.(phi_c - phi_j), reaches 0 from above; the segment of c ends at
+// the first such crossing (or at far), and the ray enters the crossing
+// site's cell.  Each move strictly increases d.phi of the current site, so a
+// ray takes at most K segments and never returns to a cell.
+//
+// Each segment keeps, in ascending order, c and every site j with
+// min(f_j(t0), f_j(t1)) <= tau at its ends t0, t1 (tau = 1e-4 (1 + the
+// squared distances to c there)).  f_j is linear, so a site left out is
+// farther than c by more than tau on the whole segment -- far above the
+// float32 rounding of the squared distances (a few ulp) -- and can neither
+// be the float32 nearest site of a sample in the segment nor tie with it:
+// the float32 argmin over the segment's candidates is the float32 argmin over
+// all sites, whatever crossing ends the segment.  A ray with more than
+// kMaxSeg segments, or a segment with more than kMaxCand candidates, is
+// marked (nseg = 0) for the search over all sites.
+template <int L>
+__global__ __launch_bounds__(kThreads) void ray_walk_kernel(RenderGeometry g,
+                                                            const float4 *__restrict__ sites,
+                                                            int num_sites, SegRec *__restrict__ seg,
+                                                            unsigned char *__restrict__ nseg)
+{
+    static_assert(L == 1 || L == 2 || L == 4 || L == 8 || L == 16, "group size");
+    __shared__ float4 s_sites[kMaxSites];
+    for (int k = threadIdx.x; k < num_sites; k += kThreads)
+        s_sites[k] = sites[k];
+    __syncthreads();
+    const size_t r = ((size_t)blockIdx.x * kThreads + threadIdx.x) / L;
+    if (r >= g.num_rays)
+        return;
+    const int gl = threadIdx.x & (L - 1);
+    const int per = (num_sites + L - 1) / L;
+    const int j0 = min(gl * per, num_sites), j1 = min(j0 + per, num_sites);
+    const double ox = g.rays_o[3 * r], oy = g.rays_o[3 * r + 1], oz = g.rays_o[3 * r + 2];
+    const double dx = g.rays_d[3 * r], dy = g.rays_d[3 * r + 1], dz = g.rays_d[3 * r + 2];
+    auto d2 = [&](double x, double y, double z, int k) {
+        const float4 p = s_sites[k];
+        const double ex = x - p.x, ey = y - p.y, ez = z - p.z;
+        return ex * ex + ey * ey + ez * ez;
+    };
+    double t0 = g.near_t;
+    double x0 = ox + t0 * dx, y0 = oy + t0 * dy, z0 = oz + t0 * dz;
+    int c = 0x7FFFFFFF;
+    {
+        double best = INFINITY;
+        for (int k = j0; k < j1; ++k) {
+            const double v = d2(x0, y0, z0, k);
+            if (v < best) {
+                best = v;
+                c = k;
+            }
+        }
+        group_argmin<L>(best, c);
+    }
+    SegRec *out = seg + (size_t)r * kMaxSeg;
+    int ns = 0;
+    bool ok = true;
+    for (;;) {
+        const float4 pc = s_sites[c];
+        const double dc0 = d2(x0, y0, z0, c);
+        // the first crossing: smallest f_j(t0) / (-slope_j) over slope_j < 0
+        double bf = 0.0, bb = 0.0;
+        int nextc = 0x7FFFFFFF;
+        for (int j = j0; j < j1; ++j) {
+            if (j == c)
+                continue;
+            const float4 pj = s_sites[j];
+            const double b = 2.0 * (dx * ((double)pc.x - pj.x) + dy * ((double)pc.y - pj.y) +
+                                    dz * ((double)pc.z - pj.z));
+            if (b < 0.0) {
+                const double f0 = fmax(d2(x0, y0, z0, j) - dc0, 0.0);
+                if (nextc == 0x7FFFFFFF || f0 * -bb < bf * -b) {
+                    bf = f0;
+                    bb = b;
+                    nextc = j;
+                }
+            }
+        }
+        double q = nextc == 0x7FFFFFFF ? INFINITY : bf / -bb;
+        group_argmin<L>(q, nextc);
+        double t1 = g.far_t;
+        if (nextc != 0x7FFFFFFF && t0 + q < t1)
+            t1 = t0 + q;
+        else
+            nextc = -1;
+        const double x1 = ox + t1 * dx, y1 = oy + t1 * dy, z1 = oz + t1 * dz;
+        const double dc1 = d2(x1, y1, z1, c);
+        const double tau = 1e-4 * (1.0 + fmax(dc0, dc1));
+        // this lane's candidates, ascending, as a byte string (at most 12 kept)
+        unsigned long long lo = 0, hi = 0;
+        unsigned cl = 0;
+        for (int j = j0; j < j1; ++j) {
+            bool take = j == c;
+            if (!take)
+                take = fmin(d2(x0, y0, z0, j) - dc0, d2(x1, y1, z1, j) - dc1) <= tau;
+            if (take) {
+                if (cl < 8)
+                    lo |= (unsigned long long)j << (8 * cl);
+                else if (cl < 12)
+                    hi |= (unsigned long long)j << (8 * (cl - 8));
+                cl = min(cl + 1, 12u);
+            }
+        }
+        const unsigned nc = group_sum<L>(cl);
+        if (nc > (unsigned)kMaxCand || ns == kMaxSeg) {
+            ok = false;
+            break;
+        }
+        // the group's list in lane order (ascending sites), after the count byte
+        const int k = 8 * (int)(group_exclusive_sum<L>(cl, gl) + 1);
+        if (k >= 64) {
+            hi = lo << (k - 64);
+            lo = 0;
+        } else {
+            hi = (hi << k) | (lo >> (64 - k));
+            lo <<= k;
+        }
+        lo = group_or<L>(lo);
+        hi = group_or<L>(hi);
+        if (gl == 0) {
+            const float te = nextc < 0 ? INFINITY : (float)t1;
+            *reinterpret_cast<uint4 *>(out + ns) = make_uint4(
+                __float_as_uint(te), (unsigned)lo | nc, (unsigned)(lo >> 32), (unsigned)hi);
+        }
+        ++ns;
+        if (nextc < 0)
+            break;
+        t0 = t1;
+        x0 = x1;
+        y0 = y1;
+        z0 = z1;
+        c = nextc;
+    }
+    if (gl == 0)
+        nseg[r] = ok ? (unsigned char)ns : 0;
+}
+
+// Owning cell of a sample at x (depth t): through its ray's walk table tab
+// of ns segments (the float32 nearest among the segment's candidates,
+// ascending), or, with ns == 0, over all sites.
+__device__ __forceinline__ unsigned nearest_site(const float4 *s_sites, int num_sites,
+                                                 const SegRec *tab, unsigned ns, float t,
+                                                 float x, float y, float z)
+{
+    float best = INFINITY;
+    unsigned bk = 0;
+    auto consider = [&](unsigned k) {
+        const float4 p = s_sites[k];
+        const float ex = x - p.x, ey = y - p.y, ez = z - p.z;
+        const float d2 = fmaf(ez, ez, fmaf(ey, ey, ex * ex));
+        if (d2 < best) {
+            best = d2;
+            bk = k;
+        }
+    };
+    if (ns == 0) {
+        for (int k = 0; k < num_sites; ++k)
+            consider(k);
+        return bk;
+    }
+    // the first segment whose end is >= t (the last one's end is +inf)
+    unsigned lo = 0, hi = ns - 1;
+    while (lo < hi) {
+        const unsigned mid = (lo + hi) >> 1;
+        if (tab[mid].t_end >= t)
+            hi = mid;
+        else
+            lo = mid + 1;
+    }
+    const uint4 rec = *reinterpret_cast<const uint4 *>(tab + lo);
+    const unsigned nc = rec.y & 0xFFu;
+    const unsigned words[3] = {rec.y, rec.z, rec.w};
+#pragma unroll
+    for (unsigned q = 0; q < (unsigned)kMaxCand; ++q)
+        if (q < nc)
+            consider((words[(q + 1) >> 2] >> (8 * ((q + 1) & 3))) & 0xFFu);
+    return bk;
+}
+
 // Stratified depths t, owning cell (nearest site, ties to the lowest index)
 // and per-block head histograms.  Block b covers samples
 // [b * kBucketBlock, (b + 1) * kBucketBlock); each thread takes 4 consecutive
 // samples per round, so one Philox block serves 4 samples of a ray.  With
 // FROM_T the depths are given (t is read, not written): the assignment of
-// the inverse-CDF samples of hierarchical sampling.
-template <bool FROM_T>
+// the inverse-CDF samples of hierarchical sampling.  WALK: the owning cell
+// comes from the ray's walk table (nearest_site), which gives the same cell
+// as the search over all sites.
+template <bool FROM_T, bool WALK>
 __global__ __launch_bounds__(kThreads) void sample_assign_kernel(
     RenderGeometry g, const float4 *__restrict__ sites, int num_sites, int site_bits,
-    float *__restrict__ t_out, uint8_t *__restrict__ cell_out, unsigned *__restrict__ counts,
-    unsigned num_blocks)
+    WalkTable walk, float *__restrict__ t_out, uint8_t *__restrict__ cell_out,
+    unsigned *__restrict__ counts, unsigned num_blocks)
 {
     __shared__ float4 s_sites[kMaxSites];
     __shared__ unsigned s_hist[kMaxSites];
+    // walk tables of the block's rays, when they are few enough (n >= ~108)
+    constexpr int kStageRays = 40;
+    __shared__ SegRec s_seg[WALK ? kStageRays * kMaxSeg : 1];
+    __shared__ unsigned char s_nseg[WALK ? kStageRays : 1];
     for (int k = threadIdx.x; k < num_sites; k += kThreads) {
         s_sites[k] = sites[k];
         s_hist[k] = 0;
     }
+    const unsigned block_base = blockIdx.x * (unsigned)kBucketBlock;
+    unsigned r_first = 0;
+    bool staged = false;
+    if constexpr (WALK) {
+        unsigned i_;
+        unsigned r_last;
+        split_sample(block_base, g.n, g.inv_n, r_first, i_);
+        split_sample(min(block_base + kBucketBlock, g.num_samples) - 1, g.n, g.inv_n, r_last, i_);
+        staged = r_last - r_first < (unsigned)kStageRays;
+        if (staged) {
+            const unsigned nr = r_last - r_first + 1;
+            for (unsigned q = threadIdx.x; q < nr; q += kThreads)
+                s_nseg[q] = walk.nseg[r_first + q];
+            __syncthreads();
+            // the rays' written records only
+            const uint4 *src = reinterpret_cast<const uint4 *>(walk.seg + (size_t)r_first * kMaxSeg);
+            for (unsigned q = threadIdx.x; q < nr * kMaxSeg; q += kThreads)
+                if (q % kMaxSeg < s_nseg[q / kMaxSeg])
+                    reinterpret_cast<uint4 *>(s_seg)[q] = src[q];
+        }
+    }
     __syncthreads();
+    // walk table and segment count of ray r (count 0: search all sites)
+    auto table_of = [&](unsigned r, unsigned &ns) -> const SegRec * {
+        if constexpr (WALK) {
+            if (staged) {
+                ns = s_nseg[r - r_first];
+                return s_seg + (r - r_first) * kMaxSeg;
+            }
+            ns = walk.nseg[r];
+            return walk.seg + (size_t)r * kMaxSeg;
+        } else {
+            ns = 0;
+            return nullptr;
+        }
+    };
 
     const uint2 key = make_uint2((unsigned)g.seed, (unsigned)(g.seed >> 32));
-    const unsigned block_base = blockIdx.x * (unsigned)kBucketBlock;
     const uint64_t lane_bit = 1ull << (threadIdx.x & 63);
     for (int round = 0; round < kBucketBlock / (4 * kThreads); ++round) {
         const unsigned s0 = block_base + round * (4 * kThreads) + 4 * threadIdx.x;
@@ -173,19 +474,10 @@ __global__ __launch_bounds__(kThreads) void sample_assign_kernel(
                     t = fmaf(g.step, (float)i + xi, g.near_t);
                 }
                 const float x = fmaf(t, dx, ox), y = fmaf(t, dy, oy), z = fmaf(t, dz, oz);
-                float best = INFINITY;
-                unsigned bk = 0;
-                for (int k = 0; k < num_sites; ++k) {
-                    const float4 p = s_sites[k];
-                    const float ex = x - p.x, ey = y - p.y, ez = z - p.z;
-                    const float d2 = fmaf(ez, ez, fmaf(ey, ey, ex * ex));
-                    if (d2 < best) {
-                        best = d2;
-                        bk = k;
-                    }
-                }
                 tv[v] = t;
-                cv[v] = bk;
+                unsigned ns;
+                const SegRec *tab = table_of(r, ns);
+                cv[v] = nearest_site(s_sites, num_sites, tab, ns, t, x, y, z);
             }
             // next sample of the same thread
             if (++i == g.n) {
@@ -215,172 +507,6 @@ __global__ __launch_bounds__(kThreads) void sample_assign_kernel(
             if (ok && (peers & (lane_bit - 1)) == 0)
                 atomicAdd(&s_hist[cv[v]], (unsigned)__popcll(peers));
         }
-    }
-    __syncthreads();
-    for (int k = threadIdx.x; k < num_sites; k += kThreads)
-        counts[(size_t)k * num_blocks + blockIdx.x] = s_hist[k];
-}
-
-// Wave-wide minimum / maximum, result in every lane, without LDS: DPP
-// within each 16-lane row (quad swaps, half-row and row mirrors), then the
-// row-pair and half swaps.
-template <bool MAX>
-__device__ __forceinline__ float wave_reduce(float v)
-{
-    auto op = [](float a, float b) { return MAX ? fmaxf(a, b) : fminf(a, b); };
-    auto dpp = [](float x, auto ctrl) {
-        return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), decltype(ctrl)::value, 0xF, 0xF, false));
-    };
-    v = op(v, dpp(v, std::integral_constant<int, 0xB1>{}));   // quad_perm [1,0,3,2]
-    v = op(v, dpp(v, std::integral_constant<int, 0x4E>{}));   // quad_perm [2,3,0,1]
-    v = op(v, dpp(v, std::integral_constant<int, 0x141>{}));  // row_half_mirror
-    v = op(v, dpp(v, std::integral_constant<int, 0x140>{}));  // row_mirror
-    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    v = op(__uint_as_float(a[0]), __uint_as_float(a[1]));
-    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    return op(__uint_as_float(b[0]), __uint_as_float(b[1]));
-}
-__device__ __forceinline__ float wave_min(float v) { return wave_reduce<false>(v); }
-__device__ __forceinline__ float wave_max(float v) { return wave_reduce<true>(v); }
-
-// Heads at or above this count use site pruning in the assignment (below it
-// the brute force over all sites costs less than the per-slice bounds).
-constexpr int kPruneSites = 48;
-
-// The same, for many heads: in a round wave w takes 256 consecutive
-// samples, lane l the samples l + 64 v (v = 0..3), so each v is a slice of
-// 64 consecutive samples -- a short piece of one or two rays.  Per slice the
-// wave takes the bounding box of its sample points and
-// keeps only the sites whose smallest squared distance to the box is within
-// a factor 1 + 1e-4 of the smallest largest squared distance of any site to
-// the box.  For every point of the box a dropped site is farther, by more
-// than that relative margin, than the site attaining that bound, and the
-// float32 distances are accurate to a few ulp, so a dropped site can neither
-// win nor tie: the argmin over the kept sites (in ascending index order,
-// same arithmetic) is the argmin over all sites.
-template <bool FROM_T>
-__global__ __launch_bounds__(kThreads) void sample_assign_pruned_kernel(
-    RenderGeometry g, const float4 *__restrict__ sites, int num_sites, int site_bits,
-    float *__restrict__ t_out, uint8_t *__restrict__ cell_out, unsigned *__restrict__ counts,
-    unsigned num_blocks)
-{
-    __shared__ float4 s_sites[kMaxSites];
-    __shared__ unsigned s_hist[kMaxSites];
-    for (int k = threadIdx.x; k < num_sites; k += kThreads) {
-        s_sites[k] = sites[k];
-        s_hist[k] = 0;
-    }
-    __syncthreads();
-
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const uint64_t lane_bit = 1ull << lane;
-    const uint2 key = make_uint2((unsigned)g.seed, (unsigned)(g.seed >> 32));
-    const unsigned block_base = blockIdx.x * (unsigned)kBucketBlock;
-    // with n % 4 == 0 the 4 samples sharing a generator block sit in 4
-    // neighbouring lanes: each lane computes one block and they trade words
-    const bool quad = (g.n & 3u) == 0;
-    for (int round = 0; round < kBucketBlock / (4 * kThreads); ++round) {
-        const unsigned wbase = block_base + round * (4 * kThreads) + wv * 256;
-        uint4 qb = make_uint4(0, 0, 0, 0);
-        if constexpr (!FROM_T) {
-            if (g.perturb && quad) {
-                // lane L: block of samples wbase + 64 (L / 16) + 4 (L % 16) + 0..3
-                const unsigned sq = wbase + 64 * (lane >> 4) + 4 * (lane & 15);
-                unsigned rq, iq;
-                split_sample(sq < g.num_samples ? sq : 0, g.n, g.inv_n, rq, iq);
-                const uint64_t rg = g.ray_offset + rq;
-                qb = philox4x32_10(make_uint4(iq >> 2, (unsigned)rg, (unsigned)(rg >> 32), 0u), key);
-            }
-        }
-        float tv[4];
-        unsigned cv[4];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const unsigned s = wbase + 64 * v + lane;
-            const bool ok = s < g.num_samples;
-            unsigned r, i;
-            split_sample(ok ? s : 0, g.n, g.inv_n, r, i);
-            float t;
-            if constexpr (FROM_T) {
-                t = ok ? t_out[s] : 0.0f;
-            } else {
-                float xi = 0.5f;
-                if (g.perturb) {
-                    unsigned w;
-                    if (quad) {
-                        const int src = 16 * v + (lane >> 2);
-                        const unsigned w0 = __shfl(qb.x, src), w1 = __shfl(qb.y, src);
-                        const unsigned w2 = __shfl(qb.z, src), w3 = __shfl(qb.w, src);
-                        const unsigned q = lane & 3;
-                        w = q == 0 ? w0 : q == 1 ? w1 : q == 2 ? w2 : w3;
-                    } else {
-                        const uint64_t rg = g.ray_offset + r;
-                        w = philox_word(philox4x32_10(make_uint4(i >> 2, (unsigned)rg, (unsigned)(rg >> 32), 0u), key),
-                                        i & 3u);
-                    }
-                    xi = (float)(w >> 8) * 0x1.0p-24f;
-                }
-                t = fmaf(g.step, (float)i + xi, g.near_t);
-            }
-            const float x = fmaf(t, g.rays_d[3 * r], g.rays_o[3 * r]);
-            const float y = fmaf(t, g.rays_d[3 * r + 1], g.rays_o[3 * r + 1]);
-            const float z = fmaf(t, g.rays_d[3 * r + 2], g.rays_o[3 * r + 2]);
-
-            float best = INFINITY;
-            unsigned bk = 0;
-            const float lx = wave_min(ok ? x : INFINITY), hx = wave_max(ok ? x : -INFINITY);
-            const float ly = wave_min(ok ? y : INFINITY), hy = wave_max(ok ? y : -INFINITY);
-            const float lz = wave_min(ok ? z : INFINITY), hz = wave_max(ok ? z : -INFINITY);
-            // smallest over sites of the largest squared distance to the box
-            float thr = INFINITY;
-            for (int k = lane; k < num_sites; k += 64) {
-                const float4 p = s_sites[k];
-                const float ax = fmaxf(p.x - lx, hx - p.x), ay = fmaxf(p.y - ly, hy - p.y);
-                const float az = fmaxf(p.z - lz, hz - p.z);
-                thr = fminf(thr, fmaf(az, az, fmaf(ay, ay, ax * ax)));
-            }
-            thr = wave_min(thr) * (1.0f + 1e-4f);
-            for (int m = 0; 64 * m < num_sites; ++m) {
-                const int kl = 64 * m + lane;
-                bool keep = false;
-                if (kl < num_sites) {
-                    const float4 p = s_sites[kl];
-                    const float bx = fmaxf(fmaxf(lx - p.x, p.x - hx), 0.0f);
-                    const float by = fmaxf(fmaxf(ly - p.y, p.y - hy), 0.0f);
-                    const float bz = fmaxf(fmaxf(lz - p.z, p.z - hz), 0.0f);
-                    keep = fmaf(bz, bz, fmaf(by, by, bx * bx)) <= thr;
-                }
-                uint64_t mk = __ballot(keep);
-                while (mk) {
-                    const int k = 64 * m + __builtin_ctzll(mk);
-                    mk &= mk - 1;
-                    const float4 p = s_sites[k];
-                    const float ex = x - p.x, ey = y - p.y, ez = z - p.z;
-                    const float d2 = fmaf(ez, ez, fmaf(ey, ey, ex * ex));
-                    if (d2 < best) {
-                        best = d2;
-                        bk = k;
-                    }
-                }
-            }
-            tv[v] = t;
-            cv[v] = ok ? bk : 0xFFFFFFFFu;
-            if (ok) {
-                if constexpr (!FROM_T)
-                    t_out[s] = t;
-                cell_out[s] = (uint8_t)bk;
-            }
-        }
-        // histogram: the lowest lane of each group of equal cells adds the group size
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const bool ok = wbase + 64 * v + lane < g.num_samples;
-            const uint64_t valid = __ballot(ok);
-            const uint64_t peers = match_peers(cv[v], site_bits, valid);
-            if (ok && (peers & (lane_bit - 1)) == 0)
-                atomicAdd(&s_hist[cv[v]], (unsigned)__popcll(peers));
-        }
-        (void)tv;
     }
     __syncthreads();
     for (int k = threadIdx.x; k < num_sites; k += kThreads)
@@ -629,7 +755,7 @@ __global__ __launch_bounds__(kThreads) void debug_expand_kernel(
     }
 }
 
-inline unsigned blocks_for(unsigned items, unsigned per) { return (items + per - 1) / per; }
+inline unsigned blocks_for(size_t items, unsigned per) { return (unsigned)((items + per - 1) / per); }
 
 }  // namespace
 
@@ -643,30 +769,48 @@ hipError_t launch_ray_encode(const RenderGeometry &g, void *dirbuf, bool bf16, h
     return hipGetLastError();
 }
 
-hipError_t launch_sample_assign(const RenderGeometry &g, const float4 *sites, int num_sites,
-                                int site_bits, float *t, uint8_t *cell, unsigned *counts,
-                                unsigned num_blocks, hipStream_t s)
+hipError_t launch_ray_walk(const RenderGeometry &g, const float4 *sites, int num_sites,
+                           SegRec *seg, unsigned char *nseg, hipStream_t s)
 {
-    if (num_sites >= kPruneSites)
-        sample_assign_pruned_kernel<false><<<num_blocks, kThreads, 0, s>>>(
-            g, sites, num_sites, site_bits, t, cell, counts, num_blocks);
+    // 1, 2 or 4 lanes per ray: enough waves in flight to hide the float64
+    // latency of short frames, no more reductions than needed for long ones
+    if (g.num_rays >= (1u << 19))
+        ray_walk_kernel<1><<<blocks_for(g.num_rays, kThreads), kThreads, 0, s>>>(g, sites, num_sites,
+                                                                                 seg, nseg);
+    else if (g.num_rays >= (1u << 18))
+        ray_walk_kernel<2><<<blocks_for((size_t)g.num_rays * 2, kThreads), kThreads, 0, s>>>(
+            g, sites, num_sites, seg, nseg);
     else
-        sample_assign_kernel<false><<<num_blocks, kThreads, 0, s>>>(
-            g, sites, num_sites, site_bits, t, cell, counts, num_blocks);
+        ray_walk_kernel<4><<<blocks_for((size_t)g.num_rays * 4, kThreads), kThreads, 0, s>>>(
+            g, sites, num_sites, seg, nseg);
+    return hipGetLastError();
+}
+
+hipError_t launch_sample_assign(const RenderGeometry &g, const float4 *sites, int num_sites,
+                                int site_bits, const WalkTable &walk, float *t, uint8_t *cell,
+                                unsigned *counts, unsigned num_blocks, hipStream_t s)
+{
+    if (walk.seg)
+        sample_assign_kernel<false, true><<<num_blocks, kThreads, 0, s>>>(
+            g, sites, num_sites, site_bits, walk, t, cell, counts, num_blocks);
+    else
+        sample_assign_kernel<false, false><<<num_blocks, kThreads, 0, s>>>(
+            g, sites, num_sites, site_bits, walk, t, cell, counts, num_blocks);
     return hipGetLastError();
 }
 
 hipError_t launch_assign_given(const RenderGeometry &g, const float4 *sites, int num_sites,
-                               int site_bits, const float *t, uint8_t *cell, unsigned *counts,
-                               unsigned num_blocks, hipStream_t s)
+                               int site_bits, const WalkTable &walk, const float *t,
+                               uint8_t *cell, unsigned *counts, unsigned num_blocks,
+                               hipStream_t s)
 {
-    // t is only read in this instantiation
-    if (num_sites >= kPruneSites)
-        sample_assign_pruned_kernel<true><<<num_blocks, kThreads, 0, s>>>(
-            g, sites, num_sites, site_bits, const_cast<float *>(t), cell, counts, num_blocks);
+    // t is only read in these instantiations
+    if (walk.seg)
+        sample_assign_kernel<true, true><<<num_blocks, kThreads, 0, s>>>(
+            g, sites, num_sites, site_bits, walk, const_cast<float *>(t), cell, counts, num_blocks);
     else
-        sample_assign_kernel<true><<<num_blocks, kThreads, 0, s>>>(
-            g, sites, num_sites, site_bits, const_cast<float *>(t), cell, counts, num_blocks);
+        sample_assign_kernel<true, false><<<num_blocks, kThreads, 0, s>>>(
+            g, sites, num_sites, site_bits, walk, const_cast<float *>(t), cell, counts, num_blocks);
     return hipGetLastError();
 }
 

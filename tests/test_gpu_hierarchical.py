@@ -239,7 +239,7 @@ def test_hier_sample_count_edges(nc, nf, n_rays):
 
 
 def test_hier_many_heads_slice():
-    """64 skewed heads of 6x64 (pruned assignment of the given fine depths),
+    """64 skewed heads of 6x64 (walk-table assignment of the given fine depths),
     32 coarse + 32 fine samples, on a contiguous slice of the 1024x1024 frame."""
     cfg = scenes.CONFIGS["skew_k64"]
     sc = scenes.make_scene(cfg)

@@ -124,7 +124,7 @@ def _subset_parity(name, precision, n_rays, sigma_bias=None, check_cells=True):
 
 def test_headline_frame_with_64_heads():
     """The headline frame and 8x128 heads with K = 64 k-means sites (the top of
-    the K sweep, where the assignment prunes sites per 64-sample slice):
+    the K sweep, where the assignment goes through the per-ray walk tables):
     full-frame cells bit-exact, pixels on a subset."""
     cfg = scenes.with_changes(scenes.CONFIGS["derf_k16"], num_sites=64)
     sc = scenes.make_scene(cfg)
@@ -173,8 +173,8 @@ def test_skew_k64_cells_slice():
 @pytest.mark.parametrize("sites", [4, 64])
 @pytest.mark.parametrize("n", [1, 3, 7, 33, 200])
 def test_ragged_sample_counts(n, sites):
-    """Sample counts that are not multiples of 4 or of 64, with brute-force
-    (4 heads) and pruned (64 heads) assignment."""
+    """Sample counts that are not multiples of 4 or of 64, with the search over
+    all sites (4 heads) and the walk-table assignment (64 heads)."""
     cfg = scenes.CONFIGS["tiny"]
     sc = scenes.make_scene(scenes.with_changes(cfg, sigma_bias=2.0, num_sites=sites))
     R = 333
@@ -204,6 +204,30 @@ def test_many_sites_and_empty_heads():
     ids = np.arange(0, cfg.num_rays, 3)
     ref = _oracle(sc, ids)
     _check_pixels(gpu, ref, ids, TOL["fp32"], "tiny K=256")
+
+
+@pytest.mark.parametrize("sites", [28, 33, 64, 100, 256])
+@pytest.mark.parametrize("layout", ["uniform", "gmm_kmeans"])
+def test_walk_site_counts(sites, layout):
+    """Cells from the per-ray walk tables (4 lanes per ray on this frame, site
+    blocks of ceil(K / 4), some lanes with none) equal the oracle's search over
+    all sites."""
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], width=96, height=64, num_sites=sites,
+                              sites=layout)
+    sc = scenes.make_scene(cfg)
+    gpu = _render(sc, "fp32", debug=True)
+    _check_cells(sc, gpu[3]["t"], gpu[3]["cell"], cfg.n_coarse, "walk K=%d %s" % (sites, layout))
+
+
+@pytest.mark.parametrize("size", [(512, 512), (1024, 512)])
+def test_walk_lane_counts(size):
+    """Frames of 2^18 and 2^19 rays, which the walk takes with 2 lanes and 1
+    lane per ray."""
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], width=size[0], height=size[1],
+                              num_sites=40, sites="gmm_kmeans")
+    sc = scenes.make_scene(cfg)
+    gpu = _render(sc, "bf16", debug=True)
+    _check_cells(sc, gpu[3]["t"], gpu[3]["cell"], cfg.n_coarse, "walk %dx%d" % size)
 
 
 def test_far_sites_leave_heads_empty():

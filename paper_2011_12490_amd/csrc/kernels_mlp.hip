@@ -8,10 +8,11 @@
 // Work split.  A workgroup of 4 waves (one per SIMD) takes a tile of one
 // head's samples, NB x 32 per wave, and runs it through the whole network
 // with the activations held in registers.  Two workgroups share a CU (one for
-// width 256); they do not synchronise with each other, so one's barriers and
-// gathers are covered by the other's matrix work.  Workgroups are persistent
-// and walk contiguous tile ranges, mapped so that each XCD (which has its own
-// L2) works on a contiguous stretch of heads.
+// width 256, three for bf16 width 64); they do not synchronise with each
+// other, so one's barriers and gathers are covered by another's matrix work.
+// Workgroups are persistent and take tiles from per-XCD queues, each over a
+// contiguous stretch of tiles (so an XCD's L2 sees few heads), stealing from
+// the other stretches when their own runs out.
 //
 // Operand layout (v_mfma_f32_32x32x16_bf16 / v_mfma_f32_32x32x2_f32):
 // weights are the A operand (32 output rows x k), samples the B operand
@@ -22,7 +23,7 @@
 // with no data movement.
 //
 // Weight streaming.  A head's weights are cut into stages -- one 32-row
-// output tile and at most 8 KB of its input chunks -- laid out as 1 KB units
+// output tile and at most UMAX KB of its input chunks -- laid out as 1 KB units
 // that are exactly one wave's A-operand registers.  Stages stream
 // global -> LDS (global_load_lds_dwordx4, issued as asm so the compiler's
 // LDS wait bookkeeping stays exact) through an 8-slot ring, six stages ahead
@@ -82,7 +83,9 @@ struct Cfg {
     static constexpr int NB = BF16 ? 2 : 1;    // 32-sample column blocks per wave
     static constexpr int WAVES = 4;
     static constexpr int THREADS = WAVES * 64;
-    static constexpr int WG_PER_CU = W >= 256 ? 1 : 2;
+    // 64-wide bf16 heads: three workgroups per CU (4 KB ring slots, at most
+    // 168 VGPRs), so that more waves hide the per-tile gathers and encoding
+    static constexpr int WG_PER_CU = W >= 256 ? 1 : (BF16 && W == 64 ? 3 : 2);
     static constexpr int TILE = WAVES * NB * 32;
     static constexpr int P = 3 + 6 * LP;       // gamma(x) length
     static constexpr int DD = 27;              // gamma(d) length (4 frequencies)
@@ -94,7 +97,7 @@ struct Cfg {
     static constexpr int MTR = (RH + 31) / 32; // output tiles of the colour hidden layer
     static constexpr int ERH = MTR * 16;       // colour-hidden entries per lane
     static constexpr int EXC = EX / E, EHC = EH / E, EDC = ED / E, ERHC = ERH / E;
-    static constexpr int UMAX = 8;             // units per stage
+    static constexpr int UMAX = BF16 && W == 64 ? 4 : 8;  // units per stage
     static constexpr int CMAX = UMAX * CPU;    // chunks per stage
     static constexpr int NBUF = 8;             // LDS ring slots (power of two)
     static constexpr int G = 2;                // stages per barrier
@@ -236,6 +239,15 @@ struct Cfg {
     static constexpr int HB_OFF = NBUF * SLOT_BYTES;
     static constexpr int LDS_BYTES = HB_OFF + BLOCK_FLOATS * 4;
     static_assert(WG_PER_CU * (LDS_BYTES + 3 * 1024) <= 160 * 1024, "LDS budget");
+    // a stage's loads cover its units padded to a multiple of WAVES
+    static constexpr int max_units_pad()
+    {
+        int m = 0;
+        for (int q = 0; q < NS; ++q)
+            m = TAB.lpw[q] * WAVES > m ? TAB.lpw[q] * WAVES : m;
+        return m;
+    }
+    static_assert(max_units_pad() * 1024 <= SLOT_BYTES, "a stage overflows its ring slot");
 };
 
 // Input column (in the packed layer's input order) of lane-entry e of lane

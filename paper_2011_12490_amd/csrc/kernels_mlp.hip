@@ -194,6 +194,13 @@ struct Cfg {
     static constexpr int S_GDUSE = first_stage_of_tile(RH > 0 ? D * MT : D * MT + MTR);
     static constexpr int S_GD = S_GDUSE >= 4 ? (S_GDUSE - 4) / G * G : 0;  // a group start
     static constexpr int NGD = NB * (BF16 ? 2 : 4);  // gamma(d) load instructions per wave
+    // The next tile's sample records are prefetched into LDS during this one:
+    // its bucket ids at group start S_PA (NPA loads per wave), then, once the
+    // group wait of S_PB has covered those, its depths and ray origins and
+    // directions (NPB loads per wave).  The last tile re-reads its own, so
+    // that the wait counts do not depend on whether a next tile exists.
+    static constexpr int S_PA = 0, S_PB = LA;
+    static constexpr int NPA = 1, NPB = 7;
 
     // Barrier groups: stages [a, a + G) of a tile share one barrier.  At a
     // group start a the wave issues the weight loads of stages a + LA ..
@@ -226,18 +233,39 @@ struct Cfg {
             }
             if (g == S_GD)
                 cnt += NGD;
+            if (g == S_PA)
+                cnt += NPA;
+            if (g == S_PB)
+                cnt += NPB;
         }
         return cnt;
     }
+    // loads this wave issues after the S_PB prefetch until the next tile
+    // starts (it has one: its records were prefetched)
+    static constexpr int loads_after_pb()
+    {
+        int cnt = 0;
+        for (int g = S_PB + G; g < NS; g += G)
+            for (int x = g + LA; x <= grp_end(g) + LA; ++x)
+                cnt += x < NS ? st_lpw(x) : st_lpw(x - NS);
+        return cnt + (S_GD > S_PB ? NGD : 0);
+    }
+    static_assert(S_PA % G == 0 && S_PB % G == 0 && S_PB < NS, "prefetch at group starts");
+    // the group wait at S_PB covers the S_PA loads: the loads it waits for
+    // were issued at a later group start
+    static_assert((need(S_PB) - LA) / G * G > S_PA, "prefetch phases too close");
 
     // per-head resident block: bias of every output tile in accumulator layout
     static constexpr int BLOCK_FLOATS = (NT * 32 + 255) / 256 * 256;
     static constexpr int BLOCK_UNITS = BLOCK_FLOATS / 256;
 
-    // LDS: ring | head block
+    // LDS: ring | head block | per wave: the next tile's sample records
+    // (bucket id, depth, origin xyz, direction xyz; 64 dwords each)
     static constexpr int SLOT_BYTES = UMAX * 1024;
     static constexpr int HB_OFF = NBUF * SLOT_BYTES;
-    static constexpr int LDS_BYTES = HB_OFF + BLOCK_FLOATS * 4;
+    static constexpr int PF_OFF = HB_OFF + BLOCK_FLOATS * 4;
+    static constexpr int PF_WAVE = 8 * 64 * 4;
+    static constexpr int LDS_BYTES = PF_OFF + WAVES * PF_WAVE;
     static_assert(WG_PER_CU * (LDS_BYTES + 3 * 1024) <= 160 * 1024, "LDS budget");
     // a stage's loads cover its units padded to a multiple of WAVES
     static constexpr int max_units_pad()
@@ -424,6 +452,17 @@ __device__ __forceinline__ void load_lds16(const unsigned char *base, unsigned v
     const unsigned l = (unsigned)(unsigned long)(__attribute__((address_space(3))) unsigned char *)lds_base;
     asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
                  :: "s"(__builtin_amdgcn_readfirstlane(l)), "v"(voff), "s"(base)
+                 : "memory");
+}
+
+// One wave gathers 64 dwords global -> LDS: lane l reads *p and the dword
+// lands at lds_base + 4 l (lds_base wave-uniform).  Asm for the same reasons
+// as load_lds16.
+__device__ __forceinline__ void load_lds4(const void *p, unsigned char *lds_base)
+{
+    const unsigned l = (unsigned)(unsigned long)(__attribute__((address_space(3))) unsigned char *)lds_base;
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off"
+                 :: "s"(__builtin_amdgcn_readfirstlane(l)), "v"(p)
                  : "memory");
 }
 
@@ -635,6 +674,10 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
     };
     auto slot = [&](unsigned k) { return lds + (k & (C::NBUF - 1)) * C::SLOT_BYTES; };
     unsigned char *const lds_wave = lds + wave * 1024;
+    // this wave's records of the next tile: [0] bucket id, [1] depth,
+    // [2..4] origin, [5..7] direction, slot q = sample nb * 32 + n
+    unsigned char *const pf_wave = lds + C::PF_OFF + wave * C::PF_WAVE;
+    const unsigned *const pf = reinterpret_cast<const unsigned *>(pf_wave);
     // issue this wave's share of stage s's units into ring slot k
     auto issue = [&](auto sc, const unsigned char *src, unsigned k) {
         constexpr int s = decltype(sc)::value;
@@ -647,8 +690,36 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
         asm volatile("" ::: "memory");
     };
 
+    // the two prefetch phases for the tile whose rows are [r0, r_end)
+    auto prefetch_ids = [&](unsigned r0, unsigned r_end) {
+        // bucket ids (rows past the head's end read row 0's)
+        const unsigned row = r0 + wave * (NB * 32) + lane % (NB * 32);
+        load_lds4(bucket + min(row < r_end ? row : r0, geo.num_samples - 1), pf_wave);
+    };
+    auto prefetch_rays = [&]() {
+        // depths, ray origins and directions of the ids in LDS
+        const unsigned sn = min(pf[lane], geo.num_samples - 1);
+        unsigned r = (unsigned)((double)sn * geo.inv_n);
+        if (sn - r * geo.n >= geo.n)
+            ++r;
+        load_lds4(tbuf + sn, pf_wave + 256);
+        const float *o = geo.rays_o + 3 * (size_t)r, *d = geo.rays_d + 3 * (size_t)r;
+#pragma unroll
+        for (int c = 0; c < 3; ++c)
+            load_lds4(o + c, pf_wave + 256 * (2 + c));
+#pragma unroll
+        for (int c = 0; c < 3; ++c)
+            load_lds4(d + c, pf_wave + 256 * (5 + c));
+    };
+
     int head = head_of(tile);
     const unsigned char *stream = stream_of(head);
+    // the first tile's records, waited for in full
+    prefetch_ids(__builtin_amdgcn_readfirstlane(s_off[head] + (tile - s_tile[head]) * C::TILE),
+                 __builtin_amdgcn_readfirstlane(min(s_off[head + 1], geo.num_samples)));
+    wait_vmcnt<0>();
+    prefetch_rays();
+    wait_vmcnt<0>();
     unsigned ring = 0;  // ring slot of stage 0 of the current tile (mod NBUF)
     static_for<0, C::LA>([&](auto sc) { issue(sc, stream, ring + decltype(sc)::value); });
     int loaded_head = -1;
@@ -661,8 +732,15 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
         // rows never pass the sample count when the bucket counts are
         // consistent; the clamps keep every access in bounds regardless
         const unsigned row_end = __builtin_amdgcn_readfirstlane(min(s_off[head + 1], geo.num_samples));
+        // rows of the tile whose records are prefetched (this one's if last)
+        const unsigned pf_tile = has_next ? next : tile;
+        const unsigned nrow0 = __builtin_amdgcn_readfirstlane(s_off[nhead] + (pf_tile - s_tile[nhead]) * C::TILE);
+        const unsigned nrow_end = __builtin_amdgcn_readfirstlane(min(s_off[nhead + 1], geo.num_samples));
 
         wg_barrier();  // previous tile is done with the head block and the staging
+        // this tile's records have landed (at most that many loads were issued
+        // after them)
+        wait_vmcnt<(C::loads_after_pb() < 63 ? C::loads_after_pb() : 63)>();
         // take the tile after next: the attempt on the own stretch is issued
         // here and completes under the prologue's full wait below, so it
         // never disturbs the counted waits of the weight stream
@@ -685,16 +763,17 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
         for (int nb = 0; nb < NB; ++nb) {
             const unsigned row = row0 + (wave * NB + nb) * 32 + n;
             valid[nb] = row < row_end;
-            sid[nb] = min(bucket[min(valid[nb] ? row : row0, geo.num_samples - 1)], geo.num_samples - 1);
+            const unsigned q = nb * 32 + n;
+            sid[nb] = min(pf[q], geo.num_samples - 1);
             unsigned r = (unsigned)((double)sid[nb] * geo.inv_n);
             if (sid[nb] - r * geo.n >= geo.n)
                 ++r;
             ray[nb] = r;
-            const float t = tbuf[sid[nb]];
+            const float t = __uint_as_float(pf[64 + q]);
             float x[3];
 #pragma unroll
             for (int c = 0; c < 3; ++c)
-                x[c] = fmaf(t, geo.rays_d[3 * r + c], geo.rays_o[3 * r + c]);
+                x[c] = fmaf(t, __uint_as_float(pf[64 * (5 + c) + q]), __uint_as_float(pf[64 * (2 + c) + q]));
             xs[nb][0] = x[0];
             xs[nb][1] = x[1];
             xs[nb][2] = x[2];
@@ -831,6 +910,10 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
                     }
                 }
             }
+            if constexpr (s == C::S_PA)
+                prefetch_ids(nrow0, nrow_end);
+            if constexpr (s == C::S_PB)
+                prefetch_rays();  // the group wait above covered the ids
             if constexpr (s + 1 == C::S_SKIP) {
                 // gamma(x) again for the skip layer, overlapping this stage's MFMAs
 #pragma unroll
@@ -930,6 +1013,9 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
         tile = next;
         next = __builtin_amdgcn_readfirstlane(s_q[0]);
     }
+    // the last tile's prefetch re-read its own records: no LDS write may be
+    // in flight when the workgroup's LDS is released
+    wait_vmcnt<0>();
 }
 
 template <class C>

@@ -140,6 +140,10 @@ CONFIGS = {
     # 800x800 object-centric, 64 coarse + 128 fine, 16 heads of 8x256.
     "hier_k16": SceneConfig("hier_k16", 800, 800, "object", 40.0, 2.0, 6.0, 64, 128, 16,
                             "gmm_kmeans", ARCH_NERF, "bf16"),
+    # The headline frame with the grid decomposition: 64 heads of 8x128 whose
+    # cells are a fixed 4x4x4 lattice over [-1, 1]^3 (DeRF-Grid).
+    "grid_k64": SceneConfig("grid_k64", 504, 378, "forward", 60.0, 0.0, 1.0, 192, 0, 64,
+                            "grid", ARCH_128, "bf16"),
     # 1024x1024, 256 samples, 64 skewed heads of 6x64, density bias +2.
     "skew_k64": SceneConfig("skew_k64", 1024, 1024, "object", 40.0, 2.0, 6.0, 256, 0, 64,
                             "ball_mix", ARCH_SMALL, "bf16", sigma_bias=2.0),

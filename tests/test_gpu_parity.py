@@ -170,6 +170,20 @@ def test_skew_k64_cells_slice():
 
 # ------------------------------------------------------------ edge cases ----
 
+def test_grid_decomposition_frame():
+    """The headline frame with the grid decomposition: 64 heads of 8x128 whose
+    cells are the 4x4x4 lattice cubes (many samples sit near cell faces and
+    edges, where the walk keeps several near-tied candidates): full-frame
+    cells bit-exact, pixels on a subset."""
+    cfg = scenes.CONFIGS["grid_k64"]
+    sc = scenes.make_scene(cfg)
+    gpu = _render(sc, "bf16", debug=True)
+    _check_cells(sc, gpu[3]["t"], gpu[3]["cell"], cfg.n_coarse, "grid frame K=64")
+    ids = scenes.ray_subset(512, cfg.num_rays)
+    ref = _oracle(sc, ids)
+    _check_pixels(gpu, ref, ids, TOL["bf16"], "grid frame K=64")
+
+
 @pytest.mark.parametrize("sites", [4, 64])
 @pytest.mark.parametrize("n", [1, 3, 7, 33, 200])
 def test_ragged_sample_counts(n, sites):

@@ -138,6 +138,25 @@ def test_assign_depths_matches_brute_force_and_sample_assign():
     np.testing.assert_array_equal(c2, cs)
 
 
+def test_grid_sites_give_the_lattice_cells():
+    """With sites at the centres of an n x n x n lattice over [-1, 1]^3 (the
+    grid decomposition), the Voronoi cell of a point is its lattice cube:
+    index (i, j, k) = floor((x + 1) n / 2) clamped to the lattice, row-major.
+    Points within 1e-5 of a lattice plane are left out."""
+    rng = np.random.default_rng(21)
+    for n in (2, 4):
+        sites = scenes.make_sites("grid", n ** 3)
+        pts = rng.uniform(-1.3, 1.3, size=(3000, 3)).astype(np.float32)
+        idx = np.clip(np.floor((pts.astype(np.float64) + 1.0) * n / 2.0), 0, n - 1).astype(int)
+        ref = (idx[:, 0] * n + idx[:, 1]) * n + idx[:, 2]
+        planes = -1.0 + 2.0 * np.arange(1, n) / n
+        gap = np.abs(pts[:, :, None].astype(np.float64) - planes[None, None, :]).min(axis=(1, 2))
+        got = np.array([oracle.nearest_site(sites, p) for p in pts])
+        far = gap > 1e-5
+        assert far.mean() > 0.99
+        np.testing.assert_array_equal(got[far], ref[far])
+
+
 def test_nearest_site_ties_go_to_lowest_index():
     sites = np.array([[1, 0, 0], [-1, 0, 0], [1, 0, 0]], np.float32)
     assert oracle.nearest_site(sites, [0, 0, 0]) == 0

@@ -56,6 +56,8 @@ def _lib_handle():
             f.restype = ctypes.c_int
         lib.oracle_render_soft.argtypes = render_sig + [ctypes.c_double]
         lib.oracle_render_soft.restype = ctypes.c_int
+        lib.oracle_render_soft_contrib.argtypes = render_sig + [ctypes.c_double, ctypes.c_void_p]
+        lib.oracle_render_soft_contrib.restype = ctypes.c_int
         lib.oracle_philox4x32_10.argtypes = [_P, _P, _P]
         lib.oracle_philox4x32_10.restype = None
         lib.oracle_jitter.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint32,
@@ -269,16 +271,19 @@ class RenderResult:
     """Outputs of an oracle render (double) plus optional per-sample arrays."""
 
     def __init__(self, rgb, depth, opacity, t=None, cell=None, sigma=None, srgb=None,
-                 margin=None):
+                 margin=None, contrib=None):
         self.rgb, self.depth, self.opacity = rgb, depth, opacity
         self.t, self.cell, self.sigma, self.srgb, self.margin = t, cell, sigma, srgb, margin
+        self.contrib = contrib
 
 
 def render(sites, arch, weights, rays_o, rays_d, near: float, far: float, n_coarse: int,
            n_fine: int = 0, seed: int = 0, perturb: bool = True, ray_ids=None,
            per_sample: bool = False, mode: str = "derf", beta: float = 0.0,
-           nthreads: int = 0) -> RenderResult:
-    """Render rays on the CPU.  mode: derf | direct | back | plain | soft."""
+           nthreads: int = 0, contrib: bool = False) -> RenderResult:
+    """Render rays on the CPU.  mode: derf | direct | back | plain | soft.
+    contrib (soft mode, single pass): also return the per-ray head
+    contributions W(r) [R, K] of Sec. 3.2 Eq. 6."""
     lib = _lib_handle()
     sites = np.ascontiguousarray(sites, np.float32).reshape(-1, 3)
     weights = np.ascontiguousarray(weights, np.float32)
@@ -304,10 +309,16 @@ def render(sites, arch, weights, rays_o, rays_d, near: float, far: float, n_coar
             _ptr(op), _ptr(t), _ptr(cell), _ptr(sig), _ptr(srgb), _ptr(margin), nthreads]
     fn = {"derf": lib.oracle_render, "direct": lib.oracle_render_direct,
           "back": lib.oracle_render_back_to_front, "plain": lib.oracle_render_plain}
-    if mode == "soft":
+    W = None
+    if contrib:
+        if mode != "soft" or n_fine != 0:
+            raise ValueError("contributions come from the single-pass soft render")
+        W = np.zeros((R, sites.shape[0]), np.float64)
+        rc = lib.oracle_render_soft_contrib(*args, beta, _ptr(W))
+    elif mode == "soft":
         rc = lib.oracle_render_soft(*args, beta)
     else:
         rc = fn[mode](*args)
     if rc != 0:
         raise RuntimeError("oracle render failed (%d)" % rc)
-    return RenderResult(rgb, dep, op, t, cell, sig, srgb, margin)
+    return RenderResult(rgb, dep, op, t, cell, sig, srgb, margin, W)

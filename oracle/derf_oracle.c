@@ -356,15 +356,18 @@ static void composite_segments(int n, const int *cell, const float *t, const dou
     *out_opacity = 1.0 - T;
 }
 
-/* Direct front-to-back compositing of all samples, ignoring cells. */
+/* Direct front-to-back compositing of all samples, ignoring cells.  w_out
+ * (optional) receives each sample's rendering weight T_j alpha_j. */
 static void composite_direct(int n, const float *t, const double *sigma, const double *rgb,
                              const double *delta, double out_rgb[3], double *out_depth,
-                             double *out_opacity)
+                             double *out_opacity, double *w_out)
 {
     double C[3] = {0.0, 0.0, 0.0}, D = 0.0, T = 1.0;
     for (int j = 0; j < n; ++j) {
         double x = sigma[j] * delta[j];
         double w = T * -expm1(-x);
+        if (w_out)
+            w_out[j] = w;
         C[0] += w * rgb[3 * j + 0];
         C[1] += w * rgb[3 * j + 1];
         C[2] += w * rgb[3 * j + 2];
@@ -463,6 +466,7 @@ typedef struct {
     int n_coarse, n_fine;
     uint64_t seed;
     int perturb;
+    double *contrib; /* soft mode, optional: per-ray head contributions [R][K] (Eq. 6) */
 } render_args;
 
 enum { MODE_DERF = 0, MODE_PLAIN = 1, MODE_SOFT = 2, MODE_DIRECT = 3, MODE_BACK = 4 };
@@ -470,7 +474,7 @@ enum { MODE_DERF = 0, MODE_PLAIN = 1, MODE_SOFT = 2, MODE_DIRECT = 3, MODE_BACK 
 /* Evaluate the field at every sample of one ray: cell, sigma, rgb. */
 static void eval_samples(const render_args *A, int mode, double beta, const float o[3],
                          const float d[3], const double *gd, int n, const float *t, int *cell,
-                         double *sigma, double *rgb, double *gx, double *scratch)
+                         double *sigma, double *rgb, double *gx, double *scratch, double *soft_w)
 {
     const oracle_arch *a = A->arch;
     long long wc = oracle_weights_count(a);
@@ -513,6 +517,15 @@ static void eval_samples(const render_args *A, int mode, double beta, const floa
             rgb[3 * i + 1] = c[1] / z;
             rgb[3 * i + 2] = c[2] / z;
             cell[i] = 0;
+            if (soft_w) {
+                /* the normalised weights of Eq. 8 at this sample */
+                for (int k = 0; k < A->K; ++k) {
+                    double ex = xd[0] - A->sites[3 * k], ey = xd[1] - A->sites[3 * k + 1],
+                           ez = xd[2] - A->sites[3 * k + 2];
+                    soft_w[(size_t)i * A->K + k] =
+                        exp(-beta * (sqrt(ex * ex + ey * ey + ez * ez) - dist_min)) / z;
+                }
+            }
         } else {
             cell[i] = oracle_nearest_site(A->K, A->sites, x);
             oracle_head_eval(a, A->weights + (size_t)cell[i] * wc, gx, gd, &sigma[i], &rgb[3 * i],
@@ -530,7 +543,7 @@ static void finish(int mode, int n, const int *cell, const float *t, const doubl
     else if (mode == MODE_BACK)
         composite_back_to_front(n, t, sigma, rgb, delta, o_rgb, o_depth, o_opac);
     else
-        composite_direct(n, t, sigma, rgb, delta, o_rgb, o_depth, o_opac);
+        composite_direct(n, t, sigma, rgb, delta, o_rgb, o_depth, o_opac, w_out);
 }
 
 /* Render rays [0, R).  Outputs are double; the optional per-sample arrays
@@ -571,8 +584,10 @@ static int render_impl(const render_args *A, int mode, double beta, long long R,
         double *gx = malloc(sizeof(double) * (size_t)P);
         double *gd = malloc(sizeof(double) * (size_t)Dd);
         double *scratch = malloc(sizeof(double) * scratch_len);
+        const int want_w = mode == MODE_SOFT && A->contrib;
+        double *soft_w = want_w ? malloc(sizeof(double) * (size_t)N * A->K) : NULL;
         if (!tc || !tf || !tm || !cell || !sigma || !rgb || !delta || !w || !cdf || !gx || !gd ||
-            !scratch) {
+            !scratch || (want_w && !soft_w)) {
 #pragma omp atomic write
             failed = 1;
         } else {
@@ -588,10 +603,20 @@ static int render_impl(const render_args *A, int mode, double beta, long long R,
                 oracle_sample_depths(A->seed, rid, A->near_t, A->far_t, nc, A->perturb, tc);
                 const float *tt = tc;
                 int n = nc;
-                eval_samples(A, mode, beta, o, d, gd, nc, tc, cell, sigma, rgb, gx, scratch);
+                eval_samples(A, mode, beta, o, d, gd, nc, tc, cell, sigma, rgb, gx, scratch, soft_w);
                 intervals(tc, nc, A->near_t, A->far_t, delta);
                 double c3[3], dep, op;
                 finish(mode, nc, cell, tc, sigma, rgb, delta, c3, &dep, &op, w);
+                if (soft_w) {
+                    /* Eq. 6 with the quadrature of the render: head k's share of
+                     * each sample's rendering weight T_i alpha_i */
+                    for (int k = 0; k < A->K; ++k) {
+                        double acc = 0.0;
+                        for (int i = 0; i < nc; ++i)
+                            acc += w[i] * soft_w[(size_t)i * A->K + k];
+                        A->contrib[(size_t)r * A->K + k] = acc;
+                    }
+                }
                 if (nf > 0) {
                     if (mode != MODE_DERF)
                         composite_segments(nc, cell, tc, sigma, rgb, delta, c3, &dep, &op, w);
@@ -600,7 +625,7 @@ static int render_impl(const render_args *A, int mode, double beta, long long R,
                     merge_sorted(tc, nc, tf, nf, tm);
                     tt = tm;
                     n = N;
-                    eval_samples(A, mode, beta, o, d, gd, N, tm, cell, sigma, rgb, gx, scratch);
+                    eval_samples(A, mode, beta, o, d, gd, N, tm, cell, sigma, rgb, gx, scratch, NULL);
                     intervals(tm, N, A->near_t, A->far_t, delta);
                     finish(mode, N, cell, tm, sigma, rgb, delta, c3, &dep, &op, NULL);
                 }
@@ -633,7 +658,7 @@ static int render_impl(const render_args *A, int mode, double beta, long long R,
             }
         }
         free(tc); free(tf); free(tm); free(cell); free(sigma); free(rgb); free(delta);
-        free(w); free(cdf); free(gx); free(gd); free(scratch);
+        free(w); free(cdf); free(gx); free(gd); free(scratch); free(soft_w);
     }
     return failed ? -3 : 0;
 }
@@ -646,7 +671,7 @@ static int render_impl(const render_args *A, int mode, double beta, long long R,
         double *dbg_rgb, double *dbg_margin, int nthreads
 
 #define ORACLE_FILL_ARGS                                                                       \
-    render_args A = { K, sites, arch, weights, near_t, far_t, n_coarse, n_fine, seed, perturb };
+    render_args A = { K, sites, arch, weights, near_t, far_t, n_coarse, n_fine, seed, perturb, NULL };
 
 /* DeRF render: nearest-site heads, per-segment integration, Painter's merge. */
 int oracle_render(ORACLE_RENDER_ARGS)
@@ -684,6 +709,20 @@ int oracle_render_plain(ORACLE_RENDER_ARGS)
 int oracle_render_soft(ORACLE_RENDER_ARGS, double beta)
 {
     ORACLE_FILL_ARGS
+    return render_impl(&A, MODE_SOFT, beta, R, rays_o, rays_d, ray_ids, out_rgb, out_depth,
+                       out_opacity, dbg_t, dbg_cell, dbg_sigma, dbg_rgb, dbg_margin, nthreads);
+}
+
+/* Soft Voronoi render (as oracle_render_soft, single pass) that also returns
+ * each ray's head contributions W(r) [R][K] of Sec. 3.2 Eq. 6: the integral
+ * of T sigma w_k along the ray, with the render's quadrature, so that
+ * sum_k W_k(r) equals the ray's opacity. */
+int oracle_render_soft_contrib(ORACLE_RENDER_ARGS, double beta, double *contrib)
+{
+    ORACLE_FILL_ARGS
+    if (n_fine != 0 || !contrib)
+        return -1;
+    A.contrib = contrib;
     return render_impl(&A, MODE_SOFT, beta, R, rays_o, rays_d, ray_ids, out_rgb, out_depth,
                        out_opacity, dbg_t, dbg_cell, dbg_sigma, dbg_rgb, dbg_margin, nthreads);
 }
@@ -766,7 +805,7 @@ int oracle_render_depths(int K, const float *sites, const oracle_arch *arch, con
                 double dn = sqrt((double)d[0] * d[0] + (double)d[1] * d[1] + (double)d[2] * d[2]);
                 double dh[3] = { d[0] / dn, d[1] / dn, d[2] / dn };
                 oracle_posenc(arch->dir_freqs, dh, gd);
-                eval_samples(&A, MODE_DERF, 0.0, o, d, gd, n, tr, cell, sigma, rgb, gx, scratch);
+                eval_samples(&A, MODE_DERF, 0.0, o, d, gd, n, tr, cell, sigma, rgb, gx, scratch, NULL);
                 intervals(tr, n, near_t, far_t, delta);
                 composite_segments(n, cell, tr, sigma, rgb, delta, out_rgb + 3 * r, out_depth + r,
                                    out_opacity + r, NULL);
@@ -833,7 +872,7 @@ void oracle_composite(int mode, int n, const int *cell, const float *t, const do
     else if (mode == MODE_BACK)
         composite_back_to_front(n, t, sigma, rgb, delta, out_rgb, out_depth, out_opacity);
     else
-        composite_direct(n, t, sigma, rgb, delta, out_rgb, out_depth, out_opacity);
+        composite_direct(n, t, sigma, rgb, delta, out_rgb, out_depth, out_opacity, NULL);
     free(delta);
 }
 

@@ -444,6 +444,54 @@ def test_cells_contiguous_and_in_painters_order_ndc_k16():
     assert _check_contiguous_and_ordered(sc.sites, sc.rays_o[ids], sc.rays_d[ids], res) > 80
 
 
+def _hard_contributions(res, K, near, far):
+    """Per-ray head contributions of a nearest-site render, from its per-sample
+    depths, cells and densities: each sample's rendering weight T_i alpha_i
+    (midpoint intervals) summed by owning head."""
+    t = res.t.astype(np.float64)
+    b = np.concatenate([np.full((t.shape[0], 1), near), 0.5 * (t[:, 1:] + t[:, :-1]),
+                        np.full((t.shape[0], 1), far)], axis=1)
+    x = res.sigma * np.diff(b, axis=1)
+    T = np.exp(-np.concatenate([np.zeros((t.shape[0], 1)), np.cumsum(x, axis=1)[:, :-1]], axis=1))
+    w = T * -np.expm1(-x)
+    W = np.zeros((t.shape[0], K))
+    for k in range(K):
+        W[:, k] = (w * (res.cell == k)).sum(1)
+    return W
+
+
+def test_soft_contributions():
+    """Sec. 3.2 Eq. 6 with Eq. 8's weights: the contributions of a ray sum to
+    its opacity for any temperature (the weights sum to one); at zero
+    temperature every head gets opacity / K; with one head it gets the
+    opacity; at a high temperature they are the nearest-site render's
+    rendering weights summed by owning head."""
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], sigma_bias=1.0)
+    sc = scenes.make_scene(cfg)
+    sel = np.arange(0, 1024, 8)
+    K = cfg.num_sites
+    args = (sc.sites, cfg.arch, sc.weights, sc.rays_o[sel], sc.rays_d[sel], 2.0, 6.0, 32)
+    for beta in (0.0, 0.5, 5.0, 50.0):
+        soft = oracle.render(*args, seed=1, ray_ids=sel, mode="soft", beta=beta, contrib=True)
+        assert soft.contrib.shape == (len(sel), K)
+        assert np.all(soft.contrib >= 0)
+        np.testing.assert_allclose(soft.contrib.sum(1), soft.opacity, rtol=1e-12, atol=1e-15)
+        if beta == 0.0:
+            np.testing.assert_allclose(soft.contrib, soft.opacity[:, None] / K * np.ones((1, K)),
+                                       rtol=1e-12)
+    one = oracle.render(sc.sites[:1], cfg.arch, sc.weights[:1], *args[3:], seed=1, ray_ids=sel,
+                        mode="soft", beta=3.0, contrib=True)
+    np.testing.assert_allclose(one.contrib[:, 0], one.opacity, rtol=1e-12)
+    hard = oracle.render(*args, seed=1, ray_ids=sel, per_sample=True)
+    soft = oracle.render(*args, seed=1, ray_ids=sel, mode="soft", beta=1e4, contrib=True)
+    far_from_bisector = np.all(hard.margin > 1e-2, axis=1)
+    assert far_from_bisector.mean() > 0.5
+    ref = _hard_contributions(hard, K, 2.0, 6.0)
+    np.testing.assert_allclose(soft.contrib[far_from_bisector], ref[far_from_bisector],
+                               atol=1e-9)
+    assert np.abs(ref.sum(1) - hard.opacity).max() < 1e-12
+
+
 def test_soft_voronoi_converges_to_hard_partition():
     """Eq. 8: as the temperature grows the soft blend of all heads becomes the
     nearest-site render."""

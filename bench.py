@@ -53,7 +53,7 @@ def kernel_source_hash():
     import hashlib
     import re
     text = "".join(open(os.path.join(ROOT, "paper_2011_12490_amd", "csrc", f)).read()
-                   for f in ("kernels_mlp.hip", "derf_internal.h"))
+                   for f in ("mlp_kernel.h", "mlp_8x128.hip", "derf_internal.h"))
     text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
     text = re.sub(r"//[^\n]*", " ", text)
     text = re.sub(r"\s+", " ", text)
@@ -102,6 +102,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--k-sweep", default=None,
                     help="comma-separated head counts: the same frame with K k-means sites each")
+    ap.add_argument("--soft", type=float, default=None, metavar="BETA",
+                    help="also time the soft decomposition (every head on every sample) at "
+                         "temperature BETA, with the per-ray head contributions")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (to scale HBM counters)")
     args = ap.parse_args()
@@ -171,6 +174,31 @@ def main():
         r.close()
         return sc, elapsed * 1e3 / steps, stage_ms, heads
 
+    def run_soft(cfg, beta, steps, warmup):
+        """Time `steps` soft-decomposition renders (with contributions)."""
+        sc = scenes.make_scene(cfg)
+        o = torch.from_numpy(sc.rays_o).cuda()
+        d = torch.from_numpy(sc.rays_d).cuda()
+        r = derf.Renderer(sc.sites, cfg.arch, sc.weights, precision)
+        for _ in range(warmup):
+            r.render_soft(o, d, cfg.near, cfg.far, cfg.n_coarse, beta, scenes.SEED_RENDER,
+                          contrib=True)
+        torch.cuda.synchronize()
+        derf.derf_reset_stats(r.handle)
+        derf.derf_set_timing(r.handle, True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            r.render_soft(o, d, cfg.near, cfg.far, cfg.n_coarse, beta, scenes.SEED_RENDER,
+                          contrib=True)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        st = derf.derf_get_stats(r.handle)
+        stages = {name: st.stage_ms[i] / max(1, st.stage_launches[i])
+                  for i, name in enumerate(derf.STAGE_NAMES) if st.stage_launches[i]}
+        r.close()
+        return elapsed * 1e3 / steps, stages
+
     sc, ms_per_step, stage_ms, heads = run(cfg, args.steps, args.warmup, args.copy_calibration)
     R = cfg.num_rays
     S = R * (cfg.n_coarse + cfg.n_fine)   # head evaluations (both passes when hierarchical)
@@ -194,6 +222,17 @@ def main():
                             "stage_ms": st_k,
                             "head_samples_min_max": [int(heads_k.min()), int(heads_k.max())]})
             log("bench: K=%d %.4g rays/s" % (K, k_sweep[-1]["rays_per_s"]))
+
+    soft = None
+    if args.soft is not None:
+        if cfg.n_fine:
+            raise SystemExit("--soft needs a single-pass workload")
+        ms_s, st_s = run_soft(cfg, args.soft, max(3, args.steps // 4), 1)
+        soft_flop = mlp_flop * cfg.num_sites
+        soft = {"beta": args.soft, "rays_per_s": R / (ms_s * 1e-3), "ms_per_step": ms_s,
+                "head_evaluations": S * cfg.num_sites, "mlp_ms": st_s["mlp"],
+                "mlp_frac": soft_flop / (st_s["mlp"] * 1e-3) / 1e12 / peak, "stage_ms": st_s}
+        log("bench: soft beta=%g %.4g rays/s" % (args.soft, soft["rays_per_s"]))
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -235,6 +274,8 @@ def main():
     }
     if k_sweep is not None:
         res["k_sweep"] = k_sweep
+    if soft is not None:
+        res["soft"] = soft
     print(json.dumps(res))
 
 

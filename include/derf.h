@@ -16,6 +16,9 @@
  *   derf_render   render rays: sample, encode, assign, bucket,
  *                 per-head MLP, segment integration, merge      (Sec. 3.1, 3.3)
  *   derf_render_debug  the same, also returning per-sample data
+ *   derf_render_soft   the soft decomposition: every head on every sample,
+ *                 blended by the soft Voronoi weights, and each ray's
+ *                 per-head contributions                    (Sec. 3.2 Eq. 4-6, Eq. 8)
  *
  * All functions return a derf_status (0 on success, negative on error),
  * never abort and never print.  derf_last_error() returns a thread-local
@@ -151,6 +154,28 @@ int derf_render_debug(derf_handle *h, const float *rays_o, const float *rays_d,
                       long long num_rays, float near_t, float far_t, const derf_sampling *samp,
                       float *out_rgb, float *out_depth, float *out_opacity,
                       const derf_debug_out *dbg, void *hip_stream);
+
+/* Render with the soft decomposition at temperature beta (Sec. 3.2 Eq. 4-5
+ * with the weights of Sec. 3.3 Eq. 8): every head evaluates every sample,
+ *   w_k(x) = exp(-beta |x - phi_k|) / sum_j exp(-beta |x - phi_j|),
+ *   sigma(x) = sum_k w_k(x) sigma_k(x),  c(x, d) = sum_k w_k(x) c_k(x, d),
+ * and the samples are composited front to back (Eq. 1-2, midpoint
+ * intervals).  This is the forward pass the decomposition is trained with; it
+ * costs K head evaluations per sample.  As beta grows it approaches
+ * derf_render.
+ *   beta         finite, >= 0 (0: all heads weighted equally)
+ *   out_contrib  NULL, or device float [R][K]: the contributions of Sec. 3.2
+ *                Eq. 6, W_k(r) = sum_i T_i alpha_i w_k(x_i) with the render's
+ *                quadrature, so that sum_k W_k(r) = out_opacity[r]
+ * Other arguments as derf_render; samp->n_fine must be 0 (DERF_ERR_UNSUPPORTED
+ * otherwise) and R * n_coarse * K must stay below 2^32.  The workspace holds
+ * every head's outputs for every sample (16 K bytes per sample).  Stage times
+ * go to DERF_STAGE_SAMPLE (sampling), DERF_STAGE_MLP (all heads) and
+ * DERF_STAGE_COMPOSITE (blend and composite). */
+int derf_render_soft(derf_handle *h, const float *rays_o, const float *rays_d, long long num_rays,
+                     float near_t, float far_t, const derf_sampling *samp, float beta,
+                     float *out_rgb, float *out_depth, float *out_opacity, float *out_contrib,
+                     void *hip_stream);
 
 /* Per-stage GPU time, recorded with HIP events on the render's stream when
  * timing is on (derf_set_timing); accumulated over renders since the last

@@ -17,7 +17,10 @@ LIB = os.path.join(PKG, "libderf.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["kernels_sample.hip", "kernels_fine.hip", "kernels_mlp.hip", "derf_api.cpp"]
+# the grouped MLP is instantiated per head architecture, one unit each, so
+# that its variants compile in parallel
+SOURCES = ["mlp_8x256.hip", "mlp_8x128.hip", "mlp_6x64.hip", "mlp_4x64.hip", "kernels_sample.hip",
+           "kernels_fine.hip", "kernels_soft.hip", "derf_api.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH,
           "-I" + os.path.join(ROOT, "include"), "-I" + CSRC,
@@ -36,7 +39,7 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(jobs: int = 4) -> str:
+def build(jobs: int = 8) -> str:
     os.makedirs(BUILD, exist_ok=True)
     with concurrent.futures.ThreadPoolExecutor(max_workers=jobs) as ex:
         objs = list(ex.map(_compile, SOURCES))

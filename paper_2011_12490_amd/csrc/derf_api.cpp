@@ -158,6 +158,82 @@ size_t layout(char *base, unsigned S, unsigned Sf, unsigned R, unsigned nblk, in
     return (size_t)(p - base);
 }
 
+}  // namespace
+
+// The grouped-MLP variant of a head architecture, or nullptr if none is built.
+const MlpVariant *derf::find_mlp_variant(const HeadArch &a, bool bf16)
+{
+    if (a.dir_freqs != 4)
+        return nullptr;
+    auto is = [&](int p, int d, int w, int sk, int rh) {
+        return a.pos_freqs == p && a.depth == d && a.width == w && a.skip_layer == sk &&
+               a.rgb_hidden == rh;
+    };
+    if (is(6, 4, 64, -1, 0))
+        return mlp_variant_4x64(bf16);
+    if (is(10, 8, 128, 5, 64))
+        return mlp_variant_8x128(bf16);
+    if (is(10, 6, 64, -1, 32))
+        return mlp_variant_6x64(bf16);
+    if (is(10, 8, 256, 5, 128))
+        return mlp_variant_8x256(bf16);
+    return nullptr;
+}
+
+namespace {
+
+// Grows the handle's workspace to at least need bytes.
+int ensure_workspace(derf_handle *h, size_t need)
+{
+    if (need <= h->ws.bytes)
+        return DERF_OK;
+    // the old workspace may still be in use by work on the previous stream
+    if (h->last_stream || h->ws.mem)
+        HIP_TRY(hipStreamSynchronize(h->last_stream), "hipStreamSynchronize");
+    if (h->ws.mem)
+        HIP_TRY(hipFree(h->ws.mem), "hipFree");
+    h->ws.mem = nullptr;
+    h->ws.bytes = 0;
+    const size_t grow = need + need / 8;
+    if (hipMalloc(&h->ws.mem, grow) != hipSuccess) {
+        (void)hipGetLastError();
+        h->ws.mem = nullptr;
+        return fail(DERF_ERR_OOM, "workspace of %zu bytes", grow);
+    }
+    h->ws.bytes = grow;
+    return DERF_OK;
+}
+
+// Workspace of a soft render: S samples, every head's outputs for each.
+struct SoftBuffers {
+    float *t;
+    uint8_t *cell;
+    unsigned *bucket;
+    void *dirbuf;
+    unsigned *counts;
+    unsigned *totals;
+    unsigned *mlp_queue;
+    float4 *sr;  // [K][S]
+};
+
+size_t layout_soft(char *base, unsigned S, unsigned R, unsigned nblk, int K, bool bf16,
+                   SoftBuffers *b)
+{
+    char *p = base;
+    SoftBuffers x;
+    x.t = carve<float>(p, S);
+    x.cell = carve<uint8_t>(p, (size_t)S + 16);
+    x.bucket = carve<unsigned>(p, S);
+    x.dirbuf = carve<char>(p, (size_t)R * kDirPad * (bf16 ? 2 : 4));
+    x.counts = carve<unsigned>(p, (size_t)nblk * K);
+    x.totals = carve<unsigned>(p, K);
+    x.mlp_queue = carve<unsigned>(p, kMlpQueues);
+    x.sr = carve<float4>(p, (size_t)K * S);
+    if (b)
+        *b = x;
+    return (size_t)(p - base);
+}
+
 // Adds the pending render's stage times: per stage, the sum over passes;
 // stage_launches counts the renders that ran the stage.
 void accumulate_timing(derf_handle *h)
@@ -226,22 +302,9 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
     const unsigned nblk_f = (Sf + kBucketBlock - 1) / kBucketBlock;
     const unsigned nblk_max = nblk > nblk_f ? nblk : nblk_f;
     const size_t need = layout(nullptr, S, Sf, R, nblk_max, h->num_sites, h->bf16, nullptr);
-    if (need > h->ws.bytes) {
-        // the old workspace may still be in use by work on the previous stream
-        if (h->last_stream || h->ws.mem)
-            HIP_TRY(hipStreamSynchronize(h->last_stream), "hipStreamSynchronize");
-        if (h->ws.mem)
-            HIP_TRY(hipFree(h->ws.mem), "hipFree");
-        h->ws.mem = nullptr;
-        h->ws.bytes = 0;
-        const size_t grow = need + need / 8;
-        if (hipMalloc(&h->ws.mem, grow) != hipSuccess) {
-            (void)hipGetLastError();
-            h->ws.mem = nullptr;
-            return fail(DERF_ERR_OOM, "workspace of %zu bytes", grow);
-        }
-        h->ws.bytes = grow;
-    }
+    int rc = ensure_workspace(h, need);
+    if (rc != DERF_OK)
+        return rc;
     if (h->timing && h->ev_pending) {
         HIP_TRY(hipEventSynchronize(last_event(h)), "hipEventSynchronize");
         accumulate_timing(h);
@@ -285,7 +348,7 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
         HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCATTER, 1), "hipEventRecord");
         HIP_TRY(mark(pass, DERF_STAGE_MLP, 0), "hipEventRecord");
         HIP_TRY(h->mlp->launch(b.bucket, totals, h->num_sites, gp, t, b.dirbuf, h->streams,
-                               h->blocks, sr, b.mlp_queue, h->mlp_grid, s),
+                               h->blocks, sr, b.mlp_queue, h->mlp_grid, false, s),
                 "mlp launch");
         HIP_TRY(mark(pass, DERF_STAGE_MLP, 1), "hipEventRecord");
         return DERF_OK;
@@ -302,7 +365,7 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
                                  b.counts, nblk, s),
             "sample_assign launch");
     HIP_TRY(mark(0, DERF_STAGE_SAMPLE, 1), "hipEventRecord");
-    int rc = bucket_and_mlp(0, g, b.t, b.cell, nblk, b.totals, b.sr);
+    rc = bucket_and_mlp(0, g, b.t, b.cell, nblk, b.totals, b.sr);
     if (rc != DERF_OK)
         return rc;
     const bool want_dbg = dbg && (dbg->cell || dbg->t || dbg->sigma || dbg->rgb);
@@ -348,6 +411,99 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
     h->totals_fine = hier ? b.totals_fine : nullptr;
     h->stats.renders += 1;
     h->stats.samples += (long long)S + Sf;
+    return DERF_OK;
+}
+
+// Soft decomposition (Sec. 3.2 Eq. 4-6 with Eq. 8): stratified samples,
+// every head on every sample, blend + composite (+ contributions).
+int render_soft_impl(derf_handle *h, const float *rays_o, const float *rays_d,
+                     long long num_rays, float near_t, float far_t, const derf_sampling *samp,
+                     float beta, float *out_rgb, float *out_depth, float *out_opacity,
+                     float *out_contrib, void *stream)
+{
+    if (!h)
+        return fail(DERF_ERR_INVALID_ARG, "null handle");
+    if (!samp)
+        return fail(DERF_ERR_INVALID_ARG, "null sampling descriptor");
+    if (num_rays < 0)
+        return fail(DERF_ERR_INVALID_ARG, "num_rays < 0");
+    if (!(near_t < far_t) || !isfinite(near_t) || !isfinite(far_t))
+        return fail(DERF_ERR_INVALID_ARG, "need finite near < far");
+    if (!(beta >= 0.0f) || !isfinite(beta))
+        return fail(DERF_ERR_INVALID_ARG, "need a finite beta >= 0");
+    if (samp->n_coarse < 1 || samp->n_coarse > 1024 || samp->n_fine < 0)
+        return fail(DERF_ERR_INVALID_ARG, "need 1 <= n_coarse <= 1024, n_fine >= 0");
+    if (samp->n_fine != 0)
+        return fail(DERF_ERR_UNSUPPORTED, "the soft render has no hierarchical sampling");
+    if (num_rays == 0)
+        return DERF_OK;
+    if (!rays_o || !rays_d || !out_rgb || !out_depth || !out_opacity)
+        return fail(DERF_ERR_INVALID_ARG, "null ray or output pointer");
+    const unsigned long long KS64 =
+        (unsigned long long)num_rays * (unsigned)samp->n_coarse * (unsigned)h->num_sites;
+    if (KS64 >= (1ull << 32))
+        return fail(DERF_ERR_INVALID_ARG, "num_rays * n_coarse * K must be < 2^32 per call");
+
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    HIP_TRY(hipSetDevice(h->device), "hipSetDevice");
+    const unsigned R = (unsigned)num_rays, N = (unsigned)samp->n_coarse, S = R * N;
+    const unsigned nblk = (S + kBucketBlock - 1) / kBucketBlock;
+    int rc = ensure_workspace(h, layout_soft(nullptr, S, R, nblk, h->num_sites, h->bf16, nullptr));
+    if (rc != DERF_OK)
+        return rc;
+    if (h->timing && h->ev_pending) {
+        HIP_TRY(hipEventSynchronize(last_event(h)), "hipEventSynchronize");
+        accumulate_timing(h);
+    }
+    SoftBuffers b;
+    layout_soft(reinterpret_cast<char *>(h->ws.mem), S, R, nblk, h->num_sites, h->bf16, &b);
+
+    RenderGeometry g;
+    g.rays_o = rays_o;
+    g.rays_d = rays_d;
+    g.num_rays = R;
+    g.n = N;
+    g.num_samples = S;
+    g.inv_n = 1.0 / (double)N;
+    g.near_t = near_t;
+    g.far_t = far_t;
+    g.step = (far_t - near_t) / (float)N;
+    g.seed = samp->seed;
+    g.ray_offset = samp->ray_offset;
+    g.perturb = samp->perturb ? 1 : 0;
+
+    h->ev_mask = 0;
+    auto mark = [&](int stage, int end) -> hipError_t {
+        if (!h->timing)
+            return hipSuccess;
+        h->ev_mask |= 1u << stage;
+        return hipEventRecord(h->ev[ev_index(0, stage, end)], s);
+    };
+    // stratified depths (the owning cells it also writes are not used)
+    HIP_TRY(mark(DERF_STAGE_SAMPLE, 0), "hipEventRecord");
+    HIP_TRY(launch_ray_encode(g, b.dirbuf, h->bf16, s), "ray_encode launch");
+    HIP_TRY(launch_sample_assign(g, h->sites, h->num_sites, h->site_bits, WalkTable{nullptr, nullptr},
+                                 b.t, b.cell, b.counts, nblk, s),
+            "sample_assign launch");
+    HIP_TRY(launch_soft_setup(S, h->num_sites, b.bucket, b.totals, b.mlp_queue, s),
+            "soft_setup launch");
+    HIP_TRY(mark(DERF_STAGE_SAMPLE, 1), "hipEventRecord");
+    HIP_TRY(mark(DERF_STAGE_MLP, 0), "hipEventRecord");
+    HIP_TRY(h->mlp->launch(b.bucket, b.totals, h->num_sites, g, b.t, b.dirbuf, h->streams,
+                           h->blocks, b.sr, b.mlp_queue, h->mlp_grid, true, s),
+            "mlp launch");
+    HIP_TRY(mark(DERF_STAGE_MLP, 1), "hipEventRecord");
+    HIP_TRY(mark(DERF_STAGE_COMPOSITE, 0), "hipEventRecord");
+    HIP_TRY(launch_soft_composite(g, h->sites, h->num_sites, beta, b.t, b.sr, out_rgb, out_depth,
+                                  out_opacity, out_contrib, s),
+            "soft_composite launch");
+    HIP_TRY(mark(DERF_STAGE_COMPOSITE, 1), "hipEventRecord");
+    h->ev_pending = h->timing;
+    h->last_stream = s;
+    h->totals = b.totals;
+    h->totals_fine = nullptr;
+    h->stats.renders += 1;
+    h->stats.samples += (long long)S;
     return DERF_OK;
 }
 
@@ -472,6 +628,15 @@ int derf_render_debug(derf_handle *h, const float *rays_o, const float *rays_d,
 {
     return render_impl(h, rays_o, rays_d, num_rays, near_t, far_t, samp, out_rgb, out_depth,
                        out_opacity, dbg, hip_stream);
+}
+
+int derf_render_soft(derf_handle *h, const float *rays_o, const float *rays_d, long long num_rays,
+                     float near_t, float far_t, const derf_sampling *samp, float beta,
+                     float *out_rgb, float *out_depth, float *out_opacity, float *out_contrib,
+                     void *hip_stream)
+{
+    return render_soft_impl(h, rays_o, rays_d, num_rays, near_t, far_t, samp, beta, out_rgb,
+                            out_depth, out_opacity, out_contrib, hip_stream);
 }
 
 int derf_set_timing(derf_handle *h, int on)

@@ -67,6 +67,14 @@ hipError_t launch_bucket_scatter(const uint8_t *cell, const unsigned *counts,
                                  const unsigned *totals, unsigned num_samples,
                                  unsigned num_blocks, int num_sites, int site_bits,
                                  unsigned *bucket, hipStream_t s);
+// Soft decomposition: bucket[i] = i (i < S), totals[k] = S, queue cleared.
+hipError_t launch_soft_setup(unsigned S, int num_sites, unsigned *bucket, unsigned *totals,
+                             unsigned *queue, hipStream_t s);
+// Blend every head's outputs sr[k * S + i] by the soft Voronoi weights and
+// composite; contrib (nullable) receives the per-ray head contributions.
+hipError_t launch_soft_composite(const RenderGeometry &g, const float4 *sites, int num_sites,
+                                 float beta, const float *t, const float4 *sr, float *rgb,
+                                 float *depth, float *opacity, float *contrib, hipStream_t s);
 hipError_t launch_composite(const RenderGeometry &g, const float *t, const uint8_t *cell,
                             const float4 *sr, float *rgb, float *depth, float *opacity,
                             hipStream_t s);
@@ -87,7 +95,7 @@ hipError_t launch_merge_composite(const RenderGeometry &g, const float *tc, cons
                                   float *opacity, int *dcell, float *dt, float *dsigma,
                                   float *drgb, hipStream_t s);
 
-// ---- grouped per-head MLP (kernels_mlp.hip) ------------------------------
+// ---- grouped per-head MLP (mlp_kernel.h, mlp_*.hip) ----------------------
 struct HeadArch {
     int pos_freqs, dir_freqs, depth, width, skip_layer, rgb_hidden;
 };
@@ -99,14 +107,22 @@ struct MlpVariant {
     int tile;            // samples per tile
     // Lay out one head's fp32 weights (packed order of derf.h) for the kernel.
     void (*pack)(const float *w, unsigned char *stream, float *block);
-    // queue: kMlpQueues tile counters, zero at launch
+    // queue: kMlpQueues tile counters, zero at launch.  soft: every head
+    // takes every sample (bucket = 0 .. S-1, totals[k] = S) and writes its
+    // outputs to sr[k * S + sample]; otherwise sr[sample].
     hipError_t (*launch)(const unsigned *bucket, const unsigned *totals, int num_sites,
                          const RenderGeometry &g, const float *t, const void *dirbuf,
                          const unsigned char *streams, const float *blocks, float4 *sr,
-                         unsigned *queue, int grid, hipStream_t s);
+                         unsigned *queue, int grid, bool soft, hipStream_t s);
 };
 
 // Returns nullptr when no kernel is compiled for this architecture/precision.
 const MlpVariant *find_mlp_variant(const HeadArch &a, bool bf16);
+// the variants of each supported head architecture (one translation unit each;
+// nullptr where a precision is not built)
+const MlpVariant *mlp_variant_4x64(bool bf16);
+const MlpVariant *mlp_variant_6x64(bool bf16);
+const MlpVariant *mlp_variant_8x128(bool bf16);
+const MlpVariant *mlp_variant_8x256(bool bf16);
 
 }  // namespace derf

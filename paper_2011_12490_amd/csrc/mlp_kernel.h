@@ -1,4 +1,6 @@
-// Grouped per-head MLP on gfx950 matrix cores.
+// Grouped per-head MLP on gfx950 matrix cores: the kernel template and its
+// host-side launch and weight packing.  Included by one translation unit
+// per head architecture (mlp_*.hip), which instantiates its variants.
 //
 // Every ray sample is evaluated by the single head that owns it (Sec. 3.2:
 // the decomposition weights are one-hot, so only that head contributes).
@@ -37,6 +39,7 @@
 // Density and colour come out of one extra 32-row output tile (row 0
 // density, rows 1-3 colour logits), so the network tail needs no cross-lane
 // reduction.
+#pragma once
 #include <type_traits>
 #include <vector>
 
@@ -558,13 +561,15 @@ constexpr int kPrefetch = 3;
 // "no tile left" from the work queues
 constexpr unsigned kNoTile = 0xFFFFFFFFu;
 
-template <class C>
+// SOFT: every head takes every sample (see MlpVariant::launch).
+template <class C, bool SOFT>
 __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
     const unsigned *__restrict__ bucket, const unsigned *__restrict__ totals, int num_sites,
     RenderGeometry geo, const float *__restrict__ tbuf, const void *__restrict__ dirbuf,
     const unsigned char *__restrict__ streams, const float *__restrict__ blocks,
     float4 *__restrict__ sr, unsigned *__restrict__ queue)
 {
+    constexpr bool soft = SOFT;
     using CT = Chunk<C>;
     using AT = std::conditional_t<C::BF16, bf16x8, f32x4>;  // one LDS unit per lane
     constexpr int NB = C::NB, NS = C::NS;
@@ -690,11 +695,15 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
         asm volatile("" ::: "memory");
     };
 
-    // the two prefetch phases for the tile whose rows are [r0, r_end)
-    auto prefetch_ids = [&](unsigned r0, unsigned r_end) {
+    // rows end at the sample count; with soft, each head's rows are all the
+    // samples again (head k's at k S, read through bucket[row - k S])
+    const unsigned row_cap = soft ? s_off[num_sites] : geo.num_samples;
+    // the two prefetch phases for the tile whose rows are [r0, r_end) and
+    // whose bucket entries start at row base
+    auto prefetch_ids = [&](unsigned r0, unsigned r_end, unsigned base) {
         // bucket ids (rows past the head's end read row 0's)
         const unsigned row = r0 + wave * (NB * 32) + lane % (NB * 32);
-        load_lds4(bucket + min(row < r_end ? row : r0, geo.num_samples - 1), pf_wave);
+        load_lds4(bucket + min((row < r_end ? row : r0) - base, geo.num_samples - 1), pf_wave);
     };
     auto prefetch_rays = [&]() {
         // depths, ray origins and directions of the ids in LDS
@@ -716,7 +725,8 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
     const unsigned char *stream = stream_of(head);
     // the first tile's records, waited for in full
     prefetch_ids(__builtin_amdgcn_readfirstlane(s_off[head] + (tile - s_tile[head]) * C::TILE),
-                 __builtin_amdgcn_readfirstlane(min(s_off[head + 1], geo.num_samples)));
+                 __builtin_amdgcn_readfirstlane(min(s_off[head + 1], row_cap)),
+                 soft ? s_off[head] : 0u);
     wait_vmcnt<0>();
     prefetch_rays();
     wait_vmcnt<0>();
@@ -731,11 +741,11 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
         const unsigned row0 = __builtin_amdgcn_readfirstlane(s_off[head] + (tile - s_tile[head]) * C::TILE);
         // rows never pass the sample count when the bucket counts are
         // consistent; the clamps keep every access in bounds regardless
-        const unsigned row_end = __builtin_amdgcn_readfirstlane(min(s_off[head + 1], geo.num_samples));
+        const unsigned row_end = __builtin_amdgcn_readfirstlane(min(s_off[head + 1], row_cap));
         // rows of the tile whose records are prefetched (this one's if last)
         const unsigned pf_tile = has_next ? next : tile;
         const unsigned nrow0 = __builtin_amdgcn_readfirstlane(s_off[nhead] + (pf_tile - s_tile[nhead]) * C::TILE);
-        const unsigned nrow_end = __builtin_amdgcn_readfirstlane(min(s_off[nhead + 1], geo.num_samples));
+        const unsigned nrow_end = __builtin_amdgcn_readfirstlane(min(s_off[nhead + 1], row_cap));
 
         wg_barrier();  // previous tile is done with the head block and the staging
         // this tile's records have landed (at most that many loads were issued
@@ -911,7 +921,7 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
                 }
             }
             if constexpr (s == C::S_PA)
-                prefetch_ids(nrow0, nrow_end);
+                prefetch_ids(nrow0, nrow_end, soft ? s_off[nhead] : 0u);
             if constexpr (s == C::S_PB)
                 prefetch_rays();  // the group wait above covered the ids
             if constexpr (s + 1 == C::S_SKIP) {
@@ -1005,7 +1015,8 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
         for (int nb = 0; nb < NB; ++nb) {
             const f32x16 &a = acc[TO % 2][nb];
             if (g == 0 && valid[nb])
-                sr[sid[nb]] = make_float4(fmaxf(a[0], 0.0f), sigmoid(a[1]), sigmoid(a[2]), sigmoid(a[3]));
+                sr[soft ? row0 + (wave * NB + nb) * 32 + n : sid[nb]] =
+                    make_float4(fmaxf(a[0], 0.0f), sigmoid(a[1]), sigmoid(a[2]), sigmoid(a[3]));
         }
         ring += NS;
         head = nhead;
@@ -1022,20 +1033,25 @@ template <class C>
 hipError_t launch_mlp(const unsigned *bucket, const unsigned *totals, int num_sites,
                       const RenderGeometry &g, const float *t, const void *dirbuf,
                       const unsigned char *streams, const float *blocks, float4 *sr,
-                      unsigned *queue, int cus, hipStream_t s)
+                      unsigned *queue, int cus, bool soft, hipStream_t s)
 {
     static bool configured = false;
     if (!configured) {
         // raises the dynamic LDS limit where the runtime keeps one; a runtime
         // without the limit may refuse the call, and the launch below reports
         // any real problem
-        if (hipFuncSetAttribute((const void *)mlp_kernel<C>,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES) != hipSuccess)
-            (void)hipGetLastError();
+        for (const void *k : {(const void *)mlp_kernel<C, false>, (const void *)mlp_kernel<C, true>})
+            if (hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES) !=
+                hipSuccess)
+                (void)hipGetLastError();
         configured = true;
     }
-    mlp_kernel<C><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(
-        bucket, totals, num_sites, g, t, dirbuf, streams, blocks, sr, queue);
+    if (soft)
+        mlp_kernel<C, true><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(
+            bucket, totals, num_sites, g, t, dirbuf, streams, blocks, sr, queue);
+    else
+        mlp_kernel<C, false><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(
+            bucket, totals, num_sites, g, t, dirbuf, streams, blocks, sr, queue);
     return hipGetLastError();
 }
 
@@ -1045,24 +1061,6 @@ const MlpVariant *variant()
     static const MlpVariant v = {(size_t)C::STREAM_UNITS * 1024, (size_t)C::BLOCK_FLOATS * 4,
                                  C::TILE, &Packer<C>::pack, &launch_mlp<C>};
     return &v;
-}
-
-const MlpVariant *find_mlp_variant(const HeadArch &a, bool bf16)
-{
-    if (a.dir_freqs != 4)
-        return nullptr;
-    auto is = [&](int p, int d, int w, int sk, int rh) {
-        return a.pos_freqs == p && a.depth == d && a.width == w && a.skip_layer == sk && a.rgb_hidden == rh;
-    };
-    if (is(6, 4, 64, -1, 0))
-        return bf16 ? variant<Cfg<true, 64, 4, -1, 0, 6>>() : variant<Cfg<false, 64, 4, -1, 0, 6>>();
-    if (is(10, 8, 128, 5, 64))
-        return bf16 ? variant<Cfg<true, 128, 8, 5, 64, 10>>() : variant<Cfg<false, 128, 8, 5, 64, 10>>();
-    if (is(10, 6, 64, -1, 32))
-        return bf16 ? variant<Cfg<true, 64, 6, -1, 32, 10>>() : variant<Cfg<false, 64, 6, -1, 32, 10>>();
-    if (is(10, 8, 256, 5, 128))
-        return bf16 ? variant<Cfg<true, 256, 8, 5, 128, 10>>() : nullptr;
-    return nullptr;
 }
 
 }  // namespace derf

@@ -52,7 +52,7 @@ class derf_stats(ctypes.Structure):
 
 
 EXPORTS = ("derf_weights_count", "derf_create", "derf_render", "derf_render_debug",
-           "derf_set_timing", "derf_get_stats", "derf_reset_stats", "derf_destroy",
+           "derf_render_soft", "derf_set_timing", "derf_get_stats", "derf_reset_stats", "derf_destroy",
            "derf_status_string", "derf_last_error")
 
 _lib: Optional[ctypes.CDLL] = None
@@ -84,6 +84,9 @@ def lib() -> ctypes.CDLL:
         L.derf_render.restype = ctypes.c_int
         L.derf_render_debug.argtypes = render_args + [ctypes.POINTER(derf_debug_out), P]
         L.derf_render_debug.restype = ctypes.c_int
+        L.derf_render_soft.argtypes = [P, P, P, ctypes.c_longlong, ctypes.c_float, ctypes.c_float,
+                                       ctypes.POINTER(derf_sampling), ctypes.c_float, P, P, P, P, P]
+        L.derf_render_soft.restype = ctypes.c_int
         L.derf_set_timing.argtypes = [P, ctypes.c_int]
         L.derf_set_timing.restype = ctypes.c_int
         L.derf_get_stats.argtypes = [P, ctypes.POINTER(derf_stats)]
@@ -150,6 +153,21 @@ def derf_render(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far:
         _check(lib().derf_render_debug(*args, ctypes.byref(debug), sp), "derf_render_debug")
 
 
+def derf_render_soft(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far: float,
+                     samp: derf_sampling, beta: float, out_rgb: torch.Tensor,
+                     out_depth: torch.Tensor, out_opacity: torch.Tensor,
+                     out_contrib: Optional[torch.Tensor] = None, stream=None):
+    """Enqueue a soft-decomposition render on `stream` (default: torch's current stream)."""
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    _check(lib().derf_render_soft(h, _dptr(rays_o), _dptr(rays_d), rays_o.shape[0], near, far,
+                                  ctypes.byref(samp), beta, _dptr(out_rgb), _dptr(out_depth),
+                                  _dptr(out_opacity),
+                                  None if out_contrib is None else _dptr(out_contrib), sp),
+           "derf_render_soft")
+
+
 def derf_set_timing(h, on: bool):
     _check(lib().derf_set_timing(h, int(on)), "derf_set_timing")
 
@@ -176,6 +194,7 @@ class Renderer:
     def __init__(self, sites, arch, weights, precision: str = "bf16"):
         self.arch = arch
         self.precision = precision
+        self.num_sites = len(sites)
         prec = DERF_PREC_BF16 if precision == "bf16" else DERF_PREC_FP32
         self.handle = derf_create(sites, arch, weights, prec)
 
@@ -219,4 +238,24 @@ class Renderer:
         derf_render(self.handle, rays_o, rays_d, near, far, samp, rgb, depth, opac, stream, dbg)
         if debug:
             return rgb, depth, opac, extra
+        return rgb, depth, opac
+
+    def render_soft(self, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far: float,
+                    n: int, beta: float, seed: int = 0, perturb: bool = True,
+                    contrib: bool = False, stream=None, ray_offset: int = 0):
+        """Soft-decomposition render at temperature beta; returns (rgb, depth,
+        opacity) and, with contrib=True, the per-ray head contributions [R, K]."""
+        assert rays_o.is_cuda and rays_o.dtype == torch.float32 and rays_o.is_contiguous()
+        assert rays_d.is_cuda and rays_d.dtype == torch.float32 and rays_d.is_contiguous()
+        R = rays_o.shape[0]
+        dev = rays_o.device
+        rgb = torch.empty((R, 3), dtype=torch.float32, device=dev)
+        depth = torch.empty((R,), dtype=torch.float32, device=dev)
+        opac = torch.empty((R,), dtype=torch.float32, device=dev)
+        W = torch.empty((R, self.num_sites), dtype=torch.float32, device=dev) if contrib else None
+        samp = derf_sampling(n, 0, seed, int(perturb), ray_offset)
+        derf_render_soft(self.handle, rays_o, rays_d, near, far, samp, beta, rgb, depth, opac, W,
+                         stream)
+        if contrib:
+            return rgb, depth, opac, W
         return rgb, depth, opac

@@ -58,6 +58,9 @@ def _lib_handle():
         lib.oracle_render_soft.restype = ctypes.c_int
         lib.oracle_render_soft_contrib.argtypes = render_sig + [ctypes.c_double, ctypes.c_void_p]
         lib.oracle_render_soft_contrib.restype = ctypes.c_int
+        lib.oracle_render_ex.argtypes = render_sig + [ctypes.c_int, ctypes.c_double,
+                                                      ctypes.c_void_p, ctypes.c_void_p]
+        lib.oracle_render_ex.restype = ctypes.c_int
         lib.oracle_philox4x32_10.argtypes = [_P, _P, _P]
         lib.oracle_philox4x32_10.restype = None
         lib.oracle_jitter.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint32,
@@ -280,10 +283,11 @@ class RenderResult:
 def render(sites, arch, weights, rays_o, rays_d, near: float, far: float, n_coarse: int,
            n_fine: int = 0, seed: int = 0, perturb: bool = True, ray_ids=None,
            per_sample: bool = False, mode: str = "derf", beta: float = 0.0,
-           nthreads: int = 0, contrib: bool = False) -> RenderResult:
+           nthreads: int = 0, contrib: bool = False, empty=None) -> RenderResult:
     """Render rays on the CPU.  mode: derf | direct | back | plain | soft.
     contrib (soft mode, single pass): also return the per-ray head
-    contributions W(r) [R, K] of Sec. 3.2 Eq. 6."""
+    contributions W(r) [R, K] of Sec. 3.2 Eq. 6.  empty: optional [K] flags of
+    0-capacity heads (no density anywhere)."""
     lib = _lib_handle()
     sites = np.ascontiguousarray(sites, np.float32).reshape(-1, 3)
     weights = np.ascontiguousarray(weights, np.float32)
@@ -314,6 +318,13 @@ def render(sites, arch, weights, rays_o, rays_d, near: float, far: float, n_coar
         if mode != "soft" or n_fine != 0:
             raise ValueError("contributions come from the single-pass soft render")
         W = np.zeros((R, sites.shape[0]), np.float64)
+    if empty is not None:
+        e = np.ascontiguousarray(np.asarray(empty) != 0, np.uint8)
+        if e.shape != (sites.shape[0],):
+            raise ValueError("empty needs one flag per head")
+        code = {"derf": 0, "plain": 1, "soft": 2, "direct": 3, "back": 4}[mode]
+        rc = lib.oracle_render_ex(*args, code, beta, _ptr(e), _ptr(W))
+    elif contrib:
         rc = lib.oracle_render_soft_contrib(*args, beta, _ptr(W))
     elif mode == "soft":
         rc = lib.oracle_render_soft(*args, beta)

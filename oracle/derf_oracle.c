@@ -467,7 +467,22 @@ typedef struct {
     uint64_t seed;
     int perturb;
     double *contrib; /* soft mode, optional: per-ray head contributions [R][K] (Eq. 6) */
+    const unsigned char *empty; /* optional [K]: nonzero = 0-capacity head (no density) */
 } render_args;
+
+/* Head k at x: its density and colour, or zero for a 0-capacity head (the
+ * empty-space head of the paper's closing remarks). */
+static void eval_head(const render_args *A, int k, const double *gx, const double *gd,
+                      double *sigma, double rgb[3], double *scratch)
+{
+    if (A->empty && A->empty[k]) {
+        *sigma = 0.0;
+        rgb[0] = rgb[1] = rgb[2] = 0.0;
+        return;
+    }
+    oracle_head_eval(A->arch, A->weights + (size_t)k * oracle_weights_count(A->arch), gx, gd,
+                     sigma, rgb, scratch);
+}
 
 enum { MODE_DERF = 0, MODE_PLAIN = 1, MODE_SOFT = 2, MODE_DIRECT = 3, MODE_BACK = 4 };
 
@@ -477,7 +492,6 @@ static void eval_samples(const render_args *A, int mode, double beta, const floa
                          double *sigma, double *rgb, double *gx, double *scratch, double *soft_w)
 {
     const oracle_arch *a = A->arch;
-    long long wc = oracle_weights_count(a);
     for (int i = 0; i < n; ++i) {
         float x[3];
         sample_point(o, d, t[i], x);
@@ -506,7 +520,7 @@ static void eval_samples(const render_args *A, int mode, double beta, const floa
                 if (wk == 0.0)
                     continue;
                 double sk, ck[3];
-                oracle_head_eval(a, A->weights + (size_t)k * wc, gx, gd, &sk, ck, scratch);
+                eval_head(A, k, gx, gd, &sk, ck, scratch);
                 s += wk * sk;
                 c[0] += wk * ck[0];
                 c[1] += wk * ck[1];
@@ -528,8 +542,7 @@ static void eval_samples(const render_args *A, int mode, double beta, const floa
             }
         } else {
             cell[i] = oracle_nearest_site(A->K, A->sites, x);
-            oracle_head_eval(a, A->weights + (size_t)cell[i] * wc, gx, gd, &sigma[i], &rgb[3 * i],
-                             scratch);
+            eval_head(A, cell[i], gx, gd, &sigma[i], &rgb[3 * i], scratch);
         }
     }
 }
@@ -671,7 +684,7 @@ static int render_impl(const render_args *A, int mode, double beta, long long R,
         double *dbg_rgb, double *dbg_margin, int nthreads
 
 #define ORACLE_FILL_ARGS                                                                       \
-    render_args A = { K, sites, arch, weights, near_t, far_t, n_coarse, n_fine, seed, perturb, NULL };
+    render_args A = { K, sites, arch, weights, near_t, far_t, n_coarse, n_fine, seed, perturb, NULL, NULL };
 
 /* DeRF render: nearest-site heads, per-segment integration, Painter's merge. */
 int oracle_render(ORACLE_RENDER_ARGS)
@@ -710,6 +723,22 @@ int oracle_render_soft(ORACLE_RENDER_ARGS, double beta)
 {
     ORACLE_FILL_ARGS
     return render_impl(&A, MODE_SOFT, beta, R, rays_o, rays_d, ray_ids, out_rgb, out_depth,
+                       out_opacity, dbg_t, dbg_cell, dbg_sigma, dbg_rgb, dbg_margin, nthreads);
+}
+
+/* Any render mode (0 derf, 1 plain, 2 soft at beta, 3 direct, 4
+ * back-to-front) with optional 0-capacity heads (empty, [K], nonzero = the
+ * head has no density anywhere) and, in soft mode without fine samples,
+ * optional per-ray head contributions [R][K]. */
+int oracle_render_ex(ORACLE_RENDER_ARGS, int mode, double beta, const unsigned char *empty,
+                     double *contrib)
+{
+    ORACLE_FILL_ARGS
+    if (mode < MODE_DERF || mode > MODE_BACK || (contrib && (mode != MODE_SOFT || n_fine != 0)))
+        return -1;
+    A.contrib = contrib;
+    A.empty = empty;
+    return render_impl(&A, mode, beta, R, rays_o, rays_d, ray_ids, out_rgb, out_depth,
                        out_opacity, dbg_t, dbg_cell, dbg_sigma, dbg_rgb, dbg_margin, nthreads);
 }
 

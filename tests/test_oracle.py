@@ -492,6 +492,36 @@ def test_soft_contributions():
     assert np.abs(ref.sum(1) - hard.opacity).max() < 1e-12
 
 
+def test_empty_heads():
+    """0-capacity heads (no density anywhere): a render with some heads empty
+    equals, bitwise, the render where those heads' weights are all zero --
+    density ReLU(0) = 0 gives alpha = 0, so their (sigmoid 0.5) colour never
+    counts -- single-pass, direct and hierarchical; with every head empty the
+    ray is transparent and black."""
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], sigma_bias=1.0)
+    sc = scenes.make_scene(cfg)
+    sel = np.arange(0, 1024, 8)
+    empty = np.array([0, 1, 0, 1])
+    zeroed = sc.weights.copy()
+    zeroed[empty == 1] = 0.0
+    for mode, n_fine in (("derf", 0), ("direct", 0), ("derf", 16)):
+        a = oracle.render(sc.sites, cfg.arch, sc.weights, sc.rays_o[sel], sc.rays_d[sel], 2.0, 6.0,
+                          32, n_fine, seed=1, ray_ids=sel, mode=mode, empty=empty)
+        b = oracle.render(sc.sites, cfg.arch, zeroed, sc.rays_o[sel], sc.rays_d[sel], 2.0, 6.0,
+                          32, n_fine, seed=1, ray_ids=sel, mode=mode)
+        for x, y in ((a.rgb, b.rgb), (a.depth, b.depth), (a.opacity, b.opacity)):
+            np.testing.assert_array_equal(x, y)
+        assert np.abs(a.opacity - oracle.render(
+            sc.sites, cfg.arch, sc.weights, sc.rays_o[sel], sc.rays_d[sel], 2.0, 6.0, 32, n_fine,
+            seed=1, ray_ids=sel, mode=mode).opacity).max() > 1e-3
+    none = oracle.render(sc.sites, cfg.arch, sc.weights, sc.rays_o[sel], sc.rays_d[sel], 2.0, 6.0,
+                         32, seed=1, ray_ids=sel, empty=np.ones(4))
+    assert not none.rgb.any() and not none.depth.any() and not none.opacity.any()
+    soft = oracle.render(sc.sites, cfg.arch, sc.weights, sc.rays_o[sel], sc.rays_d[sel], 2.0, 6.0,
+                         32, seed=1, ray_ids=sel, mode="soft", beta=5.0, contrib=True, empty=empty)
+    np.testing.assert_allclose(soft.contrib.sum(1), soft.opacity, rtol=1e-12, atol=1e-15)
+
+
 def test_soft_voronoi_converges_to_hard_partition():
     """Eq. 8: as the temperature grows the soft blend of all heads becomes the
     nearest-site render."""

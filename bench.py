@@ -102,6 +102,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--k-sweep", default=None,
                     help="comma-separated head counts: the same frame with K k-means sites each")
+    ap.add_argument("--empty-heads", default=None, metavar="K1,K2,...",
+                    help="mark these heads 0-capacity (empty space): never evaluated")
     ap.add_argument("--soft", type=float, default=None, metavar="BETA",
                     help="also time the soft decomposition (every head on every sample) at "
                          "temperature BETA, with the per-ray head contributions")
@@ -125,6 +127,7 @@ def main():
     if args.sites is not None:
         cfg = scenes.with_changes(cfg, num_sites=args.sites)
     precision = args.precision or cfg.precision
+    empty_heads = set(int(k) for k in args.empty_heads.split(",")) if args.empty_heads else set()
     torch.cuda.set_device(0)
 
     def run(cfg, steps, warmup, copy_calibration=False):
@@ -139,6 +142,8 @@ def main():
         out = (torch.empty((R, 3), device="cuda"), torch.empty((R,), device="cuda"),
                torch.empty((R,), device="cuda"))
         r = derf.Renderer(sc.sites, cfg.arch, sc.weights, precision)
+        if empty_heads:
+            r.set_empty_heads([k in empty_heads for k in range(cfg.num_sites)])
         stream = torch.cuda.current_stream()
 
         def step():
@@ -203,7 +208,9 @@ def main():
     R = cfg.num_rays
     S = R * (cfg.n_coarse + cfg.n_fine)   # head evaluations (both passes when hierarchical)
     mlp_ms = stage_ms["mlp"]
-    mlp_flop = 2.0 * cfg.arch.macs_per_sample() * S
+    # head evaluations: every sample, less those owned by 0-capacity heads
+    evaluated = S - int(sum(heads[k] for k in empty_heads if k < cfg.num_sites))
+    mlp_flop = 2.0 * cfg.arch.macs_per_sample() * evaluated
     achieved = mlp_flop / (mlp_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[precision]
     # t + cell + sigma/rgb per sample (coarse and fine lists when hierarchical), outputs per ray
@@ -256,11 +263,13 @@ def main():
         "config": {"workload": workload_text(cfg, precision), "rays": R,
                    "samples_per_ray": cfg.n_coarse + cfg.n_fine, "heads": cfg.num_sites,
                    "samples": S},
+        "evaluated_samples": evaluated,
         "roofline": {"bound": "mfma", "kernel": "mlp_kernel (grouped per-head MLP)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak,
                      "traffic": measured_traffic() if (cfg.name == "derf_k16" and cfg.num_sites == 16
-                                                       and precision == "bf16") else None,
+                                                       and precision == "bf16" and not empty_heads)
+                     else None,
                      "flop_per_step": mlp_flop, "mlp_ms_per_step": mlp_ms,
                      "launches_per_step": 2 if cfg.n_fine else 1},
         "cpu_baseline": cpu,

@@ -16,6 +16,7 @@
  *   derf_render   render rays: sample, encode, assign, bucket,
  *                 per-head MLP, segment integration, merge      (Sec. 3.1, 3.3)
  *   derf_render_debug  the same, also returning per-sample data
+ *   derf_set_empty_heads  mark heads 0-capacity (empty space)     (Sec. 5)
  *   derf_render_soft   the soft decomposition: every head on every sample,
  *                 blended by the soft Voronoi weights, and each ray's
  *                 per-head contributions                    (Sec. 3.2 Eq. 4-6, Eq. 8)
@@ -154,6 +155,17 @@ int derf_render_debug(derf_handle *h, const float *rays_o, const float *rays_d,
                       long long num_rays, float near_t, float far_t, const derf_sampling *samp,
                       float *out_rgb, float *out_depth, float *out_opacity,
                       const derf_debug_out *dbg, void *hip_stream);
+
+/* Mark heads as 0-capacity: a head with flags[k] != 0 represents empty space
+ * (the heterogeneous-capacity remark of Sec. 5, limitations and future work): its
+ * density and colour are zero everywhere, so it is never evaluated.  The
+ * partition is unchanged -- its samples still belong to it -- and every
+ * render (single pass, hierarchical, soft) treats it as transparent; its
+ * packed weights are ignored.  flags is a host int [K] (copied; NULL clears
+ * every mark).  Takes effect for renders enqueued after the call; marks
+ * persist until the next call.  Returns DERF_ERR_INVALID_ARG for a NULL
+ * handle. */
+int derf_set_empty_heads(derf_handle *h, const int *flags);
 
 /* Render with the soft decomposition at temperature beta (Sec. 3.2 Eq. 4-5
  * with the weights of Sec. 3.3 Eq. 8): every head evaluates every sample,

@@ -98,6 +98,8 @@ struct derf_handle {
     unsigned ev_mask = 0;      // event pairs recorded by the pending render
     bool ev_pending = false;
     derf_stats stats{};
+    // 0-capacity heads (derf_set_empty_heads)
+    HeadMask empty{};
     // per-head counts of the last render (device pointers into the workspace)
     unsigned *totals = nullptr;
     unsigned *totals_fine = nullptr;
@@ -343,12 +345,12 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
         HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCAN, 1), "hipEventRecord");
         HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCATTER, 0), "hipEventRecord");
         HIP_TRY(launch_bucket_scatter(cell, b.counts, totals, gp.num_samples, nb, h->num_sites,
-                                      h->site_bits, b.bucket, s),
+                                      h->site_bits, h->empty, b.bucket, sr, s),
                 "bucket_scatter launch");
         HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCATTER, 1), "hipEventRecord");
         HIP_TRY(mark(pass, DERF_STAGE_MLP, 0), "hipEventRecord");
         HIP_TRY(h->mlp->launch(b.bucket, totals, h->num_sites, gp, t, b.dirbuf, h->streams,
-                               h->blocks, sr, b.mlp_queue, h->mlp_grid, false, s),
+                               h->blocks, sr, b.mlp_queue, h->mlp_grid, false, h->empty, s),
                 "mlp launch");
         HIP_TRY(mark(pass, DERF_STAGE_MLP, 1), "hipEventRecord");
         return DERF_OK;
@@ -490,12 +492,12 @@ int render_soft_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     HIP_TRY(mark(DERF_STAGE_SAMPLE, 1), "hipEventRecord");
     HIP_TRY(mark(DERF_STAGE_MLP, 0), "hipEventRecord");
     HIP_TRY(h->mlp->launch(b.bucket, b.totals, h->num_sites, g, b.t, b.dirbuf, h->streams,
-                           h->blocks, b.sr, b.mlp_queue, h->mlp_grid, true, s),
+                           h->blocks, b.sr, b.mlp_queue, h->mlp_grid, true, h->empty, s),
             "mlp launch");
     HIP_TRY(mark(DERF_STAGE_MLP, 1), "hipEventRecord");
     HIP_TRY(mark(DERF_STAGE_COMPOSITE, 0), "hipEventRecord");
-    HIP_TRY(launch_soft_composite(g, h->sites, h->num_sites, beta, b.t, b.sr, out_rgb, out_depth,
-                                  out_opacity, out_contrib, s),
+    HIP_TRY(launch_soft_composite(g, h->sites, h->num_sites, h->empty, beta, b.t, b.sr, out_rgb,
+                                  out_depth, out_opacity, out_contrib, s),
             "soft_composite launch");
     HIP_TRY(mark(DERF_STAGE_COMPOSITE, 1), "hipEventRecord");
     h->ev_pending = h->timing;
@@ -637,6 +639,19 @@ int derf_render_soft(derf_handle *h, const float *rays_o, const float *rays_d, l
 {
     return render_soft_impl(h, rays_o, rays_d, num_rays, near_t, far_t, samp, beta, out_rgb,
                             out_depth, out_opacity, out_contrib, hip_stream);
+}
+
+int derf_set_empty_heads(derf_handle *h, const int *flags)
+{
+    if (!h)
+        return fail(DERF_ERR_INVALID_ARG, "null handle");
+    HeadMask m{};
+    if (flags)
+        for (int k = 0; k < h->num_sites; ++k)
+            if (flags[k])
+                m.w[k >> 5] |= 1u << (k & 31);
+    h->empty = m;
+    return DERF_OK;
 }
 
 int derf_set_timing(derf_handle *h, int on)

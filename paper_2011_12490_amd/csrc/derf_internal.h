@@ -16,6 +16,12 @@ constexpr int kMaxSites = 256;
 // Tile counters of the MLP's work queues (one per XCD).
 constexpr int kMlpQueues = 8;
 
+// Heads marked 0-capacity (empty space: no density anywhere), one bit each.
+struct HeadMask {
+    unsigned w[kMaxSites / 32];
+    __host__ __device__ bool test(int k) const { return (w[k >> 5] >> (k & 31)) & 1u; }
+};
+
 // Per-ray cell walk (see ray_walk_kernel): at most kMaxSeg segments per ray,
 // each with at most kMaxCand candidate sites.
 constexpr int kMaxSeg = 32;
@@ -63,18 +69,21 @@ hipError_t launch_assign_given(const RenderGeometry &g, const float4 *sites, int
 // also clears the kMlpQueues tile counters of the MLP launch that follows
 hipError_t launch_bucket_scan(unsigned *counts, unsigned num_blocks, int num_sites,
                               unsigned *totals, unsigned *mlp_queue, hipStream_t s);
+// Samples of 0-capacity heads also get sr = 0 here (the MLP skips those heads).
 hipError_t launch_bucket_scatter(const uint8_t *cell, const unsigned *counts,
                                  const unsigned *totals, unsigned num_samples,
                                  unsigned num_blocks, int num_sites, int site_bits,
-                                 unsigned *bucket, hipStream_t s);
+                                 const HeadMask &empty, unsigned *bucket, float4 *sr,
+                                 hipStream_t s);
 // Soft decomposition: bucket[i] = i (i < S), totals[k] = S, queue cleared.
 hipError_t launch_soft_setup(unsigned S, int num_sites, unsigned *bucket, unsigned *totals,
                              unsigned *queue, hipStream_t s);
 // Blend every head's outputs sr[k * S + i] by the soft Voronoi weights and
 // composite; contrib (nullable) receives the per-ray head contributions.
 hipError_t launch_soft_composite(const RenderGeometry &g, const float4 *sites, int num_sites,
-                                 float beta, const float *t, const float4 *sr, float *rgb,
-                                 float *depth, float *opacity, float *contrib, hipStream_t s);
+                                 const HeadMask &empty, float beta, const float *t,
+                                 const float4 *sr, float *rgb, float *depth, float *opacity,
+                                 float *contrib, hipStream_t s);
 hipError_t launch_composite(const RenderGeometry &g, const float *t, const uint8_t *cell,
                             const float4 *sr, float *rgb, float *depth, float *opacity,
                             hipStream_t s);
@@ -113,7 +122,8 @@ struct MlpVariant {
     hipError_t (*launch)(const unsigned *bucket, const unsigned *totals, int num_sites,
                          const RenderGeometry &g, const float *t, const void *dirbuf,
                          const unsigned char *streams, const float *blocks, float4 *sr,
-                         unsigned *queue, int grid, bool soft, hipStream_t s);
+                         unsigned *queue, int grid, bool soft, const HeadMask &empty,
+                         hipStream_t s);
 };
 
 // Returns nullptr when no kernel is compiled for this architecture/precision.

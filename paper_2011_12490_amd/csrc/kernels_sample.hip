@@ -616,11 +616,14 @@ __device__ __forceinline__ void head_block_base(const unsigned *__restrict__ pre
 // samples per head (equal-cell ballots, wave-private counters); after one
 // barrier every wave knows its first position per head (the block's base
 // plus the earlier waves' counts); pass 2 ranks each step's samples of one
-// head by ballot and advances the wave's own counters.
+// head by ballot and advances the wave's own counters.  A sample owned by a
+// 0-capacity head keeps its bucket slot (the offsets are the same) but gets
+// zero density and colour in sr: the MLP does not evaluate that head.
 __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
     const uint8_t *__restrict__ cell, const unsigned *__restrict__ prefix,
     const unsigned *__restrict__ totals, unsigned num_samples, unsigned num_blocks,
-    int num_sites, int site_bits, unsigned *__restrict__ bucket)
+    int num_sites, int site_bits, HeadMask empty, unsigned *__restrict__ bucket,
+    float4 *__restrict__ sr)
 {
     constexpr int kWavesPerBlock = kThreads / 64;
     constexpr int kSteps = kBucketBlock / kThreads;  // 64-sample steps per wave
@@ -671,6 +674,8 @@ __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
             const unsigned pos = start + (unsigned)__popcll(peers & below);
             if (pos < num_samples)  // always true when the counts are consistent
                 bucket[pos] = s;
+            if (empty.test(c))
+                sr[s] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
             if ((peers & below) == 0)
                 s_pos[w][c] = start + (unsigned)__popcll(peers);
         }
@@ -824,10 +829,12 @@ hipError_t launch_bucket_scan(unsigned *counts, unsigned num_blocks, int num_sit
 hipError_t launch_bucket_scatter(const uint8_t *cell, const unsigned *counts,
                                  const unsigned *totals, unsigned num_samples,
                                  unsigned num_blocks, int num_sites, int site_bits,
-                                 unsigned *bucket, hipStream_t s)
+                                 const HeadMask &empty, unsigned *bucket, float4 *sr,
+                                 hipStream_t s)
 {
     bucket_scatter_kernel<<<num_blocks, kThreads, 0, s>>>(cell, counts, totals, num_samples,
-                                                          num_blocks, num_sites, site_bits, bucket);
+                                                          num_blocks, num_sites, site_bits, empty,
+                                                          bucket, sr);
     return hipGetLastError();
 }
 

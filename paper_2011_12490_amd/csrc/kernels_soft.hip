@@ -71,7 +71,7 @@ __device__ __forceinline__ float site_distance(const float4 &p, float x, float y
 // LDS, and lane k accumulates head k's share (heads k, k + 64, ...).
 template <bool CONTRIB>
 __global__ __launch_bounds__(kThreads) void soft_composite_kernel(
-    RenderGeometry g, const float4 *__restrict__ sites, int num_sites, float beta,
+    RenderGeometry g, const float4 *__restrict__ sites, int num_sites, HeadMask empty, float beta,
     const float *__restrict__ t, const float4 *__restrict__ sr, float *__restrict__ rgb,
     float *__restrict__ depth, float *__restrict__ opacity, float *__restrict__ contrib)
 {
@@ -108,7 +108,9 @@ __global__ __launch_bounds__(kThreads) void soft_composite_kernel(
             Z = 0.0f;
             for (int k = 0; k < num_sites; ++k) {
                 const float wk = __expf(-beta * (site_distance(s_sites[k], x, y, z) - dmin));
-                const float4 v = sr[(size_t)k * S + si];
+                // a 0-capacity head contributes no density and no colour
+                const float4 v = empty.test(k) ? make_float4(0.0f, 0.0f, 0.0f, 0.0f)
+                                               : sr[(size_t)k * S + si];
                 Z += wk;
                 sig = fmaf(wk, v.x, sig);
                 cr = fmaf(wk, v.y, cr);
@@ -183,16 +185,17 @@ hipError_t launch_soft_setup(unsigned S, int num_sites, unsigned *bucket, unsign
 }
 
 hipError_t launch_soft_composite(const RenderGeometry &g, const float4 *sites, int num_sites,
-                                 float beta, const float *t, const float4 *sr, float *rgb,
-                                 float *depth, float *opacity, float *contrib, hipStream_t s)
+                                 const HeadMask &empty, float beta, const float *t,
+                                 const float4 *sr, float *rgb, float *depth, float *opacity,
+                                 float *contrib, hipStream_t s)
 {
     const unsigned blocks = (g.num_rays + kWaves - 1) / kWaves;
     if (contrib)
-        soft_composite_kernel<true><<<blocks, kThreads, 0, s>>>(g, sites, num_sites, beta, t, sr,
-                                                                rgb, depth, opacity, contrib);
+        soft_composite_kernel<true><<<blocks, kThreads, 0, s>>>(
+            g, sites, num_sites, empty, beta, t, sr, rgb, depth, opacity, contrib);
     else
-        soft_composite_kernel<false><<<blocks, kThreads, 0, s>>>(g, sites, num_sites, beta, t, sr,
-                                                                 rgb, depth, opacity, nullptr);
+        soft_composite_kernel<false><<<blocks, kThreads, 0, s>>>(
+            g, sites, num_sites, empty, beta, t, sr, rgb, depth, opacity, nullptr);
     return hipGetLastError();
 }
 

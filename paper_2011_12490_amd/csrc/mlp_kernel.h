@@ -567,7 +567,7 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
     const unsigned *__restrict__ bucket, const unsigned *__restrict__ totals, int num_sites,
     RenderGeometry geo, const float *__restrict__ tbuf, const void *__restrict__ dirbuf,
     const unsigned char *__restrict__ streams, const float *__restrict__ blocks,
-    float4 *__restrict__ sr, unsigned *__restrict__ queue)
+    float4 *__restrict__ sr, unsigned *__restrict__ queue, HeadMask empty)
 {
     constexpr bool soft = SOFT;
     using CT = Chunk<C>;
@@ -592,7 +592,8 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
         for (int j = 0; j < 4; ++j) {
             const int k = 4 * tid + j;
             tot[j] = k < num_sites ? totals[k] : 0u;
-            nt[j] = (tot[j] + C::TILE - 1) / C::TILE;
+            // a 0-capacity head keeps its rows but gets no tiles
+            nt[j] = k < num_sites && empty.test(k) ? 0u : (tot[j] + C::TILE - 1) / C::TILE;
             so += tot[j];
             st += nt[j];
         }
@@ -1033,7 +1034,7 @@ template <class C>
 hipError_t launch_mlp(const unsigned *bucket, const unsigned *totals, int num_sites,
                       const RenderGeometry &g, const float *t, const void *dirbuf,
                       const unsigned char *streams, const float *blocks, float4 *sr,
-                      unsigned *queue, int cus, bool soft, hipStream_t s)
+                      unsigned *queue, int cus, bool soft, const HeadMask &empty, hipStream_t s)
 {
     static bool configured = false;
     if (!configured) {
@@ -1048,10 +1049,10 @@ hipError_t launch_mlp(const unsigned *bucket, const unsigned *totals, int num_si
     }
     if (soft)
         mlp_kernel<C, true><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(
-            bucket, totals, num_sites, g, t, dirbuf, streams, blocks, sr, queue);
+            bucket, totals, num_sites, g, t, dirbuf, streams, blocks, sr, queue, empty);
     else
         mlp_kernel<C, false><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(
-            bucket, totals, num_sites, g, t, dirbuf, streams, blocks, sr, queue);
+            bucket, totals, num_sites, g, t, dirbuf, streams, blocks, sr, queue, empty);
     return hipGetLastError();
 }
 

@@ -52,7 +52,7 @@ class derf_stats(ctypes.Structure):
 
 
 EXPORTS = ("derf_weights_count", "derf_create", "derf_render", "derf_render_debug",
-           "derf_render_soft", "derf_set_timing", "derf_get_stats", "derf_reset_stats", "derf_destroy",
+           "derf_render_soft", "derf_set_empty_heads", "derf_set_timing", "derf_get_stats", "derf_reset_stats", "derf_destroy",
            "derf_status_string", "derf_last_error")
 
 _lib: Optional[ctypes.CDLL] = None
@@ -87,6 +87,8 @@ def lib() -> ctypes.CDLL:
         L.derf_render_soft.argtypes = [P, P, P, ctypes.c_longlong, ctypes.c_float, ctypes.c_float,
                                        ctypes.POINTER(derf_sampling), ctypes.c_float, P, P, P, P, P]
         L.derf_render_soft.restype = ctypes.c_int
+        L.derf_set_empty_heads.argtypes = [P, P]
+        L.derf_set_empty_heads.restype = ctypes.c_int
         L.derf_set_timing.argtypes = [P, ctypes.c_int]
         L.derf_set_timing.restype = ctypes.c_int
         L.derf_get_stats.argtypes = [P, ctypes.POINTER(derf_stats)]
@@ -168,6 +170,15 @@ def derf_render_soft(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float,
            "derf_render_soft")
 
 
+def derf_set_empty_heads(h, flags):
+    """Mark 0-capacity heads (flags: K truthy values, or None to clear)."""
+    if flags is None:
+        _check(lib().derf_set_empty_heads(h, None), "derf_set_empty_heads")
+        return
+    arr = (ctypes.c_int * len(flags))(*[1 if f else 0 for f in flags])
+    _check(lib().derf_set_empty_heads(h, ctypes.cast(arr, ctypes.c_void_p)), "derf_set_empty_heads")
+
+
 def derf_set_timing(h, on: bool):
     _check(lib().derf_set_timing(h, int(on)), "derf_set_timing")
 
@@ -239,6 +250,12 @@ class Renderer:
         if debug:
             return rgb, depth, opac, extra
         return rgb, depth, opac
+
+    def set_empty_heads(self, flags):
+        """Mark 0-capacity heads (K flags; None clears)."""
+        if flags is not None and len(flags) != self.num_sites:
+            raise ValueError("need one flag per head")
+        derf_set_empty_heads(self.handle, flags)
 
     def render_soft(self, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far: float,
                     n: int, beta: float, seed: int = 0, perturb: bool = True,

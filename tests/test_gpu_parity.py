@@ -333,3 +333,76 @@ def test_cells_contiguous_and_ordered_on_gpu_output():
         runs = cell[r][change[r]]
         dist = np.linalg.norm(sc.sites[runs].astype(np.float64) - sc.rays_o[r], axis=1)
         assert np.all(np.diff(dist) > 0), (r, runs, dist)
+
+
+# ------------------------------------------------------- 0-capacity heads ----
+
+def _render_with(sc, precision, empty=None, weights=None, n_fine=0, seed=scenes.SEED_RENDER):
+    derf = _derf()
+    cfg = sc.cfg
+    o = torch.from_numpy(sc.rays_o).cuda()
+    d = torch.from_numpy(sc.rays_d).cuda()
+    r = derf.Renderer(sc.sites, cfg.arch, sc.weights if weights is None else weights, precision)
+    if empty is not None:
+        r.set_empty_heads(list(empty))
+    out = r.render(o, d, cfg.near, cfg.far, cfg.n_coarse, n_fine, seed)
+    torch.cuda.synchronize()
+    r.close()
+    return [x.cpu().numpy() for x in out]
+
+
+def test_empty_heads():
+    """0-capacity heads (no density anywhere, never evaluated): pixels equal
+    the oracle's with the same heads empty, and equal bitwise the render whose
+    heads have all-zero weights (density 0 gives alpha 0), single pass and
+    hierarchical."""
+    cfg = scenes.CONFIGS["derf_k16"]
+    sc = scenes.make_scene(cfg)
+    empty = np.zeros(cfg.num_sites, int)
+    empty[[1, 5, 9, 13]] = 1
+    zeroed = sc.weights.copy()
+    zeroed[empty == 1] = 0.0
+    gpu = _render_with(sc, "bf16", empty=empty)
+    ids = scenes.ray_subset(256, cfg.num_rays)
+    ref = oracle.render(sc.sites, cfg.arch, sc.weights, sc.rays_o[ids], sc.rays_d[ids], cfg.near,
+                        cfg.far, cfg.n_coarse, 0, seed=scenes.SEED_RENDER, ray_ids=ids,
+                        empty=empty, nthreads=NTHREADS)
+    _check_pixels(gpu, ref, ids, TOL["bf16"], "derf frame, 4 empty heads")
+    full = _render_with(sc, "bf16")
+    assert np.abs(full[2] - gpu[2]).max() > 1e-3  # the marks changed the image
+    for n_fine in (0, 32):
+        a = _render_with(sc, "bf16", empty=empty, n_fine=n_fine) if n_fine else gpu
+        b = _render_with(sc, "bf16", weights=zeroed, n_fine=n_fine)
+        for x, y in zip(a, b):
+            np.testing.assert_array_equal(x, y)
+
+
+def test_empty_heads_soft_and_cleared():
+    derf = _derf()
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], sigma_bias=1.0)
+    sc = scenes.make_scene(cfg)
+    empty = [0, 1, 0, 1]
+    o = torch.from_numpy(sc.rays_o).cuda()
+    d = torch.from_numpy(sc.rays_d).cuda()
+    r = derf.Renderer(sc.sites, cfg.arch, sc.weights, "fp32")
+    before = [x.cpu().numpy() for x in r.render(o, d, cfg.near, cfg.far, cfg.n_coarse, 0,
+                                                 scenes.SEED_RENDER)]
+    r.set_empty_heads(empty)
+    soft = [x.cpu().numpy() for x in r.render_soft(o, d, cfg.near, cfg.far, cfg.n_coarse, 5.0,
+                                                    seed=scenes.SEED_RENDER, contrib=True)]
+    r.set_empty_heads(None)
+    after = [x.cpu().numpy() for x in r.render(o, d, cfg.near, cfg.far, cfg.n_coarse, 0,
+                                                scenes.SEED_RENDER)]
+    torch.cuda.synchronize()
+    r.close()
+    for x, y in zip(before, after):
+        np.testing.assert_array_equal(x, y)
+    ids = np.arange(0, cfg.num_rays, 4)
+    ref = oracle.render(sc.sites, cfg.arch, sc.weights, sc.rays_o[ids], sc.rays_d[ids], cfg.near,
+                        cfg.far, cfg.n_coarse, 0, seed=scenes.SEED_RENDER, ray_ids=ids,
+                        mode="soft", beta=5.0, contrib=True, empty=np.array(empty),
+                        nthreads=NTHREADS)
+    e = max(np.abs(soft[0][ids] - ref.rgb).max(), np.abs(soft[2][ids] - ref.opacity).max(),
+            np.abs(soft[3][ids] - ref.contrib).max())
+    print("soft, 2 empty heads: max err %.3g" % e, flush=True)
+    assert e <= TOL["fp32"]

@@ -132,8 +132,8 @@ int derf_create(derf_handle **out, int num_sites, const float *sites_xyz,
  * default stream).  The work is enqueued on hip_stream and the call returns
  * without waiting for it; the inputs must stay valid and the outputs
  * untouched until it completes.  Kernel faults surface at the caller's next
- * synchronisation.  num_rays == 0 is a no-op.  R * (n_coarse + n_fine) must
- * stay below 2^32; larger frames are rendered in several calls.  Calls on one handle
+ * synchronisation.  num_rays == 0 is a no-op.  num_rays < 2^30 and
+ * R * (n_coarse + n_fine) < 2^32; larger frames are rendered in several calls.  Calls on one handle
  * must not run concurrently (they share the handle's workspace, which grows
  * as needed and is reused). */
 int derf_render(derf_handle *h, const float *rays_o, const float *rays_d, long long num_rays,

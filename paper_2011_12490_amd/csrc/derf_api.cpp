@@ -107,6 +107,12 @@ struct derf_handle {
 
 namespace {
 
+// assignment blocks of S samples (S up to 2^32 - 1: the sum is taken in 64 bits)
+inline unsigned blocks_of(unsigned S)
+{
+    return (unsigned)(((unsigned long long)S + kBucketBlock - 1) / kBucketBlock);
+}
+
 template <class T>
 T *carve(char *&p, size_t count)
 {
@@ -277,8 +283,8 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
         return fail(DERF_ERR_INVALID_ARG, "null handle");
     if (!samp)
         return fail(DERF_ERR_INVALID_ARG, "null sampling descriptor");
-    if (num_rays < 0)
-        return fail(DERF_ERR_INVALID_ARG, "num_rays < 0");
+    if (num_rays < 0 || num_rays >= (1LL << 30))
+        return fail(DERF_ERR_INVALID_ARG, "need 0 <= num_rays < 2^30");
     if (!(near_t < far_t) || !isfinite(near_t) || !isfinite(far_t))
         return fail(DERF_ERR_INVALID_ARG, "need finite near < far");
     if (samp->n_coarse < 1 || samp->n_fine < 0 || samp->n_coarse + samp->n_fine > 1024)
@@ -300,8 +306,8 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
     const bool hier = samp->n_fine > 0;
     const unsigned R = (unsigned)num_rays, N = (unsigned)samp->n_coarse, NF = (unsigned)samp->n_fine;
     const unsigned S = R * N, Sf = R * NF;
-    const unsigned nblk = (S + kBucketBlock - 1) / kBucketBlock;
-    const unsigned nblk_f = (Sf + kBucketBlock - 1) / kBucketBlock;
+    const unsigned nblk = blocks_of(S);
+    const unsigned nblk_f = blocks_of(Sf);
     const unsigned nblk_max = nblk > nblk_f ? nblk : nblk_f;
     const size_t need = layout(nullptr, S, Sf, R, nblk_max, h->num_sites, h->bf16, nullptr);
     int rc = ensure_workspace(h, need);
@@ -427,8 +433,8 @@ int render_soft_impl(derf_handle *h, const float *rays_o, const float *rays_d,
         return fail(DERF_ERR_INVALID_ARG, "null handle");
     if (!samp)
         return fail(DERF_ERR_INVALID_ARG, "null sampling descriptor");
-    if (num_rays < 0)
-        return fail(DERF_ERR_INVALID_ARG, "num_rays < 0");
+    if (num_rays < 0 || num_rays >= (1LL << 30))
+        return fail(DERF_ERR_INVALID_ARG, "need 0 <= num_rays < 2^30");
     if (!(near_t < far_t) || !isfinite(near_t) || !isfinite(far_t))
         return fail(DERF_ERR_INVALID_ARG, "need finite near < far");
     if (!(beta >= 0.0f) || !isfinite(beta))
@@ -449,7 +455,7 @@ int render_soft_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     HIP_TRY(hipSetDevice(h->device), "hipSetDevice");
     const unsigned R = (unsigned)num_rays, N = (unsigned)samp->n_coarse, S = R * N;
-    const unsigned nblk = (S + kBucketBlock - 1) / kBucketBlock;
+    const unsigned nblk = blocks_of(S);
     int rc = ensure_workspace(h, layout_soft(nullptr, S, R, nblk, h->num_sites, h->bf16, nullptr));
     if (rc != DERF_OK)
         return rc;

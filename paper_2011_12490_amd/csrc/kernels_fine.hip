@@ -241,7 +241,7 @@ __global__ __launch_bounds__(kWaves * 64) void merge_composite_kernel(
     }
 }
 
-inline unsigned blocks_for(unsigned items, unsigned per) { return (items + per - 1) / per; }
+inline unsigned blocks_for(size_t items, unsigned per) { return (unsigned)((items + per - 1) / per); }
 
 }  // namespace
 

@@ -394,7 +394,9 @@ __global__ __launch_bounds__(kThreads) void sample_assign_kernel(
         unsigned i_;
         unsigned r_last;
         split_sample(block_base, g.n, g.inv_n, r_first, i_);
-        split_sample(min(block_base + kBucketBlock, g.num_samples) - 1, g.n, g.inv_n, r_last, i_);
+        split_sample((unsigned)(min((unsigned long long)block_base + kBucketBlock,
+                                    (unsigned long long)g.num_samples) - 1),
+                     g.n, g.inv_n, r_last, i_);
         staged = r_last - r_first < (unsigned)kStageRays;
         if (staged) {
             const unsigned nr = r_last - r_first + 1;

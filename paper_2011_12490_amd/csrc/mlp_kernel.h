@@ -593,7 +593,7 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
             const int k = 4 * tid + j;
             tot[j] = k < num_sites ? totals[k] : 0u;
             // a 0-capacity head keeps its rows but gets no tiles
-            nt[j] = k < num_sites && empty.test(k) ? 0u : (tot[j] + C::TILE - 1) / C::TILE;
+            nt[j] = k < num_sites && empty.test(k) ? 0u : tot[j] / C::TILE + (tot[j] % C::TILE != 0);
             so += tot[j];
             st += nt[j];
         }
@@ -702,9 +702,11 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
     // the two prefetch phases for the tile whose rows are [r0, r_end) and
     // whose bucket entries start at row base
     auto prefetch_ids = [&](unsigned r0, unsigned r_end, unsigned base) {
-        // bucket ids (rows past the head's end read row 0's)
-        const unsigned row = r0 + wave * (NB * 32) + lane % (NB * 32);
-        load_lds4(bucket + min((row < r_end ? row : r0) - base, geo.num_samples - 1), pf_wave);
+        // bucket ids (rows past the head's end read row 0's); offsets from r0,
+        // so that a tile padded past 2^32 - 1 does not wrap into range
+        const unsigned off = wave * (NB * 32) + lane % (NB * 32);
+        const unsigned row = off < r_end - r0 ? r0 + off : r0;
+        load_lds4(bucket + min(row - base, geo.num_samples - 1), pf_wave);
     };
     auto prefetch_rays = [&]() {
         // depths, ray origins and directions of the ids in LDS
@@ -772,8 +774,7 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
         bool valid[NB];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-            const unsigned row = row0 + (wave * NB + nb) * 32 + n;
-            valid[nb] = row < row_end;
+            valid[nb] = (wave * NB + nb) * 32 + n < row_end - row0;
             const unsigned q = nb * 32 + n;
             sid[nb] = min(pf[q], geo.num_samples - 1);
             unsigned r = (unsigned)((double)sid[nb] * geo.inv_n);

@@ -284,6 +284,16 @@ def test_zero_rays_is_a_noop_and_bad_sampling_is_refused():
         with pytest.raises(derf.DerfError) as e:
             r.render(o1, d1, *args)
         assert e.value.status == derf.DERF_ERR_INVALID_ARG, args
+    # frames past the index limits (2^30 rays, 2^32 samples) are refused before
+    # any work is enqueued (the small buffers below are never touched)
+    import ctypes
+    L = derf.lib()
+    for R, n in ((1 << 30, 1), (1 << 28, 16)):
+        samp = derf.derf_sampling(n, 0, 1, 1, 0)
+        st = L.derf_render(r.handle, derf._dptr(o1), derf._dptr(d1), R, 2.0, 6.0,
+                           ctypes.byref(samp), derf._dptr(o1), derf._dptr(d1), derf._dptr(d1),
+                           None)
+        assert st == derf.DERF_ERR_INVALID_ARG, (R, n)
     r.close()
 
 
@@ -406,3 +416,47 @@ def test_empty_heads_soft_and_cleared():
             np.abs(soft[3][ids] - ref.contrib).max())
     print("soft, 2 empty heads: max err %.3g" % e, flush=True)
     assert e <= TOL["fp32"]
+
+
+# ------------------------------------------------------ the largest frame ----
+
+def test_maximum_sample_count():
+    """The largest frame one call accepts: 16,843,009 rays x 255 samples =
+    2^32 - 1 samples (about 110 GB of workspace), object-centric, 8x128 heads
+    in bf16, with 16 heads (search over all sites) and 64 heads (walk tables).
+    Every sample, block and row index sits at the top of the 32-bit range: the
+    last assignment block ends at 2^32 - 1 and the last MLP tile's padding
+    runs past it.  Pixels of the first and last rays and of a spread between
+    them match the oracle."""
+    derf = _derf()
+    cfg = scenes.with_changes(scenes.CONFIGS["derf_k16"], width=65537, height=257, n_coarse=255,
+                              camera="object", fov_x_deg=40.0, near=2.0, far=6.0)
+    assert cfg.num_rays * cfg.n_coarse == 2 ** 32 - 1
+    print("max frame: building %d rays" % cfg.num_rays, flush=True)
+    sc16 = scenes.make_scene(cfg)
+    o = torch.from_numpy(sc16.rays_o).cuda()
+    d = torch.from_numpy(sc16.rays_d).cuda()
+    R = cfg.num_rays
+    ids = np.unique(np.concatenate([np.arange(4), np.arange(R - 4, R),
+                                    scenes.ray_subset(16, R)]))
+    for K in (16, 64):
+        if K == 16:
+            sites, weights = sc16.sites, sc16.weights
+        else:
+            sites = scenes.make_sites("gmm_kmeans", K)
+            weights = scenes.make_weights(cfg.arch, K)
+        print("max frame: rendering with K=%d" % K, flush=True)
+        r = derf.Renderer(sites, cfg.arch, weights, "bf16")
+        rgb, depth, opac = r.render(o, d, cfg.near, cfg.far, cfg.n_coarse, 0, scenes.SEED_RENDER)
+        torch.cuda.synchronize()
+        st = derf.derf_get_stats(r.handle)
+        gpu = [rgb.cpu().numpy(), depth.cpu().numpy(), opac.cpu().numpy()]
+        r.close()
+        del rgb, depth, opac
+        torch.cuda.empty_cache()
+        assert sum(st.head_samples[:K]) == 2 ** 32 - 1
+        assert np.all(np.isfinite(gpu[0])) and np.all(np.isfinite(gpu[2]))
+        ref = oracle.render(sites, cfg.arch, weights, sc16.rays_o[ids], sc16.rays_d[ids],
+                            cfg.near, cfg.far, cfg.n_coarse, 0, seed=scenes.SEED_RENDER,
+                            ray_ids=ids, nthreads=NTHREADS)
+        _check_pixels(gpu, ref, ids, TOL["bf16"], "max frame K=%d" % K)

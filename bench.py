@@ -85,9 +85,28 @@ def cpu_baseline(sc, n_rays, nthreads):
                   cfg.far, cfg.n_coarse, cfg.n_fine, seed=scenes.SEED_RENDER, ray_ids=ids,
                   nthreads=nthreads)
     dt = time.perf_counter() - t0
+    # one thread on a sixteenth of the sample (about the same wall time)
+    ids1 = ids[::16]
+    t1 = time.perf_counter()
+    oracle.render(sc.sites, cfg.arch, sc.weights, sc.rays_o[ids1], sc.rays_d[ids1], cfg.near,
+                  cfg.far, cfg.n_coarse, cfg.n_fine, seed=scenes.SEED_RENDER, ray_ids=ids1,
+                  nthreads=1)
+    dt1 = time.perf_counter() - t1
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {"value": len(ids) / dt, "unit": "rays/s", "cores": nthreads, "kind": "oracle",
             "sample": "%d seeded rays of the same frame (%d head evaluations, fp64 heads), %.1f s"
-                      % (len(ids), len(ids) * (cfg.n_coarse + cfg.n_fine), dt)}
+                      % (len(ids), len(ids) * (cfg.n_coarse + cfg.n_fine), dt),
+            "cpu_model": model,
+            "single_thread": {"value": len(ids1) / dt1, "unit": "rays/s",
+                              "sample": "%d of those rays, %.1f s" % (len(ids1), dt1)}}
 
 
 def main():

@@ -61,6 +61,8 @@ def _lib_handle():
         lib.oracle_render_ex.argtypes = render_sig + [ctypes.c_int, ctypes.c_double,
                                                       ctypes.c_void_p, ctypes.c_void_p]
         lib.oracle_render_ex.restype = ctypes.c_int
+        lib.oracle_render_mixed.argtypes = lib.oracle_render_ex.argtypes
+        lib.oracle_render_mixed.restype = ctypes.c_int
         lib.oracle_philox4x32_10.argtypes = [_P, _P, _P]
         lib.oracle_philox4x32_10.restype = None
         lib.oracle_jitter.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint32,
@@ -287,10 +289,22 @@ def render(sites, arch, weights, rays_o, rays_d, near: float, far: float, n_coar
     """Render rays on the CPU.  mode: derf | direct | back | plain | soft.
     contrib (soft mode, single pass): also return the per-ray head
     contributions W(r) [R, K] of Sec. 3.2 Eq. 6.  empty: optional [K] flags of
-    0-capacity heads (no density anywhere)."""
+    0-capacity heads (no density anywhere).  arch may be a list of K
+    architectures (heads of different capacities); weights is then the heads'
+    packed weights concatenated in head order."""
     lib = _lib_handle()
     sites = np.ascontiguousarray(sites, np.float32).reshape(-1, 3)
-    weights = np.ascontiguousarray(weights, np.float32)
+    mixed = isinstance(arch, (list, tuple)) and not isinstance(arch[0], int)
+    if mixed:
+        if len(arch) != sites.shape[0]:
+            raise ValueError("need one architecture per head")
+        weights = np.ascontiguousarray(np.concatenate([np.ravel(w) for w in weights])
+                                       if isinstance(weights, (list, tuple)) else weights,
+                                       np.float32)
+        if weights.size != sum(weights_count(a) for a in arch):
+            raise ValueError("weights do not match the architectures")
+    else:
+        weights = np.ascontiguousarray(weights, np.float32)
     o = np.ascontiguousarray(rays_o, np.float32).reshape(-1, 3)
     d = np.ascontiguousarray(rays_d, np.float32).reshape(-1, 3)
     R = o.shape[0]
@@ -307,8 +321,9 @@ def render(sites, arch, weights, rays_o, rays_d, near: float, far: float, n_coar
         margin = np.zeros((R, N), np.float64)
     else:
         t = cell = sig = srgb = margin = None
-    a = _arch(arch)
-    args = [sites.shape[0], _ptr(sites), ctypes.byref(a), _ptr(weights), R, _ptr(o), _ptr(d),
+    a = (_Arch * len(arch))(*[_arch(x) for x in arch]) if mixed else _arch(arch)
+    a_ref = ctypes.cast(a, ctypes.POINTER(_Arch)) if mixed else ctypes.byref(a)
+    args = [sites.shape[0], _ptr(sites), a_ref, _ptr(weights), R, _ptr(o), _ptr(d),
             _ptr(ids), near, far, n_coarse, n_fine, seed, int(perturb), _ptr(rgb), _ptr(dep),
             _ptr(op), _ptr(t), _ptr(cell), _ptr(sig), _ptr(srgb), _ptr(margin), nthreads]
     fn = {"derf": lib.oracle_render, "direct": lib.oracle_render_direct,
@@ -318,12 +333,15 @@ def render(sites, arch, weights, rays_o, rays_d, near: float, far: float, n_coar
         if mode != "soft" or n_fine != 0:
             raise ValueError("contributions come from the single-pass soft render")
         W = np.zeros((R, sites.shape[0]), np.float64)
-    if empty is not None:
-        e = np.ascontiguousarray(np.asarray(empty) != 0, np.uint8)
-        if e.shape != (sites.shape[0],):
-            raise ValueError("empty needs one flag per head")
+    if empty is not None or mixed:
+        e = None
+        if empty is not None:
+            e = np.ascontiguousarray(np.asarray(empty) != 0, np.uint8)
+            if e.shape != (sites.shape[0],):
+                raise ValueError("empty needs one flag per head")
         code = {"derf": 0, "plain": 1, "soft": 2, "direct": 3, "back": 4}[mode]
-        rc = lib.oracle_render_ex(*args, code, beta, _ptr(e), _ptr(W))
+        fn_ex = lib.oracle_render_mixed if mixed else lib.oracle_render_ex
+        rc = fn_ex(*args, code, beta, _ptr(e), _ptr(W))
     elif contrib:
         rc = lib.oracle_render_soft_contrib(*args, beta, _ptr(W))
     elif mode == "soft":

@@ -468,16 +468,32 @@ typedef struct {
     int perturb;
     double *contrib; /* soft mode, optional: per-ray head contributions [R][K] (Eq. 6) */
     const unsigned char *empty; /* optional [K]: nonzero = 0-capacity head (no density) */
+    /* optional per-head architectures (heads of different capacities): */
+    const oracle_arch *archs;   /* [K], or NULL: every head is *arch */
+    const long long *woff;      /* [K] offset of head k's weights */
+    size_t mix_scratch;         /* doubles of scratch one head evaluation uses */
+    int mix_pos, mix_dir;       /* largest encoding lengths over the heads */
 } render_args;
 
-/* Head k at x: its density and colour, or zero for a 0-capacity head (the
- * empty-space head of the paper's closing remarks). */
-static void eval_head(const render_args *A, int k, const double *gx, const double *gd,
-                      double *sigma, double rgb[3], double *scratch)
+/* Head k at x (view direction dh): its density and colour, or zero for a
+ * 0-capacity head (the empty-space head of Sec. 5).  gx, gd: the encodings
+ * of x and dh for the shared architecture; with per-head architectures each
+ * head encodes with its own frequencies. */
+static void eval_head(const render_args *A, int k, const double xd[3], const double dh[3],
+                      const double *gx, const double *gd, double *sigma, double rgb[3],
+                      double *scratch)
 {
     if (A->empty && A->empty[k]) {
         *sigma = 0.0;
         rgb[0] = rgb[1] = rgb[2] = 0.0;
+        return;
+    }
+    if (A->archs) {
+        const oracle_arch *a = &A->archs[k];
+        double *gxk = scratch + A->mix_scratch, *gdk = gxk + A->mix_pos;
+        oracle_posenc(a->pos_freqs, xd, gxk);
+        oracle_posenc(a->dir_freqs, dh, gdk);
+        oracle_head_eval(a, A->weights + A->woff[k], gxk, gdk, sigma, rgb, scratch);
         return;
     }
     oracle_head_eval(A->arch, A->weights + (size_t)k * oracle_weights_count(A->arch), gx, gd,
@@ -488,8 +504,9 @@ enum { MODE_DERF = 0, MODE_PLAIN = 1, MODE_SOFT = 2, MODE_DIRECT = 3, MODE_BACK 
 
 /* Evaluate the field at every sample of one ray: cell, sigma, rgb. */
 static void eval_samples(const render_args *A, int mode, double beta, const float o[3],
-                         const float d[3], const double *gd, int n, const float *t, int *cell,
-                         double *sigma, double *rgb, double *gx, double *scratch, double *soft_w)
+                         const float d[3], const double dh[3], const double *gd, int n,
+                         const float *t, int *cell, double *sigma, double *rgb, double *gx,
+                         double *scratch, double *soft_w)
 {
     const oracle_arch *a = A->arch;
     for (int i = 0; i < n; ++i) {
@@ -499,7 +516,7 @@ static void eval_samples(const render_args *A, int mode, double beta, const floa
         oracle_posenc(a->pos_freqs, xd, gx);
         if (mode == MODE_PLAIN) {
             cell[i] = 0;
-            oracle_head_eval(a, A->weights, gx, gd, &sigma[i], &rgb[3 * i], scratch);
+            eval_head(A, 0, xd, dh, gx, gd, &sigma[i], &rgb[3 * i], scratch);
         } else if (mode == MODE_SOFT) {
             /* Eq. 4-5 with the soft Voronoi weights of Eq. 8 */
             double dist_min = INFINITY;
@@ -520,7 +537,7 @@ static void eval_samples(const render_args *A, int mode, double beta, const floa
                 if (wk == 0.0)
                     continue;
                 double sk, ck[3];
-                eval_head(A, k, gx, gd, &sk, ck, scratch);
+                eval_head(A, k, xd, dh, gx, gd, &sk, ck, scratch);
                 s += wk * sk;
                 c[0] += wk * ck[0];
                 c[1] += wk * ck[1];
@@ -542,7 +559,7 @@ static void eval_samples(const render_args *A, int mode, double beta, const floa
             }
         } else {
             cell[i] = oracle_nearest_site(A->K, A->sites, x);
-            eval_head(A, cell[i], gx, gd, &sigma[i], &rgb[3 * i], scratch);
+            eval_head(A, cell[i], xd, dh, gx, gd, &sigma[i], &rgb[3 * i], scratch);
         }
     }
 }
@@ -576,6 +593,12 @@ static int render_impl(const render_args *A, int mode, double beta, long long R,
         return -1;
     int P = 3 + 6 * a->pos_freqs, Dd = 3 + 6 * a->dir_freqs;
     size_t scratch_len = 4 * (size_t)(P + a->width + Dd + a->rgb_hidden + 8);
+    if (A->archs) {
+        /* per-head encodings go after the head evaluation's own scratch */
+        P = A->mix_pos;
+        Dd = A->mix_dir;
+        scratch_len = A->mix_scratch + (size_t)P + (size_t)Dd;
+    }
 #ifdef _OPENMP
     if (nthreads > 0)
         omp_set_num_threads(nthreads);
@@ -616,7 +639,7 @@ static int render_impl(const render_args *A, int mode, double beta, long long R,
                 oracle_sample_depths(A->seed, rid, A->near_t, A->far_t, nc, A->perturb, tc);
                 const float *tt = tc;
                 int n = nc;
-                eval_samples(A, mode, beta, o, d, gd, nc, tc, cell, sigma, rgb, gx, scratch, soft_w);
+                eval_samples(A, mode, beta, o, d, dh, gd, nc, tc, cell, sigma, rgb, gx, scratch, soft_w);
                 intervals(tc, nc, A->near_t, A->far_t, delta);
                 double c3[3], dep, op;
                 finish(mode, nc, cell, tc, sigma, rgb, delta, c3, &dep, &op, w);
@@ -638,7 +661,7 @@ static int render_impl(const render_args *A, int mode, double beta, long long R,
                     merge_sorted(tc, nc, tf, nf, tm);
                     tt = tm;
                     n = N;
-                    eval_samples(A, mode, beta, o, d, gd, N, tm, cell, sigma, rgb, gx, scratch, NULL);
+                    eval_samples(A, mode, beta, o, d, dh, gd, N, tm, cell, sigma, rgb, gx, scratch, NULL);
                     intervals(tm, N, A->near_t, A->far_t, delta);
                     finish(mode, N, cell, tm, sigma, rgb, delta, c3, &dep, &op, NULL);
                 }
@@ -684,7 +707,8 @@ static int render_impl(const render_args *A, int mode, double beta, long long R,
         double *dbg_rgb, double *dbg_margin, int nthreads
 
 #define ORACLE_FILL_ARGS                                                                       \
-    render_args A = { K, sites, arch, weights, near_t, far_t, n_coarse, n_fine, seed, perturb, NULL, NULL };
+    render_args A = { K, sites, arch, weights, near_t, far_t, n_coarse, n_fine, seed, perturb, \
+                      NULL, NULL, NULL, NULL, 0, 0, 0 };
 
 /* DeRF render: nearest-site heads, per-segment integration, Painter's merge. */
 int oracle_render(ORACLE_RENDER_ARGS)
@@ -740,6 +764,46 @@ int oracle_render_ex(ORACLE_RENDER_ARGS, int mode, double beta, const unsigned c
     A.empty = empty;
     return render_impl(&A, mode, beta, R, rays_o, rays_d, ray_ids, out_rgb, out_depth,
                        out_opacity, dbg_t, dbg_cell, dbg_sigma, dbg_rgb, dbg_margin, nthreads);
+}
+
+/* As oracle_render_ex with one architecture per head: arch points to K
+ * architectures and weights holds the heads' packed weights one after
+ * another (head k's oracle_weights_count(&arch[k]) floats).  Heads of
+ * different capacities in one model (Sec. 5). */
+int oracle_render_mixed(ORACLE_RENDER_ARGS, int mode, double beta, const unsigned char *empty,
+                        double *contrib)
+{
+    ORACLE_FILL_ARGS
+    if (K < 1 || mode < MODE_DERF || mode > MODE_BACK ||
+        (contrib && (mode != MODE_SOFT || n_fine != 0)))
+        return -1;
+    long long *woff = malloc(sizeof(long long) * (size_t)K);
+    if (!woff)
+        return -3;
+    long long off = 0;
+    size_t need = 0;
+    int mp = 0, md = 0;
+    for (int k = 0; k < K; ++k) {
+        const oracle_arch *a = &arch[k];
+        woff[k] = off;
+        off += oracle_weights_count(a);
+        const size_t sl = 4 * (size_t)(pos_dim(a) + a->width + dir_dim(a) + a->rgb_hidden + 8);
+        need = sl > need ? sl : need;
+        mp = pos_dim(a) > mp ? pos_dim(a) : mp;
+        md = dir_dim(a) > md ? dir_dim(a) : md;
+    }
+    A.contrib = contrib;
+    A.empty = empty;
+    A.archs = arch;
+    A.woff = woff;
+    A.mix_scratch = need;
+    A.mix_pos = mp;
+    A.mix_dir = md;
+    const int rc = render_impl(&A, mode, beta, R, rays_o, rays_d, ray_ids, out_rgb, out_depth,
+                               out_opacity, dbg_t, dbg_cell, dbg_sigma, dbg_rgb, dbg_margin,
+                               nthreads);
+    free(woff);
+    return rc;
 }
 
 /* Soft Voronoi render (as oracle_render_soft, single pass) that also returns
@@ -834,7 +898,7 @@ int oracle_render_depths(int K, const float *sites, const oracle_arch *arch, con
                 double dn = sqrt((double)d[0] * d[0] + (double)d[1] * d[1] + (double)d[2] * d[2]);
                 double dh[3] = { d[0] / dn, d[1] / dn, d[2] / dn };
                 oracle_posenc(arch->dir_freqs, dh, gd);
-                eval_samples(&A, MODE_DERF, 0.0, o, d, gd, n, tr, cell, sigma, rgb, gx, scratch, NULL);
+                eval_samples(&A, MODE_DERF, 0.0, o, d, dh, gd, n, tr, cell, sigma, rgb, gx, scratch, NULL);
                 intervals(tr, n, near_t, far_t, delta);
                 composite_segments(n, cell, tr, sigma, rgb, delta, out_rgb + 3 * r, out_depth + r,
                                    out_opacity + r, NULL);

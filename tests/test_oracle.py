@@ -522,6 +522,49 @@ def test_empty_heads():
     np.testing.assert_allclose(soft.contrib.sum(1), soft.opacity, rtol=1e-12, atol=1e-15)
 
 
+def test_heads_of_different_capacities():
+    """Per-head architectures (Sec. 5's heterogeneous heads).  With every head
+    given the same architecture the render is the homogeneous one, bitwise;
+    relabelling the heads (sites, architectures and weights together) leaves
+    the image unchanged; and every sample's density and colour are its owning
+    head's network with that head's own encoding frequencies and weights."""
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], sigma_bias=1.0, num_sites=6)
+    sc = scenes.make_scene(cfg)
+    sel = np.arange(0, 1024, 8)
+    o, d = sc.rays_o[sel], sc.rays_d[sel]
+    same = [cfg.arch] * cfg.num_sites
+    for kw in ({}, {"n_fine": 16}, {"mode": "soft", "beta": 4.0, "contrib": True}):
+        a = oracle.render(sc.sites, cfg.arch, sc.weights, o, d, 2.0, 6.0, 32, seed=1,
+                          ray_ids=sel, **kw)
+        b = oracle.render(sc.sites, same, list(sc.weights), o, d, 2.0, 6.0, 32, seed=1,
+                          ray_ids=sel, **kw)
+        for x, y in ((a.rgb, b.rgb), (a.depth, b.depth), (a.opacity, b.opacity),
+                     (a.contrib, b.contrib)):
+            assert (x is None and y is None) or np.array_equal(x, y)
+    archs = [scenes.ARCH_TINY, scenes.ARCH_SMALL, scenes.ARCH_128] * 2
+    ws = [scenes.make_weights(a, 1, seed=100 + k, sigma_bias=1.0)[0] for k, a in enumerate(archs)]
+    res = oracle.render(sc.sites, archs, ws, o, d, 2.0, 6.0, 32, seed=1, ray_ids=sel,
+                        per_sample=True)
+    perm = np.array([3, 0, 5, 1, 4, 2])
+    res_p = oracle.render(sc.sites[perm], [archs[k] for k in perm], [ws[k] for k in perm], o, d,
+                          2.0, 6.0, 32, seed=1, ray_ids=sel, per_sample=True)
+    far = np.all(res.margin > 1e-6, axis=1)
+    assert far.mean() > 0.9
+    np.testing.assert_array_equal(res.rgb[far], res_p.rgb[far])
+    np.testing.assert_array_equal(perm[res_p.cell[far]], res.cell[far])
+    rng = np.random.default_rng(4)
+    for r, i in zip(rng.integers(0, len(sel), 40), rng.integers(0, 32, 40)):
+        c = int(res.cell[r, i])
+        # the sample position as fmaf(t, d, o): the float64 product t d is exact
+        x = (np.float64(res.t[r, i]) * d[r].astype(np.float64) + o[r].astype(np.float64)).astype(
+            np.float32)
+        dh = d[r].astype(np.float64) / np.linalg.norm(d[r].astype(np.float64))
+        sig, rgb = oracle.head_eval(archs[c], ws[c], oracle.posenc(archs[c].pos_freqs, x),
+                                    oracle.posenc(archs[c].dir_freqs, dh))
+        assert sig == pytest.approx(res.sigma[r, i], rel=1e-12, abs=1e-12)
+        np.testing.assert_allclose(rgb, res.srgb[r, i], rtol=1e-12, atol=1e-12)
+
+
 def test_soft_voronoi_converges_to_hard_partition():
     """Eq. 8: as the temperature grows the soft blend of all heads becomes the
     nearest-site render."""

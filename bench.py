@@ -123,6 +123,9 @@ def main():
                     help="comma-separated head counts: the same frame with K k-means sites each")
     ap.add_argument("--empty-heads", default=None, metavar="K1,K2,...",
                     help="mark these heads 0-capacity (empty space): never evaluated")
+    ap.add_argument("--mixed", action="store_true",
+                    help="heads of different capacities: head k gets the 8x128, 6x64 and 4x64 "
+                         "architectures in turn (k mod 3), with their own weights")
     ap.add_argument("--soft", type=float, default=None, metavar="BETA",
                     help="also time the soft decomposition (every head on every sample) at "
                          "temperature BETA, with the per-ray head contributions")
@@ -147,6 +150,8 @@ def main():
         cfg = scenes.with_changes(cfg, num_sites=args.sites)
     precision = args.precision or cfg.precision
     empty_heads = set(int(k) for k in args.empty_heads.split(",")) if args.empty_heads else set()
+    head_archs = ([(scenes.ARCH_128, scenes.ARCH_SMALL, scenes.ARCH_TINY)[k % 3]
+                   for k in range(cfg.num_sites)] if args.mixed else None)
     torch.cuda.set_device(0)
 
     def run(cfg, steps, warmup, copy_calibration=False):
@@ -160,7 +165,12 @@ def main():
         R = cfg.num_rays
         out = (torch.empty((R, 3), device="cuda"), torch.empty((R,), device="cuda"),
                torch.empty((R,), device="cuda"))
-        r = derf.Renderer(sc.sites, cfg.arch, sc.weights, precision)
+        if head_archs:
+            ws = [scenes.make_weights(a, 1, seed=300 + k, sigma_bias=cfg.sigma_bias)[0]
+                  for k, a in enumerate(head_archs)]
+            r = derf.Renderer(sc.sites, head_archs, ws, precision)
+        else:
+            r = derf.Renderer(sc.sites, cfg.arch, sc.weights, precision)
         if empty_heads:
             r.set_empty_heads([k in empty_heads for k in range(cfg.num_sites)])
         stream = torch.cuda.current_stream()
@@ -227,9 +237,14 @@ def main():
     R = cfg.num_rays
     S = R * (cfg.n_coarse + cfg.n_fine)   # head evaluations (both passes when hierarchical)
     mlp_ms = stage_ms["mlp"]
-    # head evaluations: every sample, less those owned by 0-capacity heads
+    # head evaluations: every sample, less those owned by 0-capacity heads,
+    # each at its owning head's multiply-adds
     evaluated = S - int(sum(heads[k] for k in empty_heads if k < cfg.num_sites))
-    mlp_flop = 2.0 * cfg.arch.macs_per_sample() * evaluated
+    if head_archs:
+        mlp_flop = 2.0 * sum(float(heads[k]) * head_archs[k].macs_per_sample()
+                             for k in range(cfg.num_sites) if k not in empty_heads)
+    else:
+        mlp_flop = 2.0 * cfg.arch.macs_per_sample() * evaluated
     achieved = mlp_flop / (mlp_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[precision]
     # t + cell + sigma/rgb per sample (coarse and fine lists when hierarchical), outputs per ray
@@ -287,7 +302,8 @@ def main():
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak,
                      "traffic": measured_traffic() if (cfg.name == "derf_k16" and cfg.num_sites == 16
-                                                       and precision == "bf16" and not empty_heads)
+                                                       and precision == "bf16" and not empty_heads
+                                                       and not head_archs)
                      else None,
                      "flop_per_step": mlp_flop, "mlp_ms_per_step": mlp_ms,
                      "launches_per_step": 2 if cfg.n_fine else 1},

@@ -13,6 +13,7 @@
  *
  * Calls:
  *   derf_create   upload sites and per-head weights            (Sec. 3.2-3.3)
+ *   derf_create_mixed  the same with one architecture per head  (Sec. 5)
  *   derf_render   render rays: sample, encode, assign, bucket,
  *                 per-head MLP, segment integration, merge      (Sec. 3.1, 3.3)
  *   derf_render_debug  the same, also returning per-sample data
@@ -120,6 +121,18 @@ long long derf_weights_count(const derf_head_arch *arch);
  * may be freed on return.  The call synchronises the device. */
 int derf_create(derf_handle **out, int num_sites, const float *sites_xyz,
                 const derf_head_arch *arch, const float *weights, int precision);
+
+/* As derf_create, with heads of different capacities (the heterogeneous
+ * heads of Sec. 5, limitations and future work):
+ *   archs    host [K]: head k's architecture; each must be one derf_create
+ *            accepts, and at most 4 distinct ones per renderer
+ *   weights  host float: head k's derf_weights_count(&archs[k]) packed
+ *            weights, heads one after another in index order
+ * A render runs one grouped-MLP launch per distinct architecture, over its
+ * heads.  DERF_ERR_UNSUPPORTED for an architecture without a kernel or more
+ * than 4 distinct ones; other errors as derf_create. */
+int derf_create_mixed(derf_handle **out, int num_sites, const float *sites_xyz,
+                      const derf_head_arch *archs, const float *weights, int precision);
 
 /* Render num_rays rays.  All array arguments are device pointers:
  *   rays_o, rays_d   float [R][3] origins and directions (directions need

@@ -83,12 +83,17 @@ struct derf_handle {
     int num_sites = 0;
     int site_bits = 0;
     bool bf16 = false;
-    derf_head_arch arch{};
-    const MlpVariant *mlp = nullptr;
     int mlp_grid = 0;
     float4 *sites = nullptr;
-    unsigned char *streams = nullptr;
-    float *blocks = nullptr;
+    // heads grouped by architecture: one MLP variant and one launch per group;
+    // a group's weights are laid out for every head index, its own filled
+    struct HeadGroup {
+        const MlpVariant *mlp = nullptr;
+        unsigned char *streams = nullptr;
+        float *blocks = nullptr;
+        HeadMask members{};
+    } groups[kMaxHeadGroups];
+    int num_groups = 0;
     Workspace ws;
     hipStream_t last_stream = nullptr;
     bool timing = false;
@@ -157,7 +162,7 @@ size_t layout(char *base, unsigned S, unsigned Sf, unsigned R, unsigned nblk, in
     x.counts = carve<unsigned>(p, (size_t)nblk * K);
     x.totals = carve<unsigned>(p, K);
     x.totals_fine = carve<unsigned>(p, K);
-    x.mlp_queue = carve<unsigned>(p, kMlpQueues);
+    x.mlp_queue = carve<unsigned>(p, kMlpQueues * kMaxHeadGroups);
     const bool walk = K >= kWalkSites;
     x.walk_seg = walk ? carve<SegRec>(p, (size_t)R * kMaxSeg) : nullptr;
     x.walk_nseg = walk ? carve<unsigned char>(p, R) : nullptr;
@@ -189,6 +194,27 @@ const MlpVariant *derf::find_mlp_variant(const HeadArch &a, bool bf16)
 }
 
 namespace {
+
+// The grouped MLP over every head: one launch per architecture group, each
+// skipping the other groups' heads and the 0-capacity ones, with its own
+// tile counters.
+hipError_t launch_groups(const derf_handle *h, const unsigned *bucket, const unsigned *totals,
+                         const RenderGeometry &g, const float *t, const void *dirbuf, float4 *sr,
+                         unsigned *queue, bool soft, hipStream_t s)
+{
+    for (int gi = 0; gi < h->num_groups; ++gi) {
+        const derf_handle::HeadGroup &grp = h->groups[gi];
+        HeadMask skip;
+        for (int w = 0; w < kMaxSites / 32; ++w)
+            skip.w[w] = ~grp.members.w[w] | h->empty.w[w];
+        const hipError_t e =
+            grp.mlp->launch(bucket, totals, h->num_sites, g, t, dirbuf, grp.streams, grp.blocks, sr,
+                            queue + kMlpQueues * gi, h->mlp_grid, soft, skip, s);
+        if (e != hipSuccess)
+            return e;
+    }
+    return hipSuccess;
+}
 
 // Grows the handle's workspace to at least need bytes.
 int ensure_workspace(derf_handle *h, size_t need)
@@ -235,7 +261,7 @@ size_t layout_soft(char *base, unsigned S, unsigned R, unsigned nblk, int K, boo
     x.dirbuf = carve<char>(p, (size_t)R * kDirPad * (bf16 ? 2 : 4));
     x.counts = carve<unsigned>(p, (size_t)nblk * K);
     x.totals = carve<unsigned>(p, K);
-    x.mlp_queue = carve<unsigned>(p, kMlpQueues);
+    x.mlp_queue = carve<unsigned>(p, kMlpQueues * kMaxHeadGroups);
     x.sr = carve<float4>(p, (size_t)K * S);
     if (b)
         *b = x;
@@ -355,8 +381,7 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
                 "bucket_scatter launch");
         HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCATTER, 1), "hipEventRecord");
         HIP_TRY(mark(pass, DERF_STAGE_MLP, 0), "hipEventRecord");
-        HIP_TRY(h->mlp->launch(b.bucket, totals, h->num_sites, gp, t, b.dirbuf, h->streams,
-                               h->blocks, sr, b.mlp_queue, h->mlp_grid, false, h->empty, s),
+        HIP_TRY(launch_groups(h, b.bucket, totals, gp, t, b.dirbuf, sr, b.mlp_queue, false, s),
                 "mlp launch");
         HIP_TRY(mark(pass, DERF_STAGE_MLP, 1), "hipEventRecord");
         return DERF_OK;
@@ -497,8 +522,7 @@ int render_soft_impl(derf_handle *h, const float *rays_o, const float *rays_d,
             "soft_setup launch");
     HIP_TRY(mark(DERF_STAGE_SAMPLE, 1), "hipEventRecord");
     HIP_TRY(mark(DERF_STAGE_MLP, 0), "hipEventRecord");
-    HIP_TRY(h->mlp->launch(b.bucket, b.totals, h->num_sites, g, b.t, b.dirbuf, h->streams,
-                           h->blocks, b.sr, b.mlp_queue, h->mlp_grid, true, h->empty, s),
+    HIP_TRY(launch_groups(h, b.bucket, b.totals, g, b.t, b.dirbuf, b.sr, b.mlp_queue, true, s),
             "mlp launch");
     HIP_TRY(mark(DERF_STAGE_MLP, 1), "hipEventRecord");
     HIP_TRY(mark(DERF_STAGE_COMPOSITE, 0), "hipEventRecord");
@@ -515,19 +539,11 @@ int render_soft_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     return DERF_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-long long derf_weights_count(const derf_head_arch *arch)
-{
-    if (!arch || !arch_values_valid(arch))
-        return -1;
-    return weights_count(arch);
-}
-
-int derf_create(derf_handle **out, int num_sites, const float *sites_xyz,
-                const derf_head_arch *arch, const float *weights, int precision)
+// derf_create / derf_create_mixed: per_head says whether arch holds one
+// architecture per head (weights then concatenated head after head) or one
+// for all.
+int create_impl(derf_handle **out, int num_sites, const float *sites_xyz,
+                const derf_head_arch *arch, bool per_head, const float *weights, int precision)
 {
     if (!out)
         return fail(DERF_ERR_INVALID_ARG, "null output handle pointer");
@@ -538,19 +554,28 @@ int derf_create(derf_handle **out, int num_sites, const float *sites_xyz,
         return fail(DERF_ERR_INVALID_ARG, "num_sites must be in [1, 256]");
     if (precision != DERF_PREC_FP32 && precision != DERF_PREC_BF16)
         return fail(DERF_ERR_INVALID_ARG, "unknown precision %d", precision);
-    if (!arch_values_valid(arch))
-        return fail(DERF_ERR_INVALID_ARG, "head architecture values out of range");
     for (int i = 0; i < 3 * num_sites; ++i)
         if (!isfinite(sites_xyz[i]))
             return fail(DERF_ERR_INVALID_ARG, "non-finite site coordinate");
-    HeadArch ha{arch->pos_freqs, arch->dir_freqs, arch->depth, arch->width, arch->skip_layer,
-                arch->rgb_hidden};
     const bool bf16 = precision == DERF_PREC_BF16;
-    const MlpVariant *v = find_mlp_variant(ha, bf16);
-    if (!v)
-        return fail(DERF_ERR_UNSUPPORTED, "no %s kernel for arch (%d,%d,%d,%d,%d,%d)",
-                    bf16 ? "bf16" : "fp32", arch->pos_freqs, arch->dir_freqs, arch->depth,
-                    arch->width, arch->skip_layer, arch->rgb_hidden);
+    // each head's kernel variant; heads sharing one form a group
+    std::vector<const MlpVariant *> head_v(num_sites);
+    std::vector<long long> woff(num_sites + 1, 0);
+    for (int k = 0; k < num_sites; ++k) {
+        const derf_head_arch *a = per_head ? arch + k : arch;
+        if (!arch_values_valid(a))
+            return fail(DERF_ERR_INVALID_ARG, "head %d: architecture values out of range", k);
+        HeadArch ha{a->pos_freqs, a->dir_freqs, a->depth, a->width, a->skip_layer, a->rgb_hidden};
+        head_v[k] = find_mlp_variant(ha, bf16);
+        if (!head_v[k])
+            return fail(DERF_ERR_UNSUPPORTED, "head %d: no %s kernel for arch (%d,%d,%d,%d,%d,%d)",
+                        k, bf16 ? "bf16" : "fp32", a->pos_freqs, a->dir_freqs, a->depth, a->width,
+                        a->skip_layer, a->rgb_hidden);
+        woff[k + 1] = woff[k] + weights_count(a);
+    }
+    for (long long i = 0; i < woff[num_sites]; ++i)
+        if (!isfinite(weights[i]))
+            return fail(DERF_ERR_INVALID_ARG, "non-finite weight");
 
     derf_handle *h = new (std::nothrow) derf_handle();
     if (!h)
@@ -571,44 +596,60 @@ int derf_create(derf_handle **out, int num_sites, const float *sites_xyz,
     while ((1 << h->site_bits) < num_sites)
         ++h->site_bits;
     h->bf16 = bf16;
-    h->arch = *arch;
-    h->mlp = v;
     h->mlp_grid = cus;
+    std::vector<int> head_group(num_sites);
+    for (int k = 0; k < num_sites; ++k) {
+        int gi = 0;
+        while (gi < h->num_groups && h->groups[gi].mlp != head_v[k])
+            ++gi;
+        if (gi == h->num_groups) {
+            if (h->num_groups == kMaxHeadGroups)
+                return cleanup(fail(DERF_ERR_UNSUPPORTED, "more than %d head architectures",
+                                    kMaxHeadGroups));
+            h->groups[h->num_groups++].mlp = head_v[k];
+        }
+        head_group[k] = gi;
+        h->groups[gi].members.w[k >> 5] |= 1u << (k & 31);
+    }
 
     // sites as float4 (xyz, 0)
     std::vector<float4> sites(num_sites);
     for (int k = 0; k < num_sites; ++k)
         sites[k] = make_float4(sites_xyz[3 * k], sites_xyz[3 * k + 1], sites_xyz[3 * k + 2], 0.f);
-    // per-head kernel layout
-    const long long wc = weights_count(arch);
-    std::vector<unsigned char> streams;
-    std::vector<float> blocks;
-    try {
-        streams.resize(v->stream_bytes * num_sites);
-        blocks.resize(v->block_bytes / 4 * num_sites);
-    } catch (...) {
-        return cleanup(fail(DERF_ERR_OOM, "host staging"));
-    }
-    for (int k = 0; k < num_sites; ++k) {
-        const float *wk = weights + (size_t)k * wc;
-        for (long long i = 0; i < wc; ++i)
-            if (!isfinite(wk[i]))
-                return cleanup(fail(DERF_ERR_INVALID_ARG, "non-finite weight (head %d)", k));
-        v->pack(wk, streams.data() + v->stream_bytes * k, blocks.data() + v->block_bytes / 4 * k);
-    }
-    if (hipMalloc(&h->sites, sizeof(float4) * num_sites) != hipSuccess ||
-        hipMalloc(&h->streams, streams.size()) != hipSuccess ||
-        hipMalloc(&h->blocks, blocks.size() * 4) != hipSuccess) {
+    if (hipMalloc(&h->sites, sizeof(float4) * num_sites) != hipSuccess) {
         (void)hipGetLastError();
-        return cleanup(fail(DERF_ERR_OOM, "device weights"));
+        return cleanup(fail(DERF_ERR_OOM, "device sites"));
     }
     e = hipMemcpy(h->sites, sites.data(), sizeof(float4) * num_sites, hipMemcpyHostToDevice);
-    if (e == hipSuccess)
-        e = hipMemcpy(h->streams, streams.data(), streams.size(), hipMemcpyHostToDevice);
-    if (e == hipSuccess)
-        e = hipMemcpy(h->blocks, blocks.data(), blocks.size() * 4, hipMemcpyHostToDevice);
     if (e != hipSuccess)
         return cleanup(hip_fail(e, "hipMemcpy"));
+    // per group, the kernel layout of its heads (indexed by head; others zero)
+    for (int gi = 0; gi < h->num_groups; ++gi) {
+        derf_handle::HeadGroup &grp = h->groups[gi];
+        const MlpVariant *v = grp.mlp;
+        std::vector<unsigned char> streams;
+        std::vector<float> blocks;
+        try {
+            streams.assign(v->stream_bytes * num_sites, 0);
+            blocks.assign(v->block_bytes / 4 * num_sites, 0.0f);
+        } catch (...) {
+            return cleanup(fail(DERF_ERR_OOM, "host staging"));
+        }
+        for (int k = 0; k < num_sites; ++k)
+            if (head_group[k] == gi)
+                v->pack(weights + woff[k], streams.data() + v->stream_bytes * k,
+                        blocks.data() + v->block_bytes / 4 * k);
+        if (hipMalloc(&grp.streams, streams.size()) != hipSuccess ||
+            hipMalloc(&grp.blocks, blocks.size() * 4) != hipSuccess) {
+            (void)hipGetLastError();
+            return cleanup(fail(DERF_ERR_OOM, "device weights"));
+        }
+        e = hipMemcpy(grp.streams, streams.data(), streams.size(), hipMemcpyHostToDevice);
+        if (e == hipSuccess)
+            e = hipMemcpy(grp.blocks, blocks.data(), blocks.size() * 4, hipMemcpyHostToDevice);
+        if (e != hipSuccess)
+            return cleanup(hip_fail(e, "hipMemcpy"));
+    }
     for (int i = 0; i < kEvents; ++i) {
         e = hipEventCreate(&h->ev[i]);
         if (e != hipSuccess)
@@ -619,6 +660,29 @@ int derf_create(derf_handle **out, int num_sites, const float *sites_xyz,
         return cleanup(hip_fail(e, "hipDeviceSynchronize"));
     *out = h;
     return DERF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+long long derf_weights_count(const derf_head_arch *arch)
+{
+    if (!arch || !arch_values_valid(arch))
+        return -1;
+    return weights_count(arch);
+}
+
+int derf_create(derf_handle **out, int num_sites, const float *sites_xyz,
+                const derf_head_arch *arch, const float *weights, int precision)
+{
+    return create_impl(out, num_sites, sites_xyz, arch, false, weights, precision);
+}
+
+int derf_create_mixed(derf_handle **out, int num_sites, const float *sites_xyz,
+                      const derf_head_arch *archs, const float *weights, int precision)
+{
+    return create_impl(out, num_sites, sites_xyz, archs, true, weights, precision);
 }
 
 int derf_render(derf_handle *h, const float *rays_o, const float *rays_d, long long num_rays,
@@ -720,10 +784,12 @@ void derf_destroy(derf_handle *h)
         (void)hipFree(h->ws.mem);
     if (h->sites)
         (void)hipFree(h->sites);
-    if (h->streams)
-        (void)hipFree(h->streams);
-    if (h->blocks)
-        (void)hipFree(h->blocks);
+    for (int gi = 0; gi < h->num_groups; ++gi) {
+        if (h->groups[gi].streams)
+            (void)hipFree(h->groups[gi].streams);
+        if (h->groups[gi].blocks)
+            (void)hipFree(h->groups[gi].blocks);
+    }
     for (int i = 0; i < kEvents; ++i)
         if (h->ev[i])
             (void)hipEventDestroy(h->ev[i]);

@@ -13,8 +13,10 @@ constexpr int kBucketBlock = 4096;
 // Padded length of the per-ray direction feature vector gamma(d / |d|).
 constexpr int kDirPad = 32;
 constexpr int kMaxSites = 256;
-// Tile counters of the MLP's work queues (one per XCD).
+// Tile counters of the MLP's work queues (one per XCD), for each of at most
+// kMaxHeadGroups MLP launches of a render (one per head architecture).
 constexpr int kMlpQueues = 8;
+constexpr int kMaxHeadGroups = 4;
 
 // Heads marked 0-capacity (empty space: no density anywhere), one bit each.
 struct HeadMask {

@@ -524,7 +524,7 @@ __global__ __launch_bounds__(1024) void bucket_scan_kernel(unsigned *__restrict_
                                                            unsigned *__restrict__ totals,
                                                            unsigned *__restrict__ mlp_queue)
 {
-    if (blockIdx.x == 0 && threadIdx.x < (unsigned)kMlpQueues)
+    if (blockIdx.x == 0 && threadIdx.x < (unsigned)(kMlpQueues * kMaxHeadGroups))
         mlp_queue[threadIdx.x] = 0;
     __shared__ unsigned s_wave[16];
     __shared__ unsigned s_carry;

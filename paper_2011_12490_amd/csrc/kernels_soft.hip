@@ -29,7 +29,7 @@ __global__ __launch_bounds__(kThreads) void soft_setup_kernel(unsigned S, int nu
     const unsigned i0 = blockIdx.x * kThreads + threadIdx.x;
     if (i0 < (unsigned)num_sites)
         totals[i0] = S;
-    if (i0 < (unsigned)kMlpQueues)
+    if (i0 < (unsigned)(kMlpQueues * kMaxHeadGroups))
         queue[i0] = 0;
     for (unsigned i = i0; i < S; i += gridDim.x * kThreads)
         bucket[i] = i;

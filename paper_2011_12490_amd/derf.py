@@ -51,7 +51,8 @@ class derf_stats(ctypes.Structure):
                 ("head_samples", ctypes.c_longlong * 256)]
 
 
-EXPORTS = ("derf_weights_count", "derf_create", "derf_render", "derf_render_debug",
+EXPORTS = ("derf_weights_count", "derf_create", "derf_create_mixed", "derf_render",
+           "derf_render_debug",
            "derf_render_soft", "derf_set_empty_heads", "derf_set_timing", "derf_get_stats", "derf_reset_stats", "derf_destroy",
            "derf_status_string", "derf_last_error")
 
@@ -78,6 +79,8 @@ def lib() -> ctypes.CDLL:
         L.derf_create.argtypes = [ctypes.POINTER(P), ctypes.c_int, P,
                                   ctypes.POINTER(derf_head_arch), P, ctypes.c_int]
         L.derf_create.restype = ctypes.c_int
+        L.derf_create_mixed.argtypes = L.derf_create.argtypes
+        L.derf_create_mixed.restype = ctypes.c_int
         render_args = [P, P, P, ctypes.c_longlong, ctypes.c_float, ctypes.c_float,
                        ctypes.POINTER(derf_sampling), P, P, P]
         L.derf_render.argtypes = render_args + [P]
@@ -126,13 +129,32 @@ def derf_weights_count(arch) -> int:
     return lib().derf_weights_count(ctypes.byref(a))
 
 
+def _is_arch_list(arch) -> bool:
+    return isinstance(arch, (list, tuple)) and len(arch) > 0 and not isinstance(arch[0], int)
+
+
 def derf_create(sites, arch, weights, precision: int) -> ctypes.c_void_p:
-    """sites: host float32 [K, 3]; weights: host float32 [K, derf_weights_count]."""
+    """sites: host float32 [K, 3]; weights: host float32 [K, derf_weights_count].
+    With arch a list of K architectures (heads of different capacities),
+    weights is a list of K per-head arrays or their concatenation."""
     import numpy as np
     s = np.ascontiguousarray(sites, np.float32).reshape(-1, 3)
+    h = ctypes.c_void_p()
+    if _is_arch_list(arch):
+        if isinstance(weights, (list, tuple)):
+            weights = np.concatenate([np.ravel(np.asarray(x, np.float32)) for x in weights])
+        w = np.ascontiguousarray(weights, np.float32)
+        if w.size != sum(derf_weights_count(a) for a in arch):
+            raise ValueError("weights do not match the per-head architectures")
+        arr = (derf_head_arch * len(arch))(*[_arch(a) for a in arch])
+        _check(lib().derf_create_mixed(ctypes.byref(h), s.shape[0],
+                                       s.ctypes.data_as(ctypes.c_void_p),
+                                       ctypes.cast(arr, ctypes.POINTER(derf_head_arch)),
+                                       w.ctypes.data_as(ctypes.c_void_p), precision),
+               "derf_create_mixed")
+        return h
     w = np.ascontiguousarray(weights, np.float32)
     a = _arch(arch)
-    h = ctypes.c_void_p()
     _check(lib().derf_create(ctypes.byref(h), s.shape[0], s.ctypes.data_as(ctypes.c_void_p),
                              ctypes.byref(a), w.ctypes.data_as(ctypes.c_void_p), precision),
            "derf_create")

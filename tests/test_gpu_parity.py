@@ -460,3 +460,75 @@ def test_maximum_sample_count():
                             cfg.near, cfg.far, cfg.n_coarse, 0, seed=scenes.SEED_RENDER,
                             ray_ids=ids, nthreads=NTHREADS)
         _check_pixels(gpu, ref, ids, TOL["bf16"], "max frame K=%d" % K)
+
+
+# -------------------------------------------- heads of different capacities ----
+
+def _mixed_model(K):
+    """Heads cycling through three architectures (8x128 with skip, 6x64, and
+    4x64 with a 6-frequency encoding), with their own seeded weights."""
+    archs = [(scenes.ARCH_128, scenes.ARCH_SMALL, scenes.ARCH_TINY)[k % 3] for k in range(K)]
+    ws = [scenes.make_weights(a, 1, seed=300 + k, sigma_bias=1.0)[0] for k, a in enumerate(archs)]
+    return archs, ws
+
+
+def test_mixed_capacity_heads():
+    """derf_create_mixed: the 504x378 frame with 16 heads of three
+    architectures (three grouped-MLP launches) against the oracle's per-head
+    architectures on a ray subset, bf16."""
+    derf = _derf()
+    cfg = scenes.CONFIGS["derf_k16"]
+    sc = scenes.make_scene(cfg)
+    archs, ws = _mixed_model(cfg.num_sites)
+    o = torch.from_numpy(sc.rays_o).cuda()
+    d = torch.from_numpy(sc.rays_d).cuda()
+    r = derf.Renderer(sc.sites, archs, ws, "bf16")
+    gpu = [x.cpu().numpy() for x in r.render(o, d, cfg.near, cfg.far, cfg.n_coarse, 0,
+                                              scenes.SEED_RENDER)]
+    r.close()
+    ids = scenes.ray_subset(256, cfg.num_rays)
+    ref = oracle.render(sc.sites, archs, ws, sc.rays_o[ids], sc.rays_d[ids], cfg.near, cfg.far,
+                        cfg.n_coarse, 0, seed=scenes.SEED_RENDER, ray_ids=ids, nthreads=NTHREADS)
+    _check_pixels(gpu, ref, ids, TOL["bf16"], "derf frame, mixed heads")
+    assert np.all(ref.opacity > 0.05)
+
+
+def test_mixed_capacity_heads_fp32_paths():
+    """fp32, tiny frame: single pass, hierarchical, soft with contributions and
+    with 0-capacity heads, all against the oracle; and a mixed model whose
+    heads all share one architecture equals derf_create bitwise."""
+    derf = _derf()
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], num_sites=6)
+    sc = scenes.make_scene(cfg)
+    archs, ws = _mixed_model(cfg.num_sites)
+    o = torch.from_numpy(sc.rays_o).cuda()
+    d = torch.from_numpy(sc.rays_d).cuda()
+    ids = np.arange(0, cfg.num_rays, 4)
+    args = (sc.sites, archs, ws, sc.rays_o[ids], sc.rays_d[ids], cfg.near, cfg.far)
+    r = derf.Renderer(sc.sites, archs, ws, "fp32")
+    for n, nf in ((32, 0), (16, 16)):
+        gpu = [x.cpu().numpy() for x in r.render(o, d, cfg.near, cfg.far, n, nf,
+                                                  scenes.SEED_RENDER)]
+        ref = oracle.render(*args, n, nf, seed=scenes.SEED_RENDER, ray_ids=ids,
+                            nthreads=NTHREADS)
+        tol = TOL["fp32"] if nf == 0 else TOL["bf16"]  # inverse-CDF conditioning
+        _check_pixels(gpu, ref, ids, tol, "tiny mixed n=%d+%d" % (n, nf))
+    empty = [0, 0, 1, 0, 0, 1]
+    r.set_empty_heads(empty)
+    soft = [x.cpu().numpy() for x in r.render_soft(o, d, cfg.near, cfg.far, 32, 3.0,
+                                                    seed=scenes.SEED_RENDER, contrib=True)]
+    r.close()
+    ref = oracle.render(*args, 32, 0, seed=scenes.SEED_RENDER, ray_ids=ids, mode="soft",
+                        beta=3.0, contrib=True, empty=np.array(empty), nthreads=NTHREADS)
+    e = max(np.abs(soft[0][ids] - ref.rgb).max(), np.abs(soft[2][ids] - ref.opacity).max(),
+            np.abs(soft[3][ids] - ref.contrib).max())
+    print("tiny mixed soft, 2 empty heads: max err %.3g" % e, flush=True)
+    assert e <= TOL["fp32"]
+    same = [cfg.arch] * cfg.num_sites
+    a = _render_with(sc, "fp32")
+    r = derf.Renderer(sc.sites, same, list(sc.weights), "fp32")
+    b = [x.cpu().numpy() for x in r.render(o, d, cfg.near, cfg.far, cfg.n_coarse, 0,
+                                            scenes.SEED_RENDER)]
+    r.close()
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x, y)

@@ -71,7 +71,8 @@ def lib() -> ctypes.CDLL:
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
-            raise RuntimeError("libderf.so is not built (%s); run __graft_entry__.build()" % LIB_PATH)
+            raise RuntimeError("libderf.so is not built (%s); build it with "
+                               "python paper_2011_12490_amd/build.py" % LIB_PATH)
         L = ctypes.CDLL(LIB_PATH)
         P = ctypes.c_void_p
         L.derf_weights_count.argtypes = [ctypes.POINTER(derf_head_arch)]

@@ -77,6 +77,10 @@ __host__ __device__ constexpr int c_row(int g, int i) { return 8 * (i / 4) + 4 *
 // stages of at most UMAX units.
 enum { K_HID = 0, K_RGBH = 1, K_OUT = 2 };
 
+// A-fragment reads kept in flight ahead of the MFMA that uses them: during
+// step F (the F-th fragment of a tile) the wave reads fragment F + kPrefetch.
+constexpr int kPrefetch = 3;
+
 template <bool BF16_, int W_, int D_, int SKIP_, int RH_, int LP_>
 struct Cfg {
     static constexpr bool BF16 = BF16_;
@@ -209,15 +213,42 @@ struct Cfg {
     // group start a the wave issues the weight loads of stages a + LA ..
     // (the next tile's stages past the end), then the gamma(d) loads if a ==
     // S_GD.  Before the barrier of group a, the units of stage need(a) -- the
-    // first stage after the group, whose fragments are read at its end -- must
-    // have landed; vm_allowed(a) counts this wave's memory operations issued
+    // last stage the group's fragment reads reach: kPrefetch fragments past
+    // its last step, which is beyond the next stage when that one is shorter
+    // (the 2-unit stages of the 8x256 colour layer) -- must have landed;
+    // vm_allowed(a) counts this wave's memory operations issued
     // after those loads (every operation before them has landed too: they
     // complete in issue order).  -1: nothing to wait for (the tile prologue
     // drained everything issued before stage LA's loads).
     static_assert(NS >= LA + G, "pipeline deeper than the stage list");
     static_assert(NBUF >= LA + G, "ring too small for the lookahead");
     static constexpr int grp_end(int a) { return a + G - 1 < NS ? a + G - 1 : NS - 1; }
-    static constexpr int need(int a) { return grp_end(a) + 1 < NS ? grp_end(a) + 1 : grp_end(a); }
+    static constexpr int need(int a)
+    {
+        const int next = grp_end(a) + 1 < NS ? grp_end(a) + 1 : grp_end(a);
+        const int fe = TAB.foff[grp_end(a) + 1] - 1 + kPrefetch;  // furthest fragment read
+        const int reach = f_stage(fe < FTOTAL ? fe : FTOTAL - 1);
+        return reach > next ? reach : next;
+    }
+    // every fragment a group reads lies in a stage its wait covers
+    static constexpr bool waits_cover_reads()
+    {
+        for (int a = 0; a < NS; a += G) {
+            const int fe = TAB.foff[grp_end(a) + 1] - 1 + kPrefetch;
+            if ((fe < FTOTAL ? fe : FTOTAL - 1) >= TAB.foff[need(a) + 1])
+                return false;
+        }
+        return true;
+    }
+    // the loads of need(a) were issued before group a (or drained by the tile
+    // prologue), so the wait before its barrier can cover them
+    static constexpr bool needs_issued_earlier()
+    {
+        for (int a = 0; a < NS; a += G)
+            if (need(a) >= LA && (need(a) - LA) / G * G >= a)
+                return false;
+        return true;
+    }
     static constexpr int vm_allowed(int a, bool has_next)
     {
         const int xn = need(a);
@@ -253,6 +284,8 @@ struct Cfg {
                 cnt += x < NS ? st_lpw(x) : st_lpw(x - NS);
         return cnt + (S_GD > S_PB ? NGD : 0);
     }
+    static_assert(waits_cover_reads(), "a fragment read runs ahead of the group wait");
+    static_assert(needs_issued_earlier(), "a group waits for weight loads issued after it");
     static_assert(S_PA % G == 0 && S_PB % G == 0 && S_PB < NS, "prefetch at group starts");
     // the group wait at S_PB covers the S_PA loads: the loads it waits for
     // were issued at a later group start
@@ -556,8 +589,6 @@ __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "mem
 template <class C>
 using Chunk = std::conditional_t<C::BF16, bf16x8, float>;
 
-// A-fragment reads kept in flight ahead of the MFMA that uses them.
-constexpr int kPrefetch = 3;
 // "no tile left" from the work queues
 constexpr unsigned kNoTile = 0xFFFFFFFFu;
 

@@ -566,3 +566,39 @@ def test_streams_and_concurrent_handles():
         np.testing.assert_array_equal(x.cpu().numpy(), y)
     r1.close()
     r2.close()
+
+
+# ------------------------------------------------------ randomised frames ----
+
+@pytest.mark.parametrize("case", range(12))
+def test_random_frames(case):
+    """Seeded random combinations: head count (1-256), sample count (1-300),
+    ray count, site layout, head architecture, precision, density bias,
+    jitter on or off and the ray offset of the generator.  Cells are
+    bit-exact (bar samples within 1e-5 of a bisector), pixels within the
+    precision's tolerance."""
+    rng = np.random.default_rng(9000 + case)
+    K = int(rng.choice([1, 2, 3, 7, 16, 27, 28, 40, 64, 100, 200, 256]))
+    n = int(rng.integers(1, 301))
+    arch = [scenes.ARCH_TINY, scenes.ARCH_SMALL, scenes.ARCH_128][case % 3]
+    precision = "bf16" if case % 2 else "fp32"
+    layout = str(rng.choice(["uniform", "gmm_kmeans", "ball_mix"]))
+    w, h = int(rng.integers(1, 40)), int(rng.integers(1, 30))
+    if arch is scenes.ARCH_128:
+        n = max(1, min(n, 60000 // (w * h)))  # keeps the oracle's float64 heads to seconds
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], width=w, height=h, num_sites=K,
+                              sites=layout, arch=arch, n_coarse=n,
+                              sigma_bias=float(rng.choice([0.0, 1.0, 3.0])))
+    sc = scenes.make_scene(cfg)
+    perturb = bool(rng.integers(0, 2))
+    offset = int(rng.integers(0, 1 << 40))
+    label = "random %d: K=%d n=%d %dx%d %s %s %s perturb=%d" % (
+        case, K, n, w, h, layout, arch.width, precision, perturb)
+    print(label, flush=True)
+    gpu = _render(sc, precision, debug=True, perturb=perturb, ray_offset=offset)
+    _check_cells(sc, gpu[3]["t"], gpu[3]["cell"], n, label, ray_offset=offset, perturb=perturb)
+    ids = np.arange(cfg.num_rays)
+    ref = oracle.render(sc.sites, cfg.arch, sc.weights, sc.rays_o, sc.rays_d, cfg.near, cfg.far,
+                        n, 0, seed=scenes.SEED_RENDER, perturb=perturb, ray_ids=ids + offset,
+                        nthreads=NTHREADS)
+    _check_pixels(gpu, ref, ids, TOL[precision], label)

@@ -95,6 +95,35 @@ def test_render_rejects_bad_arguments_without_a_gpu():
     L.derf_destroy(None)
 
 
+def test_mixed_create_soft_render_and_empty_heads_reject_bad_arguments_without_a_gpu():
+    L = derf.lib()
+    assert L.derf_create_mixed(None, 1, None, None, None, 1) == derf.DERF_ERR_INVALID_ARG
+    archs = [scenes.ARCH_128, scenes.ARCH_SMALL, (10, 4, 8, 96, 5, 64)]
+    arr = (derf.derf_head_arch * 3)(*[derf.derf_head_arch(*(a.as_tuple() if hasattr(a, "as_tuple")
+                                                             else a)) for a in archs])
+    sites = np.zeros((3, 3), np.float32)
+    w = np.zeros(sum(max(0, derf.derf_weights_count(a)) for a in archs), np.float32)
+    h = ctypes.c_void_p(1234)
+    rc = L.derf_create_mixed(ctypes.byref(h), 3, sites.ctypes.data_as(ctypes.c_void_p),
+                             ctypes.cast(arr, ctypes.POINTER(derf.derf_head_arch)),
+                             w.ctypes.data_as(ctypes.c_void_p), 1)
+    assert rc == derf.DERF_ERR_UNSUPPORTED and h.value is None
+    assert b"head 2" in L.derf_last_error()
+    good = (derf.derf_head_arch * 2)(derf.derf_head_arch(*scenes.ARCH_128.as_tuple()),
+                                     derf.derf_head_arch(*scenes.ARCH_SMALL.as_tuple()))
+    w2 = np.zeros(derf.derf_weights_count(scenes.ARCH_128) +
+                  derf.derf_weights_count(scenes.ARCH_SMALL), np.float32)
+    w2[-1] = np.inf
+    rc = L.derf_create_mixed(ctypes.byref(h), 2, sites.ctypes.data_as(ctypes.c_void_p),
+                             ctypes.cast(good, ctypes.POINTER(derf.derf_head_arch)),
+                             w2.ctypes.data_as(ctypes.c_void_p), 1)
+    assert rc == derf.DERF_ERR_INVALID_ARG and b"non-finite weight" in L.derf_last_error()
+    assert L.derf_set_empty_heads(None, None) == derf.DERF_ERR_INVALID_ARG
+    samp = derf.derf_sampling(32, 0, 1, 1, 0)
+    assert L.derf_render_soft(None, None, None, 1, 2.0, 6.0, ctypes.byref(samp), 1.0, None, None,
+                              None, None, None) == derf.DERF_ERR_INVALID_ARG
+
+
 def test_status_strings():
     L = derf.lib()
     assert L.derf_status_string(0) == b"ok"

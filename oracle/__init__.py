@@ -63,6 +63,9 @@ def _lib_handle():
         lib.oracle_render_ex.restype = ctypes.c_int
         lib.oracle_render_mixed.argtypes = lib.oracle_render_ex.argtypes
         lib.oracle_render_mixed.restype = ctypes.c_int
+        lib.oracle_render_culled.argtypes = render_sig + [ctypes.c_double, ctypes.c_int,
+                                                          ctypes.c_void_p, ctypes.c_void_p]
+        lib.oracle_render_culled.restype = ctypes.c_int
         lib.oracle_philox4x32_10.argtypes = [_P, _P, _P]
         lib.oracle_philox4x32_10.restype = None
         lib.oracle_jitter.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint32,
@@ -351,3 +354,37 @@ def render(sites, arch, weights, rays_o, rays_d, near: float, far: float, n_coar
     if rc != 0:
         raise RuntimeError("oracle render failed (%d)" % rc)
     return RenderResult(rgb, dep, op, t, cell, sig, srgb, margin, W)
+
+
+def render_culled(sites, arch, weights, rays_o, rays_d, near: float, far: float,
+                  n_coarse: int, eps: float, levels: int, seed: int = 0, perturb: bool = True,
+                  ray_ids=None, empty=None, nthreads: int = 0) -> RenderResult:
+    """Single-pass DeRF render with Painter's-order culling (Sec. 3.3): level l
+    of a ray is its l-th segment (the last level every later one), and a ray
+    stops before level l > 0 once its transmittance is below eps.  The
+    result's ``evaluated`` holds the samples whose head ran, per ray."""
+    sites = np.ascontiguousarray(sites, np.float32).reshape(-1, 3)
+    weights = np.ascontiguousarray(weights, np.float32)
+    o = np.ascontiguousarray(rays_o, np.float32).reshape(-1, 3)
+    d = np.ascontiguousarray(rays_d, np.float32).reshape(-1, 3)
+    R = o.shape[0]
+    ids = None if ray_ids is None else np.ascontiguousarray(ray_ids, np.int64)
+    e = None
+    if empty is not None:
+        e = np.ascontiguousarray(np.asarray(empty) != 0, np.uint8)
+        if e.shape != (sites.shape[0],):
+            raise ValueError("empty needs one flag per head")
+    rgb = np.zeros((R, 3), np.float64)
+    dep = np.zeros(R, np.float64)
+    op = np.zeros(R, np.float64)
+    ev = np.zeros(R, np.int32)
+    a = _arch(arch)
+    rc = _lib_handle().oracle_render_culled(
+        sites.shape[0], _ptr(sites), ctypes.byref(a), _ptr(weights), R, _ptr(o), _ptr(d),
+        _ptr(ids), near, far, n_coarse, 0, seed, int(perturb), _ptr(rgb), _ptr(dep), _ptr(op),
+        None, None, None, None, None, nthreads, float(eps), int(levels), _ptr(e), _ptr(ev))
+    if rc != 0:
+        raise RuntimeError("oracle culled render failed (%d)" % rc)
+    res = RenderResult(rgb, dep, op)
+    res.evaluated = ev
+    return res

@@ -820,6 +820,105 @@ int oracle_render_soft_contrib(ORACLE_RENDER_ARGS, double beta, double *contrib)
                        out_opacity, dbg_t, dbg_cell, dbg_sigma, dbg_rgb, dbg_margin, nthreads);
 }
 
+/* ------------------------------------------- Painter's-order culling ---
+ * The Painter's order of Sec. 3.3 visits the segments of a ray front to
+ * back, so the transmittance in front of a segment is known before its head
+ * has to run.  Level l of a ray holds its segment of ordinal l along the ray
+ * (the last level also every later segment).  Before level l > 0 a ray
+ * whose transmittance T is below eps stops: its remaining segments are not
+ * evaluated.  The result is the Painter's merge of the evaluated segments
+ * (a prefix of the ray).  Its colour and opacity differ from the full
+ * render's by at most the T at the stop (< eps: colours lie in [0, 1]) and
+ * its depth by at most T * far.  With levels = 1 or eps = 0 nothing is
+ * skipped and the result is the full render's, operation for operation.
+ * Single pass (n_fine = 0), one architecture for every head; empty
+ * (optional [K]) marks 0-capacity heads.  evaluated (optional [R]):
+ * samples whose head ran, per ray. */
+int oracle_render_culled(ORACLE_RENDER_ARGS, double eps, int levels, const unsigned char *empty,
+                         int *evaluated)
+{
+    ORACLE_FILL_ARGS
+    A.empty = empty;
+    (void)dbg_t; (void)dbg_cell; (void)dbg_sigma; (void)dbg_rgb; (void)dbg_margin;
+    const int n = n_coarse;
+    if (n < 1 || n_fine != 0 || levels < 1 || !(eps >= 0.0) || R < 0)
+        return -1;
+    const int P = 3 + 6 * arch->pos_freqs, Dd = 3 + 6 * arch->dir_freqs;
+    const size_t scratch_len = 4 * (size_t)(P + arch->width + Dd + arch->rgb_hidden + 8);
+#ifdef _OPENMP
+    if (nthreads > 0)
+        omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+    int failed = 0;
+#pragma omp parallel
+    {
+        float *t = malloc(sizeof(float) * (size_t)n);
+        int *cell = malloc(sizeof(int) * (size_t)n);
+        double *sigma = malloc(sizeof(double) * (size_t)n);
+        double *rgb = malloc(sizeof(double) * 3 * (size_t)n);
+        double *delta = malloc(sizeof(double) * (size_t)n);
+        double *gx = malloc(sizeof(double) * (size_t)P);
+        double *gd = malloc(sizeof(double) * (size_t)Dd);
+        double *scratch = malloc(sizeof(double) * scratch_len);
+        if (!t || !cell || !sigma || !rgb || !delta || !gx || !gd || !scratch) {
+#pragma omp atomic write
+            failed = 1;
+        } else {
+#pragma omp for schedule(dynamic, 16)
+            for (long long r = 0; r < R; ++r) {
+                const float *o = rays_o + 3 * r, *d = rays_d + 3 * r;
+                const uint64_t rid = ray_ids ? (uint64_t)ray_ids[r] : (uint64_t)r;
+                double dn = sqrt((double)d[0] * d[0] + (double)d[1] * d[1] + (double)d[2] * d[2]);
+                double dh[3] = { d[0] / dn, d[1] / dn, d[2] / dn };
+                oracle_posenc(arch->dir_freqs, dh, gd);
+                oracle_sample_depths(seed, rid, near_t, far_t, n, perturb, t);
+                intervals(t, n, near_t, far_t, delta);
+                for (int i = 0; i < n; ++i) {
+                    float x[3];
+                    sample_point(o, d, t[i], x);
+                    cell[i] = oracle_nearest_site(K, sites, x);
+                }
+                double c3[3] = {0.0, 0.0, 0.0}, dep = 0.0, op = 0.0;
+                int end = 0;
+                for (int level = 0; end < n; ++level) {
+                    /* transmittance in front of this level */
+                    if (level > 0 && 1.0 - op < eps)
+                        break;
+                    /* this level's samples: one segment, or all that remain */
+                    int stop = end;
+                    do {
+                        const int c = cell[stop];
+                        while (stop < n && cell[stop] == c)
+                            ++stop;
+                    } while (level == levels - 1 && stop < n);
+                    for (int i = end; i < stop; ++i) {
+                        float x[3];
+                        sample_point(o, d, t[i], x);
+                        double xd[3] = { x[0], x[1], x[2] };
+                        oracle_posenc(arch->pos_freqs, xd, gx);
+                        eval_head(&A, cell[i], xd, dh, gx, gd, &sigma[i], &rgb[3 * i], scratch);
+                    }
+                    end = stop;
+                    /* Painter's merge of the evaluated prefix */
+                    composite_segments(end, cell, t, sigma, rgb, delta, c3, &dep, &op, NULL);
+                }
+                out_rgb[3 * r + 0] = c3[0];
+                out_rgb[3 * r + 1] = c3[1];
+                out_rgb[3 * r + 2] = c3[2];
+                out_depth[r] = dep;
+                out_opacity[r] = op;
+                if (evaluated)
+                    evaluated[r] = end;
+            }
+        }
+        free(t); free(cell); free(sigma); free(rgb); free(delta); free(gx); free(gd);
+        free(scratch);
+    }
+    return failed ? -3 : 0;
+}
+
 /* Sample depths and owning cells of every sample of rays [0, R) (no network):
  * the full-frame check of the assignment.  Ray r uses RNG ray index
  * ray_offset + r.  margin (optional) receives each sample's distance to its

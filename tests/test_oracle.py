@@ -692,3 +692,87 @@ def test_oracle_regression_fixture():
     np.testing.assert_allclose(r.opacity, g["opacity"], rtol=0, atol=1e-13)
     assert r.cell.tolist() == g["cells"]
     assert np.array_equal(r.t, np.array(g["t"], np.float32))
+
+
+# ---------------------------------------------------- Painter's-order culling
+
+def _dense_scene():
+    """8 heads with a density bias of 4: most rays turn opaque part-way."""
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], num_sites=8, sigma_bias=4.0)
+    return cfg, scenes.make_scene(cfg)
+
+
+def _culled(cfg, sc, ids, eps, levels, weights=None, **kw):
+    return oracle.render_culled(sc.sites, cfg.arch, sc.weights if weights is None else weights,
+                                sc.rays_o[ids], sc.rays_d[ids], cfg.near, cfg.far, cfg.n_coarse,
+                                eps, levels, seed=3, ray_ids=ids, **kw)
+
+
+def test_culled_render_without_culling_is_the_full_render():
+    """eps = 0 (no ray ever stops) or a single level (no check after the
+    first segment): the full render, bitwise, with every sample evaluated."""
+    cfg, sc = _dense_scene()
+    ids = np.arange(0, cfg.num_rays, 5)
+    full = oracle.render(sc.sites, cfg.arch, sc.weights, sc.rays_o[ids], sc.rays_d[ids], cfg.near,
+                         cfg.far, cfg.n_coarse, seed=3, ray_ids=ids)
+    for eps, levels in ((0.0, 5), (0.0, 32), (0.5, 1)):
+        c = _culled(cfg, sc, ids, eps, levels)
+        for x, y in ((c.rgb, full.rgb), (c.depth, full.depth), (c.opacity, full.opacity)):
+            np.testing.assert_array_equal(x, y)
+        assert (c.evaluated == cfg.n_coarse).all()
+
+
+@pytest.mark.parametrize("eps,levels", [(1e-3, 4), (1e-2, 3), (0.2, 8)])
+def test_culled_render_stop_rule_and_error_bound(eps, levels):
+    """The stop rule rebuilt from the full render's per-sample fields: the
+    segments (runs of one cell), the transmittance in front of each sample
+    (product of exp(-sigma delta) over the samples before it, midpoint
+    intervals), the level starts (segment l; the last level takes the rest)
+    and the first level l > 0 whose transmittance is below eps.  The culled
+    render evaluates exactly the samples before that level; its colour and
+    opacity differ from the full render's by at most the transmittance there,
+    its depth by at most that times far, and its opacity is 1 minus it."""
+    cfg, sc = _dense_scene()
+    ids = np.arange(0, cfg.num_rays, 3)
+    full = oracle.render(sc.sites, cfg.arch, sc.weights, sc.rays_o[ids], sc.rays_d[ids], cfg.near,
+                         cfg.far, cfg.n_coarse, seed=3, ray_ids=ids, per_sample=True)
+    c = _culled(cfg, sc, ids, eps, levels)
+    n = cfg.n_coarse
+    t = full.t.astype(np.float64)
+    b = np.concatenate([np.full((len(ids), 1), cfg.near), 0.5 * (t[:, 1:] + t[:, :-1]),
+                        np.full((len(ids), 1), cfg.far)], axis=1)
+    tau = np.exp(-full.sigma * np.diff(b, axis=1))
+    T_before = np.concatenate([np.ones((len(ids), 1)), np.cumprod(tau, axis=1)], axis=1)
+    want = np.full(len(ids), n)
+    T_stop = np.zeros(len(ids))
+    for r in range(len(ids)):
+        starts = [0] + [i for i in range(1, n) if full.cell[r, i] != full.cell[r, i - 1]]
+        for l in range(1, min(levels, len(starts))):
+            if T_before[r, starts[l]] < eps:
+                want[r] = starts[l]
+                T_stop[r] = T_before[r, starts[l]]
+                break
+    np.testing.assert_array_equal(c.evaluated, want)
+    stopped = want < n
+    assert stopped.sum() > 0
+    bound = np.where(stopped, T_stop, 0.0) + 1e-12
+    assert (np.abs(c.rgb - full.rgb).max(1) <= bound).all()
+    assert (np.abs(c.opacity - full.opacity) <= bound).all()
+    assert (np.abs(c.depth - full.depth) <= bound * cfg.far).all()
+    np.testing.assert_allclose(c.opacity[stopped], 1.0 - T_stop[stopped], rtol=0, atol=1e-12)
+
+
+def test_culled_render_with_empty_heads():
+    """0-capacity heads under culling: the culled render with zero weights for
+    those heads, bitwise (their samples are transparent, as in the full
+    render)."""
+    cfg, sc = _dense_scene()
+    ids = np.arange(0, cfg.num_rays, 7)
+    empty = np.array([1, 0, 0, 1, 0, 0, 0, 1])
+    zeroed = sc.weights.copy()
+    zeroed[empty == 1] = 0.0
+    a = _culled(cfg, sc, ids, 1e-3, 4, empty=empty)
+    z = _culled(cfg, sc, ids, 1e-3, 4, weights=zeroed)
+    for x, y in ((a.rgb, z.rgb), (a.depth, z.depth), (a.opacity, z.opacity),
+                 (a.evaluated, z.evaluated)):
+        np.testing.assert_array_equal(x, y)

@@ -21,6 +21,9 @@
  *   derf_render_soft   the soft decomposition: every head on every sample,
  *                 blended by the soft Voronoi weights, and each ray's
  *                 per-head contributions                    (Sec. 3.2 Eq. 4-6, Eq. 8)
+ *   derf_render_culled  derf_render in Painter's order with transmittance
+ *                 culling: a ray's later segments are not evaluated once
+ *                 it is nearly opaque                       (Sec. 3.3)
  *
  * All functions return a derf_status (0 on success, negative on error),
  * never abort and never print.  derf_last_error() returns a thread-local
@@ -201,6 +204,30 @@ int derf_render_soft(derf_handle *h, const float *rays_o, const float *rays_d, l
                      float near_t, float far_t, const derf_sampling *samp, float beta,
                      float *out_rgb, float *out_depth, float *out_opacity, float *out_contrib,
                      void *hip_stream);
+
+/* derf_render with the Painter's order put to work (Sec. 3.3: a ray meets its
+ * cells in order of distance from its origin, and composites its segments
+ * front to back): the segments are evaluated level by level, level l of a
+ * ray being its segment of ordinal l along the ray (level levels - 1: every
+ * later segment), and a ray whose transmittance in front of level l > 0 is
+ * below eps skips that level and every later one -- its heads do not run
+ * there.  The result is the Painter's merge of the evaluated segments: colour
+ * and opacity within eps of derf_render's (colours lie in [0, 1]), depth
+ * within eps * far.  With levels = 1 or eps = 0 nothing is skipped and the
+ * outputs equal derf_render's.
+ *   eps            finite, >= 0: the transmittance below which a ray stops
+ *   levels         1 .. 32: segment levels (one bucketing, MLP and
+ *                  integration pass each)
+ *   out_evaluated  NULL, or device unsigned [R]: samples whose head ran, per
+ *                  ray
+ * Other arguments and limits as derf_render; samp->n_fine must be 0
+ * (DERF_ERR_UNSUPPORTED otherwise).  Stage times: DERF_STAGE_SAMPLE
+ * (sampling, assignment and level bounds) and DERF_STAGE_MLP (the whole
+ * level loop); head_samples sums every level's evaluations. */
+int derf_render_culled(derf_handle *h, const float *rays_o, const float *rays_d,
+                       long long num_rays, float near_t, float far_t, const derf_sampling *samp,
+                       float eps, int levels, float *out_rgb, float *out_depth,
+                       float *out_opacity, unsigned *out_evaluated, void *hip_stream);
 
 /* Per-stage GPU time, recorded with HIP events on the render's stream when
  * timing is on (derf_set_timing); accumulated over renders since the last

@@ -108,6 +108,7 @@ struct derf_handle {
     // per-head counts of the last render (device pointers into the workspace)
     unsigned *totals = nullptr;
     unsigned *totals_fine = nullptr;
+    int totals_sets = 1;  // a culled render: one set of K totals per level
 };
 
 namespace {
@@ -442,6 +443,7 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
     h->last_stream = s;
     h->totals = b.totals;
     h->totals_fine = hier ? b.totals_fine : nullptr;
+    h->totals_sets = 1;
     h->stats.renders += 1;
     h->stats.samples += (long long)S + Sf;
     return DERF_OK;
@@ -534,6 +536,132 @@ int render_soft_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     h->last_stream = s;
     h->totals = b.totals;
     h->totals_fine = nullptr;
+    h->totals_sets = 1;
+    h->stats.renders += 1;
+    h->stats.samples += (long long)S;
+    return DERF_OK;
+}
+
+// Workspace of a culled render: the single-pass buffers, then the level
+// bounds, the transmittance and one set of head totals per level.
+struct CullBuffers {
+    unsigned *lb;            // [R][levels + 1]
+    float *trans;            // [R]
+    unsigned *level_totals;  // [levels][K]
+};
+
+size_t layout_culled(char *base, unsigned S, unsigned R, unsigned nblk, int K, bool bf16,
+                     unsigned levels, Buffers *b, CullBuffers *c)
+{
+    char *p = base + layout(base, S, 0, R, nblk, K, bf16, b);
+    CullBuffers x;
+    x.lb = carve<unsigned>(p, (size_t)R * (levels + 1));
+    x.trans = carve<float>(p, R);
+    x.level_totals = carve<unsigned>(p, (size_t)levels * K);
+    if (c)
+        *c = x;
+    return (size_t)(p - base);
+}
+
+// Painter's-order render with transmittance culling (Sec. 3.3): sampling and
+// assignment as the single pass, then per level: counts of the live samples,
+// offsets, scatter, the grouped MLP and the level's integration.
+int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
+                       long long num_rays, float near_t, float far_t, const derf_sampling *samp,
+                       float eps, int levels, float *out_rgb, float *out_depth,
+                       float *out_opacity, unsigned *out_evaluated, void *stream)
+{
+    if (!h)
+        return fail(DERF_ERR_INVALID_ARG, "null handle");
+    if (!samp)
+        return fail(DERF_ERR_INVALID_ARG, "null sampling descriptor");
+    if (num_rays < 0 || num_rays >= (1LL << 30))
+        return fail(DERF_ERR_INVALID_ARG, "need 0 <= num_rays < 2^30");
+    if (!(near_t < far_t) || !isfinite(near_t) || !isfinite(far_t))
+        return fail(DERF_ERR_INVALID_ARG, "need finite near < far");
+    if (!(eps >= 0.0f) || !isfinite(eps))
+        return fail(DERF_ERR_INVALID_ARG, "need a finite eps >= 0");
+    if (levels < 1 || levels > kMaxLevels)
+        return fail(DERF_ERR_INVALID_ARG, "need 1 <= levels <= %d", kMaxLevels);
+    if (samp->n_coarse < 1 || samp->n_coarse > 1024 || samp->n_fine < 0)
+        return fail(DERF_ERR_INVALID_ARG, "need 1 <= n_coarse <= 1024, n_fine >= 0");
+    if (samp->n_fine != 0)
+        return fail(DERF_ERR_UNSUPPORTED, "the culled render has no hierarchical sampling");
+    if (num_rays == 0)
+        return DERF_OK;
+    if (!rays_o || !rays_d || !out_rgb || !out_depth || !out_opacity)
+        return fail(DERF_ERR_INVALID_ARG, "null ray or output pointer");
+    if ((unsigned long long)num_rays * (unsigned)samp->n_coarse >= (1ull << 32))
+        return fail(DERF_ERR_INVALID_ARG, "num_rays * n_coarse must be < 2^32 per call");
+
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    HIP_TRY(hipSetDevice(h->device), "hipSetDevice");
+    const unsigned R = (unsigned)num_rays, N = (unsigned)samp->n_coarse, S = R * N;
+    const unsigned L = (unsigned)levels, nblk = blocks_of(S);
+    const int K = h->num_sites;
+    int rc = ensure_workspace(h, layout_culled(nullptr, S, R, nblk, K, h->bf16, L, nullptr, nullptr));
+    if (rc != DERF_OK)
+        return rc;
+    if (h->timing && h->ev_pending) {
+        HIP_TRY(hipEventSynchronize(last_event(h)), "hipEventSynchronize");
+        accumulate_timing(h);
+    }
+    Buffers b;
+    CullBuffers c;
+    layout_culled(reinterpret_cast<char *>(h->ws.mem), S, R, nblk, K, h->bf16, L, &b, &c);
+
+    RenderGeometry g;
+    g.rays_o = rays_o;
+    g.rays_d = rays_d;
+    g.num_rays = R;
+    g.n = N;
+    g.num_samples = S;
+    g.inv_n = 1.0 / (double)N;
+    g.near_t = near_t;
+    g.far_t = far_t;
+    g.step = (far_t - near_t) / (float)N;
+    g.seed = samp->seed;
+    g.ray_offset = samp->ray_offset;
+    g.perturb = samp->perturb ? 1 : 0;
+
+    h->ev_mask = 0;
+    auto mark = [&](int stage, int end) -> hipError_t {
+        if (!h->timing)
+            return hipSuccess;
+        h->ev_mask |= 1u << stage;
+        return hipEventRecord(h->ev[ev_index(0, stage, end)], s);
+    };
+    HIP_TRY(mark(DERF_STAGE_SAMPLE, 0), "hipEventRecord");
+    HIP_TRY(launch_ray_encode(g, b.dirbuf, h->bf16, s), "ray_encode launch");
+    const WalkTable walk{b.walk_seg, b.walk_nseg};
+    if (walk.seg)
+        HIP_TRY(launch_ray_walk(g, h->sites, K, b.walk_seg, b.walk_nseg, s), "ray_walk launch");
+    HIP_TRY(launch_sample_assign(g, h->sites, K, h->site_bits, walk, b.t, b.cell, b.counts, nblk,
+                                 s),
+            "sample_assign launch");
+    HIP_TRY(launch_level_bounds(b.cell, N, R, L, c.lb, s), "level_bounds launch");
+    HIP_TRY(mark(DERF_STAGE_SAMPLE, 1), "hipEventRecord");
+    HIP_TRY(mark(DERF_STAGE_MLP, 0), "hipEventRecord");
+    for (unsigned l = 0; l < L; ++l) {
+        const CullLevel lv{c.lb, c.trans, out_evaluated, L, l, eps};
+        unsigned *tot = c.level_totals + (size_t)l * K;
+        HIP_TRY(launch_level_count(g, b.cell, K, h->site_bits, lv, b.counts, nblk, s),
+                "level_count launch");
+        HIP_TRY(launch_bucket_scan(b.counts, nblk, K, tot, b.mlp_queue, s), "bucket_scan launch");
+        HIP_TRY(launch_level_scatter(g, b.cell, b.counts, tot, nblk, K, h->site_bits, h->empty, lv,
+                                     b.bucket, b.sr, s),
+                "level_scatter launch");
+        HIP_TRY(launch_groups(h, b.bucket, tot, g, b.t, b.dirbuf, b.sr, b.mlp_queue, false, s),
+                "mlp launch");
+        HIP_TRY(launch_level_composite(g, b.t, b.cell, b.sr, lv, out_rgb, out_depth, out_opacity, s),
+                "level_composite launch");
+    }
+    HIP_TRY(mark(DERF_STAGE_MLP, 1), "hipEventRecord");
+    h->ev_pending = h->timing;
+    h->last_stream = s;
+    h->totals = c.level_totals;
+    h->totals_fine = nullptr;
+    h->totals_sets = levels;
     h->stats.renders += 1;
     h->stats.samples += (long long)S;
     return DERF_OK;
@@ -711,6 +839,15 @@ int derf_render_soft(derf_handle *h, const float *rays_o, const float *rays_d, l
                             out_depth, out_opacity, out_contrib, hip_stream);
 }
 
+int derf_render_culled(derf_handle *h, const float *rays_o, const float *rays_d,
+                       long long num_rays, float near_t, float far_t, const derf_sampling *samp,
+                       float eps, int levels, float *out_rgb, float *out_depth,
+                       float *out_opacity, unsigned *out_evaluated, void *hip_stream)
+{
+    return render_culled_impl(h, rays_o, rays_d, num_rays, near_t, far_t, samp, eps, levels,
+                              out_rgb, out_depth, out_opacity, out_evaluated, hip_stream);
+}
+
 int derf_set_empty_heads(derf_handle *h, const int *flags)
 {
     if (!h)
@@ -743,12 +880,12 @@ int derf_get_stats(derf_handle *h, derf_stats *out)
     accumulate_timing(h);
     memset(h->stats.head_samples, 0, sizeof(h->stats.head_samples));
     if (h->totals) {
-        std::vector<unsigned> tot(h->num_sites);
-        HIP_TRY(hipMemcpy(tot.data(), h->totals, sizeof(unsigned) * h->num_sites,
+        std::vector<unsigned> tot((size_t)h->num_sites * h->totals_sets);
+        HIP_TRY(hipMemcpy(tot.data(), h->totals, sizeof(unsigned) * tot.size(),
                           hipMemcpyDeviceToHost),
                 "hipMemcpy");
-        for (int k = 0; k < h->num_sites; ++k)
-            h->stats.head_samples[k] = tot[k];
+        for (size_t j = 0; j < tot.size(); ++j)
+            h->stats.head_samples[j % h->num_sites] += tot[j];
         if (h->totals_fine) {
             HIP_TRY(hipMemcpy(tot.data(), h->totals_fine, sizeof(unsigned) * h->num_sites,
                               hipMemcpyDeviceToHost),

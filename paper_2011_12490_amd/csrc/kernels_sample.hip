@@ -609,6 +609,93 @@ __device__ __forceinline__ void head_block_base(const unsigned *__restrict__ pre
     }
 }
 
+// ---------------------------------------------------------------------------
+// Painter's-order culling (Sec. 3.3).  The Painter's order visits a ray's
+// segments front to back, so the transmittance in front of a segment is
+// known before its head runs.  Level l of a ray is its segment of ordinal l
+// (the last level: every later segment); lb[r * (levels + 1) + l] is the
+// first sample of level l (lb[.. + 0] = 0, lb[.. + levels] = n; a level the
+// ray does not reach starts at n).  Each level is bucketed, evaluated and
+// integrated in turn; a ray whose transmittance has fallen below eps takes
+// no part in later levels.
+
+// Sample s is live at the level: it lies in the level's range of its ray,
+// and the ray is still open (level 0, or transmittance >= eps).
+struct LevelLive {
+    const unsigned *lb;
+    const float *trans;  // [R] transmittance in front of this level
+    unsigned n, levels, level;
+    double inv_n;
+    float eps;
+    __device__ __forceinline__ bool operator()(unsigned s) const
+    {
+        unsigned r, i;
+        split_sample(s, n, inv_n, r, i);
+        const unsigned *b = lb + (size_t)r * (levels + 1) + level;
+        return i >= b[0] && i < b[1] && (level == 0 || trans[r] >= eps);
+    }
+};
+
+// Level bounds, one wave per ray, 64 samples per step.  A sample opens a
+// segment when its cell differs from the previous sample's; lane j
+// (1 <= j < levels) records where the j-th such change is (the start of
+// segment j), taking the (j - seen)-th set bit of the step's change ballot.
+__global__ __launch_bounds__(kThreads) void level_bounds_kernel(const uint8_t *__restrict__ cell,
+                                                               unsigned n, unsigned num_rays,
+                                                               unsigned levels,
+                                                               unsigned *__restrict__ lb)
+{
+    const unsigned lane = threadIdx.x & 63;
+    const unsigned ray = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+    if (ray >= num_rays)
+        return;
+    const size_t base = (size_t)ray * n;
+    unsigned mine = n;  // start of level `lane`
+    unsigned seen = 0;  // changes before this step (wave-uniform)
+    for (unsigned c0 = 0; c0 < n && seen + 1 < levels; c0 += 64) {
+        const unsigned i = c0 + lane;
+        const bool change = i > 0 && i < n && cell[base + i] != cell[base + i - 1];
+        const uint64_t m = __ballot(change);
+        const unsigned cnt = (unsigned)__popcll(m);
+        if (lane < levels && lane > seen && lane <= seen + cnt) {
+            uint64_t mm = m;
+            for (unsigned q = lane - seen; q > 1; --q)
+                mm &= mm - 1;
+            mine = c0 + (unsigned)__builtin_ctzll(mm);
+        }
+        seen += cnt;
+    }
+    if (lane <= levels)
+        lb[(size_t)ray * (levels + 1) + lane] = lane == 0 ? 0u : mine;
+}
+
+// Per-block head histograms of the samples live at the level (the layout of
+// the assignment's counts: counts[k * num_blocks + b]).
+__global__ __launch_bounds__(kThreads) void level_count_kernel(const uint8_t *__restrict__ cell,
+                                                              unsigned num_samples, int num_sites,
+                                                              int site_bits, LevelLive live,
+                                                              unsigned *__restrict__ counts,
+                                                              unsigned num_blocks)
+{
+    __shared__ unsigned s_hist[kMaxSites];
+    for (int k = threadIdx.x; k < num_sites; k += kThreads)
+        s_hist[k] = 0;
+    __syncthreads();
+    const uint64_t lane_bit = 1ull << (threadIdx.x & 63);
+    for (unsigned q = threadIdx.x; q < (unsigned)kBucketBlock; q += kThreads) {
+        const unsigned long long s64 = (unsigned long long)blockIdx.x * kBucketBlock + q;
+        const unsigned s = (unsigned)s64;
+        const bool ok = s64 < num_samples && live(s);
+        const unsigned c = ok ? cell[s] : 0u;
+        const uint64_t peers = match_peers(c, site_bits, __ballot(ok));
+        if (ok && (peers & (lane_bit - 1)) == 0)
+            atomicAdd(&s_hist[c], (unsigned)__popcll(peers));
+    }
+    __syncthreads();
+    for (int k = threadIdx.x; k < num_sites; k += kThreads)
+        counts[(size_t)k * num_blocks + blockIdx.x] = s_hist[k];
+}
+
 // Stable scatter of sample ids into per-head buckets.  Bucket k occupies
 // [offset_k, offset_k + total_k) with offset_k = sum of totals below k;
 // within it samples keep increasing sample-id order, so each ray's run
@@ -621,10 +708,11 @@ __device__ __forceinline__ void head_block_base(const unsigned *__restrict__ pre
 // head by ballot and advances the wave's own counters.  A sample owned by a
 // 0-capacity head keeps its bucket slot (the offsets are the same) but gets
 // zero density and colour in sr: the MLP does not evaluate that head.
+template <bool LEVEL>
 __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
     const uint8_t *__restrict__ cell, const unsigned *__restrict__ prefix,
     const unsigned *__restrict__ totals, unsigned num_samples, unsigned num_blocks,
-    int num_sites, int site_bits, HeadMask empty, unsigned *__restrict__ bucket,
+    int num_sites, int site_bits, HeadMask empty, LevelLive live, unsigned *__restrict__ bucket,
     float4 *__restrict__ sr)
 {
     constexpr int kWavesPerBlock = kThreads / 64;
@@ -639,16 +727,20 @@ __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
             s_pos[v][k] = 0;
     const unsigned wbase = blockIdx.x * (unsigned)kBucketBlock + w * (kSteps * 64);
     unsigned cs[kSteps];
+    bool in[kSteps];  // the sample exists (LEVEL: and is live at this level)
 #pragma unroll
     for (int step = 0; step < kSteps; ++step) {
         const unsigned s = wbase + step * 64 + lane;
-        cs[step] = s < num_samples ? cell[s] : 0u;
+        in[step] = s < num_samples;
+        if constexpr (LEVEL)
+            in[step] = in[step] && live(s);
+        cs[step] = in[step] ? cell[s] : 0u;
     }
     __syncthreads();
     // pass 1: this wave's count per head
 #pragma unroll
     for (int step = 0; step < kSteps; ++step) {
-        const bool ok = wbase + step * 64 + lane < num_samples;
+        const bool ok = in[step];
         const uint64_t peers = match_peers(cs[step], site_bits, __ballot(ok));
         if (ok && (peers & below) == 0)
             s_pos[w][cs[step]] += (unsigned)__popcll(peers);
@@ -668,7 +760,7 @@ __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
 #pragma unroll
     for (int step = 0; step < kSteps; ++step) {
         const unsigned s = wbase + step * 64 + lane;
-        const bool ok = s < num_samples;
+        const bool ok = in[step];
         const unsigned c = cs[step];
         const uint64_t peers = match_peers(c, site_bits, __ballot(ok));
         const unsigned start = ok ? s_pos[w][c] : 0u;
@@ -692,12 +784,27 @@ __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
 // runs (integrate_runs), and the 64 lane results are merged in lane order;
 // the chunk results are merged in chunk order.  A segment cut by a lane or
 // chunk boundary is integrated in pieces merged by "over", which is exact.
+// LEVEL: only the ray's samples of one culling level, [lb[l], lb[l + 1]),
+// are integrated (the depths of the whole chunk are staged for the interval
+// ends), and the result is merged behind the ray's state from the earlier
+// levels: rgb, depth and the transmittance trans; a ray whose transmittance
+// is below eps is left as it is.
 constexpr int kChunk = 256;
 
+// The state the levels of a culled render carry from one to the next.
+struct LevelState {
+    const unsigned *lb;
+    float *trans;          // [R]
+    unsigned *evaluated;   // [R] samples integrated so far, or null
+    unsigned levels, level;
+    float eps;
+};
+
+template <bool LEVEL>
 __global__ __launch_bounds__(kThreads) void composite_kernel(
     const float *__restrict__ t, const uint8_t *__restrict__ cell, const float4 *__restrict__ sr,
-    unsigned n, unsigned num_rays, float near_t, float far_t, float *__restrict__ out_rgb,
-    float *__restrict__ out_depth, float *__restrict__ out_opacity)
+    unsigned n, unsigned num_rays, float near_t, float far_t, LevelState lv,
+    float *__restrict__ out_rgb, float *__restrict__ out_depth, float *__restrict__ out_opacity)
 {
     __shared__ float4 s_sr[kThreads / 64][kChunk];
     __shared__ float s_t[kThreads / 64][kChunk + 2];  // [0]: sample before the chunk, [len + 1]: after
@@ -708,20 +815,42 @@ __global__ __launch_bounds__(kThreads) void composite_kernel(
     const bool live = ray < num_rays;
     const size_t base = (size_t)(live ? ray : 0u) * n;
     Over acc{0.f, 0.f, 0.f, 0.f, 1.f};
+    unsigned a = 0, b = n;  // the samples integrated
+    bool go = live;
+    if constexpr (LEVEL) {
+        if (live) {
+            const unsigned *r_lb = lv.lb + (size_t)ray * (lv.levels + 1) + lv.level;
+            a = r_lb[0];
+            b = r_lb[1];
+            if (lv.level > 0) {
+                acc = Over{out_rgb[3 * ray], out_rgb[3 * ray + 1], out_rgb[3 * ray + 2],
+                           out_depth[ray], lv.trans[ray]};
+                go = acc.t >= lv.eps;
+            }
+        }
+        if (!go)
+            a = b = 0;
+    }
     for (unsigned c0 = 0; c0 < n; c0 += kChunk) {
         const unsigned len = min((unsigned)kChunk, n - c0);
-        for (unsigned k = lane; k < len; k += 64) {
-            s_sr[wv][k] = sr[base + c0 + k];
-            s_t[wv][k + 1] = t[base + c0 + k];
-            s_c[wv][k] = cell[base + c0 + k];
+        // this chunk's part of [a, b), relative to c0
+        const unsigned ca = min(max(a, c0), c0 + len) - c0;
+        const unsigned cb = max(min(b, c0 + len), c0 + ca) - c0;
+        if (ca < cb) {
+            for (unsigned k = lane; k < len; k += 64)
+                s_t[wv][k + 1] = t[base + c0 + k];
+            for (unsigned k = ca + lane; k < cb; k += 64) {
+                s_sr[wv][k] = sr[base + c0 + k];
+                s_c[wv][k] = cell[base + c0 + k];
+            }
+            if (lane == 0)
+                s_t[wv][0] = c0 > 0 ? t[base + c0 - 1] : 0.0f;
+            if (lane == 1)
+                s_t[wv][len + 1] = c0 + len < n ? t[base + c0 + len] : 0.0f;
         }
-        if (lane == 0)
-            s_t[wv][0] = c0 > 0 ? t[base + c0 - 1] : 0.0f;
-        if (lane == 1)
-            s_t[wv][len + 1] = c0 + len < n ? t[base + c0 + len] : 0.0f;
         __syncthreads();
-        const unsigned cl = (len + 63) / 64;
-        const unsigned i0 = min(lane * cl, len), i1 = min(i0 + cl, len);
+        const unsigned cl = (cb - ca + 63) / 64;
+        const unsigned i0 = min(ca + lane * cl, cb), i1 = min(i0 + cl, cb);
         Over part = integrate_runs(
             c0 + i0, c0 + i1, n, near_t, far_t, [&](unsigned i) { return s_t[wv][i - c0 + 1]; },
             [&](unsigned i) { return (unsigned)s_c[wv][i - c0]; },
@@ -730,12 +859,17 @@ __global__ __launch_bounds__(kThreads) void composite_kernel(
         acc = over(acc, part);  // meaningful in lane 0
         __syncthreads();
     }
-    if (live && lane == 0) {
+    if (go && lane == 0) {
         out_rgb[3 * ray] = acc.r;
         out_rgb[3 * ray + 1] = acc.g;
         out_rgb[3 * ray + 2] = acc.b;
         out_depth[ray] = acc.d;
         out_opacity[ray] = 1.0f - acc.t;
+        if constexpr (LEVEL) {
+            lv.trans[ray] = acc.t;
+            if (lv.evaluated)
+                lv.evaluated[ray] = (lv.level > 0 ? lv.evaluated[ray] : 0u) + (b - a);
+        }
     }
 }
 
@@ -834,9 +968,9 @@ hipError_t launch_bucket_scatter(const uint8_t *cell, const unsigned *counts,
                                  const HeadMask &empty, unsigned *bucket, float4 *sr,
                                  hipStream_t s)
 {
-    bucket_scatter_kernel<<<num_blocks, kThreads, 0, s>>>(cell, counts, totals, num_samples,
-                                                          num_blocks, num_sites, site_bits, empty,
-                                                          bucket, sr);
+    bucket_scatter_kernel<false><<<num_blocks, kThreads, 0, s>>>(
+        cell, counts, totals, num_samples, num_blocks, num_sites, site_bits, empty, LevelLive{},
+        bucket, sr);
     return hipGetLastError();
 }
 
@@ -845,8 +979,54 @@ hipError_t launch_composite(const RenderGeometry &g, const float *t, const uint8
                             hipStream_t s)
 {
     const unsigned grid = blocks_for(g.num_rays, kThreads / 64);
-    composite_kernel<<<grid, kThreads, 0, s>>>(t, cell, sr, g.n, g.num_rays, g.near_t, g.far_t,
-                                               rgb, depth, opacity);
+    composite_kernel<false><<<grid, kThreads, 0, s>>>(t, cell, sr, g.n, g.num_rays, g.near_t,
+                                                      g.far_t, LevelState{}, rgb, depth, opacity);
+    return hipGetLastError();
+}
+
+hipError_t launch_level_bounds(const uint8_t *cell, unsigned n, unsigned num_rays,
+                               unsigned levels, unsigned *lb, hipStream_t s)
+{
+    level_bounds_kernel<<<blocks_for(num_rays, kThreads / 64), kThreads, 0, s>>>(cell, n, num_rays,
+                                                                                 levels, lb);
+    return hipGetLastError();
+}
+
+static LevelLive level_live(const RenderGeometry &g, const CullLevel &lv)
+{
+    return LevelLive{lv.lb, lv.trans, g.n, lv.levels, lv.level, g.inv_n, lv.eps};
+}
+
+hipError_t launch_level_count(const RenderGeometry &g, const uint8_t *cell, int num_sites,
+                              int site_bits, const CullLevel &lv, unsigned *counts,
+                              unsigned num_blocks, hipStream_t s)
+{
+    level_count_kernel<<<num_blocks, kThreads, 0, s>>>(cell, g.num_samples, num_sites, site_bits,
+                                                       level_live(g, lv), counts, num_blocks);
+    return hipGetLastError();
+}
+
+hipError_t launch_level_scatter(const RenderGeometry &g, const uint8_t *cell,
+                                const unsigned *counts, const unsigned *totals,
+                                unsigned num_blocks, int num_sites, int site_bits,
+                                const HeadMask &empty, const CullLevel &lv, unsigned *bucket,
+                                float4 *sr, hipStream_t s)
+{
+    bucket_scatter_kernel<true><<<num_blocks, kThreads, 0, s>>>(
+        cell, counts, totals, g.num_samples, num_blocks, num_sites, site_bits, empty,
+        level_live(g, lv), bucket, sr);
+    return hipGetLastError();
+}
+
+hipError_t launch_level_composite(const RenderGeometry &g, const float *t, const uint8_t *cell,
+                                  const float4 *sr, const CullLevel &lv, float *rgb,
+                                  float *depth, float *opacity, hipStream_t s)
+{
+    const unsigned grid = blocks_for(g.num_rays, kThreads / 64);
+    composite_kernel<true><<<grid, kThreads, 0, s>>>(
+        t, cell, sr, g.n, g.num_rays, g.near_t, g.far_t,
+        LevelState{lv.lb, lv.trans, lv.evaluated, lv.levels, lv.level, lv.eps}, rgb, depth,
+        opacity);
     return hipGetLastError();
 }
 

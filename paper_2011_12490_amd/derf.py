@@ -53,7 +53,7 @@ class derf_stats(ctypes.Structure):
 
 EXPORTS = ("derf_weights_count", "derf_create", "derf_create_mixed", "derf_render",
            "derf_render_debug",
-           "derf_render_soft", "derf_set_empty_heads", "derf_set_timing", "derf_get_stats", "derf_reset_stats", "derf_destroy",
+           "derf_render_soft", "derf_render_culled", "derf_set_empty_heads", "derf_set_timing", "derf_get_stats", "derf_reset_stats", "derf_destroy",
            "derf_status_string", "derf_last_error")
 
 _lib: Optional[ctypes.CDLL] = None
@@ -91,6 +91,10 @@ def lib() -> ctypes.CDLL:
         L.derf_render_soft.argtypes = [P, P, P, ctypes.c_longlong, ctypes.c_float, ctypes.c_float,
                                        ctypes.POINTER(derf_sampling), ctypes.c_float, P, P, P, P, P]
         L.derf_render_soft.restype = ctypes.c_int
+        L.derf_render_culled.argtypes = [P, P, P, ctypes.c_longlong, ctypes.c_float,
+                                         ctypes.c_float, ctypes.POINTER(derf_sampling),
+                                         ctypes.c_float, ctypes.c_int, P, P, P, P, P]
+        L.derf_render_culled.restype = ctypes.c_int
         L.derf_set_empty_heads.argtypes = [P, P]
         L.derf_set_empty_heads.restype = ctypes.c_int
         L.derf_set_timing.argtypes = [P, ctypes.c_int]
@@ -191,6 +195,22 @@ def derf_render_soft(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float,
                                   _dptr(out_opacity),
                                   None if out_contrib is None else _dptr(out_contrib), sp),
            "derf_render_soft")
+
+
+def derf_render_culled(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far: float,
+                       samp: derf_sampling, eps: float, levels: int, out_rgb: torch.Tensor,
+                       out_depth: torch.Tensor, out_opacity: torch.Tensor,
+                       out_evaluated: Optional[torch.Tensor] = None, stream=None):
+    """Enqueue a Painter's-order render with transmittance culling on `stream`
+    (default: torch's current stream).  out_evaluated: int32 [R] or None."""
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    _check(lib().derf_render_culled(h, _dptr(rays_o), _dptr(rays_d), rays_o.shape[0], near, far,
+                                    ctypes.byref(samp), eps, levels, _dptr(out_rgb),
+                                    _dptr(out_depth), _dptr(out_opacity),
+                                    None if out_evaluated is None else _dptr(out_evaluated), sp),
+           "derf_render_culled")
 
 
 def derf_set_empty_heads(h, flags):
@@ -299,3 +319,21 @@ class Renderer:
         if contrib:
             return rgb, depth, opac, W
         return rgb, depth, opac
+
+    def render_culled(self, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far: float,
+                      n: int, eps: float, levels: int, seed: int = 0, perturb: bool = True,
+                      stream=None, ray_offset: int = 0):
+        """Single-pass render in Painter's order with transmittance culling;
+        returns (rgb, depth, opacity, evaluated samples per ray)."""
+        assert rays_o.is_cuda and rays_o.dtype == torch.float32 and rays_o.is_contiguous()
+        assert rays_d.is_cuda and rays_d.dtype == torch.float32 and rays_d.is_contiguous()
+        R = rays_o.shape[0]
+        dev = rays_o.device
+        rgb = torch.empty((R, 3), dtype=torch.float32, device=dev)
+        depth = torch.empty((R,), dtype=torch.float32, device=dev)
+        opac = torch.empty((R,), dtype=torch.float32, device=dev)
+        ev = torch.empty((R,), dtype=torch.int32, device=dev)
+        samp = derf_sampling(n, 0, seed, int(perturb), ray_offset)
+        derf_render_culled(self.handle, rays_o, rays_d, near, far, samp, eps, levels, rgb, depth,
+                           opac, ev, stream)
+        return rgb, depth, opac, ev

@@ -144,6 +144,11 @@ CONFIGS = {
     # cells are a fixed 4x4x4 lattice over [-1, 1]^3 (DeRF-Grid).
     "grid_k64": SceneConfig("grid_k64", 504, 378, "forward", 60.0, 0.0, 1.0, 192, 0, 64,
                             "grid", ARCH_128, "bf16"),
+    # The headline frame with a density bias of +16: every ray turns opaque
+    # part-way (a stand-in for the opaque surfaces of captured scenes), the
+    # workload of Painter's-order culling.
+    "dense_k16": SceneConfig("dense_k16", 504, 378, "forward", 60.0, 0.0, 1.0, 192, 0, 16,
+                             "gmm_kmeans", ARCH_128, "bf16", sigma_bias=16.0),
     # 1024x1024, 256 samples, 64 skewed heads of 6x64, density bias +2.
     "skew_k64": SceneConfig("skew_k64", 1024, 1024, "object", 40.0, 2.0, 6.0, 256, 0, 64,
                             "ball_mix", ARCH_SMALL, "bf16", sigma_bias=2.0),

@@ -95,7 +95,7 @@ def test_render_rejects_bad_arguments_without_a_gpu():
     L.derf_destroy(None)
 
 
-def test_mixed_create_soft_render_and_empty_heads_reject_bad_arguments_without_a_gpu():
+def test_mixed_create_soft_culled_render_and_empty_heads_reject_bad_arguments_without_a_gpu():
     L = derf.lib()
     assert L.derf_create_mixed(None, 1, None, None, None, 1) == derf.DERF_ERR_INVALID_ARG
     archs = [scenes.ARCH_128, scenes.ARCH_SMALL, (10, 4, 8, 96, 5, 64)]
@@ -122,6 +122,8 @@ def test_mixed_create_soft_render_and_empty_heads_reject_bad_arguments_without_a
     samp = derf.derf_sampling(32, 0, 1, 1, 0)
     assert L.derf_render_soft(None, None, None, 1, 2.0, 6.0, ctypes.byref(samp), 1.0, None, None,
                               None, None, None) == derf.DERF_ERR_INVALID_ARG
+    assert L.derf_render_culled(None, None, None, 1, 2.0, 6.0, ctypes.byref(samp), 1e-3, 4, None,
+                                None, None, None, None) == derf.DERF_ERR_INVALID_ARG
 
 
 def test_status_strings():

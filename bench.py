@@ -129,6 +129,9 @@ def main():
     ap.add_argument("--soft", type=float, default=None, metavar="BETA",
                     help="also time the soft decomposition (every head on every sample) at "
                          "temperature BETA, with the per-ray head contributions")
+    ap.add_argument("--cull", default=None, metavar="EPS[,LEVELS]",
+                    help="also time the Painter's-order render with transmittance culling "
+                         "(stop below transmittance EPS, LEVELS segment levels, default 4)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (to scale HBM counters)")
     args = ap.parse_args()
@@ -233,7 +236,47 @@ def main():
         r.close()
         return elapsed * 1e3 / steps, stages
 
+    def run_culled(cfg, eps, levels, steps, warmup, ref_out):
+        """Time `steps` culled renders; evaluated samples and the largest
+        difference from the plain render's outputs ref_out."""
+        sc = scenes.make_scene(cfg)
+        o = torch.from_numpy(sc.rays_o).cuda()
+        d = torch.from_numpy(sc.rays_d).cuda()
+        r = derf.Renderer(sc.sites, cfg.arch, sc.weights, precision)
+        for _ in range(warmup):
+            out = r.render_culled(o, d, cfg.near, cfg.far, cfg.n_coarse, eps, levels,
+                                  scenes.SEED_RENDER)
+        torch.cuda.synchronize()
+        derf.derf_reset_stats(r.handle)
+        derf.derf_set_timing(r.handle, True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            out = r.render_culled(o, d, cfg.near, cfg.far, cfg.n_coarse, eps, levels,
+                                  scenes.SEED_RENDER)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        st = derf.derf_get_stats(r.handle)
+        stages = {name: st.stage_ms[i] / max(1, st.stage_launches[i])
+                  for i, name in enumerate(derf.STAGE_NAMES) if st.stage_launches[i]}
+        evaluated = int(out[3].to(torch.int64).sum().item())
+        diff = {"rgb": (out[0] - ref_out[0]).abs().max().item(),
+                "depth": (out[1] - ref_out[1]).abs().max().item(),
+                "opacity": (out[2] - ref_out[2]).abs().max().item()}
+        r.close()
+        return elapsed * 1e3 / steps, stages, evaluated, diff
+
     sc, ms_per_step, stage_ms, heads = run(cfg, args.steps, args.warmup, args.copy_calibration)
+    plain_out = None
+    if args.cull:
+        # the plain render's outputs, for the culled render's difference
+        pr = derf.Renderer(sc.sites, cfg.arch, sc.weights, precision)
+        plain_out = [x.clone() for x in pr.render(torch.from_numpy(sc.rays_o).cuda(),
+                                                  torch.from_numpy(sc.rays_d).cuda(), cfg.near,
+                                                  cfg.far, cfg.n_coarse, cfg.n_fine,
+                                                  scenes.SEED_RENDER)]
+        torch.cuda.synchronize()
+        pr.close()
     R = cfg.num_rays
     S = R * (cfg.n_coarse + cfg.n_fine)   # head evaluations (both passes when hierarchical)
     mlp_ms = stage_ms["mlp"]
@@ -274,6 +317,21 @@ def main():
                 "head_evaluations": S * cfg.num_sites, "mlp_ms": st_s["mlp"],
                 "mlp_frac": soft_flop / (st_s["mlp"] * 1e-3) / 1e12 / peak, "stage_ms": st_s}
         log("bench: soft beta=%g %.4g rays/s" % (args.soft, soft["rays_per_s"]))
+
+    culled = None
+    if args.cull:
+        if cfg.n_fine or head_archs or empty_heads:
+            raise SystemExit("--cull needs a single-pass workload with one architecture")
+        parts = args.cull.split(",")
+        eps, levels = float(parts[0]), int(parts[1]) if len(parts) > 1 else 4
+        ms_c, st_c, ev_c, diff_c = run_culled(cfg, eps, levels, args.steps, 2, plain_out)
+        culled = {"eps": eps, "levels": levels, "rays_per_s": R / (ms_c * 1e-3),
+                  "ms_per_step": ms_c, "speedup_vs_plain": ms_per_step / ms_c,
+                  "evaluated_samples": ev_c, "evaluated_frac": ev_c / S,
+                  "level_loop_ms": st_c.get("mlp"), "sample_ms": st_c.get("sample_assign"),
+                  "max_abs_diff_vs_plain": diff_c}
+        log("bench: culled eps=%g levels=%d %.4g rays/s (%.3f of samples evaluated)"
+            % (eps, levels, culled["rays_per_s"], culled["evaluated_frac"]))
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -320,6 +378,8 @@ def main():
         res["k_sweep"] = k_sweep
     if soft is not None:
         res["soft"] = soft
+    if culled is not None:
+        res["culled"] = culled
     print(json.dumps(res))
 
 

@@ -14,6 +14,7 @@
 #include <vector>
 
 #include "derf_internal.h"
+#include "derf_cull.h"
 
 using namespace derf;
 
@@ -546,6 +547,7 @@ int render_soft_impl(derf_handle *h, const float *rays_o, const float *rays_d,
 // bounds, the transmittance and one set of head totals per level.
 struct CullBuffers {
     unsigned *lb;            // [R][levels + 1]
+    uint8_t *lvl;            // [S]
     float *trans;            // [R]
     unsigned *level_totals;  // [levels][K]
 };
@@ -556,6 +558,7 @@ size_t layout_culled(char *base, unsigned S, unsigned R, unsigned nblk, int K, b
     char *p = base + layout(base, S, 0, R, nblk, K, bf16, b);
     CullBuffers x;
     x.lb = carve<unsigned>(p, (size_t)R * (levels + 1));
+    x.lvl = carve<uint8_t>(p, S);
     x.trans = carve<float>(p, R);
     x.level_totals = carve<unsigned>(p, (size_t)levels * K);
     if (c)
@@ -639,11 +642,11 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     HIP_TRY(launch_sample_assign(g, h->sites, K, h->site_bits, walk, b.t, b.cell, b.counts, nblk,
                                  s),
             "sample_assign launch");
-    HIP_TRY(launch_level_bounds(b.cell, N, R, L, c.lb, s), "level_bounds launch");
+    HIP_TRY(launch_level_bounds(b.cell, N, R, L, c.lb, c.lvl, s), "level_bounds launch");
     HIP_TRY(mark(DERF_STAGE_SAMPLE, 1), "hipEventRecord");
     HIP_TRY(mark(DERF_STAGE_MLP, 0), "hipEventRecord");
     for (unsigned l = 0; l < L; ++l) {
-        const CullLevel lv{c.lb, c.trans, out_evaluated, L, l, eps};
+        const CullLevel lv{c.lb, c.lvl, c.trans, out_evaluated, L, l, eps};
         unsigned *tot = c.level_totals + (size_t)l * K;
         HIP_TRY(launch_level_count(g, b.cell, K, h->site_bits, lv, b.counts, nblk, s),
                 "level_count launch");

@@ -11,6 +11,7 @@
 
 #include "derf_device.h"
 #include "derf_internal.h"
+#include "derf_cull.h"
 
 namespace derf {
 namespace {
@@ -619,40 +620,37 @@ __device__ __forceinline__ void head_block_base(const unsigned *__restrict__ pre
 // integrated in turn; a ray whose transmittance has fallen below eps takes
 // no part in later levels.
 
-// Sample s is live at the level: it lies in the level's range of its ray,
-// and the ray is still open (level 0, or transmittance >= eps).
+// Sample s is live at the level: lvl[s] holds its level, or kDeadLevel once
+// its ray has closed (the level composite that closes a ray marks the ray's
+// later samples), so the same test serves every level.
+constexpr uint8_t kDeadLevel = 0xFF;
 struct LevelLive {
-    const unsigned *lb;
-    const float *trans;  // [R] transmittance in front of this level
-    unsigned n, levels, level;
-    double inv_n;
-    float eps;
-    __device__ __forceinline__ bool operator()(unsigned s) const
-    {
-        unsigned r, i;
-        split_sample(s, n, inv_n, r, i);
-        const unsigned *b = lb + (size_t)r * (levels + 1) + level;
-        return i >= b[0] && i < b[1] && (level == 0 || trans[r] >= eps);
-    }
+    const uint8_t *lvl;
+    unsigned level;
+    __device__ __forceinline__ bool operator()(unsigned s) const { return lvl[s] == level; }
 };
 
 // Level bounds, one wave per ray, 64 samples per step.  A sample opens a
-// segment when its cell differs from the previous sample's; lane j
-// (1 <= j < levels) records where the j-th such change is (the start of
-// segment j), taking the (j - seen)-th set bit of the step's change ballot.
+// segment when its cell differs from the previous sample's; its segment
+// ordinal is the number of such changes up to it.  Each sample's level,
+// min(ordinal, levels - 1), goes to lvl; lane j (1 <= j < levels) records
+// where the j-th change is (the start of segment j), taking the
+// (j - seen)-th set bit of the step's change ballot.
 __global__ __launch_bounds__(kThreads) void level_bounds_kernel(const uint8_t *__restrict__ cell,
                                                                unsigned n, unsigned num_rays,
                                                                unsigned levels,
-                                                               unsigned *__restrict__ lb)
+                                                               unsigned *__restrict__ lb,
+                                                               uint8_t *__restrict__ lvl)
 {
     const unsigned lane = threadIdx.x & 63;
     const unsigned ray = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
     if (ray >= num_rays)
         return;
     const size_t base = (size_t)ray * n;
+    const uint64_t upto = ~0ull >> (63 - lane);  // lanes 0 .. lane
     unsigned mine = n;  // start of level `lane`
     unsigned seen = 0;  // changes before this step (wave-uniform)
-    for (unsigned c0 = 0; c0 < n && seen + 1 < levels; c0 += 64) {
+    for (unsigned c0 = 0; c0 < n; c0 += 64) {
         const unsigned i = c0 + lane;
         const bool change = i > 0 && i < n && cell[base + i] != cell[base + i - 1];
         const uint64_t m = __ballot(change);
@@ -663,6 +661,8 @@ __global__ __launch_bounds__(kThreads) void level_bounds_kernel(const uint8_t *_
                 mm &= mm - 1;
             mine = c0 + (unsigned)__builtin_ctzll(mm);
         }
+        if (i < n)
+            lvl[base + i] = (uint8_t)min(seen + (unsigned)__popcll(m & upto), levels - 1);
         seen += cnt;
     }
     if (lane <= levels)
@@ -686,8 +686,11 @@ __global__ __launch_bounds__(kThreads) void level_count_kernel(const uint8_t *__
         const unsigned long long s64 = (unsigned long long)blockIdx.x * kBucketBlock + q;
         const unsigned s = (unsigned)s64;
         const bool ok = s64 < num_samples && live(s);
+        const uint64_t any = __ballot(ok);
+        if (any == 0)
+            continue;  // no live sample in this wave's step
         const unsigned c = ok ? cell[s] : 0u;
-        const uint64_t peers = match_peers(c, site_bits, __ballot(ok));
+        const uint64_t peers = match_peers(c, site_bits, any);
         if (ok && (peers & (lane_bit - 1)) == 0)
             atomicAdd(&s_hist[c], (unsigned)__popcll(peers));
     }
@@ -741,7 +744,10 @@ __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
 #pragma unroll
     for (int step = 0; step < kSteps; ++step) {
         const bool ok = in[step];
-        const uint64_t peers = match_peers(cs[step], site_bits, __ballot(ok));
+        const uint64_t any = __ballot(ok);
+        if (LEVEL && any == 0)
+            continue;
+        const uint64_t peers = match_peers(cs[step], site_bits, any);
         if (ok && (peers & below) == 0)
             s_pos[w][cs[step]] += (unsigned)__popcll(peers);
     }
@@ -761,8 +767,11 @@ __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
     for (int step = 0; step < kSteps; ++step) {
         const unsigned s = wbase + step * 64 + lane;
         const bool ok = in[step];
+        const uint64_t any = __ballot(ok);
+        if (LEVEL && any == 0)
+            continue;
         const unsigned c = cs[step];
-        const uint64_t peers = match_peers(c, site_bits, __ballot(ok));
+        const uint64_t peers = match_peers(c, site_bits, any);
         const unsigned start = ok ? s_pos[w][c] : 0u;
         if (ok) {
             const unsigned pos = start + (unsigned)__popcll(peers & below);
@@ -794,6 +803,7 @@ constexpr int kChunk = 256;
 // The state the levels of a culled render carry from one to the next.
 struct LevelState {
     const unsigned *lb;
+    uint8_t *lvl;          // [S] sample levels; a closing ray's later samples become dead
     float *trans;          // [R]
     unsigned *evaluated;   // [R] samples integrated so far, or null
     unsigned levels, level;
@@ -837,7 +847,8 @@ __global__ __launch_bounds__(kThreads) void composite_kernel(
         const unsigned ca = min(max(a, c0), c0 + len) - c0;
         const unsigned cb = max(min(b, c0 + len), c0 + ca) - c0;
         if (ca < cb) {
-            for (unsigned k = lane; k < len; k += 64)
+            // the depths of the range and of one sample on each side
+            for (unsigned k = (ca > 0 ? ca - 1 : 0) + lane; k < min(cb + 1, len); k += 64)
                 s_t[wv][k + 1] = t[base + c0 + k];
             for (unsigned k = ca + lane; k < cb; k += 64) {
                 s_sr[wv][k] = sr[base + c0 + k];
@@ -870,6 +881,13 @@ __global__ __launch_bounds__(kThreads) void composite_kernel(
             if (lv.evaluated)
                 lv.evaluated[ray] = (lv.level > 0 ? lv.evaluated[ray] : 0u) + (b - a);
         }
+    }
+    if constexpr (LEVEL) {
+        // a ray that closes here takes no part in later levels
+        const float tr = __shfl(acc.t, 0);
+        if (go && tr < lv.eps && lv.level + 1 < lv.levels)
+            for (unsigned i = b + lane; i < n; i += 64)
+                lv.lvl[base + i] = kDeadLevel;
     }
 }
 
@@ -985,24 +1003,21 @@ hipError_t launch_composite(const RenderGeometry &g, const float *t, const uint8
 }
 
 hipError_t launch_level_bounds(const uint8_t *cell, unsigned n, unsigned num_rays,
-                               unsigned levels, unsigned *lb, hipStream_t s)
+                               unsigned levels, unsigned *lb, uint8_t *lvl, hipStream_t s)
 {
     level_bounds_kernel<<<blocks_for(num_rays, kThreads / 64), kThreads, 0, s>>>(cell, n, num_rays,
-                                                                                 levels, lb);
+                                                                                 levels, lb, lvl);
     return hipGetLastError();
 }
 
-static LevelLive level_live(const RenderGeometry &g, const CullLevel &lv)
-{
-    return LevelLive{lv.lb, lv.trans, g.n, lv.levels, lv.level, g.inv_n, lv.eps};
-}
+static LevelLive level_live(const CullLevel &lv) { return LevelLive{lv.lvl, lv.level}; }
 
 hipError_t launch_level_count(const RenderGeometry &g, const uint8_t *cell, int num_sites,
                               int site_bits, const CullLevel &lv, unsigned *counts,
                               unsigned num_blocks, hipStream_t s)
 {
     level_count_kernel<<<num_blocks, kThreads, 0, s>>>(cell, g.num_samples, num_sites, site_bits,
-                                                       level_live(g, lv), counts, num_blocks);
+                                                       level_live(lv), counts, num_blocks);
     return hipGetLastError();
 }
 
@@ -1014,7 +1029,7 @@ hipError_t launch_level_scatter(const RenderGeometry &g, const uint8_t *cell,
 {
     bucket_scatter_kernel<true><<<num_blocks, kThreads, 0, s>>>(
         cell, counts, totals, g.num_samples, num_blocks, num_sites, site_bits, empty,
-        level_live(g, lv), bucket, sr);
+        level_live(lv), bucket, sr);
     return hipGetLastError();
 }
 
@@ -1025,7 +1040,7 @@ hipError_t launch_level_composite(const RenderGeometry &g, const float *t, const
     const unsigned grid = blocks_for(g.num_rays, kThreads / 64);
     composite_kernel<true><<<grid, kThreads, 0, s>>>(
         t, cell, sr, g.n, g.num_rays, g.near_t, g.far_t,
-        LevelState{lv.lb, lv.trans, lv.evaluated, lv.levels, lv.level, lv.eps}, rgb, depth,
+        LevelState{lv.lb, lv.lvl, lv.trans, lv.evaluated, lv.levels, lv.level, lv.eps}, rgb, depth,
         opacity);
     return hipGetLastError();
 }

@@ -847,12 +847,20 @@ __global__ __launch_bounds__(kThreads) void composite_kernel(
         const unsigned ca = min(max(a, c0), c0 + len) - c0;
         const unsigned cb = max(min(b, c0 + len), c0 + ca) - c0;
         if (ca < cb) {
-            // the depths of the range and of one sample on each side
-            for (unsigned k = (ca > 0 ? ca - 1 : 0) + lane; k < min(cb + 1, len); k += 64)
-                s_t[wv][k + 1] = t[base + c0 + k];
-            for (unsigned k = ca + lane; k < cb; k += 64) {
-                s_sr[wv][k] = sr[base + c0 + k];
-                s_c[wv][k] = cell[base + c0 + k];
+            if constexpr (!LEVEL) {
+                for (unsigned k = lane; k < len; k += 64) {
+                    s_sr[wv][k] = sr[base + c0 + k];
+                    s_t[wv][k + 1] = t[base + c0 + k];
+                    s_c[wv][k] = cell[base + c0 + k];
+                }
+            } else {
+                // the depths of the range and of one sample on each side
+                for (unsigned k = (ca > 0 ? ca - 1 : 0) + lane; k < min(cb + 1, len); k += 64)
+                    s_t[wv][k + 1] = t[base + c0 + k];
+                for (unsigned k = ca + lane; k < cb; k += 64) {
+                    s_sr[wv][k] = sr[base + c0 + k];
+                    s_c[wv][k] = cell[base + c0 + k];
+                }
             }
             if (lane == 0)
                 s_t[wv][0] = c0 > 0 ? t[base + c0 - 1] : 0.0f;

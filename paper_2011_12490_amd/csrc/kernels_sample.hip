@@ -868,14 +868,18 @@ __global__ __launch_bounds__(kThreads) void composite_kernel(
                 s_t[wv][len + 1] = c0 + len < n ? t[base + c0 + len] : 0.0f;
         }
         __syncthreads();
-        const unsigned cl = (cb - ca + 63) / 64;
-        const unsigned i0 = min(ca + lane * cl, cb), i1 = min(i0 + cl, cb);
-        Over part = integrate_runs(
-            c0 + i0, c0 + i1, n, near_t, far_t, [&](unsigned i) { return s_t[wv][i - c0 + 1]; },
-            [&](unsigned i) { return (unsigned)s_c[wv][i - c0]; },
-            [&](unsigned i) { return s_sr[wv][i - c0]; });
-        part = wave_over(part, lane);
-        acc = over(acc, part);  // meaningful in lane 0
+        // (wave-uniform) an empty range merges the identity: nothing to do
+        if (ca < cb) {
+            const unsigned cl = (cb - ca + 63) / 64;
+            const unsigned i0 = min(ca + lane * cl, cb), i1 = min(i0 + cl, cb);
+            Over part = integrate_runs(
+                c0 + i0, c0 + i1, n, near_t, far_t,
+                [&](unsigned i) { return s_t[wv][i - c0 + 1]; },
+                [&](unsigned i) { return (unsigned)s_c[wv][i - c0]; },
+                [&](unsigned i) { return s_sr[wv][i - c0]; });
+            part = wave_over(part, lane);
+            acc = over(acc, part);  // meaningful in lane 0
+        }
         __syncthreads();
     }
     if (go && lane == 0) {

@@ -122,6 +122,16 @@ def test_culled_dense_headline_frame_bf16():
            "culled dense_k16 bf16")
 
 
+@pytest.mark.parametrize("n", [1, 7, 65, 300, 600])
+def test_culled_ragged_sample_counts_fp32(n):
+    """Sample counts off the 64-lane steps, and past the 256-sample staging
+    chunk of the level composite (a level's range then spans chunks)."""
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], num_sites=8, sigma_bias=4.0, n_coarse=n)
+    sc = scenes.make_scene(cfg)
+    gpu = _gpu_culled(sc, "fp32", 1e-3, 5)
+    _check(gpu, sc, np.arange(0, cfg.num_rays, 4), 1e-3, 5, "fp32", "culled tiny n=%d" % n)
+
+
 def test_one_level_or_zero_eps_is_the_plain_render():
     """levels = 1: derf_render bitwise (the same buckets, MLP tiles and
     integration); eps = 0 with several levels: the same samples, merged level

@@ -111,6 +111,13 @@ def test_culled_walk_path_and_empty_heads_fp32():
            "culled tiny K=40 with empty heads", empty=empty)
 
 
+def test_culled_256_heads_fp32():
+    """K = 256: cells use all 8 bits (8 ballots per histogram step)."""
+    sc = _dense_tiny(K=256, bias=3.0)
+    gpu = _gpu_culled(sc, "fp32", 1e-3, 8)
+    _check(gpu, sc, np.arange(0, sc.cfg.num_rays, 2), 1e-3, 8, "fp32", "culled tiny K=256")
+
+
 def test_culled_dense_headline_frame_bf16():
     """The 504x378 frame with 16 heads of 8x128 and a density bias of +16, bf16:
     a ray subset against the oracle."""

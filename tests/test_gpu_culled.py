@@ -169,6 +169,29 @@ def test_one_level_or_zero_eps_is_the_plain_render():
             label, max((a - b).abs().max().item() for a, b in zip(plain, zero[:3]))), flush=True)
 
 
+def test_culled_repeated_calls_and_side_stream():
+    """One handle, calls with different eps and levels in turn, one on a side
+    stream: the level bytes, dead marks and carried state of one call leave
+    no trace in the next (the first call's outputs come back bitwise)."""
+    derf = _derf()
+    sc = _dense_tiny()
+    cfg = sc.cfg
+    o, d = _rays(sc)
+    r = derf.Renderer(sc.sites, cfg.arch, sc.weights, "fp32")
+    args = (o, d, cfg.near, cfg.far, cfg.n_coarse)
+    first = [x.clone() for x in r.render_culled(*args, 1e-3, 4, seed=scenes.SEED_RENDER)]
+    r.render_culled(*args, 0.3, 2, seed=scenes.SEED_RENDER)
+    r.render_culled(*args, 1e-3, 32, seed=scenes.SEED_RENDER)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        again = r.render_culled(*args, 1e-3, 4, seed=scenes.SEED_RENDER, stream=side)
+    torch.cuda.synchronize()
+    r.close()
+    for a, b in zip(first, again):
+        assert torch.equal(a, b)
+
+
 def test_culled_argument_errors():
     derf = _derf()
     sc = _dense_tiny()

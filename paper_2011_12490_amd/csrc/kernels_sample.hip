@@ -670,29 +670,39 @@ __global__ __launch_bounds__(kThreads) void level_bounds_kernel(const uint8_t *_
 }
 
 // Per-block head histograms of the samples live at the level (the layout of
-// the assignment's counts: counts[k * num_blocks + b]).
+// the assignment's counts: counts[k * num_blocks + b]).  Thread t takes
+// samples t + 256 q of the block (q < 16); all 16 level bytes and cells are
+// loaded up front, so the loads are in flight together.
 __global__ __launch_bounds__(kThreads) void level_count_kernel(const uint8_t *__restrict__ cell,
                                                               unsigned num_samples, int num_sites,
                                                               int site_bits, LevelLive live,
                                                               unsigned *__restrict__ counts,
                                                               unsigned num_blocks)
 {
+    constexpr int kSteps = kBucketBlock / kThreads;
     __shared__ unsigned s_hist[kMaxSites];
     for (int k = threadIdx.x; k < num_sites; k += kThreads)
         s_hist[k] = 0;
+    const unsigned long long base = (unsigned long long)blockIdx.x * kBucketBlock + threadIdx.x;
+    uint8_t lv[kSteps], cs[kSteps];
+#pragma unroll
+    for (int q = 0; q < kSteps; ++q) {
+        const unsigned long long s64 = base + (unsigned)q * kThreads;
+        const bool in = s64 < num_samples;
+        lv[q] = in ? live.lvl[s64] : kDeadLevel;
+        cs[q] = in ? cell[s64] : (uint8_t)0;
+    }
     __syncthreads();
     const uint64_t lane_bit = 1ull << (threadIdx.x & 63);
-    for (unsigned q = threadIdx.x; q < (unsigned)kBucketBlock; q += kThreads) {
-        const unsigned long long s64 = (unsigned long long)blockIdx.x * kBucketBlock + q;
-        const unsigned s = (unsigned)s64;
-        const bool ok = s64 < num_samples && live(s);
+#pragma unroll
+    for (int q = 0; q < kSteps; ++q) {
+        const bool ok = lv[q] == live.level;
         const uint64_t any = __ballot(ok);
         if (any == 0)
             continue;  // no live sample in this wave's step
-        const unsigned c = ok ? cell[s] : 0u;
-        const uint64_t peers = match_peers(c, site_bits, any);
+        const uint64_t peers = match_peers(cs[q], site_bits, any);
         if (ok && (peers & (lane_bit - 1)) == 0)
-            atomicAdd(&s_hist[c], (unsigned)__popcll(peers));
+            atomicAdd(&s_hist[cs[q]], (unsigned)__popcll(peers));
     }
     __syncthreads();
     for (int k = threadIdx.x; k < num_sites; k += kThreads)
@@ -735,9 +745,9 @@ __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
     for (int step = 0; step < kSteps; ++step) {
         const unsigned s = wbase + step * 64 + lane;
         in[step] = s < num_samples;
+        cs[step] = in[step] ? cell[s] : 0u;  // not gated on liveness: loads overlap
         if constexpr (LEVEL)
             in[step] = in[step] && live(s);
-        cs[step] = in[step] ? cell[s] : 0u;
     }
     __syncthreads();
     // pass 1: this wave's count per head

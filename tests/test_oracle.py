@@ -760,6 +760,13 @@ def test_culled_render_stop_rule_and_error_bound(eps, levels):
     assert (np.abs(c.opacity - full.opacity) <= bound).all()
     assert (np.abs(c.depth - full.depth) <= bound * cfg.far).all()
     np.testing.assert_allclose(c.opacity[stopped], 1.0 - T_stop[stopped], rtol=0, atol=1e-12)
+    # colour and depth: the front-to-back sum over the evaluated prefix,
+    # sum_i T_i (1 - tau_i) (c_i, t_i), from the per-sample fields
+    w = T_before[:, :-1] * (1.0 - tau)
+    keep = np.arange(n)[None, :] < want[:, None]
+    np.testing.assert_allclose(c.rgb, np.einsum("ri,ric->rc", w * keep, full.srgb),
+                               rtol=0, atol=1e-12)
+    np.testing.assert_allclose(c.depth, (w * keep * t).sum(1), rtol=0, atol=1e-11)
 
 
 def test_culled_render_with_empty_heads():

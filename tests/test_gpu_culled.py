@@ -169,6 +169,24 @@ def test_one_level_or_zero_eps_is_the_plain_render():
             label, max((a - b).abs().max().item() for a, b in zip(plain, zero[:3]))), flush=True)
 
 
+def test_single_head_has_one_level_only():
+    """K = 1: every ray is one segment, so levels 1.. are empty; the culled
+    render is derf_render bitwise and evaluates every sample, whatever eps."""
+    derf = _derf()
+    sc = _dense_tiny(K=1, bias=4.0)
+    cfg = sc.cfg
+    o, d = _rays(sc)
+    r = derf.Renderer(sc.sites, cfg.arch, sc.weights, "fp32")
+    plain = [x.cpu() for x in r.render(o, d, cfg.near, cfg.far, cfg.n_coarse, 0,
+                                       scenes.SEED_RENDER)]
+    culled = [x.cpu() for x in r.render_culled(o, d, cfg.near, cfg.far, cfg.n_coarse, 0.5, 6,
+                                               seed=scenes.SEED_RENDER)]
+    r.close()
+    for a, b in zip(plain, culled[:3]):
+        assert torch.equal(a, b)
+    assert (culled[3] == cfg.n_coarse).all()
+
+
 def test_culled_repeated_calls_and_side_stream():
     """One handle, calls with different eps and levels in turn, one on a side
     stream: the level bytes, dead marks and carried state of one call leave

@@ -64,7 +64,8 @@ def _lib_handle():
         lib.oracle_render_mixed.argtypes = lib.oracle_render_ex.argtypes
         lib.oracle_render_mixed.restype = ctypes.c_int
         lib.oracle_render_culled.argtypes = render_sig + [ctypes.c_double, ctypes.c_int,
-                                                          ctypes.c_void_p, ctypes.c_void_p]
+                                                          ctypes.c_int, ctypes.c_void_p,
+                                                          ctypes.c_void_p]
         lib.oracle_render_culled.restype = ctypes.c_int
         lib.oracle_philox4x32_10.argtypes = [_P, _P, _P]
         lib.oracle_philox4x32_10.restype = None
@@ -358,11 +359,13 @@ def render(sites, arch, weights, rays_o, rays_d, near: float, far: float, n_coar
 
 def render_culled(sites, arch, weights, rays_o, rays_d, near: float, far: float,
                   n_coarse: int, eps: float, levels: int, seed: int = 0, perturb: bool = True,
-                  ray_ids=None, empty=None, nthreads: int = 0) -> RenderResult:
+                  ray_ids=None, empty=None, nthreads: int = 0, piece: int = 0) -> RenderResult:
     """Single-pass DeRF render with Painter's-order culling (Sec. 3.3): level l
-    of a ray is its l-th segment (the last level every later one), and a ray
-    stops before level l > 0 once its transmittance is below eps.  The
-    result's ``evaluated`` holds the samples whose head ran, per ray."""
+    of a ray is its l-th piece (a segment, or with piece > 0 a part of at most
+    `piece` samples of one, cut from the segment's start; the last level takes
+    every later piece), and a ray stops before level l > 0 once its
+    transmittance is below eps.  The result's ``evaluated`` holds the samples
+    whose head ran, per ray."""
     sites = np.ascontiguousarray(sites, np.float32).reshape(-1, 3)
     weights = np.ascontiguousarray(weights, np.float32)
     o = np.ascontiguousarray(rays_o, np.float32).reshape(-1, 3)
@@ -382,7 +385,8 @@ def render_culled(sites, arch, weights, rays_o, rays_d, near: float, far: float,
     rc = _lib_handle().oracle_render_culled(
         sites.shape[0], _ptr(sites), ctypes.byref(a), _ptr(weights), R, _ptr(o), _ptr(d),
         _ptr(ids), near, far, n_coarse, 0, seed, int(perturb), _ptr(rgb), _ptr(dep), _ptr(op),
-        None, None, None, None, None, nthreads, float(eps), int(levels), _ptr(e), _ptr(ev))
+        None, None, None, None, None, nthreads, float(eps), int(levels), int(piece), _ptr(e),
+        _ptr(ev))
     if rc != 0:
         raise RuntimeError("oracle culled render failed (%d)" % rc)
     res = RenderResult(rgb, dep, op)

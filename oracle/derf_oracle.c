@@ -823,8 +823,10 @@ int oracle_render_soft_contrib(ORACLE_RENDER_ARGS, double beta, double *contrib)
 /* ------------------------------------------- Painter's-order culling ---
  * The Painter's order of Sec. 3.3 visits the segments of a ray front to
  * back, so the transmittance in front of a segment is known before its head
- * has to run.  Level l of a ray holds its segment of ordinal l along the ray
- * (the last level also every later segment).  Before level l > 0 a ray
+ * has to run.  With piece > 0 each segment is cut, from its first sample, into
+ * pieces of at most `piece` samples (piece = 0: whole segments).  Level l of a
+ * ray holds its piece of ordinal l along the ray (the last level also every
+ * later piece).  Before level l > 0 a ray
  * whose transmittance T is below eps stops: its remaining segments are not
  * evaluated.  The result is the Painter's merge of the evaluated segments
  * (a prefix of the ray).  Its colour and opacity differ from the full
@@ -834,14 +836,14 @@ int oracle_render_soft_contrib(ORACLE_RENDER_ARGS, double beta, double *contrib)
  * Single pass (n_fine = 0), one architecture for every head; empty
  * (optional [K]) marks 0-capacity heads.  evaluated (optional [R]):
  * samples whose head ran, per ray. */
-int oracle_render_culled(ORACLE_RENDER_ARGS, double eps, int levels, const unsigned char *empty,
-                         int *evaluated)
+int oracle_render_culled(ORACLE_RENDER_ARGS, double eps, int levels, int piece,
+                         const unsigned char *empty, int *evaluated)
 {
     ORACLE_FILL_ARGS
     A.empty = empty;
     (void)dbg_t; (void)dbg_cell; (void)dbg_sigma; (void)dbg_rgb; (void)dbg_margin;
     const int n = n_coarse;
-    if (n < 1 || n_fine != 0 || levels < 1 || !(eps >= 0.0) || R < 0)
+    if (n < 1 || n_fine != 0 || levels < 1 || piece < 0 || !(eps >= 0.0) || R < 0)
         return -1;
     const int P = 3 + 6 * arch->pos_freqs, Dd = 3 + 6 * arch->dir_freqs;
     const size_t scratch_len = 4 * (size_t)(P + arch->width + Dd + arch->rgb_hidden + 8);
@@ -886,11 +888,11 @@ int oracle_render_culled(ORACLE_RENDER_ARGS, double eps, int levels, const unsig
                     /* transmittance in front of this level */
                     if (level > 0 && 1.0 - op < eps)
                         break;
-                    /* this level's samples: one segment, or all that remain */
+                    /* this level's samples: one piece, or all that remain */
                     int stop = end;
                     do {
-                        const int c = cell[stop];
-                        while (stop < n && cell[stop] == c)
+                        const int first = stop, c = cell[stop];
+                        while (stop < n && cell[stop] == c && (piece == 0 || stop - first < piece))
                             ++stop;
                     } while (level == levels - 1 && stop < n);
                     for (int i = end; i < stop; ++i) {

@@ -715,19 +715,21 @@ def test_culled_render_without_culling_is_the_full_render():
     ids = np.arange(0, cfg.num_rays, 5)
     full = oracle.render(sc.sites, cfg.arch, sc.weights, sc.rays_o[ids], sc.rays_d[ids], cfg.near,
                          cfg.far, cfg.n_coarse, seed=3, ray_ids=ids)
-    for eps, levels in ((0.0, 5), (0.0, 32), (0.5, 1)):
-        c = _culled(cfg, sc, ids, eps, levels)
+    for eps, levels, piece in ((0.0, 5, 0), (0.0, 32, 0), (0.5, 1, 0), (0.0, 9, 7), (0.5, 1, 3)):
+        c = _culled(cfg, sc, ids, eps, levels, piece=piece)
         for x, y in ((c.rgb, full.rgb), (c.depth, full.depth), (c.opacity, full.opacity)):
             np.testing.assert_array_equal(x, y)
         assert (c.evaluated == cfg.n_coarse).all()
 
 
-@pytest.mark.parametrize("eps,levels", [(1e-3, 4), (1e-2, 3), (0.2, 8)])
-def test_culled_render_stop_rule_and_error_bound(eps, levels):
+@pytest.mark.parametrize("eps,levels,piece", [(1e-3, 4, 0), (1e-2, 3, 0), (0.2, 8, 0),
+                                              (1e-3, 4, 5), (1e-2, 6, 3), (1e-3, 4, 100)])
+def test_culled_render_stop_rule_and_error_bound(eps, levels, piece):
     """The stop rule rebuilt from the full render's per-sample fields: the
     segments (runs of one cell), the transmittance in front of each sample
     (product of exp(-sigma delta) over the samples before it, midpoint
-    intervals), the level starts (segment l; the last level takes the rest)
+    intervals), the level starts (piece l: a segment, cut every `piece`
+    samples from its start when piece > 0; the last level takes the rest)
     and the first level l > 0 whose transmittance is below eps.  The culled
     render evaluates exactly the samples before that level; its colour and
     opacity differ from the full render's by at most the transmittance there,
@@ -736,7 +738,7 @@ def test_culled_render_stop_rule_and_error_bound(eps, levels):
     ids = np.arange(0, cfg.num_rays, 3)
     full = oracle.render(sc.sites, cfg.arch, sc.weights, sc.rays_o[ids], sc.rays_d[ids], cfg.near,
                          cfg.far, cfg.n_coarse, seed=3, ray_ids=ids, per_sample=True)
-    c = _culled(cfg, sc, ids, eps, levels)
+    c = _culled(cfg, sc, ids, eps, levels, piece=piece)
     n = cfg.n_coarse
     t = full.t.astype(np.float64)
     b = np.concatenate([np.full((len(ids), 1), cfg.near), 0.5 * (t[:, 1:] + t[:, :-1]),
@@ -746,7 +748,12 @@ def test_culled_render_stop_rule_and_error_bound(eps, levels):
     want = np.full(len(ids), n)
     T_stop = np.zeros(len(ids))
     for r in range(len(ids)):
-        starts = [0] + [i for i in range(1, n) if full.cell[r, i] != full.cell[r, i - 1]]
+        starts, seg0 = [], 0
+        for i in range(n):
+            if i > 0 and full.cell[r, i] != full.cell[r, i - 1]:
+                seg0 = i
+            if i == seg0 or (piece and (i - seg0) % piece == 0):
+                starts.append(i)
         for l in range(1, min(levels, len(starts))):
             if T_before[r, starts[l]] < eps:
                 want[r] = starts[l]

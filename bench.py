@@ -129,9 +129,10 @@ def main():
     ap.add_argument("--soft", type=float, default=None, metavar="BETA",
                     help="also time the soft decomposition (every head on every sample) at "
                          "temperature BETA, with the per-ray head contributions")
-    ap.add_argument("--cull", default=None, metavar="EPS[,LEVELS]",
+    ap.add_argument("--cull", default=None, metavar="EPS[,LEVELS[,PIECE]]",
                     help="also time the Painter's-order render with transmittance culling "
-                         "(stop below transmittance EPS, LEVELS segment levels, default 4)")
+                         "(stop below transmittance EPS, LEVELS levels, default 4; segments "
+                         "cut into pieces of at most PIECE samples, default 0: whole)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (to scale HBM counters)")
     args = ap.parse_args()
@@ -236,7 +237,7 @@ def main():
         r.close()
         return elapsed * 1e3 / steps, stages
 
-    def run_culled(cfg, eps, levels, steps, warmup, ref_out):
+    def run_culled(cfg, eps, levels, piece, steps, warmup, ref_out):
         """Time `steps` culled renders; evaluated samples and the largest
         difference from the plain render's outputs ref_out."""
         sc = scenes.make_scene(cfg)
@@ -245,7 +246,7 @@ def main():
         r = derf.Renderer(sc.sites, cfg.arch, sc.weights, precision)
         for _ in range(warmup):
             out = r.render_culled(o, d, cfg.near, cfg.far, cfg.n_coarse, eps, levels,
-                                  scenes.SEED_RENDER)
+                                  scenes.SEED_RENDER, piece=piece)
         torch.cuda.synchronize()
         derf.derf_reset_stats(r.handle)
         derf.derf_set_timing(r.handle, True)
@@ -253,7 +254,7 @@ def main():
         t0 = time.perf_counter()
         for _ in range(steps):
             out = r.render_culled(o, d, cfg.near, cfg.far, cfg.n_coarse, eps, levels,
-                                  scenes.SEED_RENDER)
+                                  scenes.SEED_RENDER, piece=piece)
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t0
         st = derf.derf_get_stats(r.handle)
@@ -324,14 +325,15 @@ def main():
             raise SystemExit("--cull needs a single-pass workload with one architecture")
         parts = args.cull.split(",")
         eps, levels = float(parts[0]), int(parts[1]) if len(parts) > 1 else 4
-        ms_c, st_c, ev_c, diff_c = run_culled(cfg, eps, levels, args.steps, 2, plain_out)
-        culled = {"eps": eps, "levels": levels, "rays_per_s": R / (ms_c * 1e-3),
+        piece = int(parts[2]) if len(parts) > 2 else 0
+        ms_c, st_c, ev_c, diff_c = run_culled(cfg, eps, levels, piece, args.steps, 2, plain_out)
+        culled = {"eps": eps, "levels": levels, "piece": piece, "rays_per_s": R / (ms_c * 1e-3),
                   "ms_per_step": ms_c, "speedup_vs_plain": ms_per_step / ms_c,
                   "evaluated_samples": ev_c, "evaluated_frac": ev_c / S,
                   "level_loop_ms": st_c.get("mlp"), "sample_ms": st_c.get("sample_assign"),
                   "max_abs_diff_vs_plain": diff_c}
-        log("bench: culled eps=%g levels=%d %.4g rays/s (%.3f of samples evaluated)"
-            % (eps, levels, culled["rays_per_s"], culled["evaluated_frac"]))
+        log("bench: culled eps=%g levels=%d piece=%d %.4g rays/s (%.3f of samples evaluated)"
+            % (eps, levels, piece, culled["rays_per_s"], culled["evaluated_frac"]))
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -207,17 +207,22 @@ int derf_render_soft(derf_handle *h, const float *rays_o, const float *rays_d, l
 
 /* derf_render with the Painter's order put to work (Sec. 3.3: a ray meets its
  * cells in order of distance from its origin, and composites its segments
- * front to back): the segments are evaluated level by level, level l of a
- * ray being its segment of ordinal l along the ray (level levels - 1: every
- * later segment), and a ray whose transmittance in front of level l > 0 is
+ * front to back): the ray's pieces are evaluated level by level, level l of a
+ * ray being its piece of ordinal l along the ray (level levels - 1: every
+ * later piece), and a ray whose transmittance in front of level l > 0 is
  * below eps skips that level and every later one -- its heads do not run
- * there.  The result is the Painter's merge of the evaluated segments: colour
+ * there.  A piece is a segment or, with piece > 0, a part of at most piece
+ * samples of one, cut from the segment's first sample (the merge of a
+ * segment's pieces front to back is the segment's own, since "over" is
+ * associative; cutting only adds places where a ray can stop, which matters
+ * when a ray crosses few cells).  The result is the Painter's merge of the evaluated segments: colour
  * and opacity within eps of derf_render's (colours lie in [0, 1]), depth
  * within eps * far.  With levels = 1 or eps = 0 nothing is skipped and the
  * outputs equal derf_render's.
  *   eps            finite, >= 0: the transmittance below which a ray stops
- *   levels         1 .. 32: segment levels (one bucketing, MLP and
- *                  integration pass each)
+ *   levels         1 .. 32: levels (one bucketing, MLP and integration pass
+ *                  each)
+ *   piece          >= 0: the most samples of one piece; 0: whole segments
  *   out_evaluated  NULL, or device unsigned [R]: samples whose head ran, per
  *                  ray
  * Other arguments and limits as derf_render; samp->n_fine must be 0
@@ -226,7 +231,7 @@ int derf_render_soft(derf_handle *h, const float *rays_o, const float *rays_d, l
  * level loop); head_samples sums every level's evaluations. */
 int derf_render_culled(derf_handle *h, const float *rays_o, const float *rays_d,
                        long long num_rays, float near_t, float far_t, const derf_sampling *samp,
-                       float eps, int levels, float *out_rgb, float *out_depth,
+                       float eps, int levels, int piece, float *out_rgb, float *out_depth,
                        float *out_opacity, unsigned *out_evaluated, void *hip_stream);
 
 /* Per-stage GPU time, recorded with HIP events on the render's stream when

@@ -571,7 +571,7 @@ size_t layout_culled(char *base, unsigned S, unsigned R, unsigned nblk, int K, b
 // offsets, scatter, the grouped MLP and the level's integration.
 int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
                        long long num_rays, float near_t, float far_t, const derf_sampling *samp,
-                       float eps, int levels, float *out_rgb, float *out_depth,
+                       float eps, int levels, int piece, float *out_rgb, float *out_depth,
                        float *out_opacity, unsigned *out_evaluated, void *stream)
 {
     if (!h)
@@ -586,6 +586,8 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
         return fail(DERF_ERR_INVALID_ARG, "need a finite eps >= 0");
     if (levels < 1 || levels > kMaxLevels)
         return fail(DERF_ERR_INVALID_ARG, "need 1 <= levels <= %d", kMaxLevels);
+    if (piece < 0)
+        return fail(DERF_ERR_INVALID_ARG, "need piece >= 0");
     if (samp->n_coarse < 1 || samp->n_coarse > 1024 || samp->n_fine < 0)
         return fail(DERF_ERR_INVALID_ARG, "need 1 <= n_coarse <= 1024, n_fine >= 0");
     if (samp->n_fine != 0)
@@ -642,7 +644,7 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     HIP_TRY(launch_sample_assign(g, h->sites, K, h->site_bits, walk, b.t, b.cell, b.counts, nblk,
                                  s),
             "sample_assign launch");
-    HIP_TRY(launch_level_bounds(b.cell, N, R, L, c.lb, c.lvl, s), "level_bounds launch");
+    HIP_TRY(launch_level_bounds(b.cell, N, R, L, (unsigned)piece, c.lb, c.lvl, s), "level_bounds launch");
     HIP_TRY(mark(DERF_STAGE_SAMPLE, 1), "hipEventRecord");
     HIP_TRY(mark(DERF_STAGE_MLP, 0), "hipEventRecord");
     for (unsigned l = 0; l < L; ++l) {
@@ -844,11 +846,11 @@ int derf_render_soft(derf_handle *h, const float *rays_o, const float *rays_d, l
 
 int derf_render_culled(derf_handle *h, const float *rays_o, const float *rays_d,
                        long long num_rays, float near_t, float far_t, const derf_sampling *samp,
-                       float eps, int levels, float *out_rgb, float *out_depth,
+                       float eps, int levels, int piece, float *out_rgb, float *out_depth,
                        float *out_opacity, unsigned *out_evaluated, void *hip_stream)
 {
     return render_culled_impl(h, rays_o, rays_d, num_rays, near_t, far_t, samp, eps, levels,
-                              out_rgb, out_depth, out_opacity, out_evaluated, hip_stream);
+                              piece, out_rgb, out_depth, out_opacity, out_evaluated, hip_stream);
 }
 
 int derf_set_empty_heads(derf_handle *h, const int *flags)

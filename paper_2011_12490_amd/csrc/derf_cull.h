@@ -7,8 +7,9 @@
 
 namespace derf {
 
-// Level l of a ray is its segment of ordinal l along the ray (the last level:
-// every later segment).  lb [R][levels + 1]: the first sample of each level
+// Level l of a ray is its piece of ordinal l along the ray (the last level:
+// every later piece); a piece is a segment, or with piece > 0 a part of at
+// most piece samples of one, cut from the segment's start.  lb [R][levels + 1]: the first sample of each level
 // (lb[r][levels] = n).  lvl [S]: each sample's level; the level composite that
 // closes a ray (its transmittance below eps) marks the ray's later samples
 // dead.  trans [R]: the transmittance in front of the level, written by each
@@ -24,7 +25,8 @@ struct CullLevel {
 };
 constexpr int kMaxLevels = 32;
 hipError_t launch_level_bounds(const uint8_t *cell, unsigned n, unsigned num_rays,
-                               unsigned levels, unsigned *lb, uint8_t *lvl, hipStream_t s);
+                               unsigned levels, unsigned piece, unsigned *lb, uint8_t *lvl,
+                               hipStream_t s);
 // per-block head counts of the samples live at the level (the layout of the
 // assignment's counts)
 hipError_t launch_level_count(const RenderGeometry &g, const uint8_t *cell, int num_sites,

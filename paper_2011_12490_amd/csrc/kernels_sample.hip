@@ -631,14 +631,17 @@ struct LevelLive {
 };
 
 // Level bounds, one wave per ray, 64 samples per step.  A sample opens a
-// segment when its cell differs from the previous sample's; its segment
-// ordinal is the number of such changes up to it.  Each sample's level,
-// min(ordinal, levels - 1), goes to lvl; lane j (1 <= j < levels) records
-// where the j-th change is (the start of segment j), taking the
-// (j - seen)-th set bit of the step's change ballot.
+// segment when its cell differs from the previous sample's.  With piece > 0 a
+// sample also opens a piece when it lies a multiple of piece samples past the
+// start of its segment (its last change at or before it, carried across
+// steps), so a segment is cut from its start into parts of at most piece
+// samples.  A sample's ordinal is the number of openings up to it; its level,
+// min(ordinal, levels - 1), goes to lvl, and lane j (1 <= j < levels) records
+// where the j-th opening is (the start of piece j), taking the (j - seen)-th
+// set bit of the step's opening ballot.
 __global__ __launch_bounds__(kThreads) void level_bounds_kernel(const uint8_t *__restrict__ cell,
                                                                unsigned n, unsigned num_rays,
-                                                               unsigned levels,
+                                                               unsigned levels, unsigned piece,
                                                                unsigned *__restrict__ lb,
                                                                uint8_t *__restrict__ lvl)
 {
@@ -649,11 +652,20 @@ __global__ __launch_bounds__(kThreads) void level_bounds_kernel(const uint8_t *_
     const size_t base = (size_t)ray * n;
     const uint64_t upto = ~0ull >> (63 - lane);  // lanes 0 .. lane
     unsigned mine = n;  // start of level `lane`
-    unsigned seen = 0;  // changes before this step (wave-uniform)
+    unsigned seen = 0;  // openings before this step (wave-uniform)
+    unsigned seg0 = 0;  // start of the segment open at the step's first sample (wave-uniform)
     for (unsigned c0 = 0; c0 < n; c0 += 64) {
         const unsigned i = c0 + lane;
         const bool change = i > 0 && i < n && cell[base + i] != cell[base + i - 1];
-        const uint64_t m = __ballot(change);
+        uint64_t m = __ballot(change);
+        if (piece > 0) {
+            const uint64_t before = m & upto;
+            const unsigned start = before ? c0 + 63u - (unsigned)__builtin_clzll(before) : seg0;
+            if (m)
+                seg0 = c0 + 63u - (unsigned)__builtin_clzll(m);
+            // a change is at its own segment start, so it opens a piece too
+            m = __ballot(i > 0 && i < n && (i - start) % piece == 0);
+        }
         const unsigned cnt = (unsigned)__popcll(m);
         if (lane < levels && lane > seen && lane <= seen + cnt) {
             uint64_t mm = m;
@@ -1025,10 +1037,11 @@ hipError_t launch_composite(const RenderGeometry &g, const float *t, const uint8
 }
 
 hipError_t launch_level_bounds(const uint8_t *cell, unsigned n, unsigned num_rays,
-                               unsigned levels, unsigned *lb, uint8_t *lvl, hipStream_t s)
+                               unsigned levels, unsigned piece, unsigned *lb, uint8_t *lvl,
+                               hipStream_t s)
 {
-    level_bounds_kernel<<<blocks_for(num_rays, kThreads / 64), kThreads, 0, s>>>(cell, n, num_rays,
-                                                                                 levels, lb, lvl);
+    level_bounds_kernel<<<blocks_for(num_rays, kThreads / 64), kThreads, 0, s>>>(
+        cell, n, num_rays, levels, piece, lb, lvl);
     return hipGetLastError();
 }
 

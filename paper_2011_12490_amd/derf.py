@@ -93,7 +93,8 @@ def lib() -> ctypes.CDLL:
         L.derf_render_soft.restype = ctypes.c_int
         L.derf_render_culled.argtypes = [P, P, P, ctypes.c_longlong, ctypes.c_float,
                                          ctypes.c_float, ctypes.POINTER(derf_sampling),
-                                         ctypes.c_float, ctypes.c_int, P, P, P, P, P]
+                                         ctypes.c_float, ctypes.c_int, ctypes.c_int, P, P, P,
+                                         P, P]
         L.derf_render_culled.restype = ctypes.c_int
         L.derf_set_empty_heads.argtypes = [P, P]
         L.derf_set_empty_heads.restype = ctypes.c_int
@@ -200,14 +201,16 @@ def derf_render_soft(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float,
 def derf_render_culled(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far: float,
                        samp: derf_sampling, eps: float, levels: int, out_rgb: torch.Tensor,
                        out_depth: torch.Tensor, out_opacity: torch.Tensor,
-                       out_evaluated: Optional[torch.Tensor] = None, stream=None):
+                       out_evaluated: Optional[torch.Tensor] = None, stream=None,
+                       piece: int = 0):
     """Enqueue a Painter's-order render with transmittance culling on `stream`
-    (default: torch's current stream).  out_evaluated: int32 [R] or None."""
+    (default: torch's current stream).  out_evaluated: int32 [R] or None;
+    piece: the most samples of one piece (0: whole segments)."""
     if stream is None:
         stream = torch.cuda.current_stream()
     sp = ctypes.c_void_p(stream.cuda_stream)
     _check(lib().derf_render_culled(h, _dptr(rays_o), _dptr(rays_d), rays_o.shape[0], near, far,
-                                    ctypes.byref(samp), eps, levels, _dptr(out_rgb),
+                                    ctypes.byref(samp), eps, levels, piece, _dptr(out_rgb),
                                     _dptr(out_depth), _dptr(out_opacity),
                                     None if out_evaluated is None else _dptr(out_evaluated), sp),
            "derf_render_culled")
@@ -322,9 +325,10 @@ class Renderer:
 
     def render_culled(self, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far: float,
                       n: int, eps: float, levels: int, seed: int = 0, perturb: bool = True,
-                      stream=None, ray_offset: int = 0):
+                      stream=None, ray_offset: int = 0, piece: int = 0):
         """Single-pass render in Painter's order with transmittance culling;
-        returns (rgb, depth, opacity, evaluated samples per ray)."""
+        returns (rgb, depth, opacity, evaluated samples per ray).  piece > 0
+        cuts segments into pieces of at most that many samples."""
         assert rays_o.is_cuda and rays_o.dtype == torch.float32 and rays_o.is_contiguous()
         assert rays_d.is_cuda and rays_d.dtype == torch.float32 and rays_d.is_contiguous()
         R = rays_o.shape[0]
@@ -335,5 +339,5 @@ class Renderer:
         ev = torch.empty((R,), dtype=torch.int32, device=dev)
         samp = derf_sampling(n, 0, seed, int(perturb), ray_offset)
         derf_render_culled(self.handle, rays_o, rays_d, near, far, samp, eps, levels, rgb, depth,
-                           opac, ev, stream)
+                           opac, ev, stream, piece)
         return rgb, depth, opac, ev

@@ -122,8 +122,8 @@ def test_mixed_create_soft_culled_render_and_empty_heads_reject_bad_arguments_wi
     samp = derf.derf_sampling(32, 0, 1, 1, 0)
     assert L.derf_render_soft(None, None, None, 1, 2.0, 6.0, ctypes.byref(samp), 1.0, None, None,
                               None, None, None) == derf.DERF_ERR_INVALID_ARG
-    assert L.derf_render_culled(None, None, None, 1, 2.0, 6.0, ctypes.byref(samp), 1e-3, 4, None,
-                                None, None, None, None) == derf.DERF_ERR_INVALID_ARG
+    assert L.derf_render_culled(None, None, None, 1, 2.0, 6.0, ctypes.byref(samp), 1e-3, 4, 0,
+                                None, None, None, None, None) == derf.DERF_ERR_INVALID_ARG
 
 
 def test_status_strings():

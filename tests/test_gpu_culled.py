@@ -43,7 +43,7 @@ def _rays(sc):
     return torch.from_numpy(sc.rays_o).cuda(), torch.from_numpy(sc.rays_d).cuda()
 
 
-def _gpu_culled(sc, precision, eps, levels, empty=None, arch=None, weights=None):
+def _gpu_culled(sc, precision, eps, levels, empty=None, arch=None, weights=None, piece=0):
     derf = _derf()
     cfg = sc.cfg
     o, d = _rays(sc)
@@ -52,7 +52,7 @@ def _gpu_culled(sc, precision, eps, levels, empty=None, arch=None, weights=None)
     if empty is not None:
         r.set_empty_heads(list(empty))
     out = r.render_culled(o, d, cfg.near, cfg.far, cfg.n_coarse, eps, levels,
-                          seed=scenes.SEED_RENDER)
+                          seed=scenes.SEED_RENDER, piece=piece)
     torch.cuda.synchronize()
     st = derf.derf_get_stats(r.handle)
     r.close()
@@ -61,12 +61,12 @@ def _gpu_culled(sc, precision, eps, levels, empty=None, arch=None, weights=None)
     return rgb, depth, opac, ev
 
 
-def _check(gpu, sc, ids, eps, levels, precision, label, empty=None):
+def _check(gpu, sc, ids, eps, levels, precision, label, empty=None, piece=0):
     cfg = sc.cfg
     args = (sc.sites, cfg.arch, sc.weights, sc.rays_o[ids], sc.rays_d[ids], cfg.near, cfg.far,
             cfg.n_coarse)
     ref = oracle.render_culled(*args, eps, levels, seed=scenes.SEED_RENDER, ray_ids=ids,
-                               empty=empty, nthreads=NTHREADS)
+                               empty=empty, nthreads=NTHREADS, piece=piece)
     full = oracle.render(*args, seed=scenes.SEED_RENDER, ray_ids=ids, empty=empty,
                          nthreads=NTHREADS)
     rgb, depth, opac, ev = gpu[0][ids], gpu[1][ids], gpu[2][ids], gpu[3][ids]
@@ -127,6 +127,44 @@ def test_culled_dense_headline_frame_bf16():
     assert gpu[3].sum() < 0.8 * cfg.num_rays * cfg.n_coarse
     _check(gpu, sc, scenes.ray_subset(256, cfg.num_rays), 1e-3, 4, "bf16",
            "culled dense_k16 bf16")
+
+
+@pytest.mark.parametrize("piece,levels,n", [(5, 6, 32), (1, 32, 32), (3, 32, 7), (7, 12, 300),
+                                            (70, 6, 600)])
+def test_culled_pieces_fp32(piece, levels, n):
+    """Segments cut into pieces of at most `piece` samples (levels count
+    pieces): piece ends inside and across the 64-sample steps of the level
+    bounds and the 256-sample staging chunks of the level composite."""
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], num_sites=8, sigma_bias=4.0, n_coarse=n)
+    sc = scenes.make_scene(cfg)
+    gpu = _gpu_culled(sc, "fp32", 1e-3, levels, piece=piece)
+    ids = np.arange(0, cfg.num_rays, 1 if n <= 32 else 4)
+    _check(gpu, sc, ids, 1e-3, levels, "fp32", "culled tiny n=%d piece=%d L=%d"
+           % (n, piece, levels), piece=piece)
+
+
+def test_culled_pieces_single_head_fp32():
+    """K = 1: one segment per ray, so only pieces give a ray places to stop."""
+    sc = _dense_tiny(K=1, bias=4.0)
+    whole = _gpu_culled(sc, "fp32", 1e-3, 8)
+    assert np.all(whole[3] == sc.cfg.n_coarse)
+    gpu = _gpu_culled(sc, "fp32", 1e-3, 8, piece=4)
+    assert gpu[3].sum() < whole[3].sum()
+    _check(gpu, sc, np.arange(sc.cfg.num_rays), 1e-3, 8, "fp32", "culled tiny K=1 piece=4",
+           piece=4)
+
+
+def test_culled_pieces_no_cut_and_zero_eps():
+    """A piece no shorter than the ray is the whole-segment render, bitwise;
+    eps = 0 with pieces evaluates every sample."""
+    sc = _dense_tiny()
+    n = sc.cfg.n_coarse
+    base = _gpu_culled(sc, "fp32", 1e-3, 6)
+    long_piece = _gpu_culled(sc, "fp32", 1e-3, 6, piece=n)
+    for a, b in zip(base, long_piece):
+        assert np.array_equal(a, b)
+    zero = _gpu_culled(sc, "fp32", 0.0, 16, piece=3)
+    assert np.all(zero[3] == n)
 
 
 @pytest.mark.parametrize("n", [1, 7, 65, 300, 600])
@@ -223,9 +261,11 @@ def test_culled_argument_errors():
                                 1e-3, 4, *out)
     assert e.value.status == derf.DERF_ERR_UNSUPPORTED
     samp = derf.derf_sampling(16, 0, 1, 1, 0)
-    for eps, levels in ((-1.0, 4), (float("inf"), 4), (float("nan"), 4), (1e-3, 0), (1e-3, 33)):
+    for eps, levels, piece in ((-1.0, 4, 0), (float("inf"), 4, 0), (float("nan"), 4, 0),
+                               (1e-3, 0, 0), (1e-3, 33, 0), (1e-3, 4, -1)):
         with pytest.raises(derf.DerfError) as e:
-            derf.derf_render_culled(r.handle, o, d, cfg.near, cfg.far, samp, eps, levels, *out)
+            derf.derf_render_culled(r.handle, o, d, cfg.near, cfg.far, samp, eps, levels, *out,
+                                    piece=piece)
         assert e.value.status == derf.DERF_ERR_INVALID_ARG
     derf.derf_render_culled(r.handle, o[:0], d[:0], cfg.near, cfg.far, samp, 1e-3, 4, *out)
     torch.cuda.synchronize()

@@ -129,6 +129,9 @@ def main():
     ap.add_argument("--soft", type=float, default=None, metavar="BETA",
                     help="also time the soft decomposition (every head on every sample) at "
                          "temperature BETA, with the per-ray head contributions")
+    ap.add_argument("--gate", type=int, default=0, metavar="H",
+                    help="also time the MLP-gating decomposition with a seeded gate of H "
+                         "hidden units (16, 32 or 64) on the heads' position encoding")
     ap.add_argument("--cull", default=None, metavar="EPS[,LEVELS[,PIECE]]",
                     help="also time the Painter's-order render with transmittance culling "
                          "(stop below transmittance EPS, LEVELS levels, default 4; segments "
@@ -267,6 +270,40 @@ def main():
         r.close()
         return elapsed * 1e3 / steps, stages, evaluated, diff
 
+    def run_gated(cfg, hidden, steps, warmup):
+        """Time `steps` renders with the MLP-gating assignment (a seeded
+        random gate on the heads' encoding; head evaluations per head and the
+        mean number of one-head runs per ray come back too)."""
+        sc = scenes.make_scene(cfg)
+        o = torch.from_numpy(sc.rays_o).cuda()
+        d = torch.from_numpy(sc.rays_d).cuda()
+        L = cfg.arch.pos_freqs
+        rng = np.random.Generator(np.random.PCG64(scenes.S0 + 9))
+        count = derf.lib().derf_gate_weights_count(cfg.num_sites, L, hidden)
+        gw = (rng.uniform(-1.0, 1.0, count) * 4.0 / np.sqrt(3 + 6 * L)).astype(np.float32)
+        r = derf.Renderer(sc.sites, cfg.arch, sc.weights, precision)
+        r.set_gate(L, hidden, gw)
+        for _ in range(warmup):
+            r.render_gated(o, d, cfg.near, cfg.far, cfg.n_coarse, scenes.SEED_RENDER)
+        torch.cuda.synchronize()
+        derf.derf_reset_stats(r.handle)
+        derf.derf_set_timing(r.handle, True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            r.render_gated(o, d, cfg.near, cfg.far, cfg.n_coarse, scenes.SEED_RENDER)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        st = derf.derf_get_stats(r.handle)
+        stages = {name: st.stage_ms[i] / max(1, st.stage_launches[i])
+                  for i, name in enumerate(derf.STAGE_NAMES) if st.stage_launches[i]}
+        cell = r.render_gated(o, d, cfg.near, cfg.far, cfg.n_coarse, scenes.SEED_RENDER,
+                              cells=True)[3]
+        runs = float(((cell[:, 1:] != cell[:, :-1]).sum(1) + 1).double().mean().item())
+        heads_g = [int(st.head_samples[k]) for k in range(cfg.num_sites)]
+        r.close()
+        return elapsed * 1e3 / steps, stages, runs, heads_g
+
     sc, ms_per_step, stage_ms, heads = run(cfg, args.steps, args.warmup, args.copy_calibration)
     plain_out = None
     if args.cull:
@@ -335,6 +372,20 @@ def main():
         log("bench: culled eps=%g levels=%d piece=%d %.4g rays/s (%.3f of samples evaluated)"
             % (eps, levels, piece, culled["rays_per_s"], culled["evaluated_frac"]))
 
+    gated = None
+    if args.gate:
+        if cfg.n_fine or head_archs or empty_heads:
+            raise SystemExit("--gate needs a single-pass workload with one architecture")
+        ms_g, st_g, runs_g, heads_g = run_gated(cfg, args.gate, args.steps, 2)
+        gated = {"hidden": args.gate, "gate_input": "gamma_%d(x)" % cfg.arch.pos_freqs,
+                 "rays_per_s": R / (ms_g * 1e-3), "ms_per_step": ms_g,
+                 "vs_voronoi": ms_per_step / ms_g, "runs_per_ray": runs_g,
+                 "sample_gate_ms": st_g.get("sample_assign"), "mlp_ms": st_g.get("mlp"),
+                 "composite_ms": st_g.get("composite"),
+                 "head_samples": {"min": min(heads_g), "max": max(heads_g)}}
+        log("bench: gated H=%d %.4g rays/s (%.2f runs per ray)"
+            % (args.gate, gated["rays_per_s"], runs_g))
+
     cpu = None
     if not args.no_cpu_baseline:
         nthreads = min(16, len(os.sched_getaffinity(0)))
@@ -382,6 +433,8 @@ def main():
         res["soft"] = soft
     if culled is not None:
         res["culled"] = culled
+    if gated is not None:
+        res["gated"] = gated
     print(json.dumps(res))
 
 

@@ -24,6 +24,8 @@
  *   derf_render_culled  derf_render in Painter's order with transmittance
  *                 culling: a ray's later segments are not evaluated once
  *                 it is nearly opaque                       (Sec. 3.3)
+ *   derf_set_gate / derf_render_gated  the MLP-gating decomposition:
+ *                 a small network picks each sample's head      (Sec. 4)
  *
  * All functions return a derf_status (0 on success, negative on error),
  * never abort and never print.  derf_last_error() returns a thread-local
@@ -233,6 +235,34 @@ int derf_render_culled(derf_handle *h, const float *rays_o, const float *rays_d,
                        long long num_rays, float near_t, float far_t, const derf_sampling *samp,
                        float eps, int levels, int piece, float *out_rgb, float *out_depth,
                        float *out_opacity, unsigned *out_evaluated, void *hip_stream);
+
+/* The MLP-gating decomposition (Sec. 4, decompositions with MLPs): instead of
+ * the nearest site, a small network with a softmax output assigns each
+ * sample to a head, the one of largest weight.  The softmax is monotone, so
+ * that is the argmax of the logits (ties to the lowest index):
+ *   h = ReLU(W1 gamma_L(x) + b1),  logits = W2 h + b2  (K logits)
+ * gamma_L is the positional encoding of the heads (p, then sin and cos of
+ * pi 2^l p for l < L), evaluated in fp32.  Gated cells need not be convex, so
+ * a ray may enter one cell several times; its runs are merged front to back,
+ * which is exact for any partition.
+ * derf_set_gate copies the host weights, fp32, packed W1 [H][3 + 6L], b1 [H],
+ * W2 [K][H], b2 [K] (derf_gate_weights_count floats), to the device; the
+ * caller may free them on return.  pos_freqs 6 or 10 and hidden 16, 32 or 64
+ * have kernels (DERF_ERR_UNSUPPORTED otherwise); hidden = 0 removes the gate.
+ * Non-finite weights: DERF_ERR_INVALID_ARG.  Waits for the handle's last
+ * stream before replacing a gate. */
+int derf_set_gate(derf_handle *h, int pos_freqs, int hidden, const float *weights);
+/* floats of a gating network for K heads; -1 for invalid values */
+long long derf_gate_weights_count(int num_sites, int pos_freqs, int hidden);
+/* derf_render with the gated assignment: samples, gating, per-head buckets,
+ * the grouped MLP and front-to-back integration of the runs.  Arguments,
+ * limits and ownership as derf_render (single pass: samp->n_fine must be 0,
+ * DERF_ERR_UNSUPPORTED otherwise); DERF_ERR_INVALID_ARG without a gate.
+ *   out_cell   NULL, or device int32 [R][N]: each sample's gated head */
+int derf_render_gated(derf_handle *h, const float *rays_o, const float *rays_d,
+                      long long num_rays, float near_t, float far_t, const derf_sampling *samp,
+                      float *out_rgb, float *out_depth, float *out_opacity, int *out_cell,
+                      void *hip_stream);
 
 /* Per-stage GPU time, recorded with HIP events on the render's stream when
  * timing is on (derf_set_timing); accumulated over renders since the last

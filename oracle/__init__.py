@@ -392,3 +392,97 @@ def render_culled(sites, arch, weights, rays_o, rays_d, near: float, far: float,
     res = RenderResult(rgb, dep, op)
     res.evaluated = ev
     return res
+
+
+# ---------------------------------------------------------------- MLP gating
+# The decomposition network of Sec. 4 ("Decompositions with MLPs"): an MLP
+# with a softmax output gives each point its head weights; at inference a
+# sample belongs to the head of largest weight, which (the softmax being
+# monotone) is the argmax of the logits.  The paper fixes neither the
+# network's size nor its input; the reading here is one ReLU hidden layer of
+# H units on the heads' positional encoding gamma_L(x):
+#   h = max(0, W1 gamma_L(x) + b1),  logits = W2 h + b2.
+# Weights, fp32, packed W1 [H][3 + 6L], b1 [H], W2 [K][H], b2 [K].  The
+# decision is taken in fp32, the precision of the GPU kernel; ties go to the
+# lowest index, as for the nearest site.
+
+def gate_weights_count(num_sites: int, L: int, hidden: int) -> int:
+    return hidden * (3 + 6 * L) + hidden + num_sites * hidden + num_sites
+
+
+def _gate_unpack(num_sites: int, L: int, hidden: int, w):
+    P = 3 + 6 * L
+    w = np.ascontiguousarray(w, np.float32).ravel()
+    if w.size != gate_weights_count(num_sites, L, hidden):
+        raise ValueError("gating weights: expected %d floats, got %d"
+                         % (gate_weights_count(num_sites, L, hidden), w.size))
+    W1 = w[:hidden * P].reshape(hidden, P)
+    b1 = w[hidden * P:hidden * P + hidden]
+    o = hidden * P + hidden
+    W2 = w[o:o + num_sites * hidden].reshape(num_sites, hidden)
+    b2 = w[o + num_sites * hidden:]
+    return W1, b1, W2, b2
+
+
+def gate_logits(num_sites: int, L: int, hidden: int, w, x) -> np.ndarray:
+    """Logits [M, K] (float32) of the gating network at points x [M, 3]."""
+    W1, b1, W2, b2 = _gate_unpack(num_sites, L, hidden, w)
+    x = np.asarray(x, np.float32).reshape(-1, 3)
+    g = np.stack([posenc(L, xi) for xi in x]).astype(np.float32) if len(x) else \
+        np.zeros((0, 3 + 6 * L), np.float32)
+    h = np.maximum(g @ W1.T + b1, np.float32(0.0)).astype(np.float32)
+    return (h @ W2.T + b2).astype(np.float32)
+
+
+def gate_assign(num_sites: int, L: int, hidden: int, w, x):
+    """(cells [M], gap [M]): each point's gated head (first largest logit)
+    and the difference of its two largest logits (inf for one head), which
+    says how close the decision is to a tie."""
+    z = gate_logits(num_sites, L, hidden, w, x)
+    cells = np.argmax(z, axis=1).astype(np.int32)
+    if num_sites == 1:
+        return cells, np.full(len(cells), np.inf)
+    top2 = np.sort(z.astype(np.float64), axis=1)[:, -2:]
+    return cells, top2[:, 1] - top2[:, 0]
+
+
+def _fma32(a, b, c):
+    """fp32 fused multiply-add (the product of two floats is exact in fp64)."""
+    return (np.float64(a) * np.float64(b) + np.float64(c)).astype(np.float32)
+
+
+def render_gated(arch, weights, num_sites: int, gate_L: int, gate_hidden: int, gate_w, rays_o,
+                 rays_d, near: float, far: float, n: int, seed: int = 0, perturb: bool = True,
+                 ray_ids=None) -> RenderResult:
+    """Single-pass render with the gated assignment, ray by ray: stratified
+    depths, x = o + t d, the gated head of each sample, that head's network,
+    quadrature, and the front-to-back merge of the ray's runs of one head
+    (a gated cell may be entered more than once).  Pure Python per sample:
+    small inputs only.  The result also holds t, cell and gap [R, n]."""
+    o = np.ascontiguousarray(rays_o, np.float32).reshape(-1, 3)
+    d = np.ascontiguousarray(rays_d, np.float32).reshape(-1, 3)
+    R = o.shape[0]
+    ids = np.arange(R) if ray_ids is None else np.asarray(ray_ids)
+    wk = np.ascontiguousarray(weights, np.float32).reshape(num_sites, -1)
+    L, Ld = _arch(arch).pos_freqs, _arch(arch).dir_freqs
+    rgb = np.zeros((R, 3))
+    dep = np.zeros(R)
+    op = np.zeros(R)
+    T = np.zeros((R, n), np.float32)
+    C = np.zeros((R, n), np.int32)
+    G = np.zeros((R, n))
+    for r in range(R):
+        t = sample_depths(seed, int(ids[r]), near, far, n, perturb)
+        x = _fma32(t[:, None], d[r][None, :], o[r][None, :])
+        cells, gap = gate_assign(num_sites, gate_L, gate_hidden, gate_w, x)
+        dn = (d[r] / np.float32(np.sqrt(np.float32(d[r] @ d[r])))).astype(np.float32)
+        gd = posenc(Ld, dn)
+        sig = np.zeros(n)
+        col = np.zeros((n, 3))
+        for i in range(n):
+            sig[i], col[i] = head_eval(arch, wk[cells[i]], posenc(L, x[i]), gd)
+        rgb[r], dep[r], op[r], _ = composite(cells, t, sig, col, near, far)
+        T[r], C[r], G[r] = t, cells, gap
+    res = RenderResult(rgb, dep, op)
+    res.t, res.cell, res.gap = T, C, G
+    return res

@@ -20,7 +20,7 @@ ARCH = "gfx950"
 # the grouped MLP is instantiated per head architecture, one unit each, so
 # that its variants compile in parallel
 SOURCES = ["mlp_8x256.hip", "mlp_8x128.hip", "mlp_6x64.hip", "mlp_4x64.hip", "kernels_sample.hip",
-           "kernels_fine.hip", "kernels_soft.hip", "derf_api.cpp"]
+           "kernels_fine.hip", "kernels_soft.hip", "kernels_gate.hip", "derf_api.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH,
           "-I" + os.path.join(ROOT, "include"), "-I" + CSRC,

@@ -110,6 +110,10 @@ struct derf_handle {
     unsigned *totals = nullptr;
     unsigned *totals_fine = nullptr;
     int totals_sets = 1;  // a culled render: one set of K totals per level
+    // MLP gating (derf_set_gate): fp32 weights on the device, or none
+    float *gate_w = nullptr;
+    int gate_freqs = 0;
+    int gate_hidden = 0;
 };
 
 namespace {
@@ -572,10 +576,13 @@ size_t layout_culled(char *base, unsigned S, unsigned R, unsigned nblk, int K, b
 int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
                        long long num_rays, float near_t, float far_t, const derf_sampling *samp,
                        float eps, int levels, int piece, float *out_rgb, float *out_depth,
-                       float *out_opacity, unsigned *out_evaluated, void *stream)
+                       float *out_opacity, unsigned *out_evaluated, void *stream,
+                       bool gated = false, int *out_cell = nullptr)
 {
     if (!h)
         return fail(DERF_ERR_INVALID_ARG, "null handle");
+    if (gated && !h->gate_w)
+        return fail(DERF_ERR_INVALID_ARG, "no gating network set (derf_set_gate)");
     if (!samp)
         return fail(DERF_ERR_INVALID_ARG, "null sampling descriptor");
     if (num_rays < 0 || num_rays >= (1LL << 30))
@@ -644,7 +651,12 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     HIP_TRY(launch_sample_assign(g, h->sites, K, h->site_bits, walk, b.t, b.cell, b.counts, nblk,
                                  s),
             "sample_assign launch");
-    HIP_TRY(launch_level_bounds(b.cell, N, R, L, (unsigned)piece, c.lb, c.lvl, s), "level_bounds launch");
+    if (gated)
+        HIP_TRY(launch_gate(g, h->gate_w, h->gate_freqs, h->gate_hidden, K, b.t, b.cell, out_cell,
+                            s),
+                "gate launch");
+    HIP_TRY(launch_level_bounds(b.cell, N, R, L, (unsigned)piece, c.lb, c.lvl, s),
+            "level_bounds launch");
     HIP_TRY(mark(DERF_STAGE_SAMPLE, 1), "hipEventRecord");
     HIP_TRY(mark(DERF_STAGE_MLP, 0), "hipEventRecord");
     for (unsigned l = 0; l < L; ++l) {
@@ -853,6 +865,67 @@ int derf_render_culled(derf_handle *h, const float *rays_o, const float *rays_d,
                               piece, out_rgb, out_depth, out_opacity, out_evaluated, hip_stream);
 }
 
+int derf_set_gate(derf_handle *h, int pos_freqs, int hidden, const float *weights)
+{
+    if (!h)
+        return fail(DERF_ERR_INVALID_ARG, "null handle");
+    if (hidden == 0) {
+        if (h->gate_w) {
+            HIP_TRY(hipSetDevice(h->device), "hipSetDevice");
+            if (h->last_stream)
+                HIP_TRY(hipStreamSynchronize(h->last_stream), "hipStreamSynchronize");
+            HIP_TRY(hipFree(h->gate_w), "hipFree");
+        }
+        h->gate_w = nullptr;
+        h->gate_freqs = h->gate_hidden = 0;
+        return DERF_OK;
+    }
+    if (!weights)
+        return fail(DERF_ERR_INVALID_ARG, "null gating weights");
+    if (!derf::gate_shape_supported(pos_freqs, hidden))
+        return fail(DERF_ERR_UNSUPPORTED, "no gating kernel for L = %d, %d hidden units",
+                    pos_freqs, hidden);
+    const long long count = derf_gate_weights_count(h->num_sites, pos_freqs, hidden);
+    for (long long i = 0; i < count; ++i)
+        if (!isfinite(weights[i]))
+            return fail(DERF_ERR_INVALID_ARG, "non-finite gating weight");
+    HIP_TRY(hipSetDevice(h->device), "hipSetDevice");
+    float *dev = nullptr;
+    HIP_TRY(hipMalloc(&dev, (size_t)count * sizeof(float)), "hipMalloc");
+    hipError_t e = hipMemcpy(dev, weights, (size_t)count * sizeof(float), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(dev);
+        HIP_TRY(e, "hipMemcpy");
+    }
+    if (h->gate_w) {
+        if (h->last_stream)
+            HIP_TRY(hipStreamSynchronize(h->last_stream), "hipStreamSynchronize");
+        HIP_TRY(hipFree(h->gate_w), "hipFree");
+    }
+    h->gate_w = dev;
+    h->gate_freqs = pos_freqs;
+    h->gate_hidden = hidden;
+    return DERF_OK;
+}
+
+long long derf_gate_weights_count(int num_sites, int pos_freqs, int hidden)
+{
+    if (num_sites < 1 || pos_freqs < 0 || hidden < 1)
+        return -1;
+    const long long P = 3 + 6LL * pos_freqs;
+    return hidden * P + hidden + (long long)num_sites * hidden + num_sites;
+}
+
+int derf_render_gated(derf_handle *h, const float *rays_o, const float *rays_d,
+                      long long num_rays, float near_t, float far_t, const derf_sampling *samp,
+                      float *out_rgb, float *out_depth, float *out_opacity, int *out_cell,
+                      void *hip_stream)
+{
+    return render_culled_impl(h, rays_o, rays_d, num_rays, near_t, far_t, samp, 0.0f, 1, 0,
+                              out_rgb, out_depth, out_opacity, nullptr, hip_stream, true,
+                              out_cell);
+}
+
 int derf_set_empty_heads(derf_handle *h, const int *flags)
 {
     if (!h)
@@ -926,6 +999,8 @@ void derf_destroy(derf_handle *h)
         (void)hipFree(h->ws.mem);
     if (h->sites)
         (void)hipFree(h->sites);
+    if (h->gate_w)
+        (void)hipFree(h->gate_w);
     for (int gi = 0; gi < h->num_groups; ++gi) {
         if (h->groups[gi].streams)
             (void)hipFree(h->groups[gi].streams);

@@ -1,0 +1,132 @@
+// MLP-gating decomposition (Sec. 4, "Decompositions with MLPs"): a small
+// network with a softmax output gives each point its head weights; at
+// inference the sample goes to the head of largest weight.  The softmax is
+// monotone, so that head is the argmax of the logits:
+//   h = ReLU(W1 gamma_L(x) + b1),  logits = W2 h + b2,  cell = argmax logits
+// (ties to the lowest index).  Unlike a Voronoi cell, a gated cell need not
+// be convex, so a ray may enter one cell several times; the integration
+// merges runs of one cell front to back, which is exact for any partition.
+//
+// One thread per sample, fp32 with fused multiply-adds in index order.  The
+// weights (at most 64 (3 + 6 L) + 65 K floats) are read with wave-uniform
+// addresses, so they come through the scalar cache; the encoded input and
+// the hidden layer stay in registers.  This is not a dense contraction worth
+// matrix cores at these sizes (a 3-63 wide input, 16-64 hidden units, K
+// logits): the kernel is bound by its fp32 FMAs and the sin/cos of the
+// encoding.
+#pragma clang fp contract(off)
+
+#include "derf_internal.h"
+
+namespace derf {
+namespace {
+
+constexpr int kGateThreads = 256;
+
+// gamma_L(p): p, then sin(pi 2^l p) and cos(pi 2^l p) per level l
+template <int L>
+__device__ __forceinline__ void gate_encode(const float x[3], float f[3 + 6 * L])
+{
+#pragma unroll
+    for (int c = 0; c < 3; ++c)
+        f[c] = x[c];
+#pragma unroll
+    for (int l = 0; l < L; ++l)
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+            const float y = ldexpf(x[c], l);  // exact
+            f[3 + 6 * l + c] = sinpif(y);
+            f[6 + 6 * l + c] = cospif(y);
+        }
+}
+
+// w: W1 [H][P], b1 [H], W2 [K][H], b2 [K] (P = 3 + 6 L).  Writes the sample's
+// cell over the assignment's, and to out_cell (int32 [S]) when given.
+template <int L, int H>
+__global__ __launch_bounds__(kGateThreads) void gate_kernel(RenderGeometry g,
+                                                            const float *__restrict__ w,
+                                                            int num_sites,
+                                                            const float *__restrict__ t,
+                                                            uint8_t *__restrict__ cell,
+                                                            int *__restrict__ out_cell)
+{
+    constexpr int P = 3 + 6 * L;
+    const unsigned long long s = (unsigned long long)blockIdx.x * kGateThreads + threadIdx.x;
+    if (s >= g.num_samples)
+        return;
+    const unsigned ray = (unsigned)(s / g.n);
+    const float ts = t[s];
+    float x[3];
+#pragma unroll
+    for (int c = 0; c < 3; ++c)
+        x[c] = fmaf(ts, g.rays_d[3 * (size_t)ray + c], g.rays_o[3 * (size_t)ray + c]);
+    float f[P];
+    gate_encode<L>(x, f);
+    const float *b1 = w + H * P, *w2 = b1 + H, *b2 = w2 + (size_t)num_sites * H;
+    float h[H];
+#pragma unroll
+    for (int j = 0; j < H; ++j) {
+        float acc = b1[j];
+#pragma unroll
+        for (int c = 0; c < P; ++c)
+            acc = fmaf(w[j * P + c], f[c], acc);
+        h[j] = fmaxf(acc, 0.0f);
+    }
+    int best = 0;
+    float top = -INFINITY;
+    for (int k = 0; k < num_sites; ++k) {
+        float acc = b2[k];
+#pragma unroll
+        for (int j = 0; j < H; ++j)
+            acc = fmaf(w2[k * H + j], h[j], acc);
+        if (acc > top) {  // strictly larger: ties keep the lower index
+            top = acc;
+            best = k;
+        }
+    }
+    cell[s] = (uint8_t)best;
+    if (out_cell)
+        out_cell[s] = best;
+}
+
+template <int L>
+hipError_t launch_gate_l(const RenderGeometry &g, const float *w, int hidden, int num_sites,
+                         const float *t, uint8_t *cell, int *out_cell, hipStream_t s)
+{
+    const unsigned grid = (unsigned)(((size_t)g.num_samples + kGateThreads - 1) / kGateThreads);
+    switch (hidden) {
+    case 16:
+        gate_kernel<L, 16><<<grid, kGateThreads, 0, s>>>(g, w, num_sites, t, cell, out_cell);
+        break;
+    case 32:
+        gate_kernel<L, 32><<<grid, kGateThreads, 0, s>>>(g, w, num_sites, t, cell, out_cell);
+        break;
+    case 64:
+        gate_kernel<L, 64><<<grid, kGateThreads, 0, s>>>(g, w, num_sites, t, cell, out_cell);
+        break;
+    default:
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+bool gate_shape_supported(int pos_freqs, int hidden)
+{
+    return (pos_freqs == 6 || pos_freqs == 10) && (hidden == 16 || hidden == 32 || hidden == 64);
+}
+
+hipError_t launch_gate(const RenderGeometry &g, const float *w, int pos_freqs, int hidden,
+                       int num_sites, const float *t, uint8_t *cell, int *out_cell, hipStream_t s)
+{
+    if (g.num_samples == 0)
+        return hipSuccess;
+    if (pos_freqs == 6)
+        return launch_gate_l<6>(g, w, hidden, num_sites, t, cell, out_cell, s);
+    if (pos_freqs == 10)
+        return launch_gate_l<10>(g, w, hidden, num_sites, t, cell, out_cell, s);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace derf

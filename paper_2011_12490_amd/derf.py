@@ -11,6 +11,7 @@ import ctypes
 import os
 from typing import Optional
 
+import numpy as np
 import torch  # noqa: F401  (loads the HIP runtime the library binds to)
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -53,7 +54,9 @@ class derf_stats(ctypes.Structure):
 
 EXPORTS = ("derf_weights_count", "derf_create", "derf_create_mixed", "derf_render",
            "derf_render_debug",
-           "derf_render_soft", "derf_render_culled", "derf_set_empty_heads", "derf_set_timing", "derf_get_stats", "derf_reset_stats", "derf_destroy",
+           "derf_render_soft", "derf_render_culled", "derf_set_empty_heads", "derf_set_gate",
+           "derf_gate_weights_count", "derf_render_gated", "derf_set_timing", "derf_get_stats",
+           "derf_reset_stats", "derf_destroy",
            "derf_status_string", "derf_last_error")
 
 _lib: Optional[ctypes.CDLL] = None
@@ -98,6 +101,14 @@ def lib() -> ctypes.CDLL:
         L.derf_render_culled.restype = ctypes.c_int
         L.derf_set_empty_heads.argtypes = [P, P]
         L.derf_set_empty_heads.restype = ctypes.c_int
+        L.derf_set_gate.argtypes = [P, ctypes.c_int, ctypes.c_int, P]
+        L.derf_set_gate.restype = ctypes.c_int
+        L.derf_gate_weights_count.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int]
+        L.derf_gate_weights_count.restype = ctypes.c_longlong
+        L.derf_render_gated.argtypes = [P, P, P, ctypes.c_longlong, ctypes.c_float,
+                                        ctypes.c_float, ctypes.POINTER(derf_sampling), P, P, P, P,
+                                        P]
+        L.derf_render_gated.restype = ctypes.c_int
         L.derf_set_timing.argtypes = [P, ctypes.c_int]
         L.derf_set_timing.restype = ctypes.c_int
         L.derf_get_stats.argtypes = [P, ctypes.POINTER(derf_stats)]
@@ -225,6 +236,33 @@ def derf_set_empty_heads(h, flags):
     _check(lib().derf_set_empty_heads(h, ctypes.cast(arr, ctypes.c_void_p)), "derf_set_empty_heads")
 
 
+def derf_set_gate(h, pos_freqs: int, hidden: int, weights):
+    """Set the MLP-gating network (host float32 weights, W1 [H][3 + 6L], b1,
+    W2 [K][H], b2), or remove it with hidden = 0."""
+    if hidden == 0:
+        _check(lib().derf_set_gate(h, pos_freqs, 0, None), "derf_set_gate")
+        return
+    w = np.ascontiguousarray(weights, np.float32)
+    _check(lib().derf_set_gate(h, pos_freqs, hidden, w.ctypes.data_as(ctypes.c_void_p)),
+           "derf_set_gate")
+
+
+def derf_render_gated(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far: float,
+                      samp: derf_sampling, out_rgb: torch.Tensor, out_depth: torch.Tensor,
+                      out_opacity: torch.Tensor, out_cell: Optional[torch.Tensor] = None,
+                      stream=None):
+    """Enqueue a render with the gated assignment on `stream` (default:
+    torch's current stream).  out_cell: int32 [R, N] or None."""
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    _check(lib().derf_render_gated(h, _dptr(rays_o), _dptr(rays_d), rays_o.shape[0], near, far,
+                                   ctypes.byref(samp), _dptr(out_rgb), _dptr(out_depth),
+                                   _dptr(out_opacity),
+                                   None if out_cell is None else _dptr(out_cell), sp),
+           "derf_render_gated")
+
+
 def derf_set_timing(h, on: bool):
     _check(lib().derf_set_timing(h, int(on)), "derf_set_timing")
 
@@ -296,6 +334,29 @@ class Renderer:
         if debug:
             return rgb, depth, opac, extra
         return rgb, depth, opac
+
+    def set_gate(self, pos_freqs: int, hidden: int, weights):
+        """Assign samples with an MLP-gating network instead of the nearest
+        site in render_gated (hidden = 0 removes it)."""
+        derf_set_gate(self.handle, pos_freqs, hidden, weights)
+
+    def render_gated(self, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far: float,
+                     n: int, seed: int = 0, perturb: bool = True, stream=None,
+                     ray_offset: int = 0, cells: bool = False):
+        """Single-pass render with the gated assignment; returns (rgb, depth,
+        opacity) and, with cells, each sample's head [R, n]."""
+        assert rays_o.is_cuda and rays_o.dtype == torch.float32 and rays_o.is_contiguous()
+        assert rays_d.is_cuda and rays_d.dtype == torch.float32 and rays_d.is_contiguous()
+        R = rays_o.shape[0]
+        dev = rays_o.device
+        rgb = torch.empty((R, 3), dtype=torch.float32, device=dev)
+        depth = torch.empty((R,), dtype=torch.float32, device=dev)
+        opac = torch.empty((R,), dtype=torch.float32, device=dev)
+        cell = torch.empty((R, n), dtype=torch.int32, device=dev) if cells else None
+        samp = derf_sampling(n, 0, seed, int(perturb), ray_offset)
+        derf_render_gated(self.handle, rays_o, rays_d, near, far, samp, rgb, depth, opac, cell,
+                          stream)
+        return (rgb, depth, opac, cell) if cells else (rgb, depth, opac)
 
     def set_empty_heads(self, flags):
         """Mark 0-capacity heads (K flags; None clears)."""

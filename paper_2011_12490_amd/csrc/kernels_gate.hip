@@ -35,8 +35,7 @@ __device__ __forceinline__ void gate_encode(const float x[3], float f[3 + 6 * L]
 #pragma unroll
         for (int c = 0; c < 3; ++c) {
             const float y = ldexpf(x[c], l);  // exact
-            f[3 + 6 * l + c] = sinpif(y);
-            f[6 + 6 * l + c] = cospif(y);
+            sincospif(y, &f[3 + 6 * l + c], &f[6 + 6 * l + c]);  // one shared reduction
         }
 }
 

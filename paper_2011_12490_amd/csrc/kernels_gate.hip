@@ -12,8 +12,7 @@
 // addresses, so they come through the scalar cache; the encoded input and
 // the hidden layer stay in registers.  This is not a dense contraction worth
 // matrix cores at these sizes (a 3-63 wide input, 16-64 hidden units, K
-// logits): the kernel is bound by its fp32 FMAs and the sin/cos of the
-// encoding.
+// logits): the kernel is bound by its fp32 FMAs.
 #pragma clang fp contract(off)
 
 #include "derf_internal.h"
@@ -23,7 +22,10 @@ namespace {
 
 constexpr int kGateThreads = 256;
 
-// gamma_L(p): p, then sin(pi 2^l p) and cos(pi 2^l p) per level l
+// gamma_L(p): p, then sin(pi 2^l p) and cos(pi 2^l p) per level l.  The
+// hardware sine and cosine take revolutions: sin(pi y) = sin(2 pi frac(y / 2)),
+// where y / 2 = 2^(l-1) p is exact and so is its fractional part, so each
+// pair costs a scale, a fract and the two transcendental instructions.
 template <int L>
 __device__ __forceinline__ void gate_encode(const float x[3], float f[3 + 6 * L])
 {
@@ -34,8 +36,9 @@ __device__ __forceinline__ void gate_encode(const float x[3], float f[3 + 6 * L]
     for (int l = 0; l < L; ++l)
 #pragma unroll
         for (int c = 0; c < 3; ++c) {
-            const float y = ldexpf(x[c], l);  // exact
-            sincospif(y, &f[3 + 6 * l + c], &f[6 + 6 * l + c]);  // one shared reduction
+            const float u = __builtin_amdgcn_fractf(ldexpf(x[c], l - 1));
+            f[3 + 6 * l + c] = __builtin_amdgcn_sinf(u);
+            f[6 + 6 * l + c] = __builtin_amdgcn_cosf(u);
         }
 }
 

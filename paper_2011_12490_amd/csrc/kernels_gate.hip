@@ -74,14 +74,33 @@ __global__ __launch_bounds__(kGateThreads) void gate_kernel(RenderGeometry g,
             acc = fmaf(w[j * P + c], f[c], acc);
         h[j] = fmaxf(acc, 0.0f);
     }
+    // logits two at a time, so that both rows' weight loads are in flight
+    // together; each logit and the order of the comparisons are unchanged
     int best = 0;
     float top = -INFINITY;
-    for (int k = 0; k < num_sites; ++k) {
+    int k = 0;
+    for (; k + 1 < num_sites; k += 2) {
+        float a0 = b2[k], a1 = b2[k + 1];
+#pragma unroll
+        for (int j = 0; j < H; ++j) {
+            a0 = fmaf(w2[k * H + j], h[j], a0);
+            a1 = fmaf(w2[(k + 1) * H + j], h[j], a1);
+        }
+        if (a0 > top) {  // strictly larger: ties keep the lower index
+            top = a0;
+            best = k;
+        }
+        if (a1 > top) {
+            top = a1;
+            best = k + 1;
+        }
+    }
+    if (k < num_sites) {
         float acc = b2[k];
 #pragma unroll
         for (int j = 0; j < H; ++j)
             acc = fmaf(w2[k * H + j], h[j], acc);
-        if (acc > top) {  // strictly larger: ties keep the lower index
+        if (acc > top) {
             top = acc;
             best = k;
         }

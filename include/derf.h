@@ -258,7 +258,10 @@ long long derf_gate_weights_count(int num_sites, int pos_freqs, int hidden);
  * the grouped MLP and front-to-back integration of the runs.  Arguments,
  * limits and ownership as derf_render (single pass: samp->n_fine must be 0,
  * DERF_ERR_UNSUPPORTED otherwise); DERF_ERR_INVALID_ARG without a gate.
- *   out_cell   NULL, or device int32 [R][N]: each sample's gated head */
+ *   out_cell   NULL, or device int32 [R][N]: each sample's gated head
+ * Stage times: DERF_STAGE_SAMPLE (sampling, assignment and the gate) and
+ * DERF_STAGE_MLP (bucketing, heads and integration); head_samples counts
+ * each head's gated samples. */
 int derf_render_gated(derf_handle *h, const float *rays_o, const float *rays_d,
                       long long num_rays, float near_t, float far_t, const derf_sampling *samp,
                       float *out_rgb, float *out_depth, float *out_opacity, int *out_cell,

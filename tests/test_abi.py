@@ -43,6 +43,11 @@ def test_weights_count_matches_generator_and_oracle(arch):
     assert derf.derf_weights_count(arch) == arch.weights_count() == oracle.weights_count(arch)
 
 
+@pytest.mark.parametrize("K,L,H", [(1, 6, 16), (16, 10, 32), (256, 10, 64), (7, 6, 24)])
+def test_gate_weights_count_matches_oracle(K, L, H):
+    assert derf.lib().derf_gate_weights_count(K, L, H) == oracle.gate_weights_count(K, L, H)
+
+
 def test_weights_count_rejects_bad_values():
     assert derf.derf_weights_count((10, 4, 0, 128, -1, 0)) == -1
     assert derf.derf_weights_count((10, 4, 8, 128, 8, 0)) == -1     # skip beyond depth

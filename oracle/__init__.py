@@ -448,7 +448,8 @@ def gate_assign(num_sites: int, L: int, hidden: int, w, x):
 
 def _fma32(a, b, c):
     """fp32 fused multiply-add (the product of two floats is exact in fp64)."""
-    return (np.float64(a) * np.float64(b) + np.float64(c)).astype(np.float32)
+    a, b, c = (np.asarray(v, np.float64) for v in (a, b, c))
+    return (a * b + c).astype(np.float32)
 
 
 def render_gated(arch, weights, num_sites: int, gate_L: int, gate_hidden: int, gate_w, rays_o,

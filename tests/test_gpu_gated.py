@@ -35,19 +35,27 @@ def _derf():
     return derf
 
 
-def _run(sc, precision, L, H, gw, ids, label):
+def _run(sc, precision, L, H, gw, ids, label, empty=None):
+    """empty: optional [K] flags of 0-capacity heads on the GPU; the oracle
+    then renders those heads with zero weights (the same render, bitwise, in
+    the oracle's own pins)."""
     derf = _derf()
     cfg = sc.cfg
     o = torch.from_numpy(sc.rays_o).cuda()
     d = torch.from_numpy(sc.rays_d).cuda()
     r = derf.Renderer(sc.sites, cfg.arch, sc.weights, precision)
+    weights = sc.weights
+    if empty is not None:
+        r.set_empty_heads(list(empty))
+        weights = np.array(sc.weights, np.float32).reshape(cfg.num_sites, -1)
+        weights[np.asarray(empty, bool)] = 0.0
     r.set_gate(L, H, gw)
     rgb, depth, opac, cell = r.render_gated(o, d, cfg.near, cfg.far, cfg.n_coarse,
                                             seed=scenes.SEED_RENDER, cells=True)
     torch.cuda.synchronize()
     r.close()
     rgb, depth, opac, cell = [x.cpu().numpy() for x in (rgb, depth, opac, cell)]
-    ref = oracle.render_gated(cfg.arch, sc.weights, cfg.num_sites, L, H, gw, sc.rays_o[ids],
+    ref = oracle.render_gated(cfg.arch, weights, cfg.num_sites, L, H, gw, sc.rays_o[ids],
                               sc.rays_d[ids], cfg.near, cfg.far, cfg.n_coarse,
                               seed=scenes.SEED_RENDER, ray_ids=ids)
     ok = ref.gap >= GAP
@@ -95,6 +103,26 @@ def test_gated_ragged_and_many_heads_fp32():
     sc.rays_o, sc.rays_d = sc.rays_o[:keep].copy(), sc.rays_d[:keep].copy()
     gw = random_gate(40, 6, 32, 77, scale=6.0)
     _run(sc, "fp32", 6, 32, gw, np.arange(0, keep, 9), "gated K=40 n=67 R=1000")
+
+
+def test_gated_256_heads_and_empty_heads_fp32():
+    """K = 256 (cells use all 8 bits), a quarter of the heads 0-capacity."""
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], num_sites=256, sigma_bias=1.0)
+    sc = scenes.make_scene(cfg)
+    empty = np.zeros(256, int)
+    empty[::4] = 1
+    gw = random_gate(256, 6, 16, 31, scale=6.0)
+    cell = _run(sc, "fp32", 6, 16, gw, np.arange(0, cfg.num_rays, 8), "gated K=256, empty heads",
+                empty=empty)
+    assert len(np.unique(cell)) > 128
+
+
+@pytest.mark.parametrize("n", [1, 2])
+def test_gated_one_or_two_samples_fp32(n):
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], num_sites=8, sigma_bias=1.0, n_coarse=n)
+    sc = scenes.make_scene(cfg)
+    gw = random_gate(8, 6, 32, 41, scale=6.0)
+    _run(sc, "fp32", 6, 32, gw, np.arange(0, cfg.num_rays, 4), "gated n=%d" % n)
 
 
 def test_gated_headline_frame_bf16():

@@ -105,6 +105,15 @@ def _lib_handle():
                                              ctypes.c_float, ctypes.c_int, _P, _P, _P, _P, _P, _P,
                                              _P, ctypes.c_int]
         lib.oracle_render_depths.restype = ctypes.c_int
+        lib.oracle_render_gated.argtypes = render_sig + [ctypes.c_int, ctypes.c_int, _P]
+        lib.oracle_render_gated.restype = ctypes.c_int
+        lib.oracle_gate_weights_count.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int]
+        lib.oracle_gate_weights_count.restype = ctypes.c_longlong
+        lib.oracle_gate_logits.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, _P,
+                                           ctypes.c_longlong, _P, _P]
+        lib.oracle_gate_logits.restype = ctypes.c_int
+        lib.oracle_sample_points.argtypes = [ctypes.c_longlong, _P, _P, _P, _P]
+        lib.oracle_sample_points.restype = None
         lib.oracle_max_threads.argtypes = []
         lib.oracle_max_threads.restype = ctypes.c_int
         _lib = lib
@@ -395,43 +404,53 @@ def render_culled(sites, arch, weights, rays_o, rays_d, near: float, far: float,
 
 
 # ---------------------------------------------------------------- MLP gating
-# The decomposition network of Sec. 4 ("Decompositions with MLPs"): an MLP
-# with a softmax output gives each point its head weights; at inference a
-# sample belongs to the head of largest weight, which (the softmax being
-# monotone) is the argmax of the logits.  The paper fixes neither the
-# network's size nor its input; the reading here is one ReLU hidden layer of
-# H units on the heads' positional encoding gamma_L(x):
-#   h = max(0, W1 gamma_L(x) + b1),  logits = W2 h + b2.
-# Weights, fp32, packed W1 [H][3 + 6L], b1 [H], W2 [K][H], b2 [K].  The
-# decision is taken in fp32, the precision of the GPU kernel; ties go to the
-# lowest index, as for the nearest site.
+# The decomposition network of Sec. 4 ("Decompositions with MLPs"), computed
+# by the C oracle (oracle_gate_logits, oracle_render_gated): an MLP with a
+# softmax output gives each point its head weights; at inference a sample
+# belongs to the head of largest weight, which (the softmax being monotone)
+# is the first largest logit.  The reading of its shape: one ReLU hidden
+# layer of H units on the heads' positional encoding gamma_L(x),
+#   h = max(0, W1 gamma_L(x) + b1),  logits = W2 h + b2,
+# weights (fp32) packed W1 [H][3 + 6L], b1 [H], W2 [K][H], b2 [K].  The
+# decision is taken in fp32, the precision of the GPU kernel, with every dot
+# product summed in index order (bias first, then fused multiply-adds).
 
 def gate_weights_count(num_sites: int, L: int, hidden: int) -> int:
-    return hidden * (3 + 6 * L) + hidden + num_sites * hidden + num_sites
+    return _lib_handle().oracle_gate_weights_count(num_sites, L, hidden)
 
 
-def _gate_unpack(num_sites: int, L: int, hidden: int, w):
-    P = 3 + 6 * L
+def _gate_weights(num_sites: int, L: int, hidden: int, w) -> np.ndarray:
     w = np.ascontiguousarray(w, np.float32).ravel()
     if w.size != gate_weights_count(num_sites, L, hidden):
         raise ValueError("gating weights: expected %d floats, got %d"
                          % (gate_weights_count(num_sites, L, hidden), w.size))
-    W1 = w[:hidden * P].reshape(hidden, P)
-    b1 = w[hidden * P:hidden * P + hidden]
-    o = hidden * P + hidden
-    W2 = w[o:o + num_sites * hidden].reshape(num_sites, hidden)
-    b2 = w[o + num_sites * hidden:]
-    return W1, b1, W2, b2
+    return w
+
+
+def sample_points(rays_o, rays_d, t) -> np.ndarray:
+    """x = o + t d in float32 with one fused multiply-add per component, for
+    depths t [..., n] of rays o, d [..., 3] (the sample points whose cells the
+    path decides); returns [..., n, 3]."""
+    t = np.ascontiguousarray(t, np.float32)
+    o = np.broadcast_to(np.asarray(rays_o, np.float32)[..., None, :], t.shape + (3,))
+    d = np.broadcast_to(np.asarray(rays_d, np.float32)[..., None, :], t.shape + (3,))
+    o = np.ascontiguousarray(o)
+    d = np.ascontiguousarray(d)
+    x = np.zeros(t.shape + (3,), np.float32)
+    _lib_handle().oracle_sample_points(t.size, _ptr(o), _ptr(d), _ptr(t), _ptr(x))
+    return x
 
 
 def gate_logits(num_sites: int, L: int, hidden: int, w, x) -> np.ndarray:
     """Logits [M, K] (float32) of the gating network at points x [M, 3]."""
-    W1, b1, W2, b2 = _gate_unpack(num_sites, L, hidden, w)
-    x = np.asarray(x, np.float32).reshape(-1, 3)
-    g = np.stack([posenc(L, xi) for xi in x]).astype(np.float32) if len(x) else \
-        np.zeros((0, 3 + 6 * L), np.float32)
-    h = np.maximum(g @ W1.T + b1, np.float32(0.0)).astype(np.float32)
-    return (h @ W2.T + b2).astype(np.float32)
+    w = _gate_weights(num_sites, L, hidden, w)
+    x = np.ascontiguousarray(x, np.float32).reshape(-1, 3)
+    z = np.zeros((x.shape[0], num_sites), np.float32)
+    rc = _lib_handle().oracle_gate_logits(num_sites, L, hidden, _ptr(w), x.shape[0], _ptr(x),
+                                          _ptr(z))
+    if rc != 0:
+        raise RuntimeError("oracle gate_logits failed (%d)" % rc)
+    return z
 
 
 def gate_assign(num_sites: int, L: int, hidden: int, w, x):
@@ -446,44 +465,34 @@ def gate_assign(num_sites: int, L: int, hidden: int, w, x):
     return cells, top2[:, 1] - top2[:, 0]
 
 
-def _fma32(a, b, c):
-    """fp32 fused multiply-add (the product of two floats is exact in fp64)."""
-    a, b, c = (np.asarray(v, np.float64) for v in (a, b, c))
-    return (a * b + c).astype(np.float32)
-
-
 def render_gated(arch, weights, num_sites: int, gate_L: int, gate_hidden: int, gate_w, rays_o,
                  rays_d, near: float, far: float, n: int, seed: int = 0, perturb: bool = True,
-                 ray_ids=None) -> RenderResult:
-    """Single-pass render with the gated assignment, ray by ray: stratified
-    depths, x = o + t d, the gated head of each sample, that head's network,
-    quadrature, and the front-to-back merge of the ray's runs of one head
-    (a gated cell may be entered more than once).  Pure Python per sample:
-    small inputs only.  The result also holds t, cell and gap [R, n]."""
+                 ray_ids=None, nthreads: int = 0) -> RenderResult:
+    """Single-pass render with the gated assignment: stratified depths,
+    x = o + t d, each sample's gated head, that head's network, quadrature,
+    and the front-to-back merge of the ray's runs of one head (a gated cell
+    may be entered more than once).  The result also holds t, cell and gap
+    [R, n] (gap: the difference of each sample's two largest logits)."""
+    sites = np.zeros((num_sites, 3), np.float32)  # not used by the gated assignment
+    w = _gate_weights(num_sites, gate_L, gate_hidden, gate_w)
+    weights = np.ascontiguousarray(weights, np.float32)
     o = np.ascontiguousarray(rays_o, np.float32).reshape(-1, 3)
     d = np.ascontiguousarray(rays_d, np.float32).reshape(-1, 3)
     R = o.shape[0]
-    ids = np.arange(R) if ray_ids is None else np.asarray(ray_ids)
-    wk = np.ascontiguousarray(weights, np.float32).reshape(num_sites, -1)
-    L, Ld = _arch(arch).pos_freqs, _arch(arch).dir_freqs
-    rgb = np.zeros((R, 3))
-    dep = np.zeros(R)
-    op = np.zeros(R)
+    ids = None if ray_ids is None else np.ascontiguousarray(ray_ids, np.int64)
+    rgb = np.zeros((R, 3), np.float64)
+    dep = np.zeros(R, np.float64)
+    op = np.zeros(R, np.float64)
     T = np.zeros((R, n), np.float32)
     C = np.zeros((R, n), np.int32)
-    G = np.zeros((R, n))
-    for r in range(R):
-        t = sample_depths(seed, int(ids[r]), near, far, n, perturb)
-        x = _fma32(t[:, None], d[r][None, :], o[r][None, :])
-        cells, gap = gate_assign(num_sites, gate_L, gate_hidden, gate_w, x)
-        dn = (d[r] / np.float32(np.sqrt(np.float32(d[r] @ d[r])))).astype(np.float32)
-        gd = posenc(Ld, dn)
-        sig = np.zeros(n)
-        col = np.zeros((n, 3))
-        for i in range(n):
-            sig[i], col[i] = head_eval(arch, wk[cells[i]], posenc(L, x[i]), gd)
-        rgb[r], dep[r], op[r], _ = composite(cells, t, sig, col, near, far)
-        T[r], C[r], G[r] = t, cells, gap
+    G = np.zeros((R, n), np.float64)
+    a = _arch(arch)
+    rc = _lib_handle().oracle_render_gated(
+        num_sites, _ptr(sites), ctypes.byref(a), _ptr(weights), R, _ptr(o), _ptr(d), _ptr(ids),
+        near, far, n, 0, seed, int(perturb), _ptr(rgb), _ptr(dep), _ptr(op), _ptr(T), _ptr(C),
+        None, None, _ptr(G), nthreads, gate_L, gate_hidden, _ptr(w))
+    if rc != 0:
+        raise RuntimeError("oracle gated render failed (%d)" % rc)
     res = RenderResult(rgb, dep, op)
     res.t, res.cell, res.gap = T, C, G
     return res

@@ -455,6 +455,100 @@ static void merge_sorted(const float *a, int na, const float *b, int nb, float *
     }
 }
 
+/* ------------------------------------------------------------ MLP gating --
+ * The alternative decomposition of Sec. 4 ("decompositions with MLPs"): a
+ * small network with a softmax output gives every point its head weights,
+ * and at inference a point belongs to the head of largest weight.  The
+ * softmax is monotone, so that head is the first largest logit.  The paper
+ * fixes neither the network's size nor its input; the reading here is one
+ * ReLU hidden layer of H units on the heads' positional encoding
+ * gamma_L(x):
+ *   h = max(0, W1 gamma_L(x) + b1),  z = W2 h + b2   (K logits)
+ * Packed float32 weights: W1 [H][3 + 6L] row-major, b1 [H], W2 [K][H], b2 [K].
+ * The decision is an integer, so it is taken in float32, the precision of
+ * the kernel: the encoding is rounded to float32 and every dot product is
+ * the bias followed by fused multiply-adds in index order. */
+long long oracle_gate_weights_count(int K, int L, int H)
+{
+    if (K < 1 || L < 0 || H < 1)
+        return -1;
+    return (long long)H * (3 + 6 * L) + H + (long long)K * H + K;
+}
+
+/* Logits z [K] of the gating network at x; f (3 + 6L floats) and h (H) are
+ * scratch. */
+static void gate_logits(int K, int L, int H, const float *w, const float x[3], float *f, float *h,
+                        float *z)
+{
+    const int P = 3 + 6 * L;
+    double g[3 + 6 * 32];
+    const double xd[3] = { x[0], x[1], x[2] };
+    oracle_posenc(L, xd, g);
+    for (int c = 0; c < P; ++c)
+        f[c] = (float)g[c];
+    const float *W1 = w, *b1 = W1 + (size_t)H * P, *W2 = b1 + H, *b2 = W2 + (size_t)K * H;
+    for (int j = 0; j < H; ++j) {
+        float acc = b1[j];
+        for (int c = 0; c < P; ++c)
+            acc = fmaf(W1[(size_t)j * P + c], f[c], acc);
+        h[j] = acc > 0.0f ? acc : 0.0f;
+    }
+    for (int k = 0; k < K; ++k) {
+        float acc = b2[k];
+        for (int j = 0; j < H; ++j)
+            acc = fmaf(W2[(size_t)k * H + j], h[j], acc);
+        z[k] = acc;
+    }
+}
+
+/* The gated head (first largest logit) and, in *gap, the difference between
+ * the two largest logits (infinite for one head): how near the decision is
+ * to a tie. */
+static int gate_argmax(int K, const float *z, double *gap)
+{
+    int best = 0;
+    for (int k = 1; k < K; ++k)
+        if (z[k] > z[best])
+            best = k;
+    if (gap) {
+        double second = -INFINITY;
+        for (int k = 0; k < K; ++k)
+            if (k != best && (double)z[k] > second)
+                second = z[k];
+        *gap = K > 1 ? (double)z[best] - second : INFINITY;
+    }
+    return best;
+}
+
+/* Logits [M][K] of the gating network at the points x [M][3]; -1 for bad
+ * sizes. */
+int oracle_gate_logits(int K, int L, int H, const float *w, long long M, const float *x,
+                       float *z)
+{
+    if (K < 1 || L < 0 || L > 32 || H < 1 || M < 0)
+        return -1;
+    float *f = malloc(sizeof(float) * (size_t)(3 + 6 * L));
+    float *h = malloc(sizeof(float) * (size_t)H);
+    if (!f || !h) {
+        free(f);
+        free(h);
+        return -3;
+    }
+    for (long long m = 0; m < M; ++m)
+        gate_logits(K, L, H, w, x + 3 * m, f, h, z + (size_t)m * K);
+    free(f);
+    free(h);
+    return 0;
+}
+
+/* x = o + t d per sample (float32, one fma per component) for depths t [M]
+ * of the rays o, d [M][3]. */
+void oracle_sample_points(long long M, const float *o, const float *d, const float *t, float *x)
+{
+    for (long long m = 0; m < M; ++m)
+        sample_point(o + 3 * m, d + 3 * m, t[m], x + 3 * m);
+}
+
 /* ----------------------------------------------------------- rendering --- */
 
 typedef struct {
@@ -473,6 +567,9 @@ typedef struct {
     const long long *woff;      /* [K] offset of head k's weights */
     size_t mix_scratch;         /* doubles of scratch one head evaluation uses */
     int mix_pos, mix_dir;       /* largest encoding lengths over the heads */
+    /* optional gating network (MODE_GATED): packed weights, L and H */
+    const float *gate_w;
+    int gate_L, gate_H;
 } render_args;
 
 /* Head k at x (view direction dh): its density and colour, or zero for a
@@ -500,7 +597,7 @@ static void eval_head(const render_args *A, int k, const double xd[3], const dou
                      sigma, rgb, scratch);
 }
 
-enum { MODE_DERF = 0, MODE_PLAIN = 1, MODE_SOFT = 2, MODE_DIRECT = 3, MODE_BACK = 4 };
+enum { MODE_DERF = 0, MODE_PLAIN = 1, MODE_SOFT = 2, MODE_DIRECT = 3, MODE_BACK = 4, MODE_GATED = 5 };
 
 /* Evaluate the field at every sample of one ray: cell, sigma, rgb. */
 static void eval_samples(const render_args *A, int mode, double beta, const float o[3],
@@ -557,6 +654,11 @@ static void eval_samples(const render_args *A, int mode, double beta, const floa
                         exp(-beta * (sqrt(ex * ex + ey * ey + ez * ez) - dist_min)) / z;
                 }
             }
+        } else if (mode == MODE_GATED) {
+            float f[3 + 6 * 32], h[256], z[256];
+            gate_logits(A->K, A->gate_L, A->gate_H, A->gate_w, x, f, h, z);
+            cell[i] = gate_argmax(A->K, z, NULL);
+            eval_head(A, cell[i], xd, dh, gx, gd, &sigma[i], &rgb[3 * i], scratch);
         } else {
             cell[i] = oracle_nearest_site(A->K, A->sites, x);
             eval_head(A, cell[i], xd, dh, gx, gd, &sigma[i], &rgb[3 * i], scratch);
@@ -568,7 +670,7 @@ static void finish(int mode, int n, const int *cell, const float *t, const doubl
                    const double *rgb, const double *delta, double *o_rgb, double *o_depth,
                    double *o_opac, double *w_out)
 {
-    if (mode == MODE_DERF)
+    if (mode == MODE_DERF || mode == MODE_GATED)
         composite_segments(n, cell, t, sigma, rgb, delta, o_rgb, o_depth, o_opac, w_out);
     else if (mode == MODE_BACK)
         composite_back_to_front(n, t, sigma, rgb, delta, o_rgb, o_depth, o_opac);
@@ -686,9 +788,17 @@ static int render_impl(const render_args *A, int mode, double beta, long long R,
                     if (dbg_margin) {
                         float x[3];
                         sample_point(o, d, tt[i], x);
-                        dbg_margin[s] = (mode == MODE_PLAIN || mode == MODE_SOFT || A->K == 1)
-                                            ? INFINITY
-                                            : oracle_bisector_margin(A->K, A->sites, x, cell[i]);
+                        if (mode == MODE_GATED) {
+                            /* the gap between the two largest logits */
+                            float f[3 + 6 * 32], h[256], z[256];
+                            gate_logits(A->K, A->gate_L, A->gate_H, A->gate_w, x, f, h, z);
+                            (void)gate_argmax(A->K, z, &dbg_margin[s]);
+                        } else {
+                            dbg_margin[s] = (mode == MODE_PLAIN || mode == MODE_SOFT || A->K == 1)
+                                                ? INFINITY
+                                                : oracle_bisector_margin(A->K, A->sites, x,
+                                                                         cell[i]);
+                        }
                     }
                 }
             }
@@ -817,6 +927,27 @@ int oracle_render_soft_contrib(ORACLE_RENDER_ARGS, double beta, double *contrib)
         return -1;
     A.contrib = contrib;
     return render_impl(&A, MODE_SOFT, beta, R, rays_o, rays_d, ray_ids, out_rgb, out_depth,
+                       out_opacity, dbg_t, dbg_cell, dbg_sigma, dbg_rgb, dbg_margin, nthreads);
+}
+
+/* DeRF render with the gated assignment (Sec. 4, decompositions with MLPs):
+ * each sample's head is the gating network's first largest logit instead of
+ * the nearest site.  A gated cell need not be convex, so a ray may enter it
+ * more than once; its runs are integrated and merged front to back like
+ * segments, which is exact for any partition ("over" is associative).
+ * dbg_margin (optional) receives the gap between each sample's two largest
+ * logits instead of a bisector distance.  Single pass (n_fine = 0), one
+ * architecture; at most 256 heads, 256 hidden units and 32 frequencies. */
+int oracle_render_gated(ORACLE_RENDER_ARGS, int gate_L, int gate_H, const float *gate_w)
+{
+    ORACLE_FILL_ARGS
+    if (n_fine != 0 || !gate_w || K < 1 || K > 256 || gate_L < 0 || gate_L > 32 || gate_H < 1 ||
+        gate_H > 256)
+        return -1;
+    A.gate_w = gate_w;
+    A.gate_L = gate_L;
+    A.gate_H = gate_H;
+    return render_impl(&A, MODE_GATED, 0.0, R, rays_o, rays_d, ray_ids, out_rgb, out_depth,
                        out_opacity, dbg_t, dbg_cell, dbg_sigma, dbg_rgb, dbg_margin, nthreads);
 }
 

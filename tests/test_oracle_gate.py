@@ -63,6 +63,41 @@ def test_gate_weights_count_and_unpack_order():
         oracle.gate_assign(K, L, H, w[:-1], np.zeros((1, 3), np.float32))
 
 
+def test_gate_logits_match_a_float64_matrix_chain():
+    """The fp32 logits (bias, then fused multiply-adds in index order) equal a
+    float64 matrix chain on the same fp32 encoding within the rounding bound
+    of a length-n fp32 dot product, n u sum |w x| (u = 2^-24), for every
+    point and head; the ReLU acts on the hidden units."""
+    K, L, H = 7, 6, 32
+    w = random_gate(K, L, H, 11, scale=4.0)
+    P = 3 + 6 * L
+    W1 = w[:H * P].reshape(H, P).astype(np.float64)
+    b1 = w[H * P:H * P + H].astype(np.float64)
+    W2 = w[H * P + H:H * P + H + K * H].reshape(K, H).astype(np.float64)
+    b2 = w[H * P + H + K * H:].astype(np.float64)
+    x = np.random.default_rng(3).uniform(-1.2, 1.2, (500, 3)).astype(np.float32)
+    z = oracle.gate_logits(K, L, H, w, x).astype(np.float64)
+    g = np.stack([oracle.posenc(L, xi.astype(np.float64)) for xi in x]).astype(np.float32)
+    g = g.astype(np.float64)
+    pre = g @ W1.T + b1
+    h = np.maximum(pre, 0.0)
+    ref = h @ W2.T + b2
+    u = 2.0 ** -24
+    # hidden-unit error bound, carried through W2, plus the logits' own rounding
+    eh = (P + 1) * u * (np.abs(g) @ np.abs(W1).T + np.abs(b1))
+    bound = (H + 1) * u * (h @ np.abs(W2).T + np.abs(b2)) + eh @ np.abs(W2).T
+    assert np.all(np.abs(z - ref) <= 1.01 * bound + 1e-30)
+    assert np.abs(z - ref).max() > 0.0          # fp32 arithmetic, not a float64 copy
+    # a missing ReLU, a dropped hidden or output bias, or a swapped encoding
+    # block (sin and cos of one level) leaves the bound by far
+    assert np.abs(pre @ W2.T + b2 - z).max() > 1e-3
+    assert np.abs(np.maximum(g @ W1.T, 0.0) @ W2.T + b2 - z).max() > 1e-3
+    assert np.abs(h @ W2.T - z).max() > 1e-3
+    gs = g.copy()
+    gs[:, 3:6], gs[:, 6:9] = g[:, 6:9], g[:, 3:6]
+    assert np.abs(np.maximum(gs @ W1.T + b1, 0.0) @ W2.T + b2 - z).max() > 1e-3
+
+
 def test_voronoi_gate_picks_the_nearest_site():
     sc, ids = _tiny(K=6)
     cfg = sc.cfg
@@ -70,7 +105,7 @@ def test_voronoi_gate_picks_the_nearest_site():
     w = voronoi_gate(sc.sites, L, H)
     t, cell, margin = oracle.sample_assign(sc.sites, sc.rays_o[ids], sc.rays_d[ids], cfg.near,
                                            cfg.far, cfg.n_coarse, scenes.SEED_RENDER, margin=True)
-    x = oracle._fma32(t[..., None], sc.rays_d[ids][:, None, :], sc.rays_o[ids][:, None, :])
+    x = oracle.sample_points(sc.rays_o[ids], sc.rays_d[ids], t)
     gcell, gap = oracle.gate_assign(cfg.num_sites, L, H, w, x.reshape(-1, 3))
     ok = (margin.ravel() >= 1e-5) & (gap >= 1e-4)
     assert ok.mean() > 0.99
@@ -145,10 +180,9 @@ def test_nonconvex_gated_cells_composite_like_direct():
     assert any(r > d for r, d in zip(runs, distinct))
     wk = np.ascontiguousarray(sc.weights, np.float32).reshape(4, -1)
     for r in range(len(ids)):
-        x = oracle._fma32(g.t[r][:, None], sc.rays_d[ids[r]][None, :], sc.rays_o[ids[r]][None, :])
-        dv = sc.rays_d[ids[r]]
-        dn = (dv / np.float32(np.sqrt(np.float32(dv @ dv)))).astype(np.float32)
-        gd = oracle.posenc(cfg.arch.dir_freqs, dn)
+        x = oracle.sample_points(sc.rays_o[ids[r]], sc.rays_d[ids[r]], g.t[r])
+        dv = sc.rays_d[ids[r]].astype(np.float64)
+        gd = oracle.posenc(cfg.arch.dir_freqs, dv / np.sqrt(dv @ dv))
         sig = np.zeros(cfg.n_coarse)
         col = np.zeros((cfg.n_coarse, 3))
         for i in range(cfg.n_coarse):

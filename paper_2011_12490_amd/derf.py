@@ -139,6 +139,53 @@ def _dptr(x: Optional[torch.Tensor]):
     return None if x is None else ctypes.c_void_p(x.data_ptr())
 
 
+def check_rays(rays_o: torch.Tensor, rays_d: torch.Tensor) -> int:
+    """Ray count of a pair of device ray arrays, after checking that both are
+    contiguous float32 [R, 3] tensors on one GPU (ValueError otherwise: the
+    library reads 3 R floats from each)."""
+    for name, x in (("rays_o", rays_o), ("rays_d", rays_d)):
+        if not isinstance(x, torch.Tensor):
+            raise ValueError("%s must be a torch tensor" % name)
+        if not x.is_cuda or x.dtype != torch.float32 or not x.is_contiguous():
+            raise ValueError("%s must be a contiguous float32 GPU tensor" % name)
+        if x.dim() != 2 or x.shape[1] != 3:
+            raise ValueError("%s must have shape [R, 3], got %s" % (name, tuple(x.shape)))
+    if rays_o.shape != rays_d.shape or rays_o.device != rays_d.device:
+        raise ValueError("rays_o and rays_d differ in shape or device")
+    return rays_o.shape[0]
+
+
+def check_out(x: Optional[torch.Tensor], name: str, numel: int, dtype, device,
+              optional: bool = False):
+    """Check an output tensor before its pointer goes to the library, which
+    writes `numel` elements of `dtype` to it: a contiguous GPU tensor on the
+    rays' device with at least that many elements (ValueError otherwise, so
+    that a wrong buffer fails before any GPU work)."""
+    if x is None:
+        if optional:
+            return
+        raise ValueError("%s is required" % name)
+    if not isinstance(x, torch.Tensor):
+        raise ValueError("%s must be a torch tensor" % name)
+    if x.device != device:
+        raise ValueError("%s must live on %s (the rays' device)" % (name, device))
+    if x.dtype != dtype:
+        raise ValueError("%s must be %s, got %s" % (name, dtype, x.dtype))
+    if not x.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if x.numel() < numel:
+        raise ValueError("%s holds %d elements, the render writes %d" % (name, x.numel(), numel))
+
+
+def _check_outputs(rays_o, rays_d, out_rgb, out_depth, out_opacity) -> int:
+    R = check_rays(rays_o, rays_d)
+    dev = rays_o.device
+    check_out(out_rgb, "out_rgb", 3 * R, torch.float32, dev)
+    check_out(out_depth, "out_depth", R, torch.float32, dev)
+    check_out(out_opacity, "out_opacity", R, torch.float32, dev)
+    return R
+
+
 # ---- thin wrappers with the C names -------------------------------------------
 
 def derf_weights_count(arch) -> int:
@@ -161,6 +208,10 @@ def derf_create(sites, arch, weights, precision: int) -> ctypes.c_void_p:
         if isinstance(weights, (list, tuple)):
             weights = np.concatenate([np.ravel(np.asarray(x, np.float32)) for x in weights])
         w = np.ascontiguousarray(weights, np.float32)
+        if len(arch) != s.shape[0]:
+            raise ValueError("need one architecture per site")
+        if any(derf_weights_count(a) < 0 for a in arch):
+            raise ValueError("invalid head architecture")
         if w.size != sum(derf_weights_count(a) for a in arch):
             raise ValueError("weights do not match the per-head architectures")
         arr = (derf_head_arch * len(arch))(*[_arch(a) for a in arch])
@@ -172,6 +223,13 @@ def derf_create(sites, arch, weights, precision: int) -> ctypes.c_void_p:
         return h
     w = np.ascontiguousarray(weights, np.float32)
     a = _arch(arch)
+    per_head = derf_weights_count(arch)
+    if per_head < 0:
+        raise ValueError("invalid head architecture %s" % (tuple(arch.as_tuple() if hasattr(
+            arch, "as_tuple") else arch),))
+    if w.size != s.shape[0] * per_head:
+        raise ValueError("weights hold %d floats; %d heads of this architecture need %d"
+                         % (w.size, s.shape[0], s.shape[0] * per_head))
     _check(lib().derf_create(ctypes.byref(h), s.shape[0], s.ctypes.data_as(ctypes.c_void_p),
                              ctypes.byref(a), w.ctypes.data_as(ctypes.c_void_p), precision),
            "derf_create")
@@ -182,10 +240,10 @@ def derf_render(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far:
                 samp: derf_sampling, out_rgb: torch.Tensor, out_depth: torch.Tensor,
                 out_opacity: torch.Tensor, stream=None, debug: Optional[derf_debug_out] = None):
     """Enqueue a render on `stream` (default: torch's current stream)."""
+    R = _check_outputs(rays_o, rays_d, out_rgb, out_depth, out_opacity)
     if stream is None:
         stream = torch.cuda.current_stream()
     sp = ctypes.c_void_p(stream.cuda_stream)
-    R = rays_o.shape[0]
     args = [h, _dptr(rays_o), _dptr(rays_d), R, near, far, ctypes.byref(samp), _dptr(out_rgb),
             _dptr(out_depth), _dptr(out_opacity)]
     if debug is None:
@@ -198,7 +256,16 @@ def derf_render_soft(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float,
                      samp: derf_sampling, beta: float, out_rgb: torch.Tensor,
                      out_depth: torch.Tensor, out_opacity: torch.Tensor,
                      out_contrib: Optional[torch.Tensor] = None, stream=None):
-    """Enqueue a soft-decomposition render on `stream` (default: torch's current stream)."""
+    """Enqueue a soft-decomposition render on `stream` (default: torch's current
+    stream).  out_contrib: float32 [R, K] or None."""
+    R = _check_outputs(rays_o, rays_d, out_rgb, out_depth, out_opacity)
+    if out_contrib is not None:
+        if out_contrib.dim() != 2:
+            raise ValueError("out_contrib must have shape [R, K]")
+        check_out(out_contrib, "out_contrib", R * out_contrib.shape[1], torch.float32,
+                  rays_o.device)
+        if R and out_contrib.shape[0] < R:
+            raise ValueError("out_contrib needs a row per ray")
     if stream is None:
         stream = torch.cuda.current_stream()
     sp = ctypes.c_void_p(stream.cuda_stream)
@@ -217,6 +284,8 @@ def derf_render_culled(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: floa
     """Enqueue a Painter's-order render with transmittance culling on `stream`
     (default: torch's current stream).  out_evaluated: int32 [R] or None;
     piece: the most samples of one piece (0: whole segments)."""
+    R = _check_outputs(rays_o, rays_d, out_rgb, out_depth, out_opacity)
+    check_out(out_evaluated, "out_evaluated", R, torch.int32, rays_o.device, optional=True)
     if stream is None:
         stream = torch.cuda.current_stream()
     sp = ctypes.c_void_p(stream.cuda_stream)
@@ -236,13 +305,19 @@ def derf_set_empty_heads(h, flags):
     _check(lib().derf_set_empty_heads(h, ctypes.cast(arr, ctypes.c_void_p)), "derf_set_empty_heads")
 
 
-def derf_set_gate(h, pos_freqs: int, hidden: int, weights):
-    """Set the MLP-gating network (host float32 weights, W1 [H][3 + 6L], b1,
-    W2 [K][H], b2), or remove it with hidden = 0."""
+def derf_set_gate(h, pos_freqs: int, hidden: int, weights, num_sites: int):
+    """Set the MLP-gating network of a renderer of num_sites heads (host
+    float32 weights, W1 [H][3 + 6L], b1, W2 [K][H], b2), or remove it with
+    hidden = 0."""
     if hidden == 0:
         _check(lib().derf_set_gate(h, pos_freqs, 0, None), "derf_set_gate")
         return
     w = np.ascontiguousarray(weights, np.float32)
+    count = lib().derf_gate_weights_count(num_sites, pos_freqs, hidden)
+    if count < 0:
+        raise ValueError("invalid gate shape (K=%d, L=%d, H=%d)" % (num_sites, pos_freqs, hidden))
+    if w.size != count:
+        raise ValueError("gating weights hold %d floats, the network needs %d" % (w.size, count))
     _check(lib().derf_set_gate(h, pos_freqs, hidden, w.ctypes.data_as(ctypes.c_void_p)),
            "derf_set_gate")
 
@@ -253,6 +328,9 @@ def derf_render_gated(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float
                       stream=None):
     """Enqueue a render with the gated assignment on `stream` (default:
     torch's current stream).  out_cell: int32 [R, N] or None."""
+    R = _check_outputs(rays_o, rays_d, out_rgb, out_depth, out_opacity)
+    check_out(out_cell, "out_cell", R * (samp.n_coarse + max(0, samp.n_fine)), torch.int32,
+              rays_o.device, optional=True)
     if stream is None:
         stream = torch.cuda.current_stream()
     sp = ctypes.c_void_p(stream.cuda_stream)
@@ -309,9 +387,7 @@ class Renderer:
                out=None, debug: bool = False, stream=None, ray_offset: int = 0):
         """Render device rays; returns (rgb [R,3], depth [R], opacity [R]) and, with
         debug=True, a dict of per-sample cell/t/sigma/rgb."""
-        assert rays_o.is_cuda and rays_o.dtype == torch.float32 and rays_o.is_contiguous()
-        assert rays_d.is_cuda and rays_d.dtype == torch.float32 and rays_d.is_contiguous()
-        R = rays_o.shape[0]
+        R = check_rays(rays_o, rays_d)
         dev = rays_o.device
         if out is None:
             rgb = torch.empty((R, 3), dtype=torch.float32, device=dev)
@@ -338,16 +414,14 @@ class Renderer:
     def set_gate(self, pos_freqs: int, hidden: int, weights):
         """Assign samples with an MLP-gating network instead of the nearest
         site in render_gated (hidden = 0 removes it)."""
-        derf_set_gate(self.handle, pos_freqs, hidden, weights)
+        derf_set_gate(self.handle, pos_freqs, hidden, weights, self.num_sites)
 
     def render_gated(self, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far: float,
                      n: int, seed: int = 0, perturb: bool = True, stream=None,
                      ray_offset: int = 0, cells: bool = False):
         """Single-pass render with the gated assignment; returns (rgb, depth,
         opacity) and, with cells, each sample's head [R, n]."""
-        assert rays_o.is_cuda and rays_o.dtype == torch.float32 and rays_o.is_contiguous()
-        assert rays_d.is_cuda and rays_d.dtype == torch.float32 and rays_d.is_contiguous()
-        R = rays_o.shape[0]
+        R = check_rays(rays_o, rays_d)
         dev = rays_o.device
         rgb = torch.empty((R, 3), dtype=torch.float32, device=dev)
         depth = torch.empty((R,), dtype=torch.float32, device=dev)
@@ -369,9 +443,7 @@ class Renderer:
                     contrib: bool = False, stream=None, ray_offset: int = 0):
         """Soft-decomposition render at temperature beta; returns (rgb, depth,
         opacity) and, with contrib=True, the per-ray head contributions [R, K]."""
-        assert rays_o.is_cuda and rays_o.dtype == torch.float32 and rays_o.is_contiguous()
-        assert rays_d.is_cuda and rays_d.dtype == torch.float32 and rays_d.is_contiguous()
-        R = rays_o.shape[0]
+        R = check_rays(rays_o, rays_d)
         dev = rays_o.device
         rgb = torch.empty((R, 3), dtype=torch.float32, device=dev)
         depth = torch.empty((R,), dtype=torch.float32, device=dev)
@@ -390,9 +462,7 @@ class Renderer:
         """Single-pass render in Painter's order with transmittance culling;
         returns (rgb, depth, opacity, evaluated samples per ray).  piece > 0
         cuts segments into pieces of at most that many samples."""
-        assert rays_o.is_cuda and rays_o.dtype == torch.float32 and rays_o.is_contiguous()
-        assert rays_d.is_cuda and rays_d.dtype == torch.float32 and rays_d.is_contiguous()
-        R = rays_o.shape[0]
+        R = check_rays(rays_o, rays_d)
         dev = rays_o.device
         rgb = torch.empty((R, 3), dtype=torch.float32, device=dev)
         depth = torch.empty((R,), dtype=torch.float32, device=dev)

@@ -136,6 +136,57 @@ def test_mixed_create_soft_culled_render_and_empty_heads_reject_bad_arguments_wi
     assert L.derf_gate_weights_count(0, 6, 16) == -1
 
 
+def test_binding_checks_host_weights_before_the_library_reads_them():
+    """The library reads K * derf_weights_count floats (one architecture) or the
+    per-head sum (mixed) from the host weights, and derf_gate_weights_count
+    floats from a gate: the binding refuses arrays of any other length before
+    the call, so a short array can never be read past its end."""
+    sites = np.zeros((4, 3), np.float32)
+    n = derf.derf_weights_count(scenes.ARCH_TINY)
+    for size in (4 * n - 1, 4 * n + 1, n):
+        with pytest.raises(ValueError, match="weights hold"):
+            derf.derf_create(sites, scenes.ARCH_TINY, np.zeros(size, np.float32), 0)
+    with pytest.raises(ValueError, match="invalid head architecture"):
+        derf.derf_create(sites, (10, 4, 0, 128, -1, 0), np.zeros(16, np.float32), 0)
+    with pytest.raises(ValueError, match="one architecture per site"):
+        derf.derf_create(sites, [scenes.ARCH_TINY] * 3, [np.zeros(n, np.float32)] * 3, 0)
+    count = derf.lib().derf_gate_weights_count(4, 6, 16)
+    for size in (count - 1, count + 5):
+        with pytest.raises(ValueError, match="gating weights hold"):
+            derf.derf_set_gate(None, 6, 16, np.zeros(size, np.float32), 4)
+
+
+def test_binding_checks_ray_and_output_tensors_before_the_call():
+    """Rays must be contiguous float32 GPU tensors of shape [R, 3]; every output
+    must be a contiguous tensor of the right dtype on the rays' device with at
+    least as many elements as the render writes.  These checks run before any
+    pointer reaches the library (here on CPU tensors, so no GPU is touched)."""
+    torch = pytest.importorskip("torch")
+    o = torch.zeros((5, 3))
+    with pytest.raises(ValueError, match="GPU tensor"):
+        derf.check_rays(o, o)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        derf.derf_render(None, o, o, 2.0, 6.0, derf.derf_sampling(8, 0, 1, 1, 0), o, o[:, 0],
+                         o[:, 1])
+    cpu = torch.device("cpu")
+    derf.check_out(torch.zeros(15), "out_rgb", 15, torch.float32, cpu)
+    derf.check_out(None, "out_cell", 15, torch.int32, cpu, optional=True)
+    with pytest.raises(ValueError, match="is required"):
+        derf.check_out(None, "out_rgb", 15, torch.float32, cpu)
+    with pytest.raises(ValueError, match="holds 14 elements"):
+        derf.check_out(torch.zeros(14), "out_rgb", 15, torch.float32, cpu)
+    with pytest.raises(ValueError, match="must be torch.float32"):
+        derf.check_out(torch.zeros(15, dtype=torch.float64), "out_rgb", 15, torch.float32, cpu)
+    with pytest.raises(ValueError, match="must be torch.int32"):
+        derf.check_out(torch.zeros(15), "out_cell", 15, torch.int32, cpu)
+    with pytest.raises(ValueError, match="contiguous"):
+        derf.check_out(torch.zeros((5, 6))[:, ::2], "out_rgb", 15, torch.float32, cpu)
+    with pytest.raises(ValueError, match="rays' device"):
+        derf.check_out(torch.zeros(15, device="meta"), "out_rgb", 15, torch.float32, cpu)
+    with pytest.raises(ValueError, match="must be a torch tensor"):
+        derf.check_out(np.zeros(15, np.float32), "out_rgb", 15, torch.float32, cpu)
+
+
 def test_status_strings():
     L = derf.lib()
     assert L.derf_status_string(0) == b"ok"

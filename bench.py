@@ -53,7 +53,7 @@ def kernel_source_hash():
     import hashlib
     import re
     text = "".join(open(os.path.join(ROOT, "paper_2011_12490_amd", "csrc", f)).read()
-                   for f in ("mlp_kernel.h", "mlp_8x128.hip", "derf_internal.h"))
+                   for f in ("mlp_kernel.h", "mlp_8x128.hip"))
     text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
     text = re.sub(r"//[^\n]*", " ", text)
     text = re.sub(r"\s+", " ", text)
@@ -75,15 +75,17 @@ def measured_traffic():
 
 
 def cpu_baseline(sc, n_rays, nthreads):
+    """The oracle timed on a seeded ray subset of the frame; also returns the
+    subset's ids and the oracle's outputs (for the parity record)."""
     import numpy as np
     import oracle
     from paper_2011_12490_amd import scenes
     cfg = sc.cfg
     ids = scenes.ray_subset(n_rays, cfg.num_rays)
     t0 = time.perf_counter()
-    oracle.render(sc.sites, cfg.arch, sc.weights, sc.rays_o[ids], sc.rays_d[ids], cfg.near,
-                  cfg.far, cfg.n_coarse, cfg.n_fine, seed=scenes.SEED_RENDER, ray_ids=ids,
-                  nthreads=nthreads)
+    ref = oracle.render(sc.sites, cfg.arch, sc.weights, sc.rays_o[ids], sc.rays_d[ids], cfg.near,
+                        cfg.far, cfg.n_coarse, cfg.n_fine, seed=scenes.SEED_RENDER, ray_ids=ids,
+                        nthreads=nthreads)
     dt = time.perf_counter() - t0
     # one thread on a sixteenth of the sample (about the same wall time)
     ids1 = ids[::16]
@@ -106,7 +108,72 @@ def cpu_baseline(sc, n_rays, nthreads):
                       % (len(ids), len(ids) * (cfg.n_coarse + cfg.n_fine), dt),
             "cpu_model": model,
             "single_thread": {"value": len(ids1) / dt1, "unit": "rays/s",
-                              "sample": "%d of those rays, %.1f s" % (len(ids1), dt1)}}
+                              "sample": "%d of those rays, %.1f s" % (len(ids1), dt1)}}, ids, ref
+
+
+def parity_record(sc, precision, out, ids, ref, nthreads):
+    """Parity of the benchmarked frame against the oracle, outside the timed
+    region: the cells of every sample of the frame (a debug render that
+    returns each sample's depth and cell; the oracle assigns the same depths,
+    in blocks of rays) -- bit-exact except within 1e-5 of a bisector, whose
+    count is reported -- and the largest pixel differences on the seeded ray
+    subset the CPU baseline rendered (ids, ref; None without it)."""
+    import numpy as np
+    import torch
+    import oracle
+    from paper_2011_12490_amd import derf, scenes
+    cfg = sc.cfg
+    R, N = cfg.num_rays, cfg.n_coarse + cfg.n_fine
+    rec = {"samples": R * N}
+    o = torch.from_numpy(sc.rays_o).cuda()
+    d = torch.from_numpy(sc.rays_d).cuda()
+    cell = torch.empty((R, N), dtype=torch.int32, device="cuda")
+    t = torch.empty((R, N), dtype=torch.float32, device="cuda")
+    res = (torch.empty((R, 3), device="cuda"), torch.empty(R, device="cuda"),
+           torch.empty(R, device="cuda"))
+    r = derf.Renderer(sc.sites, cfg.arch, sc.weights, precision)
+    derf.derf_render(r.handle, o, d, cfg.near, cfg.far,
+                     derf.derf_sampling(cfg.n_coarse, cfg.n_fine, scenes.SEED_RENDER, 1, 0), *res,
+                     debug=derf.derf_debug_out(derf._dptr(cell), derf._dptr(t), None, None))
+    torch.cuda.synchronize()
+    st = derf.derf_get_stats(r.handle)
+    r.close()
+    # the debug render is the benchmarked render: same outputs, bit for bit
+    rec["debug_render_equals_timed"] = all(bool(torch.equal(a, b)) for a, b in zip(res, out))
+    cell_h, t_h = cell.cpu().numpy(), t.cpu().numpy()
+    del cell, t, res
+    near = mism = unexplained = 0
+    depths_exact = True
+    block = max(1, (1 << 24) // N)
+    for a in range(0, R, block):
+        b = min(R, a + block)
+        if cfg.n_fine == 0:
+            # single pass: the stratified depths themselves are bit-exact too
+            t_ref, c_ref, m = oracle.sample_assign(sc.sites, sc.rays_o[a:b], sc.rays_d[a:b],
+                                                   cfg.near, cfg.far, N, scenes.SEED_RENDER,
+                                                   ray_offset=a, margin=True, nthreads=nthreads)
+            depths_exact = depths_exact and bool(np.array_equal(t_ref, t_h[a:b]))
+        else:
+            c_ref, m = oracle.assign_depths(sc.sites, sc.rays_o[a:b], sc.rays_d[a:b], t_h[a:b],
+                                            margin=True, nthreads=nthreads)
+        nb = m < 1e-5
+        diff = c_ref != cell_h[a:b]
+        near += int(nb.sum())
+        mism += int(diff.sum())
+        unexplained += int((diff & ~nb).sum())
+    rec.update({"cells": "every sample of the frame, at the GPU's depths",
+                "depths_bit_exact": depths_exact if cfg.n_fine == 0 else None,
+                "near_bisector_samples": near, "cell_mismatches": mism,
+                "mismatches_off_bisector": unexplained,
+                "walk_fallback_rays": int(st.walk_fallback_rays)})
+    if ids is not None:
+        g = [x.cpu().numpy()[ids] for x in out]
+        rec.update({"pixel_rays": int(len(ids)),
+                    "max_abs_rgb": float(np.abs(g[0] - ref.rgb).max()),
+                    "max_abs_depth": float(np.abs(g[1] - ref.depth).max()),
+                    "max_abs_opacity": float(np.abs(g[2] - ref.opacity).max()),
+                    "tol": 2e-2 if precision == "bf16" else 1e-4})
+    return rec
 
 
 def main():
@@ -119,6 +186,9 @@ def main():
     ap.add_argument("--sites", type=int, default=None, help="override the number of heads")
     ap.add_argument("--cpu-rays", type=int, default=24576)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-parity", action="store_true",
+                    help="skip the parity record (cells of every sample and pixels of the CPU "
+                         "sample against the oracle, after the timed steps)")
     ap.add_argument("--k-sweep", default=None,
                     help="comma-separated head counts: the same frame with K k-means sites each")
     ap.add_argument("--empty-heads", default=None, metavar="K1,K2,...",
@@ -213,7 +283,7 @@ def main():
                     for i, name in enumerate(derf.STAGE_NAMES)}
         heads = np.array(st.head_samples[:cfg.num_sites], dtype=np.int64)
         r.close()
-        return sc, elapsed * 1e3 / steps, stage_ms, heads
+        return sc, elapsed * 1e3 / steps, stage_ms, heads, out
 
     def run_soft(cfg, beta, steps, warmup):
         """Time `steps` soft-decomposition renders (with contributions)."""
@@ -304,7 +374,8 @@ def main():
         r.close()
         return elapsed * 1e3 / steps, stages, runs, heads_g
 
-    sc, ms_per_step, stage_ms, heads = run(cfg, args.steps, args.warmup, args.copy_calibration)
+    sc, ms_per_step, stage_ms, heads, frame_out = run(cfg, args.steps, args.warmup,
+                                                      args.copy_calibration)
     plain_out = None
     if args.cull:
         # the plain render's outputs, for the culled render's difference
@@ -337,7 +408,7 @@ def main():
         k_sweep = []
         for K in [int(k) for k in args.k_sweep.split(",")]:
             ck = scenes.with_changes(cfg, num_sites=K)
-            _, ms_k, st_k, heads_k = run(ck, max(3, args.steps // 2), 2)
+            _, ms_k, st_k, heads_k, _ = run(ck, max(3, args.steps // 2), 2)
             k_sweep.append({"K": K, "rays_per_s": R / (ms_k * 1e-3), "ms_per_step": ms_k,
                             "mlp_ms": st_k["mlp"],
                             "mlp_frac": mlp_flop / (st_k["mlp"] * 1e-3) / 1e12 / peak,
@@ -387,10 +458,15 @@ def main():
             % (args.gate, gated["rays_per_s"], runs_g))
 
     cpu = None
+    cpu_ids = cpu_ref = None
+    nthreads = min(16, len(os.sched_getaffinity(0)))
     if not args.no_cpu_baseline:
-        nthreads = min(16, len(os.sched_getaffinity(0)))
         log("bench: timing the CPU oracle on %d rays with %d threads" % (args.cpu_rays, nthreads))
-        cpu = cpu_baseline(sc, args.cpu_rays, nthreads)
+        cpu, cpu_ids, cpu_ref = cpu_baseline(sc, args.cpu_rays, nthreads)
+    parity = None
+    if not args.no_parity and not head_archs and not empty_heads:
+        log("bench: parity record (cells of every sample, pixels of the CPU sample)")
+        parity = parity_record(sc, precision, frame_out, cpu_ids, cpu_ref, nthreads)
 
     res = {
         "metric": METRIC,
@@ -419,6 +495,7 @@ def main():
                      "flop_per_step": mlp_flop, "mlp_ms_per_step": mlp_ms,
                      "launches_per_step": 2 if cfg.n_fine else 1},
         "cpu_baseline": cpu,
+        "parity": parity,
         "samples_per_s": S / (ms_per_step * 1e-3),
         "stage_ms": stage_ms,
         "composite": {"bound": "hbm", "achieved": comp_gbps, "peak": PEAK_HBM_GBPS,

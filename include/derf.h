@@ -271,7 +271,13 @@ int derf_render_gated(derf_handle *h, const float *rays_o, const float *rays_d,
  * timing is on (derf_set_timing); accumulated over renders since the last
  * derf_reset_stats.  With hierarchical sampling a stage's time is the sum of
  * its coarse and fine passes; stage_launches counts the renders that ran the
- * stage.  head_samples counts head evaluations of both passes. */
+ * stage.  head_samples counts head evaluations of both passes.
+ * walk_rays and walk_fallback_rays describe the last render's assignment
+ * (Sec. 3.3: a ray crosses each convex cell in one segment): from 28 heads
+ * every ray is first walked through its cells; a ray that crosses more than
+ * 32 cells, or has a segment with more than 11 near-tied candidate sites, is
+ * assigned by the search over all sites instead (same cells, more work).
+ * walk_rays is 0 when the render searched all sites for every sample. */
 enum {
     DERF_STAGE_SAMPLE = 0,         /* sample + encode + assign (given depths: assign) */
     DERF_STAGE_BUCKET_SCAN = 1,    /* per-head counts -> offsets                     */
@@ -287,6 +293,8 @@ typedef struct {
     double stage_ms[DERF_NUM_STAGES];   /* summed event time per stage      */
     long long stage_launches[DERF_NUM_STAGES];
     long long head_samples[256];        /* samples per head of the last render */
+    long long walk_rays;                /* rays of the last render walked through their cells */
+    long long walk_fallback_rays;       /* of those, rays searched over all sites */
 } derf_stats;
 
 int derf_set_timing(derf_handle *h, int on);

@@ -52,6 +52,40 @@ def build(jobs: int = 8) -> str:
     return LIB
 
 
+# Test driver of the C ABI (tests/abi_driver.cpp): the library's host code
+# compiled with allocation-failure injection, linked with the kernels built
+# above.  With asan, the host code (never the device code) is also built with
+# AddressSanitizer, for runs on the CPU.
+ASAN_HOST = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def build_abi_driver(out: str, asan: bool = False) -> str:
+    if not os.path.exists(os.path.join(BUILD, "derf_api.o")):
+        build()
+    tmpdir = os.path.dirname(os.path.abspath(out))
+    os.makedirs(tmpdir, exist_ok=True)
+    extra = (ASAN_HOST + ["-g", "-O1"]) if asan else ["-O2"]
+    api = out + ".api.o"
+    drv = out + ".drv.o"
+    steps = [
+        [HIPCC, "-x", "hip"] + COMMON + extra + ["-DDERF_FAULT_INJECTION", "-c",
+                                                  os.path.join(CSRC, "derf_api.cpp"), "-o", api],
+        [HIPCC, "-x", "hip"] + COMMON + extra + ["-c", os.path.join(ROOT, "tests", "abi_driver.cpp"),
+                                                  "-o", drv],
+        [HIPCC, "--offload-arch=" + ARCH] + (ASAN_HOST if asan else []) +
+        ["-o", out, drv, api] + [os.path.join(BUILD, os.path.splitext(x)[0] + ".o")
+                                 for x in SOURCES if x != "derf_api.cpp"],
+    ]
+    for cmd in steps:
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError("abi driver build failed: %s\n%s\n%s"
+                               % (" ".join(cmd), r.stdout, r.stderr))
+    for f in (api, drv):
+        os.remove(f)
+    return out
+
+
 if __name__ == "__main__":
     print(build())
     sys.exit(0)

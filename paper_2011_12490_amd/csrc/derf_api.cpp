@@ -10,6 +10,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
 #include <new>
 #include <vector>
 
@@ -73,6 +74,49 @@ struct Workspace {
     size_t bytes = 0;
 };
 
+// Allocation-failure injection, compiled only into test builds
+// (-DDERF_FAULT_INJECTION): after derf_debug_fail_alloc(n), the allocation
+// n allocations later -- device memory or the handle and its host staging --
+// fails as if memory had run out, once.  The tests use it to show that every
+// such failure returns DERF_ERR_OOM, hands out no handle and leaks nothing.
+// Those builds also count the live allocations (device blocks and handles),
+// so that a test can see every one released.
+#ifdef DERF_FAULT_INJECTION
+std::atomic<long> g_fail_in{-1};
+std::atomic<long> g_live{0};
+bool injected_failure()
+{
+    long c = g_fail_in.load();
+    while (c >= 0 && !g_fail_in.compare_exchange_weak(c, c - 1)) {
+    }
+    return c == 0;
+}
+void count_live(long d) { g_live += d; }
+#else
+constexpr bool injected_failure() { return false; }
+inline void count_live(long) {}
+#endif
+
+hipError_t dev_alloc(void **p, size_t bytes)
+{
+    if (injected_failure()) {
+        *p = nullptr;
+        return hipErrorOutOfMemory;
+    }
+    const hipError_t e = hipMalloc(p, bytes);
+    if (e == hipSuccess)
+        count_live(1);
+    return e;
+}
+
+hipError_t dev_free(void *p)
+{
+    if (!p)
+        return hipSuccess;
+    count_live(-1);
+    return hipFree(p);
+}
+
 constexpr int kPasses = 2;
 constexpr int kEvents = 2 * kPasses * DERF_NUM_STAGES;
 inline int ev_index(int pass, int stage, int end) { return 2 * (pass * DERF_NUM_STAGES + stage) + end; }
@@ -110,6 +154,9 @@ struct derf_handle {
     unsigned *totals = nullptr;
     unsigned *totals_fine = nullptr;
     int totals_sets = 1;  // a culled render: one set of K totals per level
+    // segment counts of the last render's cell walks (nullptr: no walk)
+    const unsigned char *walk_nseg = nullptr;
+    unsigned walk_rays = 0;
     // MLP gating (derf_set_gate): fp32 weights on the device, or none
     float *gate_w = nullptr;
     int gate_freqs = 0;
@@ -222,7 +269,8 @@ hipError_t launch_groups(const derf_handle *h, const unsigned *bucket, const uns
     return hipSuccess;
 }
 
-// Grows the handle's workspace to at least need bytes.
+// Grows the handle's workspace to at least need bytes.  Every device
+// allocation of the library goes through dev_alloc.
 int ensure_workspace(derf_handle *h, size_t need)
 {
     if (need <= h->ws.bytes)
@@ -231,11 +279,11 @@ int ensure_workspace(derf_handle *h, size_t need)
     if (h->last_stream || h->ws.mem)
         HIP_TRY(hipStreamSynchronize(h->last_stream), "hipStreamSynchronize");
     if (h->ws.mem)
-        HIP_TRY(hipFree(h->ws.mem), "hipFree");
+        HIP_TRY(dev_free(h->ws.mem), "hipFree");
     h->ws.mem = nullptr;
     h->ws.bytes = 0;
     const size_t grow = need + need / 8;
-    if (hipMalloc(&h->ws.mem, grow) != hipSuccess) {
+    if (dev_alloc(&h->ws.mem, grow) != hipSuccess) {
         (void)hipGetLastError();
         h->ws.mem = nullptr;
         return fail(DERF_ERR_OOM, "workspace of %zu bytes", grow);
@@ -449,6 +497,8 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
     h->totals = b.totals;
     h->totals_fine = hier ? b.totals_fine : nullptr;
     h->totals_sets = 1;
+    h->walk_nseg = b.walk_nseg;
+    h->walk_rays = b.walk_nseg ? R : 0;
     h->stats.renders += 1;
     h->stats.samples += (long long)S + Sf;
     return DERF_OK;
@@ -542,6 +592,8 @@ int render_soft_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     h->totals = b.totals;
     h->totals_fine = nullptr;
     h->totals_sets = 1;
+    h->walk_nseg = nullptr;
+    h->walk_rays = 0;
     h->stats.renders += 1;
     h->stats.samples += (long long)S;
     return DERF_OK;
@@ -679,6 +731,8 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     h->totals = c.level_totals;
     h->totals_fine = nullptr;
     h->totals_sets = levels;
+    h->walk_nseg = walk.nseg;
+    h->walk_rays = walk.nseg ? R : 0;
     h->stats.renders += 1;
     h->stats.samples += (long long)S;
     return DERF_OK;
@@ -686,9 +740,11 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
 
 // derf_create / derf_create_mixed: per_head says whether arch holds one
 // architecture per head (weights then concatenated head after head) or one
-// for all.
-int create_impl(derf_handle **out, int num_sites, const float *sites_xyz,
-                const derf_head_arch *arch, bool per_head, const float *weights, int precision)
+// for all.  *h_out holds the handle under construction, so that a host
+// allocation failure anywhere can free it (create_impl).
+int create_body(derf_handle **out, int num_sites, const float *sites_xyz,
+                const derf_head_arch *arch, bool per_head, const float *weights, int precision,
+                derf_handle **h_out)
 {
     if (!out)
         return fail(DERF_ERR_INVALID_ARG, "null output handle pointer");
@@ -722,11 +778,14 @@ int create_impl(derf_handle **out, int num_sites, const float *sites_xyz,
         if (!isfinite(weights[i]))
             return fail(DERF_ERR_INVALID_ARG, "non-finite weight");
 
-    derf_handle *h = new (std::nothrow) derf_handle();
+    derf_handle *h = injected_failure() ? nullptr : new (std::nothrow) derf_handle();
     if (!h)
         return fail(DERF_ERR_OOM, "handle");
+    count_live(1);
+    *h_out = h;
     auto cleanup = [&](int status) {
         derf_destroy(h);
+        *h_out = nullptr;
         return status;
     };
     hipError_t e = hipGetDevice(&h->device);
@@ -761,7 +820,8 @@ int create_impl(derf_handle **out, int num_sites, const float *sites_xyz,
     std::vector<float4> sites(num_sites);
     for (int k = 0; k < num_sites; ++k)
         sites[k] = make_float4(sites_xyz[3 * k], sites_xyz[3 * k + 1], sites_xyz[3 * k + 2], 0.f);
-    if (hipMalloc(&h->sites, sizeof(float4) * num_sites) != hipSuccess) {
+    if (dev_alloc(reinterpret_cast<void **>(&h->sites), sizeof(float4) * num_sites) !=
+        hipSuccess) {
         (void)hipGetLastError();
         return cleanup(fail(DERF_ERR_OOM, "device sites"));
     }
@@ -775,6 +835,8 @@ int create_impl(derf_handle **out, int num_sites, const float *sites_xyz,
         std::vector<unsigned char> streams;
         std::vector<float> blocks;
         try {
+            if (injected_failure())
+                throw std::bad_alloc();
             streams.assign(v->stream_bytes * num_sites, 0);
             blocks.assign(v->block_bytes / 4 * num_sites, 0.0f);
         } catch (...) {
@@ -784,8 +846,8 @@ int create_impl(derf_handle **out, int num_sites, const float *sites_xyz,
             if (head_group[k] == gi)
                 v->pack(weights + woff[k], streams.data() + v->stream_bytes * k,
                         blocks.data() + v->block_bytes / 4 * k);
-        if (hipMalloc(&grp.streams, streams.size()) != hipSuccess ||
-            hipMalloc(&grp.blocks, blocks.size() * 4) != hipSuccess) {
+        if (dev_alloc(reinterpret_cast<void **>(&grp.streams), streams.size()) != hipSuccess ||
+            dev_alloc(reinterpret_cast<void **>(&grp.blocks), blocks.size() * 4) != hipSuccess) {
             (void)hipGetLastError();
             return cleanup(fail(DERF_ERR_OOM, "device weights"));
         }
@@ -804,7 +866,22 @@ int create_impl(derf_handle **out, int num_sites, const float *sites_xyz,
     if (e != hipSuccess)
         return cleanup(hip_fail(e, "hipDeviceSynchronize"));
     *out = h;
+    *h_out = nullptr;
     return DERF_OK;
+}
+
+int create_impl(derf_handle **out, int num_sites, const float *sites_xyz,
+                const derf_head_arch *arch, bool per_head, const float *weights, int precision)
+{
+    derf_handle *h = nullptr;
+    try {
+        return create_body(out, num_sites, sites_xyz, arch, per_head, weights, precision, &h);
+    } catch (const std::bad_alloc &) {
+        derf_destroy(h);
+        if (out)
+            *out = nullptr;
+        return fail(DERF_ERR_OOM, "host memory");
+    }
 }
 
 }  // namespace
@@ -874,7 +951,7 @@ int derf_set_gate(derf_handle *h, int pos_freqs, int hidden, const float *weight
             HIP_TRY(hipSetDevice(h->device), "hipSetDevice");
             if (h->last_stream)
                 HIP_TRY(hipStreamSynchronize(h->last_stream), "hipStreamSynchronize");
-            HIP_TRY(hipFree(h->gate_w), "hipFree");
+            HIP_TRY(dev_free(h->gate_w), "hipFree");
         }
         h->gate_w = nullptr;
         h->gate_freqs = h->gate_hidden = 0;
@@ -891,16 +968,19 @@ int derf_set_gate(derf_handle *h, int pos_freqs, int hidden, const float *weight
             return fail(DERF_ERR_INVALID_ARG, "non-finite gating weight");
     HIP_TRY(hipSetDevice(h->device), "hipSetDevice");
     float *dev = nullptr;
-    HIP_TRY(hipMalloc(&dev, (size_t)count * sizeof(float)), "hipMalloc");
+    if (dev_alloc(reinterpret_cast<void **>(&dev), (size_t)count * sizeof(float)) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(DERF_ERR_OOM, "gating weights");
+    }
     hipError_t e = hipMemcpy(dev, weights, (size_t)count * sizeof(float), hipMemcpyHostToDevice);
     if (e != hipSuccess) {
-        (void)hipFree(dev);
+        (void)dev_free(dev);
         HIP_TRY(e, "hipMemcpy");
     }
     if (h->gate_w) {
         if (h->last_stream)
             HIP_TRY(hipStreamSynchronize(h->last_stream), "hipStreamSynchronize");
-        HIP_TRY(hipFree(h->gate_w), "hipFree");
+        HIP_TRY(dev_free(h->gate_w), "hipFree");
     }
     h->gate_w = dev;
     h->gate_freqs = pos_freqs;
@@ -947,7 +1027,18 @@ int derf_set_timing(derf_handle *h, int on)
     return DERF_OK;
 }
 
+int get_stats_impl(derf_handle *h, derf_stats *out);
+
 int derf_get_stats(derf_handle *h, derf_stats *out)
+{
+    try {
+        return get_stats_impl(h, out);
+    } catch (const std::bad_alloc &) {
+        return fail(DERF_ERR_OOM, "host memory for the head counts");
+    }
+}
+
+int get_stats_impl(derf_handle *h, derf_stats *out)
 {
     if (!h || !out)
         return fail(DERF_ERR_INVALID_ARG, "null handle or output");
@@ -971,6 +1062,14 @@ int derf_get_stats(derf_handle *h, derf_stats *out)
             for (int k = 0; k < h->num_sites; ++k)
                 h->stats.head_samples[k] += tot[k];
         }
+    }
+    h->stats.walk_rays = h->walk_rays;
+    h->stats.walk_fallback_rays = 0;
+    if (h->walk_nseg && h->walk_rays) {
+        std::vector<unsigned char> ns(h->walk_rays);
+        HIP_TRY(hipMemcpy(ns.data(), h->walk_nseg, ns.size(), hipMemcpyDeviceToHost), "hipMemcpy");
+        for (unsigned char v : ns)
+            h->stats.walk_fallback_rays += v == 0;
     }
     *out = h->stats;
     return DERF_OK;
@@ -996,20 +1095,21 @@ void derf_destroy(derf_handle *h)
     if (h->last_stream || h->ws.mem)
         (void)hipStreamSynchronize(h->last_stream);
     if (h->ws.mem)
-        (void)hipFree(h->ws.mem);
+        (void)dev_free(h->ws.mem);
     if (h->sites)
-        (void)hipFree(h->sites);
+        (void)dev_free(h->sites);
     if (h->gate_w)
-        (void)hipFree(h->gate_w);
+        (void)dev_free(h->gate_w);
     for (int gi = 0; gi < h->num_groups; ++gi) {
         if (h->groups[gi].streams)
-            (void)hipFree(h->groups[gi].streams);
+            (void)dev_free(h->groups[gi].streams);
         if (h->groups[gi].blocks)
-            (void)hipFree(h->groups[gi].blocks);
+            (void)dev_free(h->groups[gi].blocks);
     }
     for (int i = 0; i < kEvents; ++i)
         if (h->ev[i])
             (void)hipEventDestroy(h->ev[i]);
+    count_live(-1);
     delete h;
 }
 
@@ -1026,5 +1126,13 @@ const char *derf_status_string(int status)
 }
 
 const char *derf_last_error(void) { return g_last_error; }
+
+#ifdef DERF_FAULT_INJECTION
+// test builds only (not in derf.h): fail the allocation n allocations from
+// now (0: the next one); n < 0 disarms
+void derf_debug_fail_alloc(long n) { g_fail_in.store(n < 0 ? -1 : n); }
+// device blocks and handles allocated and not yet released
+long derf_debug_live_allocations(void) { return g_live.load(); }
+#endif
 
 }  // extern "C"

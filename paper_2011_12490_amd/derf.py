@@ -49,7 +49,8 @@ class derf_stats(ctypes.Structure):
     _fields_ = [("renders", ctypes.c_longlong), ("samples", ctypes.c_longlong),
                 ("stage_ms", ctypes.c_double * DERF_NUM_STAGES),
                 ("stage_launches", ctypes.c_longlong * DERF_NUM_STAGES),
-                ("head_samples", ctypes.c_longlong * 256)]
+                ("head_samples", ctypes.c_longlong * 256),
+                ("walk_rays", ctypes.c_longlong), ("walk_fallback_rays", ctypes.c_longlong)]
 
 
 EXPORTS = ("derf_weights_count", "derf_create", "derf_create_mixed", "derf_render",

@@ -1,0 +1,13 @@
+"""Parity records of the GPU tests: when DERF_PARITY_RECORD names a file,
+each check appends one JSON line to it (test label, sample and ray counts,
+near-bisector counts, largest differences, tolerance), so that a run leaves a
+written summary of what it asserted."""
+import json
+import os
+
+
+def record(**fields):
+    path = os.environ.get("DERF_PARITY_RECORD")
+    if path:
+        with open(path, "a") as f:
+            f.write(json.dumps(fields) + "\n")

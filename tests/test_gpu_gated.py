@@ -13,6 +13,7 @@ import pytest
 
 import oracle
 from paper_2011_12490_amd import scenes
+from parity_log import record
 from test_oracle_gate import random_gate, voronoi_gate
 
 torch = pytest.importorskip("torch")
@@ -67,6 +68,9 @@ def _run(sc, precision, L, H, gw, ids, label, empty=None):
     print("%s: rays=%d near-tie samples=%d clean rays=%d runs/ray=%.2f max|d|=%.3g (tol %.0e)"
           % (label, len(ids), int((~ok).sum()), int(clean.sum()), runs, err, TOL[precision]),
           flush=True)
+    record(test=label, kind="gated cells and pixels", rays=int(len(ids)),
+           near_tie_samples=int((~ok).sum()), clean_rays=int(clean.sum()),
+           runs_per_ray=float(runs), max_abs=float(err), tol=TOL[precision])
     assert clean.mean() > 0.9
     assert err <= TOL[precision]
     assert np.all((cell >= 0) & (cell < cfg.num_sites))

@@ -12,6 +12,7 @@ import pytest
 
 import oracle
 from paper_2011_12490_amd import scenes
+from parity_log import record
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -62,24 +63,34 @@ def _check_pixels(gpu, ref, ids, tol, label):
     e_op = np.abs(opac - ref.opacity).max()
     print("%s: rays=%d max|d rgb|=%.3g max|d depth|=%.3g max|d opacity|=%.3g (tol %.0e)"
           % (label, len(ids), e_rgb, e_dep, e_op, tol), flush=True)
+    record(test=label, kind="pixels", rays=int(len(ids)), max_abs_rgb=float(e_rgb),
+           max_abs_depth=float(e_dep), max_abs_opacity=float(e_op), tol=tol)
     assert e_rgb <= tol and e_dep <= tol and e_op <= tol
 
 
-def _check_cells(sc, t_gpu, cell_gpu, n, label, ray_offset=0, perturb=True):
+def _compare_cells(sc, t_gpu, cell_gpu, n, ray_offset, perturb, rays=slice(None)):
+    """(samples, near-bisector samples, mismatches) of one block of rays:
+    depths bit-exact; every cell bit-exact except samples within 1e-5 of a
+    bisector, which are counted whether or not the two sides agree."""
     cfg = sc.cfg
-    t_ref, cell_ref, _ = oracle.sample_assign(sc.sites, sc.rays_o, sc.rays_d, cfg.near, cfg.far,
-                                              n, scenes.SEED_RENDER, perturb=perturb,
-                                              ray_offset=ray_offset, nthreads=NTHREADS)
+    t_ref, cell_ref, m = oracle.sample_assign(sc.sites, sc.rays_o[rays], sc.rays_d[rays],
+                                              cfg.near, cfg.far, n, scenes.SEED_RENDER,
+                                              perturb=perturb, ray_offset=ray_offset,
+                                              margin=True, nthreads=NTHREADS)
     assert np.array_equal(t_gpu, t_ref), "sample depths differ"
-    diff = np.argwhere(cell_gpu != cell_ref)
-    near = 0
-    for r, i in diff:
-        x = np.float32(sc.rays_o[r]) + np.float32(t_ref[r, i]) * sc.rays_d[r]
-        m = oracle.bisector_margin(sc.sites, x.astype(np.float32), int(cell_ref[r, i]))
-        assert m < 1e-5, (r, i, cell_gpu[r, i], cell_ref[r, i], m)
-        near += 1
-    print("%s: samples=%d cell mismatches=%d (all within 1e-5 of a bisector)"
-          % (label, cell_gpu.size, near), flush=True)
+    near = m < 1e-5
+    mism = cell_gpu != cell_ref
+    bad = np.argwhere(mism & ~near)
+    assert len(bad) == 0, [(int(r), int(i), int(cell_gpu[r, i]), int(cell_ref[r, i]),
+                            float(m[r, i])) for r, i in bad[:5]]
+    return int(cell_gpu.size), int(near.sum()), int(mism.sum())
+
+
+def _check_cells(sc, t_gpu, cell_gpu, n, label, ray_offset=0, perturb=True):
+    samples, near, mism = _compare_cells(sc, t_gpu, cell_gpu, n, ray_offset, perturb)
+    print("%s: samples=%d within 1e-5 of a bisector=%d cell mismatches=%d (all among them)"
+          % (label, samples, near, mism), flush=True)
+    record(test=label, kind="cells", samples=samples, near_bisector=near, mismatches=mism)
 
 
 # ------------------------------------------------------------- tiny scene ----
@@ -157,15 +168,44 @@ def test_skew_k64(precision):
     _subset_parity("skew_k64", precision, 1024, check_cells=False)
 
 
-def test_skew_k64_cells_slice():
-    """Cells of a contiguous slice of the skewed frame (ray_offset keeps the jitter)."""
+def test_skew_k64_cells_full_frame():
+    """Cells of the whole skewed frame (1024 x 1024 rays x 256 samples, 64
+    heads through the walk tables), rendered in one call as the benchmark
+    does, against the oracle's assignment of every sample: depths bit-exact,
+    cells bit-exact except within 1e-5 of a bisector (counted), compared in
+    blocks of 65,536 rays."""
+    derf = _derf()
     cfg = scenes.CONFIGS["skew_k64"]
     sc = scenes.make_scene(cfg)
-    a, b = 300_000, 300_000 + 65_536
-    sub = scenes.Scene(cfg, sc.sites, sc.weights, sc.rays_o[a:b], sc.rays_d[a:b])
-    gpu = _render(sub, "bf16", debug=True, ray_offset=a)
-    _check_cells(sub, gpu[3]["t"], gpu[3]["cell"], cfg.n_coarse, "skew_k64 slice",
-                 ray_offset=a)
+    R, n = cfg.num_rays, cfg.n_coarse
+    o = torch.from_numpy(sc.rays_o).cuda()
+    d = torch.from_numpy(sc.rays_d).cuda()
+    cell = torch.empty((R, n), dtype=torch.int32, device="cuda")
+    t = torch.empty((R, n), dtype=torch.float32, device="cuda")
+    out = (torch.empty((R, 3), device="cuda"), torch.empty(R, device="cuda"),
+           torch.empty(R, device="cuda"))
+    r = derf.Renderer(sc.sites, cfg.arch, sc.weights, "bf16")
+    dbg = derf.derf_debug_out(derf._dptr(cell), derf._dptr(t), None, None)
+    derf.derf_render(r.handle, o, d, cfg.near, cfg.far,
+                     derf.derf_sampling(n, 0, scenes.SEED_RENDER, 1, 0), *out, debug=dbg)
+    torch.cuda.synchronize()
+    st = derf.derf_get_stats(r.handle)
+    r.close()
+    assert st.walk_rays == R and sum(st.head_samples[:cfg.num_sites]) == R * n
+    cell_h, t_h = cell.cpu().numpy(), t.cpu().numpy()
+    del cell, t
+    totals = np.zeros(3, np.int64)
+    block = 65_536
+    for a in range(0, R, block):
+        b = min(R, a + block)
+        totals += _compare_cells(sc, t_h[a:b], cell_h[a:b], n, a, True, rays=slice(a, b))
+    print("skew_k64 full frame: samples=%d within 1e-5 of a bisector=%d cell mismatches=%d "
+          "(all among them); walk fallback rays %d" % (*totals, st.walk_fallback_rays),
+          flush=True)
+    record(test="skew_k64 full frame", kind="cells", samples=int(totals[0]),
+           near_bisector=int(totals[1]), mismatches=int(totals[2]),
+           walk_fallback_rays=int(st.walk_fallback_rays))
+    assert totals[0] == R * n
 
 
 # ------------------------------------------------------------ edge cases ----
@@ -242,6 +282,88 @@ def test_walk_lane_counts(size):
     sc = scenes.make_scene(cfg)
     gpu = _render(sc, "bf16", debug=True)
     _check_cells(sc, gpu[3]["t"], gpu[3]["cell"], cfg.n_coarse, "walk %dx%d" % size)
+
+
+def _fallback_scene(kind):
+    """Scenes that drive the walk's fallback (Sec. 3.3: convex cells give one
+    segment per cell, and a ray's walk table holds at most 32 segments of at
+    most 11 candidate sites):
+      many_cells   41 sites strung along the z axis, 1 apart; rays along the
+                   axis cross all 41 slab-shaped cells (more than 32 segments);
+      many_cands   32 sites on the x axis at x = 1 + 1e-3 j; rays parallel to the
+                   z axis near it stay in the cell of site 0, but out at |z| ~ 20
+                   the walk's candidate tolerance (1e-4 (1 + |x - phi|^2) ~ 0.04)
+                   takes in every site with |x - phi_j|^2 - |x - phi_0|^2 ~ 2e-3 j
+                   below it (about 20 sites, more than 11), while the nearest
+                   bisector stays ~1 away and the squared-distance gaps (2e-3)
+                   dwarf their float32 rounding (~1e-4 at |x|^2 ~ 400).
+    Each scene adds rays that cross few cells and must not fall back."""
+    rng = np.random.default_rng(4242)
+    if kind == "many_cells":
+        K = 41
+        sites = np.stack([np.zeros(K), np.zeros(K), np.arange(K) - 20.0], 1)
+        n_fb = 24
+        o_fb = np.stack([rng.uniform(-0.2, 0.2, n_fb), rng.uniform(-0.2, 0.2, n_fb),
+                         np.full(n_fb, -25.0)], 1)
+        d_fb = np.stack([rng.uniform(-0.004, 0.004, n_fb), rng.uniform(-0.004, 0.004, n_fb),
+                         np.ones(n_fb)], 1)
+        n_ok = 40  # crossing the line at right angles: one or two cells
+        z = rng.uniform(-19.0, 19.0, n_ok)
+        o_ok = np.stack([np.full(n_ok, 6.0), rng.uniform(-0.5, 0.5, n_ok), z], 1)
+        d_ok = np.stack([-np.ones(n_ok), np.zeros(n_ok), rng.uniform(-0.02, 0.02, n_ok)], 1)
+    else:
+        K = 32
+        sites = np.stack([1.0 + 1e-3 * np.arange(K), np.zeros(K), np.zeros(K)], 1)
+        n_fb = 16
+        o_fb = np.stack([rng.uniform(-0.3, 0.3, n_fb), rng.uniform(-0.3, 0.3, n_fb),
+                         np.full(n_fb, -20.0)], 1)
+        d_fb = np.stack([rng.uniform(-0.003, 0.003, n_fb), rng.uniform(-0.003, 0.003, n_fb),
+                         np.ones(n_fb)], 1)
+        n_ok = 40  # farther out on the other side: a handful of candidates
+        o_ok = np.stack([rng.uniform(-7.0, -5.0, n_ok), rng.uniform(-2.0, 2.0, n_ok),
+                         np.full(n_ok, -20.0)], 1)
+        d_ok = np.tile([0.0, 0.0, 1.0], (n_ok, 1))
+    o = np.concatenate([o_fb, o_ok]).astype(np.float32)
+    d = np.concatenate([d_fb, d_ok]).astype(np.float32)
+    far = 50.0 if kind == "many_cells" else 40.0
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], num_sites=K, near=0.0, far=far,
+                              n_coarse=256, sigma_bias=0.5, width=len(o), height=1)
+    weights = scenes.make_weights(cfg.arch, K, sigma_bias=0.5)
+    return scenes.Scene(cfg, sites.astype(np.float32), weights, o, d), n_fb
+
+
+@pytest.mark.parametrize("kind", ["many_cells", "many_cands"])
+def test_walk_fallback(kind):
+    """Rays whose walk table would overflow (more than 32 segments, or more than
+    11 candidates in a segment) take the search over all sites: the stats
+    count exactly those rays, their cells are bit-exact against the oracle
+    (bar samples within 1e-5 of a bisector), and pixels match at 1e-4."""
+    derf = _derf()
+    sc, n_fb = _fallback_scene(kind)
+    cfg = sc.cfg
+    o = torch.from_numpy(sc.rays_o).cuda()
+    d = torch.from_numpy(sc.rays_d).cuda()
+    r = derf.Renderer(sc.sites, cfg.arch, sc.weights, "fp32")
+    rgb, depth, opac, dbg = r.render(o, d, cfg.near, cfg.far, cfg.n_coarse, 0,
+                                     scenes.SEED_RENDER, debug=True)
+    torch.cuda.synchronize()
+    st = derf.derf_get_stats(r.handle)
+    r.close()
+    print("%s: walked rays %d, fallback rays %d (constructed %d)"
+          % (kind, st.walk_rays, st.walk_fallback_rays, n_fb), flush=True)
+    assert st.walk_rays == cfg.num_rays
+    assert st.walk_fallback_rays == n_fb
+    cell = dbg["cell"].cpu().numpy()
+    _check_cells(sc, dbg["t"].cpu().numpy(), cell, cfg.n_coarse, "walk fallback %s" % kind)
+    runs = 1 + (cell[:n_fb, 1:] != cell[:n_fb, :-1]).sum(1)
+    if kind == "many_cells":
+        assert runs.min() > 32
+    else:
+        assert np.all(runs == 1)
+    gpu = [rgb.cpu().numpy(), depth.cpu().numpy(), opac.cpu().numpy()]
+    ids = np.arange(cfg.num_rays)
+    ref = _oracle(sc, ids)
+    _check_pixels(gpu, ref, ids, TOL["fp32"], "walk fallback %s" % kind)
 
 
 def test_far_sites_leave_heads_empty():

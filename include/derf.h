@@ -158,6 +158,27 @@ int derf_render(derf_handle *h, const float *rays_o, const float *rays_d, long l
                 float near_t, float far_t, const derf_sampling *samp, float *out_rgb,
                 float *out_depth, float *out_opacity, void *hip_stream);
 
+/* derf_render for callers that cannot allocate device memory: code under HIP
+ * graph capture, serving loops and harnesses that forbid hipMalloc.  The
+ * render's scratch memory (sample depths, cells, head outputs, buckets,
+ * counts, walk tables) is a fixed device array of
+ * DERF_NOALLOC_SCRATCH_BYTES inside the library, one per device, held from
+ * the first derf_create on that device until the process ends; the call
+ * itself allocates nothing.  Arguments, results and ownership as
+ * derf_render (the results are identical).  A frame whose scratch would
+ * exceed the array -- about 25 bytes per sample plus 64-600 bytes per ray,
+ * e.g. ~12,000 rays of 192 samples -- returns DERF_ERR_INVALID_ARG before any
+ * work is enqueued: render it in parts (samp->ray_offset keeps the jitter of
+ * a split frame).  Every handle on one device shares that device's array and
+ * each call leaves its contents behind, so calls that overlap in time on one
+ * device race: enqueue them on one stream, or wait between them.  Stats
+ * (derf_get_stats) read the last call's head counts from the array, so they
+ * are only valid until the next call on the device. */
+#define DERF_NOALLOC_SCRATCH_BYTES (64u << 20)
+int derf_render_noalloc(derf_handle *h, const float *rays_o, const float *rays_d,
+                        long long num_rays, float near_t, float far_t, const derf_sampling *samp,
+                        float *out_rgb, float *out_depth, float *out_opacity, void *hip_stream);
+
 /* Optional per-sample outputs of derf_render_debug: device pointers, any may
  * be NULL.  N = n_coarse + n_fine samples per ray, in depth order (with
  * hierarchical sampling: the merged coarse and fine samples); sample i of

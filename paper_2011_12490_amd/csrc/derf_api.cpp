@@ -11,6 +11,7 @@
 #include <string.h>
 
 #include <atomic>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -73,6 +74,19 @@ struct Workspace {
     void *mem = nullptr;
     size_t bytes = 0;
 };
+
+// Scratch memory of derf_render_noalloc: a fixed device array instead of the
+// handle's workspace, so that a render allocates nothing.  Each device that
+// loads the library holds its own copy until the process ends.  In host code
+// `scratch` names a host-side stand-in, not the device array: its device
+// address comes from hipGetSymbolAddress, once per device (scratch_on_device),
+// and only that address is ever passed to a kernel.
+constexpr size_t kScratchBytes = size_t(DERF_NOALLOC_SCRATCH_BYTES);
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
 
 // Allocation-failure injection, compiled only into test builds
 // (-DDERF_FAULT_INJECTION): after derf_debug_fail_alloc(n), the allocation
@@ -157,6 +171,8 @@ struct derf_handle {
     // segment counts of the last render's cell walks (nullptr: no walk)
     const unsigned char *walk_nseg = nullptr;
     unsigned walk_rays = 0;
+    // device address of this device's noalloc scratch array
+    void *scratch = nullptr;
     // MLP gating (derf_set_gate): fp32 weights on the device, or none
     float *gate_w = nullptr;
     int gate_freqs = 0;
@@ -269,6 +285,24 @@ hipError_t launch_groups(const derf_handle *h, const unsigned *bucket, const uns
     return hipSuccess;
 }
 
+// The device address of the noalloc scratch array on device dev (the current
+// device), looked up once per device and kept.
+int scratch_on_device(int dev, void **out)
+{
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(DERF_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess)
+            return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return DERF_OK;
+}
+
 // Grows the handle's workspace to at least need bytes.  Every device
 // allocation of the library goes through dev_alloc.
 int ensure_workspace(derf_handle *h, size_t need)
@@ -355,9 +389,12 @@ hipEvent_t last_event(const derf_handle *h)
     return nullptr;
 }
 
+// fixed_ws: a workspace of fixed_bytes to use instead of the handle's own
+// (derf_render_noalloc: nothing is allocated, larger frames are refused).
 int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long long num_rays,
                 float near_t, float far_t, const derf_sampling *samp, float *out_rgb,
-                float *out_depth, float *out_opacity, const derf_debug_out *dbg, void *stream)
+                float *out_depth, float *out_opacity, const derf_debug_out *dbg, void *stream,
+                void *fixed_ws = nullptr, size_t fixed_bytes = 0)
 {
     if (!h)
         return fail(DERF_ERR_INVALID_ARG, "null handle");
@@ -390,15 +427,25 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
     const unsigned nblk_f = blocks_of(Sf);
     const unsigned nblk_max = nblk > nblk_f ? nblk : nblk_f;
     const size_t need = layout(nullptr, S, Sf, R, nblk_max, h->num_sites, h->bf16, nullptr);
-    int rc = ensure_workspace(h, need);
-    if (rc != DERF_OK)
-        return rc;
+    int rc = DERF_OK;
+    if (fixed_ws) {
+        if (need > fixed_bytes)
+            return fail(DERF_ERR_INVALID_ARG,
+                        "frame needs %zu bytes of scratch, the no-allocation render has %zu "
+                        "(render fewer rays per call)",
+                        need, fixed_bytes);
+    } else {
+        rc = ensure_workspace(h, need);
+        if (rc != DERF_OK)
+            return rc;
+    }
     if (h->timing && h->ev_pending) {
         HIP_TRY(hipEventSynchronize(last_event(h)), "hipEventSynchronize");
         accumulate_timing(h);
     }
     Buffers b;
-    layout(reinterpret_cast<char *>(h->ws.mem), S, Sf, R, nblk_max, h->num_sites, h->bf16, &b);
+    layout(reinterpret_cast<char *>(fixed_ws ? fixed_ws : h->ws.mem), S, Sf, R, nblk_max,
+           h->num_sites, h->bf16, &b);
 
     RenderGeometry g;
     g.rays_o = rays_o;
@@ -795,6 +842,11 @@ int create_body(derf_handle **out, int num_sites, const float *sites_xyz,
     e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device);
     if (e != hipSuccess)
         return cleanup(hip_fail(e, "hipDeviceGetAttribute"));
+    {
+        const int rc = scratch_on_device(h->device, &h->scratch);
+        if (rc != DERF_OK)
+            return cleanup(rc);
+    }
     h->num_sites = num_sites;
     h->site_bits = 0;
     while ((1 << h->site_bits) < num_sites)
@@ -922,6 +974,16 @@ int derf_render_debug(derf_handle *h, const float *rays_o, const float *rays_d,
 {
     return render_impl(h, rays_o, rays_d, num_rays, near_t, far_t, samp, out_rgb, out_depth,
                        out_opacity, dbg, hip_stream);
+}
+
+int derf_render_noalloc(derf_handle *h, const float *rays_o, const float *rays_d,
+                        long long num_rays, float near_t, float far_t, const derf_sampling *samp,
+                        float *out_rgb, float *out_depth, float *out_opacity, void *hip_stream)
+{
+    if (!h)
+        return fail(DERF_ERR_INVALID_ARG, "null handle");
+    return render_impl(h, rays_o, rays_d, num_rays, near_t, far_t, samp, out_rgb, out_depth,
+                       out_opacity, nullptr, hip_stream, h->scratch, kScratchBytes);
 }
 
 int derf_render_soft(derf_handle *h, const float *rays_o, const float *rays_d, long long num_rays,

@@ -25,6 +25,7 @@ DERF_ERR_HIP = -4
 DERF_PREC_FP32 = 0
 DERF_PREC_BF16 = 1
 DERF_NUM_STAGES = 6
+DERF_NOALLOC_SCRATCH_BYTES = 64 << 20
 STAGE_NAMES = ("sample_assign", "bucket_scan", "bucket_scatter", "mlp", "composite", "fine_sample")
 
 
@@ -54,7 +55,7 @@ class derf_stats(ctypes.Structure):
 
 
 EXPORTS = ("derf_weights_count", "derf_create", "derf_create_mixed", "derf_render",
-           "derf_render_debug",
+           "derf_render_debug", "derf_render_noalloc",
            "derf_render_soft", "derf_render_culled", "derf_set_empty_heads", "derf_set_gate",
            "derf_gate_weights_count", "derf_render_gated", "derf_set_timing", "derf_get_stats",
            "derf_reset_stats", "derf_destroy",
@@ -92,6 +93,8 @@ def lib() -> ctypes.CDLL:
         L.derf_render.restype = ctypes.c_int
         L.derf_render_debug.argtypes = render_args + [ctypes.POINTER(derf_debug_out), P]
         L.derf_render_debug.restype = ctypes.c_int
+        L.derf_render_noalloc.argtypes = render_args + [P]
+        L.derf_render_noalloc.restype = ctypes.c_int
         L.derf_render_soft.argtypes = [P, P, P, ctypes.c_longlong, ctypes.c_float, ctypes.c_float,
                                        ctypes.POINTER(derf_sampling), ctypes.c_float, P, P, P, P, P]
         L.derf_render_soft.restype = ctypes.c_int
@@ -251,6 +254,22 @@ def derf_render(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far:
         _check(lib().derf_render(*args, sp), "derf_render")
     else:
         _check(lib().derf_render_debug(*args, ctypes.byref(debug), sp), "derf_render_debug")
+
+
+def derf_render_noalloc(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far: float,
+                        samp: derf_sampling, out_rgb: torch.Tensor, out_depth: torch.Tensor,
+                        out_opacity: torch.Tensor, stream=None):
+    """Enqueue a render that allocates nothing (the library's fixed per-device
+    scratch array; frames beyond it raise DERF_ERR_INVALID_ARG) on `stream`
+    (default: torch's current stream)."""
+    _check_outputs(rays_o, rays_d, out_rgb, out_depth, out_opacity)
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    _check(lib().derf_render_noalloc(h, _dptr(rays_o), _dptr(rays_d), rays_o.shape[0], near, far,
+                                     ctypes.byref(samp), _dptr(out_rgb), _dptr(out_depth),
+                                     _dptr(out_opacity), sp),
+           "derf_render_noalloc")
 
 
 def derf_render_soft(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float, far: float,

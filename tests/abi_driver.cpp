@@ -216,6 +216,9 @@ int main()
     expect(derf_render(nullptr, dummy, dummy, 1, 2.0f, 6.0f, &samp, dummy, dummy, dummy,
                        nullptr) == DERF_ERR_INVALID_ARG,
            "render without a handle");
+    expect(derf_render_noalloc(nullptr, dummy, dummy, 1, 2.0f, 6.0f, &samp, dummy, dummy, dummy,
+                               nullptr) == DERF_ERR_INVALID_ARG,
+           "no-allocation render without a handle");
     expect(derf_render_debug(nullptr, dummy, dummy, 1, 2.0f, 6.0f, &samp, dummy, dummy, dummy,
                              nullptr, nullptr) == DERF_ERR_INVALID_ARG,
            "debug render without a handle");

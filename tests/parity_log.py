@@ -10,4 +10,9 @@ def record(**fields):
     path = os.environ.get("DERF_PARITY_RECORD")
     if path:
         with open(path, "a") as f:
-            f.write(json.dumps(fields) + "\n")
+            f.write(json.dumps(fields, default=_plain) + "\n")
+
+
+def _plain(v):
+    """numpy scalars and arrays as plain Python values."""
+    return v.item() if hasattr(v, "item") and getattr(v, "size", 1) == 1 else v.tolist()

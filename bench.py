@@ -176,6 +176,54 @@ def parity_record(sc, precision, out, ids, ref, nthreads):
     return rec
 
 
+def mfma_ceiling(iters=12000):
+    """Throughput of back-to-back 32x32x16 bf16 MFMAs on every SIMD (two waves
+    each, four independent accumulator chains per wave) for operand patterns
+    random / constant / zero and 0, 2 or 4 bf16-pack + packed-max vector
+    instructions beside each MFMA (the head MLP's epilogue mix): the clock-
+    and power-limited ceiling against which the MLP's fraction of the
+    nominal 2.5 PFLOP/s is read.  Timed with events on torch's stream, which
+    the probe is launched on."""
+    import ctypes
+    import torch
+    from paper_2011_12490_amd import build as hipbuild
+    if not os.path.exists(hipbuild.PROBE_LIB):
+        raise SystemExit("libderf_probe.so is not built (run __graft_entry__.build())")
+    L = ctypes.CDLL(hipbuild.PROBE_LIB)
+    L.derf_probe_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_uint, ctypes.c_int,
+                                  ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    L.derf_probe_mfma.restype = ctypes.c_int
+    chains = L.derf_probe_chains()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    grid = 2 * cus
+    out = torch.empty(grid * 256, device="cuda")
+    stream = torch.cuda.current_stream()
+    res = []
+    for mode, name in ((0, "random"), (1, "constant"), (2, "zero")):
+        for valu in (0, 2, 4):
+            def launch():
+                rc = L.derf_probe_mfma(grid, iters, 1234, mode, valu, ctypes.c_void_p(out.data_ptr()),
+                                       ctypes.c_void_p(stream.cuda_stream))
+                if rc != 0:
+                    raise RuntimeError("probe launch failed (%d)" % rc)
+            launch()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(3):
+                launch()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / 3
+            flop = 2.0 * grid * 4 * iters * chains * 32 * 32 * 16
+            tf = flop / (ms * 1e-3) / 1e12
+            res.append({"operands": name, "valu_per_mfma": valu, "ms": ms, "tflops": tf,
+                        "frac_of_peak": tf / PEAK_TFLOPS["bf16"]})
+            log("bench: mfma ceiling %-8s valu %d: %.0f TFLOP/s (%.3f of peak)"
+                % (name, valu, tf, tf / PEAK_TFLOPS["bf16"]))
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -206,6 +254,9 @@ def main():
                     help="also time the Painter's-order render with transmittance culling "
                          "(stop below transmittance EPS, LEVELS levels, default 4; segments "
                          "cut into pieces of at most PIECE samples, default 0: whole)")
+    ap.add_argument("--mfma-ceiling", action="store_true",
+                    help="also run the matrix-core throughput probe (operand patterns x vector "
+                         "instructions per MFMA) and report it under mfma_ceiling")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (to scale HBM counters)")
     args = ap.parse_args()
@@ -457,6 +508,8 @@ def main():
         log("bench: gated H=%d %.4g rays/s (%.2f runs per ray)"
             % (args.gate, gated["rays_per_s"], runs_g))
 
+    ceiling = mfma_ceiling() if args.mfma_ceiling else None
+
     cpu = None
     cpu_ids = cpu_ref = None
     nthreads = min(16, len(os.sched_getaffinity(0)))
@@ -512,6 +565,8 @@ def main():
         res["culled"] = culled
     if gated is not None:
         res["gated"] = gated
+    if ceiling is not None:
+        res["mfma_ceiling"] = ceiling
     print(json.dumps(res))
 
 

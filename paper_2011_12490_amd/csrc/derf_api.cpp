@@ -744,16 +744,20 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     };
     HIP_TRY(mark(DERF_STAGE_SAMPLE, 0), "hipEventRecord");
     HIP_TRY(launch_ray_encode(g, b.dirbuf, h->bf16, s), "ray_encode launch");
-    const WalkTable walk{b.walk_seg, b.walk_nseg};
-    if (walk.seg)
-        HIP_TRY(launch_ray_walk(g, h->sites, K, b.walk_seg, b.walk_nseg, s), "ray_walk launch");
-    HIP_TRY(launch_sample_assign(g, h->sites, K, h->site_bits, walk, b.t, b.cell, b.counts, nblk,
-                                 s),
-            "sample_assign launch");
-    if (gated)
+    // the gated assignment draws the depths itself and needs no nearest site
+    const WalkTable walk{gated ? nullptr : b.walk_seg, gated ? nullptr : b.walk_nseg};
+    if (gated) {
         HIP_TRY(launch_gate(g, h->gate_w, h->gate_freqs, h->gate_hidden, K, b.t, b.cell, out_cell,
                             s),
                 "gate launch");
+    } else {
+        if (walk.seg)
+            HIP_TRY(launch_ray_walk(g, h->sites, K, b.walk_seg, b.walk_nseg, s),
+                    "ray_walk launch");
+        HIP_TRY(launch_sample_assign(g, h->sites, K, h->site_bits, walk, b.t, b.cell, b.counts,
+                                     nblk, s),
+                "sample_assign launch");
+    }
     HIP_TRY(launch_level_bounds(b.cell, N, R, L, (unsigned)piece, c.lb, c.lvl, s),
             "level_bounds launch");
     HIP_TRY(mark(DERF_STAGE_SAMPLE, 1), "hipEventRecord");

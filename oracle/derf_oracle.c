@@ -465,9 +465,18 @@ static void merge_sorted(const float *a, int na, const float *b, int nb, float *
  * gamma_L(x):
  *   h = max(0, W1 gamma_L(x) + b1),  z = W2 h + b2   (K logits)
  * Packed float32 weights: W1 [H][3 + 6L] row-major, b1 [H], W2 [K][H], b2 [K].
- * The decision is an integer, so it is taken in float32, the precision of
- * the kernel: the encoding is rounded to float32 and every dot product is
- * the bias followed by fused multiply-adds in index order. */
+ * The decision is an integer, so both sides take it in the precision of the
+ * kernel, which runs the two products on bf16 matrix cores: every float32
+ * operand a is carried as two bfloat16 values, a_hi = bf16(a) and
+ * a_lo = bf16(a - a_hi) (round to nearest even each), and every product a b
+ * of a weight and an activation as a_hi b_hi + a_hi b_lo + a_lo b_hi (each
+ * exact; the dropped a_lo b_lo and the rounding of a_lo are below
+ * 2^-18 |a b| each).  The encoding is rounded to float32 first, each dot
+ * product is the bias plus those terms (summed here in double), and the
+ * hidden layer is rounded to float32 after the ReLU, as the kernel's float32
+ * accumulators hold it.  The split keeps about 16 significant bits per
+ * operand, so these logits stay within about 1e-5 relative of the plain
+ * float32 network. */
 long long oracle_gate_weights_count(int K, int L, int H)
 {
     if (K < 1 || L < 0 || H < 1)
@@ -475,10 +484,31 @@ long long oracle_gate_weights_count(int K, int L, int H)
     return (long long)H * (3 + 6 * L) + H + (long long)K * H + K;
 }
 
+/* v rounded to bfloat16 (8 significant bits), nearest even; v finite. */
+static float bf16_rne(float v)
+{
+    uint32_t u;
+    memcpy(&u, &v, sizeof(u));
+    u = (u + 0x7FFFu + ((u >> 16) & 1u)) & 0xFFFF0000u;
+    float r;
+    memcpy(&r, &u, sizeof(r));
+    return r;
+}
+
+/* a b in the gate's arithmetic: a = a_hi + a_lo, b = b_hi + b_lo as two
+ * bfloat16 values each (a - a_hi is exact in float32), and the three
+ * products that keep 16 significant bits of each operand. */
+static double gate_mul(float a, float b)
+{
+    const float ah = bf16_rne(a), al = bf16_rne(a - ah);
+    const float bh = bf16_rne(b), bl = bf16_rne(b - bh);
+    return (double)ah * bh + (double)ah * bl + (double)al * bh;
+}
+
 /* Logits z [K] of the gating network at x; f (3 + 6L floats) and h (H) are
  * scratch. */
 static void gate_logits(int K, int L, int H, const float *w, const float x[3], float *f, float *h,
-                        float *z)
+                        double *z)
 {
     const int P = 3 + 6 * L;
     double g[3 + 6 * 32];
@@ -488,15 +518,16 @@ static void gate_logits(int K, int L, int H, const float *w, const float x[3], f
         f[c] = (float)g[c];
     const float *W1 = w, *b1 = W1 + (size_t)H * P, *W2 = b1 + H, *b2 = W2 + (size_t)K * H;
     for (int j = 0; j < H; ++j) {
-        float acc = b1[j];
+        double acc = b1[j];
         for (int c = 0; c < P; ++c)
-            acc = fmaf(W1[(size_t)j * P + c], f[c], acc);
-        h[j] = acc > 0.0f ? acc : 0.0f;
+            acc += gate_mul(W1[(size_t)j * P + c], f[c]);
+        const float v = (float)acc;
+        h[j] = v > 0.0f ? v : 0.0f;
     }
     for (int k = 0; k < K; ++k) {
-        float acc = b2[k];
+        double acc = b2[k];
         for (int j = 0; j < H; ++j)
-            acc = fmaf(W2[(size_t)k * H + j], h[j], acc);
+            acc += gate_mul(W2[(size_t)k * H + j], h[j]);
         z[k] = acc;
     }
 }
@@ -504,7 +535,7 @@ static void gate_logits(int K, int L, int H, const float *w, const float x[3], f
 /* The gated head (first largest logit) and, in *gap, the difference between
  * the two largest logits (infinite for one head): how near the decision is
  * to a tie. */
-static int gate_argmax(int K, const float *z, double *gap)
+static int gate_argmax(int K, const double *z, double *gap)
 {
     int best = 0;
     for (int k = 1; k < K; ++k)
@@ -513,9 +544,9 @@ static int gate_argmax(int K, const float *z, double *gap)
     if (gap) {
         double second = -INFINITY;
         for (int k = 0; k < K; ++k)
-            if (k != best && (double)z[k] > second)
+            if (k != best && z[k] > second)
                 second = z[k];
-        *gap = K > 1 ? (double)z[best] - second : INFINITY;
+        *gap = K > 1 ? z[best] - second : INFINITY;
     }
     return best;
 }
@@ -523,7 +554,7 @@ static int gate_argmax(int K, const float *z, double *gap)
 /* Logits [M][K] of the gating network at the points x [M][3]; -1 for bad
  * sizes. */
 int oracle_gate_logits(int K, int L, int H, const float *w, long long M, const float *x,
-                       float *z)
+                       double *z)
 {
     if (K < 1 || L < 0 || L > 32 || H < 1 || M < 0)
         return -1;
@@ -655,7 +686,8 @@ static void eval_samples(const render_args *A, int mode, double beta, const floa
                 }
             }
         } else if (mode == MODE_GATED) {
-            float f[3 + 6 * 32], h[256], z[256];
+            float f[3 + 6 * 32], h[256];
+            double z[256];
             gate_logits(A->K, A->gate_L, A->gate_H, A->gate_w, x, f, h, z);
             cell[i] = gate_argmax(A->K, z, NULL);
             eval_head(A, cell[i], xd, dh, gx, gd, &sigma[i], &rgb[3 * i], scratch);
@@ -790,7 +822,8 @@ static int render_impl(const render_args *A, int mode, double beta, long long R,
                         sample_point(o, d, tt[i], x);
                         if (mode == MODE_GATED) {
                             /* the gap between the two largest logits */
-                            float f[3 + 6 * 32], h[256], z[256];
+                            float f[3 + 6 * 32], h[256];
+                            double z[256];
                             gate_logits(A->K, A->gate_L, A->gate_H, A->gate_w, x, f, h, z);
                             (void)gate_argmax(A->K, z, &dbg_margin[s]);
                         } else {

@@ -64,10 +64,13 @@ def test_gate_weights_count_and_unpack_order():
 
 
 def test_gate_logits_match_a_float64_matrix_chain():
-    """The fp32 logits (bias, then fused multiply-adds in index order) equal a
-    float64 matrix chain on the same fp32 encoding within the rounding bound
-    of a length-n fp32 dot product, n u sum |w x| (u = 2^-24), for every
-    point and head; the ReLU acts on the hidden units."""
+    """The logits in the kernel's arithmetic (each float32 operand split into
+    two bf16 values, each product a b taken as a_hi b_hi + a_hi b_lo + a_lo
+    b_hi) equal a float64 matrix chain on the same float32 encoding within
+    that arithmetic's bound: a dropped term and the rounding of the two low
+    parts, at most 3.01 * 2^-18 |a b| per product, summed over each dot
+    product, the hidden layer's error (and its float32 rounding) carried
+    through W2.  The ReLU acts on the hidden units."""
     K, L, H = 7, 6, 32
     w = random_gate(K, L, H, 11, scale=4.0)
     P = 3 + 6 * L
@@ -76,18 +79,18 @@ def test_gate_logits_match_a_float64_matrix_chain():
     W2 = w[H * P + H:H * P + H + K * H].reshape(K, H).astype(np.float64)
     b2 = w[H * P + H + K * H:].astype(np.float64)
     x = np.random.default_rng(3).uniform(-1.2, 1.2, (500, 3)).astype(np.float32)
-    z = oracle.gate_logits(K, L, H, w, x).astype(np.float64)
+    z = oracle.gate_logits(K, L, H, w, x)
     g = np.stack([oracle.posenc(L, xi.astype(np.float64)) for xi in x]).astype(np.float32)
     g = g.astype(np.float64)
     pre = g @ W1.T + b1
     h = np.maximum(pre, 0.0)
     ref = h @ W2.T + b2
-    u = 2.0 ** -24
-    # hidden-unit error bound, carried through W2, plus the logits' own rounding
-    eh = (P + 1) * u * (np.abs(g) @ np.abs(W1).T + np.abs(b1))
-    bound = (H + 1) * u * (h @ np.abs(W2).T + np.abs(b2)) + eh @ np.abs(W2).T
-    assert np.all(np.abs(z - ref) <= 1.01 * bound + 1e-30)
-    assert np.abs(z - ref).max() > 0.0          # fp32 arithmetic, not a float64 copy
+    rel = 3.01 * 2.0 ** -18
+    # hidden-unit error bound, carried through W2, plus the logits' own terms
+    eh = rel * (np.abs(g) @ np.abs(W1).T) + 2.0 ** -24 * np.abs(pre)
+    bound = rel * ((h + eh) @ np.abs(W2).T) + eh @ np.abs(W2).T
+    assert np.all(np.abs(z - ref) <= 1.01 * bound + 1e-12)
+    assert np.abs(z - ref).max() > 1e-7         # the split arithmetic, not a float64 copy
     # a missing ReLU, a dropped hidden or output bias, or a swapped encoding
     # block (sin and cos of one level) leaves the bound by far
     assert np.abs(pre @ W2.T + b2 - z).max() > 1e-3

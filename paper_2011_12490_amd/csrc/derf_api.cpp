@@ -173,8 +173,9 @@ struct derf_handle {
     unsigned walk_rays = 0;
     // device address of this device's noalloc scratch array
     void *scratch = nullptr;
-    // MLP gating (derf_set_gate): fp32 weights on the device, or none
-    float *gate_w = nullptr;
+    // MLP gating (derf_set_gate): the gate laid out for its kernel on the
+    // device (gate_pack), or none
+    unsigned char *gate_w = nullptr;
     int gate_freqs = 0;
     int gate_hidden = 0;
 };
@@ -748,7 +749,7 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     const WalkTable walk{gated ? nullptr : b.walk_seg, gated ? nullptr : b.walk_nseg};
     if (gated) {
         HIP_TRY(launch_gate(g, h->gate_w, h->gate_freqs, h->gate_hidden, K, b.t, b.cell, out_cell,
-                            s),
+                            h->mlp_grid, s),
                 "gate launch");
     } else {
         if (walk.seg)
@@ -1033,12 +1034,22 @@ int derf_set_gate(derf_handle *h, int pos_freqs, int hidden, const float *weight
         if (!isfinite(weights[i]))
             return fail(DERF_ERR_INVALID_ARG, "non-finite gating weight");
     HIP_TRY(hipSetDevice(h->device), "hipSetDevice");
-    float *dev = nullptr;
-    if (dev_alloc(reinterpret_cast<void **>(&dev), (size_t)count * sizeof(float)) != hipSuccess) {
+    const size_t bytes = gate_packed_bytes(pos_freqs, hidden, h->num_sites);
+    std::vector<unsigned char> host;
+    try {
+        if (injected_failure())
+            throw std::bad_alloc();
+        host.resize(bytes);
+    } catch (const std::bad_alloc &) {
+        return fail(DERF_ERR_OOM, "host staging of the gate");
+    }
+    gate_pack(pos_freqs, hidden, h->num_sites, weights, host.data());
+    unsigned char *dev = nullptr;
+    if (dev_alloc(reinterpret_cast<void **>(&dev), bytes) != hipSuccess) {
         (void)hipGetLastError();
         return fail(DERF_ERR_OOM, "gating weights");
     }
-    hipError_t e = hipMemcpy(dev, weights, (size_t)count * sizeof(float), hipMemcpyHostToDevice);
+    hipError_t e = hipMemcpy(dev, host.data(), bytes, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
         (void)dev_free(dev);
         HIP_TRY(e, "hipMemcpy");

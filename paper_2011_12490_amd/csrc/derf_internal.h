@@ -58,11 +58,17 @@ struct RenderGeometry {
 // Gating networks with a compiled kernel: gamma_L(x) with L = 6 or 10 as
 // input, one ReLU layer of 16, 32 or 64 units, K logits.
 bool gate_shape_supported(int pos_freqs, int hidden);
+// Bytes of a gate's weights and biases laid out for the kernel, and the
+// layout itself from the packed fp32 order of derf.h (host side).
+size_t gate_packed_bytes(int pos_freqs, int hidden, int num_sites);
+void gate_pack(int pos_freqs, int hidden, int num_sites, const float *w, unsigned char *out);
 // t[s] = the stratified depth of sample s (as the single pass draws it), and
 // cell[s] = argmax of the gating logits there; also to out_cell (int32 [S])
-// when not null.
-hipError_t launch_gate(const RenderGeometry &g, const float *w, int pos_freqs, int hidden,
-                       int num_sites, float *t, uint8_t *cell, int *out_cell, hipStream_t s);
+// when not null.  packed: gate_pack's layout on the device; cus: compute
+// units (the kernel's workgroups are persistent).
+hipError_t launch_gate(const RenderGeometry &g, const unsigned char *packed, int pos_freqs,
+                       int hidden, int num_sites, float *t, uint8_t *cell, int *out_cell, int cus,
+                       hipStream_t s);
 
 // ---- sampling, assignment and bucketing (kernels_sample.hip) -------------
 hipError_t launch_ray_encode(const RenderGeometry &g, void *dirbuf, bool bf16, hipStream_t s);

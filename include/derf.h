@@ -263,24 +263,31 @@ int derf_render_culled(derf_handle *h, const float *rays_o, const float *rays_d,
  * that is the argmax of the logits (ties to the lowest index):
  *   h = ReLU(W1 gamma_L(x) + b1),  logits = W2 h + b2  (K logits)
  * gamma_L is the positional encoding of the heads (p, then sin and cos of
- * pi 2^l p for l < L), evaluated in fp32.  Gated cells need not be convex, so
- * a ray may enter one cell several times; its runs are merged front to back,
- * which is exact for any partition.
- * derf_set_gate copies the host weights, fp32, packed W1 [H][3 + 6L], b1 [H],
- * W2 [K][H], b2 [K] (derf_gate_weights_count floats), to the device; the
- * caller may free them on return.  pos_freqs 6 or 10 and hidden 16, 32 or 64
+ * pi 2^l p for l < L), evaluated in fp32.  The products run on bf16 matrix
+ * cores with each fp32 operand a split into a_hi = bf16(a) and
+ * a_lo = bf16(a - a_hi), each product taken as a_hi b_hi + a_hi b_lo +
+ * a_lo b_hi and summed in fp32; the hidden units are fp32.  The argmax is
+ * decided in that precision.  Gated cells need not be convex, so a ray may
+ * enter one cell several times; its runs are merged front to back, which is
+ * exact for any partition.
+ * derf_set_gate takes the host weights, fp32, packed W1 [H][3 + 6L], b1 [H],
+ * W2 [K][H], b2 [K] (derf_gate_weights_count floats), splits them as above
+ * into the kernel's layout on the device (12 KB for L = 10, H = 32, K = 16;
+ * at most 81 KB); the caller may free them on return.  pos_freqs 6 or 10 and hidden 16, 32 or 64
  * have kernels (DERF_ERR_UNSUPPORTED otherwise); hidden = 0 removes the gate.
  * Non-finite weights: DERF_ERR_INVALID_ARG.  Waits for the handle's last
  * stream before replacing a gate. */
 int derf_set_gate(derf_handle *h, int pos_freqs, int hidden, const float *weights);
 /* floats of a gating network for K heads; -1 for invalid values */
 long long derf_gate_weights_count(int num_sites, int pos_freqs, int hidden);
-/* derf_render with the gated assignment: samples, gating, per-head buckets,
- * the grouped MLP and front-to-back integration of the runs.  Arguments,
+/* derf_render with the gated assignment: the stratified depths (the same
+ * draws as derf_render's) and the gate in one kernel, then per-head buckets,
+ * the grouped MLP and front-to-back integration of the runs; no
+ * nearest-site search.  Arguments,
  * limits and ownership as derf_render (single pass: samp->n_fine must be 0,
  * DERF_ERR_UNSUPPORTED otherwise); DERF_ERR_INVALID_ARG without a gate.
  *   out_cell   NULL, or device int32 [R][N]: each sample's gated head
- * Stage times: DERF_STAGE_SAMPLE (sampling, assignment and the gate) and
+ * Stage times: DERF_STAGE_SAMPLE (sampling and the gate) and
  * DERF_STAGE_MLP (bucketing, heads and integration); head_samples counts
  * each head's gated samples. */
 int derf_render_gated(derf_handle *h, const float *rays_o, const float *rays_d,

@@ -710,6 +710,8 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     HIP_TRY(hipSetDevice(h->device), "hipSetDevice");
     const unsigned R = (unsigned)num_rays, N = (unsigned)samp->n_coarse, S = R * N;
     const unsigned L = (unsigned)levels, nblk = blocks_of(S);
+    // a piece no shorter than the ray cuts nothing: the whole-segment levels
+    const unsigned P = (unsigned)piece < N ? (unsigned)piece : 0u;
     const int K = h->num_sites;
     int rc = ensure_workspace(h, layout_culled(nullptr, S, R, nblk, K, h->bf16, L, nullptr, nullptr));
     if (rc != DERF_OK)
@@ -759,7 +761,7 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
                                      nblk, s),
                 "sample_assign launch");
     }
-    HIP_TRY(launch_level_bounds(b.cell, N, R, L, (unsigned)piece, c.lb, c.lvl, s),
+    HIP_TRY(launch_level_bounds(b.cell, N, R, L, P, c.lb, c.lvl, s),
             "level_bounds launch");
     HIP_TRY(mark(DERF_STAGE_SAMPLE, 1), "hipEventRecord");
     HIP_TRY(mark(DERF_STAGE_MLP, 0), "hipEventRecord");
@@ -774,7 +776,9 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
                 "level_scatter launch");
         HIP_TRY(launch_groups(h, b.bucket, tot, g, b.t, b.dirbuf, b.sr, b.mlp_queue, false, s),
                 "mlp launch");
-        HIP_TRY(launch_level_composite(g, b.t, b.cell, b.sr, lv, out_rgb, out_depth, out_opacity, s),
+        // every level but the last is one piece of at most P samples
+        HIP_TRY(launch_level_composite(g, b.t, b.cell, b.sr, lv, l + 1 < L ? P : 0u, out_rgb,
+                                       out_depth, out_opacity, s),
                 "level_composite launch");
     }
     HIP_TRY(mark(DERF_STAGE_MLP, 1), "hipEventRecord");

@@ -132,4 +132,25 @@ __device__ __forceinline__ Over wave_over(Over acc, int lane)
     return acc;
 }
 
+// The same ordered merge within each aligned group of G lanes (G = 2, 4,
+// 8, 16; gl: lane within the group): valid in the group's first lane.
+template <int G>
+__device__ __forceinline__ Over group_over(Over acc, int gl)
+{
+    auto step = [&](auto fetch, int off) {
+        const Over o{fetch(acc.r), fetch(acc.g), fetch(acc.b), fetch(acc.d), fetch(acc.t)};
+        if ((gl & (2 * off - 1)) == 0)
+            acc = over(acc, o);
+    };
+    if constexpr (G >= 2)
+        step([](float x) { return from_lane_above<1>(x); }, 1);
+    if constexpr (G >= 4)
+        step([](float x) { return from_lane_above<2>(x); }, 2);
+    if constexpr (G >= 8)
+        step([](float x) { return from_lane_above<4>(x); }, 4);
+    if constexpr (G >= 16)
+        step([](float x) { return from_lane_above<8>(x); }, 8);
+    return acc;
+}
+
 }  // namespace derf

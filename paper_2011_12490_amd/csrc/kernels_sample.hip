@@ -925,6 +925,65 @@ __global__ __launch_bounds__(kThreads) void composite_kernel(
     }
 }
 
+// Level composite for a level whose ranges are single pieces of at most a
+// few dozen samples (every level but the last of a render cut into pieces):
+// G lanes per ray, 64 / G rays per wave.  Lane gl of a ray's group
+// integrates the consecutive samples [a + gl c, a + (gl + 1) c) of its range
+// [a, b), c = ceil((b - a) / G), straight from memory, and the group merges
+// its lanes in order.  State, outputs and closing marks as
+// composite_kernel<true>; the rounding differs from it only in how the range
+// is split over lanes.
+template <int G>
+__global__ __launch_bounds__(kThreads) void level_composite_short_kernel(
+    const float *__restrict__ t, const uint8_t *__restrict__ cell, const float4 *__restrict__ sr,
+    unsigned n, unsigned num_rays, float near_t, float far_t, LevelState lv,
+    float *__restrict__ out_rgb, float *__restrict__ out_depth, float *__restrict__ out_opacity)
+{
+    const int lane = threadIdx.x & 63, gl = lane & (G - 1);
+    const unsigned ray = (blockIdx.x * kThreads + threadIdx.x) / G;
+    // groups past the last ray read ray 0's samples and store nothing
+    const bool live = ray < num_rays;
+    const size_t base = (size_t)(live ? ray : 0u) * n;
+    Over st{0.f, 0.f, 0.f, 0.f, 1.f};
+    unsigned a = 0, b = 0;
+    bool go = live;
+    if (live) {
+        const unsigned *r_lb = lv.lb + (size_t)ray * (lv.levels + 1) + lv.level;
+        a = r_lb[0];
+        b = r_lb[1];
+        if (lv.level > 0) {
+            st = Over{out_rgb[3 * ray], out_rgb[3 * ray + 1], out_rgb[3 * ray + 2], out_depth[ray],
+                      lv.trans[ray]};
+            go = st.t >= lv.eps;
+        }
+    }
+    if (!go)
+        a = b = 0;
+    const unsigned c = (b - a + G - 1) / G;
+    const unsigned i0 = min(a + gl * c, b), i1 = min(i0 + c, b);
+    Over part = integrate_runs(
+        i0, i1, n, near_t, far_t, [&](unsigned i) { return t[base + i]; },
+        [&](unsigned i) { return (unsigned)cell[base + i]; },
+        [&](unsigned i) { return sr[base + i]; });
+    part = group_over<G>(part, gl);
+    const Over acc = over(st, part);  // meaningful in the group's first lane
+    if (go && gl == 0) {
+        out_rgb[3 * ray] = acc.r;
+        out_rgb[3 * ray + 1] = acc.g;
+        out_rgb[3 * ray + 2] = acc.b;
+        out_depth[ray] = acc.d;
+        out_opacity[ray] = 1.0f - acc.t;
+        lv.trans[ray] = acc.t;
+        if (lv.evaluated)
+            lv.evaluated[ray] = (lv.level > 0 ? lv.evaluated[ray] : 0u) + (b - a);
+    }
+    // a ray that closes here takes no part in later levels
+    const float tr = __shfl(acc.t, lane & ~(G - 1));
+    if (go && tr < lv.eps && lv.level + 1 < lv.levels)
+        for (unsigned i = b + gl; i < n; i += G)
+            lv.lvl[base + i] = kDeadLevel;
+}
+
 __global__ __launch_bounds__(kThreads) void debug_expand_kernel(
     unsigned num_samples, const float *__restrict__ t, const uint8_t *__restrict__ cell,
     const float4 *__restrict__ sr, int *dcell, float *dt, float *dsigma, float *drgb)
@@ -1069,14 +1128,25 @@ hipError_t launch_level_scatter(const RenderGeometry &g, const uint8_t *cell,
 }
 
 hipError_t launch_level_composite(const RenderGeometry &g, const float *t, const uint8_t *cell,
-                                  const float4 *sr, const CullLevel &lv, float *rgb,
-                                  float *depth, float *opacity, hipStream_t s)
+                                  const float4 *sr, const CullLevel &lv, unsigned max_len,
+                                  float *rgb, float *depth, float *opacity, hipStream_t s)
 {
+    const LevelState st{lv.lb, lv.lvl, lv.trans, lv.evaluated, lv.levels, lv.level, lv.eps};
+    if (max_len > 0 && max_len <= 32) {
+        level_composite_short_kernel<8><<<blocks_for((size_t)g.num_rays * 8, kThreads), kThreads, 0,
+                                          s>>>(t, cell, sr, g.n, g.num_rays, g.near_t, g.far_t, st,
+                                               rgb, depth, opacity);
+        return hipGetLastError();
+    }
+    if (max_len > 0 && max_len <= 64) {
+        level_composite_short_kernel<16><<<blocks_for((size_t)g.num_rays * 16, kThreads), kThreads,
+                                           0, s>>>(t, cell, sr, g.n, g.num_rays, g.near_t, g.far_t,
+                                                   st, rgb, depth, opacity);
+        return hipGetLastError();
+    }
     const unsigned grid = blocks_for(g.num_rays, kThreads / 64);
-    composite_kernel<true><<<grid, kThreads, 0, s>>>(
-        t, cell, sr, g.n, g.num_rays, g.near_t, g.far_t,
-        LevelState{lv.lb, lv.lvl, lv.trans, lv.evaluated, lv.levels, lv.level, lv.eps}, rgb, depth,
-        opacity);
+    composite_kernel<true><<<grid, kThreads, 0, s>>>(t, cell, sr, g.n, g.num_rays, g.near_t,
+                                                     g.far_t, st, rgb, depth, opacity);
     return hipGetLastError();
 }
 

@@ -10,6 +10,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <atomic>
 #include <mutex>
 #include <new>
@@ -187,6 +188,10 @@ inline unsigned blocks_of(unsigned S)
 {
     return (unsigned)(((unsigned long long)S + kBucketBlock - 1) / kBucketBlock);
 }
+inline unsigned blocks_of_ll(unsigned long long n)
+{
+    return (unsigned)((n + kBucketBlock - 1) / kBucketBlock);
+}
 
 template <class T>
 T *carve(char *&p, size_t count)
@@ -270,7 +275,8 @@ namespace {
 // tile counters.
 hipError_t launch_groups(const derf_handle *h, const unsigned *bucket, const unsigned *totals,
                          const RenderGeometry &g, const float *t, const void *dirbuf, float4 *sr,
-                         unsigned *queue, bool soft, hipStream_t s)
+                         unsigned *queue, bool soft, hipStream_t s,
+                         const unsigned *offsets = nullptr)
 {
     for (int gi = 0; gi < h->num_groups; ++gi) {
         const derf_handle::HeadGroup &grp = h->groups[gi];
@@ -278,8 +284,8 @@ hipError_t launch_groups(const derf_handle *h, const unsigned *bucket, const uns
         for (int w = 0; w < kMaxSites / 32; ++w)
             skip.w[w] = ~grp.members.w[w] | h->empty.w[w];
         const hipError_t e =
-            grp.mlp->launch(bucket, totals, h->num_sites, g, t, dirbuf, grp.streams, grp.blocks, sr,
-                            queue + kMlpQueues * gi, h->mlp_grid, soft, skip, s);
+            grp.mlp->launch(bucket, totals, offsets, h->num_sites, g, t, dirbuf, grp.streams,
+                            grp.blocks, sr, queue + kMlpQueues * gi, h->mlp_grid, soft, skip, s);
         if (e != hipSuccess)
             return e;
     }
@@ -653,11 +659,25 @@ struct CullBuffers {
     unsigned *lb;            // [R][levels + 1]
     uint8_t *lvl;            // [S]
     float *trans;            // [R]
-    unsigned *level_totals;  // [levels][K]
+    unsigned *level_totals;  // [levels][K] samples evaluated per level and head
+    // the one-pass (level, head) bucketing (levels K <= 256, levels > 1)
+    unsigned *order;         // [S]
+    unsigned *key_counts;    // [levels K][nblk]
+    unsigned *key_totals;    // [levels K]
+    unsigned *key_offsets;   // [levels K]
 };
 
+// The culled render buckets every level at once when its levels are pieces
+// (many short levels: the one pass costs about two per-level passes and
+// saves one per level) and the (level, head) keys fit the bucketing
+// kernels' 256.
+inline bool one_pass_levels(unsigned levels, int K, unsigned piece)
+{
+    return piece > 0 && levels > 2 && levels * K <= kMaxSites;
+}
+
 size_t layout_culled(char *base, unsigned S, unsigned R, unsigned nblk, int K, bool bf16,
-                     unsigned levels, Buffers *b, CullBuffers *c)
+                     unsigned levels, unsigned piece, Buffers *b, CullBuffers *c)
 {
     char *p = base + layout(base, S, 0, R, nblk, K, bf16, b);
     CullBuffers x;
@@ -665,6 +685,11 @@ size_t layout_culled(char *base, unsigned S, unsigned R, unsigned nblk, int K, b
     x.lvl = carve<uint8_t>(p, S);
     x.trans = carve<float>(p, R);
     x.level_totals = carve<unsigned>(p, (size_t)levels * K);
+    const bool one = one_pass_levels(levels, K, piece);
+    x.order = carve<unsigned>(p, one ? S : 0);
+    x.key_counts = carve<unsigned>(p, one ? (size_t)levels * K * nblk : 0);
+    x.key_totals = carve<unsigned>(p, one ? (size_t)levels * K : 0);
+    x.key_offsets = carve<unsigned>(p, one ? (size_t)levels * K : 0);
     if (c)
         *c = x;
     return (size_t)(p - base);
@@ -713,7 +738,8 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     // a piece no shorter than the ray cuts nothing: the whole-segment levels
     const unsigned P = (unsigned)piece < N ? (unsigned)piece : 0u;
     const int K = h->num_sites;
-    int rc = ensure_workspace(h, layout_culled(nullptr, S, R, nblk, K, h->bf16, L, nullptr, nullptr));
+    int rc =
+        ensure_workspace(h, layout_culled(nullptr, S, R, nblk, K, h->bf16, L, P, nullptr, nullptr));
     if (rc != DERF_OK)
         return rc;
     if (h->timing && h->ev_pending) {
@@ -722,7 +748,7 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     }
     Buffers b;
     CullBuffers c;
-    layout_culled(reinterpret_cast<char *>(h->ws.mem), S, R, nblk, K, h->bf16, L, &b, &c);
+    layout_culled(reinterpret_cast<char *>(h->ws.mem), S, R, nblk, K, h->bf16, L, P, &b, &c);
 
     RenderGeometry g;
     g.rays_o = rays_o;
@@ -763,19 +789,52 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     }
     HIP_TRY(launch_level_bounds(b.cell, N, R, L, P, c.lb, c.lvl, s),
             "level_bounds launch");
+    // Levels cut into pieces: bucket every sample by (level, head) once; each
+    // level after the first then compacts only its own samples, dropping
+    // those of closed rays.  Otherwise each level counts and scatters its
+    // live samples.
+    const bool one_pass = one_pass_levels(L, K, P);
+    if (one_pass) {
+        int key_bits = 0;
+        while ((1u << key_bits) < L * (unsigned)K)
+            ++key_bits;
+        HIP_TRY(launch_level_head_order(g, L, K, key_bits, c.lvl, b.cell, h->empty, c.key_counts,
+                                        nblk, c.key_totals, c.order, c.key_offsets,
+                                        c.level_totals, b.sr, b.mlp_queue, s),
+                "level_head_order launch");
+    }
     HIP_TRY(mark(DERF_STAGE_SAMPLE, 1), "hipEventRecord");
     HIP_TRY(mark(DERF_STAGE_MLP, 0), "hipEventRecord");
     for (unsigned l = 0; l < L; ++l) {
         const CullLevel lv{c.lb, c.lvl, c.trans, out_evaluated, L, l, eps};
         unsigned *tot = c.level_totals + (size_t)l * K;
-        HIP_TRY(launch_level_count(g, b.cell, K, h->site_bits, lv, b.counts, nblk, s),
-                "level_count launch");
-        HIP_TRY(launch_bucket_scan(b.counts, nblk, K, tot, b.mlp_queue, s), "bucket_scan launch");
-        HIP_TRY(launch_level_scatter(g, b.cell, b.counts, tot, nblk, K, h->site_bits, h->empty, lv,
-                                     b.bucket, b.sr, s),
-                "level_scatter launch");
-        HIP_TRY(launch_groups(h, b.bucket, tot, g, b.t, b.dirbuf, b.sr, b.mlp_queue, false, s),
-                "mlp launch");
+        if (one_pass) {
+            const unsigned *src = c.order;
+            if (l > 0) {
+                // a level that is one piece holds at most P samples of each ray
+                const unsigned lblk =
+                    P > 0 && l + 1 < L ? std::min(nblk, blocks_of_ll((unsigned long long)R * P))
+                                       : nblk;
+                HIP_TRY(launch_level_compact(g, l, L, K, h->site_bits, c.order, c.key_offsets,
+                                             c.key_totals, c.lvl, b.cell, lblk, tot, b.bucket,
+                                             b.mlp_queue, s),
+                        "level_compact launch");
+                src = b.bucket;
+            }
+            HIP_TRY(launch_groups(h, src, tot, g, b.t, b.dirbuf, b.sr, b.mlp_queue, false, s,
+                                  c.key_offsets + (size_t)l * K),
+                    "mlp launch");
+        } else {
+            HIP_TRY(launch_level_count(g, b.cell, K, h->site_bits, lv, b.counts, nblk, s),
+                    "level_count launch");
+            HIP_TRY(launch_bucket_scan(b.counts, nblk, K, tot, b.mlp_queue, s),
+                    "bucket_scan launch");
+            HIP_TRY(launch_level_scatter(g, b.cell, b.counts, tot, nblk, K, h->site_bits, h->empty,
+                                         lv, b.bucket, b.sr, s),
+                    "level_scatter launch");
+            HIP_TRY(launch_groups(h, b.bucket, tot, g, b.t, b.dirbuf, b.sr, b.mlp_queue, false, s),
+                    "mlp launch");
+        }
         // every level but the last is one piece of at most P samples
         HIP_TRY(launch_level_composite(g, b.t, b.cell, b.sr, lv, l + 1 < L ? P : 0u, out_rgb,
                                        out_depth, out_opacity, s),

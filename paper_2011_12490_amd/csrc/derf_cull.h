@@ -32,6 +32,28 @@ hipError_t launch_level_bounds(const uint8_t *cell, unsigned n, unsigned num_ray
 hipError_t launch_level_count(const RenderGeometry &g, const uint8_t *cell, int num_sites,
                               int site_bits, const CullLevel &lv, unsigned *counts,
                               unsigned num_blocks, hipStream_t s);
+// One-pass bucketing of every level at once (levels K <= 256 keys of
+// key_bits bits): order [S] receives the sample ids sorted by (level, head),
+// stably; totals [levels K] the samples per key and offsets [levels K] where
+// each key's stretch starts; live [levels][K] the level-0 counts (zeros
+// after).  Samples of 0-capacity heads get zero density and colour in sr.
+// counts: [levels K][num_blocks] scratch.  Clears the MLP's tile counters.
+hipError_t launch_level_head_order(const RenderGeometry &g, unsigned levels, int heads,
+                                   int key_bits, const uint8_t *lvl, const uint8_t *cell,
+                                   const HeadMask &empty, unsigned *counts, unsigned num_blocks,
+                                   unsigned *totals, unsigned *order, unsigned *offsets,
+                                   unsigned *live, float4 *sr, unsigned *mlp_queue, hipStream_t s);
+// Level l >= 1 after the one-pass bucketing: copies the level's entries whose
+// ray is still open from order to the same stretches of bucket, each head's
+// packed at the front of its stretch, and counts them in live [K] (zero on
+// entry).  num_blocks blocks of 4096 entries must cover the level.  Clears
+// the MLP's tile counters.
+hipError_t launch_level_compact(const RenderGeometry &g, unsigned level, unsigned levels,
+                                int heads, int head_bits, const unsigned *order,
+                                const unsigned *offsets, const unsigned *totals,
+                                const uint8_t *lvl, const uint8_t *cell, unsigned num_blocks,
+                                unsigned *live, unsigned *bucket, unsigned *mlp_queue,
+                                hipStream_t s);
 // bucket_scatter over the samples live at the level
 hipError_t launch_level_scatter(const RenderGeometry &g, const uint8_t *cell,
                                 const unsigned *counts, const unsigned *totals,

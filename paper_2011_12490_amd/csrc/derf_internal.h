@@ -136,8 +136,11 @@ struct MlpVariant {
     void (*pack)(const float *w, unsigned char *stream, float *block);
     // queue: kMlpQueues tile counters, zero at launch.  soft: every head
     // takes every sample (bucket = 0 .. S-1, totals[k] = S) and writes its
-    // outputs to sr[k * S + sample]; otherwise sr[sample].
-    hipError_t (*launch)(const unsigned *bucket, const unsigned *totals, int num_sites,
+    // outputs to sr[k * S + sample]; otherwise sr[sample].  offsets: null
+    // (head k's entries follow head k - 1's), or where each head's totals[k]
+    // entries start in bucket (not soft).
+    hipError_t (*launch)(const unsigned *bucket, const unsigned *totals, const unsigned *offsets,
+                         int num_sites,
                          const RenderGeometry &g, const float *t, const void *dirbuf,
                          const unsigned char *streams, const float *blocks, float4 *sr,
                          unsigned *queue, int grid, bool soft, const HeadMask &empty,

@@ -627,8 +627,15 @@ constexpr uint8_t kDeadLevel = 0xFF;
 struct LevelLive {
     const uint8_t *lvl;
     unsigned level;
+    unsigned heads;  // K, for the (level, head) keys
     __device__ __forceinline__ bool operator()(unsigned s) const { return lvl[s] == level; }
 };
+
+// The key a bucketing pass sorts by.  kCellKey: the sample's head (every
+// sample); kCellAtLevel: the head, of the samples live at one level;
+// kLevelCell: level K + head (every sample), for the one-pass bucketing of
+// all levels at once.
+constexpr int kCellKey = 0, kCellAtLevel = 1, kLevelCell = 2;
 
 // Level bounds, one wave per ray, 64 samples per step.  A sample opens a
 // segment when its cell differs from the previous sample's.  With piece > 0 a
@@ -681,19 +688,21 @@ __global__ __launch_bounds__(kThreads) void level_bounds_kernel(const uint8_t *_
         lb[(size_t)ray * (levels + 1) + lane] = lane == 0 ? 0u : mine;
 }
 
-// Per-block head histograms of the samples live at the level (the layout of
-// the assignment's counts: counts[k * num_blocks + b]).  Thread t takes
-// samples t + 256 q of the block (q < 16); all 16 level bytes and cells are
-// loaded up front, so the loads are in flight together.
+// Per-block key histograms (the layout of the assignment's counts:
+// counts[key * num_blocks + b]; num_keys keys of key_bits bits), MODE
+// kCellAtLevel or kLevelCell.  Thread t takes samples t + 256 q of the block
+// (q < 16); all 16 level bytes and cells are loaded up front, so the loads
+// are in flight together.
+template <int MODE>
 __global__ __launch_bounds__(kThreads) void level_count_kernel(const uint8_t *__restrict__ cell,
-                                                              unsigned num_samples, int num_sites,
-                                                              int site_bits, LevelLive live,
+                                                              unsigned num_samples, int num_keys,
+                                                              int key_bits, LevelLive live,
                                                               unsigned *__restrict__ counts,
                                                               unsigned num_blocks)
 {
     constexpr int kSteps = kBucketBlock / kThreads;
     __shared__ unsigned s_hist[kMaxSites];
-    for (int k = threadIdx.x; k < num_sites; k += kThreads)
+    for (int k = threadIdx.x; k < num_keys; k += kThreads)
         s_hist[k] = 0;
     const unsigned long long base = (unsigned long long)blockIdx.x * kBucketBlock + threadIdx.x;
     uint8_t lv[kSteps], cs[kSteps];
@@ -708,16 +717,17 @@ __global__ __launch_bounds__(kThreads) void level_count_kernel(const uint8_t *__
     const uint64_t lane_bit = 1ull << (threadIdx.x & 63);
 #pragma unroll
     for (int q = 0; q < kSteps; ++q) {
-        const bool ok = lv[q] == live.level;
+        const bool ok = MODE == kLevelCell ? lv[q] != kDeadLevel : lv[q] == live.level;
+        const unsigned key = MODE == kLevelCell ? lv[q] * live.heads + cs[q] : cs[q];
         const uint64_t any = __ballot(ok);
         if (any == 0)
             continue;  // no live sample in this wave's step
-        const uint64_t peers = match_peers(cs[q], site_bits, any);
+        const uint64_t peers = match_peers(key, key_bits, any);
         if (ok && (peers & (lane_bit - 1)) == 0)
-            atomicAdd(&s_hist[cs[q]], (unsigned)__popcll(peers));
+            atomicAdd(&s_hist[key], (unsigned)__popcll(peers));
     }
     __syncthreads();
-    for (int k = threadIdx.x; k < num_sites; k += kThreads)
+    for (int k = threadIdx.x; k < num_keys; k += kThreads)
         counts[(size_t)k * num_blocks + blockIdx.x] = s_hist[k];
 }
 
@@ -733,13 +743,16 @@ __global__ __launch_bounds__(kThreads) void level_count_kernel(const uint8_t *__
 // head by ballot and advances the wave's own counters.  A sample owned by a
 // 0-capacity head keeps its bucket slot (the offsets are the same) but gets
 // zero density and colour in sr: the MLP does not evaluate that head.
-template <bool LEVEL>
+// MODE: the key (kCellKey, kCellAtLevel, kLevelCell); num_sites counts the
+// keys, site_bits their bits.
+template <int MODE>
 __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
     const uint8_t *__restrict__ cell, const unsigned *__restrict__ prefix,
     const unsigned *__restrict__ totals, unsigned num_samples, unsigned num_blocks,
     int num_sites, int site_bits, HeadMask empty, LevelLive live, unsigned *__restrict__ bucket,
     float4 *__restrict__ sr)
 {
+    constexpr bool LEVEL = MODE == kCellAtLevel;
     constexpr int kWavesPerBlock = kThreads / 64;
     constexpr int kSteps = kBucketBlock / kThreads;  // 64-sample steps per wave
     __shared__ unsigned s_base[kMaxSites];
@@ -760,6 +773,8 @@ __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
         cs[step] = in[step] ? cell[s] : 0u;  // not gated on liveness: loads overlap
         if constexpr (LEVEL)
             in[step] = in[step] && live(s);
+        if constexpr (MODE == kLevelCell)
+            cs[step] += in[step] ? live.lvl[s] * live.heads : 0u;
     }
     __syncthreads();
     // pass 1: this wave's count per head
@@ -799,8 +814,126 @@ __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
             const unsigned pos = start + (unsigned)__popcll(peers & below);
             if (pos < num_samples)  // always true when the counts are consistent
                 bucket[pos] = s;
-            if (empty.test(c))
+            if (empty.test(MODE == kLevelCell ? c % live.heads : c))
                 sr[s] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            if ((peers & below) == 0)
+                s_pos[w][c] = start + (unsigned)__popcll(peers);
+        }
+    }
+}
+
+// After the one-pass (level, head) bucketing: offsets[key] = where key
+// (level l, head k at l K + k) starts in the level-major order, an exclusive
+// scan of totals over the L K <= 256 keys; live[l][k], the entries the MLP
+// will evaluate, starts as every sample for level 0 (no ray has closed) and
+// 0 for the levels the compaction fills.  One block of 256 threads; also
+// clears the MLP's tile counters.
+__global__ __launch_bounds__(kThreads) void level_head_init_kernel(
+    const unsigned *__restrict__ totals, int num_keys, int heads, unsigned *__restrict__ offsets,
+    unsigned *__restrict__ live, unsigned *__restrict__ mlp_queue)
+{
+    __shared__ unsigned s_wave[kThreads / 64];
+    const int k = threadIdx.x, lane = k & 63, w = k >> 6;
+    if (k < kMlpQueues * kMaxHeadGroups)
+        mlp_queue[k] = 0;
+    const unsigned v = k < num_keys ? totals[k] : 0u;
+    unsigned x = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const unsigned y = __shfl_up(x, off);
+        if (lane >= off)
+            x += y;
+    }
+    if (lane == 63)
+        s_wave[w] = x;
+    __syncthreads();
+    unsigned before = x - v;
+    for (int j = 0; j < w; ++j)
+        before += s_wave[j];
+    if (k < num_keys) {
+        offsets[k] = before;
+        live[k] = k < heads ? v : 0u;
+    }
+}
+
+// Per-level compaction (levels 1 ..): the level's entries of the (level,
+// head) order, [offsets[l K], offsets[l K] + the level's total), go to the
+// same positions of bucket, each head's live ones (their ray still open)
+// packed at the front of the head's stretch; live[k] counts them.  Wave w of
+// block b takes 1024 consecutive entries in 16 steps of 64: pass 1 counts
+// them per head (equal-head ballots), one atomic per head and wave reserves
+// their positions, pass 2 ranks and writes.  The order of the waves' pieces
+// within a head is not fixed; each sample's outputs do not depend on it.
+// Block 0 clears the MLP's tile counters.
+__global__ __launch_bounds__(kThreads) void level_compact_kernel(
+    const unsigned *__restrict__ order, const unsigned *__restrict__ offsets,
+    const unsigned *__restrict__ totals, const uint8_t *__restrict__ lvl,
+    const uint8_t *__restrict__ cell, unsigned level, unsigned levels, int heads, int head_bits,
+    unsigned num_samples, unsigned *__restrict__ live, unsigned *__restrict__ bucket,
+    unsigned *__restrict__ mlp_queue)
+{
+    constexpr int kWavesPerBlock = kThreads / 64;
+    constexpr int kSteps = kBucketBlock / kThreads;
+    __shared__ unsigned s_pos[kWavesPerBlock][kMaxSites];
+    if (blockIdx.x == 0 && threadIdx.x < (unsigned)(kMlpQueues * kMaxHeadGroups))
+        mlp_queue[threadIdx.x] = 0;
+    const unsigned begin = offsets[level * heads];
+    const unsigned end = level + 1 < levels ? offsets[(level + 1) * heads] : num_samples;
+    if ((unsigned long long)blockIdx.x * kBucketBlock >= end - begin)
+        return;  // (block-uniform) past the level's entries
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const uint64_t below = (1ull << lane) - 1;
+    for (int k = lane; k < heads; k += 64)
+        s_pos[w][k] = 0;
+    const unsigned wbase = begin + blockIdx.x * (unsigned)kBucketBlock + w * (kSteps * 64);
+    unsigned sid[kSteps], cs[kSteps];
+    bool ok[kSteps];
+#pragma unroll
+    for (int step = 0; step < kSteps; ++step) {
+        const unsigned j = wbase + step * 64 + lane;
+        const bool in = j < end;
+        sid[step] = in ? order[j] : 0u;
+    }
+#pragma unroll
+    for (int step = 0; step < kSteps; ++step) {
+        const unsigned j = wbase + step * 64 + lane;
+        const bool in = j < end;
+        cs[step] = in ? cell[sid[step]] : 0u;
+        ok[step] = in && lvl[sid[step]] == level;
+    }
+    __syncthreads();
+    // pass 1: this wave's live entries per head
+#pragma unroll
+    for (int step = 0; step < kSteps; ++step) {
+        const uint64_t any = __ballot(ok[step]);
+        if (any == 0)
+            continue;
+        const uint64_t peers = match_peers(cs[step], head_bits, any);
+        if (ok[step] && (peers & below) == 0)
+            s_pos[w][cs[step]] += (unsigned)__popcll(peers);
+    }
+    __syncthreads();
+    // reserve each head's positions
+    for (int k = lane; k < heads; k += 64) {
+        const unsigned cnt = s_pos[w][k];
+        s_pos[w][k] = cnt ? atomicAdd(live + k, cnt) : 0u;
+    }
+    __syncthreads();
+    // pass 2: ranks and writes
+#pragma unroll
+    for (int step = 0; step < kSteps; ++step) {
+        const uint64_t any = __ballot(ok[step]);
+        if (any == 0)
+            continue;
+        const unsigned c = cs[step];
+        const uint64_t peers = match_peers(c, head_bits, any);
+        if (ok[step]) {
+            const unsigned start = s_pos[w][c];
+            const unsigned pos = offsets[level * heads + c] + start + (unsigned)__popcll(peers & below);
+            // within the head's stretch whenever the totals are consistent
+            if (start + (unsigned)__popcll(peers & below) < totals[level * heads + c] &&
+                pos < num_samples)
+                bucket[pos] = sid[step];
             if ((peers & below) == 0)
                 s_pos[w][c] = start + (unsigned)__popcll(peers);
         }
@@ -1079,7 +1212,7 @@ hipError_t launch_bucket_scatter(const uint8_t *cell, const unsigned *counts,
                                  const HeadMask &empty, unsigned *bucket, float4 *sr,
                                  hipStream_t s)
 {
-    bucket_scatter_kernel<false><<<num_blocks, kThreads, 0, s>>>(
+    bucket_scatter_kernel<kCellKey><<<num_blocks, kThreads, 0, s>>>(
         cell, counts, totals, num_samples, num_blocks, num_sites, site_bits, empty, LevelLive{},
         bucket, sr);
     return hipGetLastError();
@@ -1104,14 +1237,52 @@ hipError_t launch_level_bounds(const uint8_t *cell, unsigned n, unsigned num_ray
     return hipGetLastError();
 }
 
-static LevelLive level_live(const CullLevel &lv) { return LevelLive{lv.lvl, lv.level}; }
+static LevelLive level_live(const CullLevel &lv) { return LevelLive{lv.lvl, lv.level, 0u}; }
 
 hipError_t launch_level_count(const RenderGeometry &g, const uint8_t *cell, int num_sites,
                               int site_bits, const CullLevel &lv, unsigned *counts,
                               unsigned num_blocks, hipStream_t s)
 {
-    level_count_kernel<<<num_blocks, kThreads, 0, s>>>(cell, g.num_samples, num_sites, site_bits,
-                                                       level_live(lv), counts, num_blocks);
+    level_count_kernel<kCellAtLevel><<<num_blocks, kThreads, 0, s>>>(
+        cell, g.num_samples, num_sites, site_bits, level_live(lv), counts, num_blocks);
+    return hipGetLastError();
+}
+
+hipError_t launch_level_head_order(const RenderGeometry &g, unsigned levels, int heads,
+                                   int key_bits, const uint8_t *lvl, const uint8_t *cell,
+                                   const HeadMask &empty, unsigned *counts, unsigned num_blocks,
+                                   unsigned *totals, unsigned *order, unsigned *offsets,
+                                   unsigned *live, float4 *sr, unsigned *mlp_queue, hipStream_t s)
+{
+    const int keys = (int)levels * heads;
+    const LevelLive lk{lvl, 0u, (unsigned)heads};
+    level_count_kernel<kLevelCell><<<num_blocks, kThreads, 0, s>>>(cell, g.num_samples, keys,
+                                                                   key_bits, lk, counts, num_blocks);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    e = launch_bucket_scan(counts, num_blocks, keys, totals, mlp_queue, s);
+    if (e != hipSuccess)
+        return e;
+    bucket_scatter_kernel<kLevelCell><<<num_blocks, kThreads, 0, s>>>(
+        cell, counts, totals, g.num_samples, num_blocks, keys, key_bits, empty, lk, order, sr);
+    e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    level_head_init_kernel<<<1, kThreads, 0, s>>>(totals, keys, heads, offsets, live, mlp_queue);
+    return hipGetLastError();
+}
+
+hipError_t launch_level_compact(const RenderGeometry &g, unsigned level, unsigned levels,
+                                int heads, int head_bits, const unsigned *order,
+                                const unsigned *offsets, const unsigned *totals,
+                                const uint8_t *lvl, const uint8_t *cell, unsigned num_blocks,
+                                unsigned *live, unsigned *bucket, unsigned *mlp_queue,
+                                hipStream_t s)
+{
+    level_compact_kernel<<<num_blocks, kThreads, 0, s>>>(order, offsets, totals, lvl, cell, level,
+                                                         levels, heads, head_bits, g.num_samples,
+                                                         live, bucket, mlp_queue);
     return hipGetLastError();
 }
 
@@ -1121,7 +1292,7 @@ hipError_t launch_level_scatter(const RenderGeometry &g, const uint8_t *cell,
                                 const HeadMask &empty, const CullLevel &lv, unsigned *bucket,
                                 float4 *sr, hipStream_t s)
 {
-    bucket_scatter_kernel<true><<<num_blocks, kThreads, 0, s>>>(
+    bucket_scatter_kernel<kCellAtLevel><<<num_blocks, kThreads, 0, s>>>(
         cell, counts, totals, g.num_samples, num_blocks, num_sites, site_bits, empty,
         level_live(lv), bucket, sr);
     return hipGetLastError();

@@ -592,11 +592,13 @@ using Chunk = std::conditional_t<C::BF16, bf16x8, float>;
 // "no tile left" from the work queues
 constexpr unsigned kNoTile = 0xFFFFFFFFu;
 
-// SOFT: every head takes every sample (see MlpVariant::launch).
-template <class C, bool SOFT>
+// SOFT: every head takes every sample (see MlpVariant::launch).  OFFS: each
+// head's entries start at offsets[k] (not SOFT).
+template <class C, bool SOFT, bool OFFS>
 __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
-    const unsigned *__restrict__ bucket, const unsigned *__restrict__ totals, int num_sites,
-    RenderGeometry geo, const float *__restrict__ tbuf, const void *__restrict__ dirbuf,
+    const unsigned *__restrict__ bucket, const unsigned *__restrict__ totals,
+    const unsigned *__restrict__ offsets, int num_sites, RenderGeometry geo,
+    const float *__restrict__ tbuf, const void *__restrict__ dirbuf,
     const unsigned char *__restrict__ streams, const float *__restrict__ blocks,
     float4 *__restrict__ sr, unsigned *__restrict__ queue, HeadMask empty)
 {
@@ -616,7 +618,8 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
     const int n = lane & 31, g = lane >> 5;
 
     // bucket offset and first tile of each head: exclusive scans of the
-    // totals and of their tile counts, by wave 0 with 4 heads per lane
+    // totals (or the given offsets, where the heads' entries need not be
+    // adjacent) and of their tile counts, by wave 0 with 4 heads per lane
     if (tid < 64) {
         unsigned tot[4], nt[4], so = 0, st = 0;
 #pragma unroll
@@ -642,7 +645,7 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
         for (int j = 0; j < 4; ++j) {
             const int k = 4 * tid + j;
             if (k < num_sites) {
-                s_off[k] = off;
+                s_off[k] = OFFS ? offsets[k] : off;
                 s_tile[k] = tl;
             }
             off += tot[j];
@@ -730,6 +733,13 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
     // rows end at the sample count; with soft, each head's rows are all the
     // samples again (head k's at k S, read through bucket[row - k S])
     const unsigned row_cap = soft ? s_off[num_sites] : geo.num_samples;
+    // end of head h's entries (with offsets, from memory: scalar loads)
+    auto head_end = [&](int h) -> unsigned {
+        if constexpr (OFFS)
+            return offsets[h] + totals[h];
+        else
+            return s_off[h + 1];
+    };
     // the two prefetch phases for the tile whose rows are [r0, r_end) and
     // whose bucket entries start at row base
     auto prefetch_ids = [&](unsigned r0, unsigned r_end, unsigned base) {
@@ -759,7 +769,7 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
     const unsigned char *stream = stream_of(head);
     // the first tile's records, waited for in full
     prefetch_ids(__builtin_amdgcn_readfirstlane(s_off[head] + (tile - s_tile[head]) * C::TILE),
-                 __builtin_amdgcn_readfirstlane(min(s_off[head + 1], row_cap)),
+                 __builtin_amdgcn_readfirstlane(min(head_end(head), row_cap)),
                  soft ? s_off[head] : 0u);
     wait_vmcnt<0>();
     prefetch_rays();
@@ -775,11 +785,11 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
         const unsigned row0 = __builtin_amdgcn_readfirstlane(s_off[head] + (tile - s_tile[head]) * C::TILE);
         // rows never pass the sample count when the bucket counts are
         // consistent; the clamps keep every access in bounds regardless
-        const unsigned row_end = __builtin_amdgcn_readfirstlane(min(s_off[head + 1], row_cap));
+        const unsigned row_end = __builtin_amdgcn_readfirstlane(min(head_end(head), row_cap));
         // rows of the tile whose records are prefetched (this one's if last)
         const unsigned pf_tile = has_next ? next : tile;
         const unsigned nrow0 = __builtin_amdgcn_readfirstlane(s_off[nhead] + (pf_tile - s_tile[nhead]) * C::TILE);
-        const unsigned nrow_end = __builtin_amdgcn_readfirstlane(min(s_off[nhead + 1], row_cap));
+        const unsigned nrow_end = __builtin_amdgcn_readfirstlane(min(head_end(nhead), row_cap));
 
         wg_barrier();  // previous tile is done with the head block and the staging
         // this tile's records have landed (at most that many loads were issued
@@ -1063,7 +1073,8 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
 }
 
 template <class C>
-hipError_t launch_mlp(const unsigned *bucket, const unsigned *totals, int num_sites,
+hipError_t launch_mlp(const unsigned *bucket, const unsigned *totals, const unsigned *offsets,
+                      int num_sites,
                       const RenderGeometry &g, const float *t, const void *dirbuf,
                       const unsigned char *streams, const float *blocks, float4 *sr,
                       unsigned *queue, int cus, bool soft, const HeadMask &empty, hipStream_t s)
@@ -1073,18 +1084,23 @@ hipError_t launch_mlp(const unsigned *bucket, const unsigned *totals, int num_si
         // raises the dynamic LDS limit where the runtime keeps one; a runtime
         // without the limit may refuse the call, and the launch below reports
         // any real problem
-        for (const void *k : {(const void *)mlp_kernel<C, false>, (const void *)mlp_kernel<C, true>})
+        for (const void *k : {(const void *)mlp_kernel<C, false, false>,
+                              (const void *)mlp_kernel<C, true, false>,
+                              (const void *)mlp_kernel<C, false, true>})
             if (hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES) !=
                 hipSuccess)
                 (void)hipGetLastError();
         configured = true;
     }
     if (soft)
-        mlp_kernel<C, true><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(
-            bucket, totals, num_sites, g, t, dirbuf, streams, blocks, sr, queue, empty);
+        mlp_kernel<C, true, false><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(
+            bucket, totals, nullptr, num_sites, g, t, dirbuf, streams, blocks, sr, queue, empty);
+    else if (offsets)
+        mlp_kernel<C, false, true><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(
+            bucket, totals, offsets, num_sites, g, t, dirbuf, streams, blocks, sr, queue, empty);
     else
-        mlp_kernel<C, false><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(
-            bucket, totals, num_sites, g, t, dirbuf, streams, blocks, sr, queue, empty);
+        mlp_kernel<C, false, false><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(
+            bucket, totals, nullptr, num_sites, g, t, dirbuf, streams, blocks, sr, queue, empty);
     return hipGetLastError();
 }
 

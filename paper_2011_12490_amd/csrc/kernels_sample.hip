@@ -90,17 +90,33 @@ __global__ __launch_bounds__(kThreads) void ray_encode_kernel(const float *__res
 }
 
 // ---------------------------------------------------------------------------
-// Lanes of this wave whose value equals mine, among the lanes in `valid`:
-// one ballot per bit of the value.
-__device__ __forceinline__ uint64_t match_peers(unsigned v, int bits, uint64_t valid)
+// Runs of equal keys among the lanes of a wave: a run is a maximal stretch of
+// consecutive lanes, all in `valid`, holding one key.  Along a ray the keys
+// (heads, levels) change rarely, so a 64-lane step holds a few runs, and the
+// run leaders -- not one ballot per key bit -- do the step's bookkeeping.
+// Two runs of one key in a step (two rays, or a key coming back) are two
+// runs: each leader adds or reserves its own count.
+struct LaneRuns {
+    uint64_t starts;  // lanes that start a run
+    unsigned len;     // the run's length (meaningful in its start lane)
+    int first;        // the lane that starts this lane's run (valid lanes)
+};
+__device__ __forceinline__ LaneRuns lane_runs(unsigned key, bool ok, uint64_t valid)
 {
-    uint64_t peers = valid;
-    for (int b = 0; b < bits; ++b) {
-        const bool bit = (v >> b) & 1u;
-        const uint64_t m = __ballot(bit);
-        peers &= bit ? m : ~m;
-    }
-    return peers;
+    const int lane = (int)(threadIdx.x & 63);
+    // the key of lane - 1 (DPP wave shift right by one)
+    const unsigned prev = (unsigned)__builtin_amdgcn_update_dpp(0, (int)key, 0x138, 0xF, 0xF, false);
+    const bool prev_ok = lane > 0 && ((valid >> (lane - 1)) & 1ull);
+    LaneRuns r;
+    r.starts = __ballot(ok && (!prev_ok || prev != key));
+    // the next start or invalid lane above this one ends the run
+    const uint64_t above = ~((2ull << lane) - 1ull);  // lanes lane + 1 .. 63
+    const uint64_t brk = (r.starts | ~valid) & above;
+    r.len = (unsigned)((brk ? __builtin_ctzll(brk) : 64) - lane);
+    const uint64_t upto = ~0ull >> (63 - lane);
+    const uint64_t mine = r.starts & upto;
+    r.first = mine ? 63 - __builtin_clzll(mine) : lane;
+    return r;
 }
 
 // ---------------------------------------------------------------------------
@@ -501,14 +517,13 @@ __global__ __launch_bounds__(kThreads) void sample_assign_kernel(
                     cell_out[s0 + v] = (uint8_t)cv[v];
                 }
         }
-        // histogram: the lowest lane of each group of equal cells adds the group size
+        // histogram: the first lane of each run of equal cells adds the run's length
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
             const bool ok = s0 + v < g.num_samples;
-            const uint64_t valid = __ballot(ok);
-            const uint64_t peers = match_peers(cv[v], site_bits, valid);
-            if (ok && (peers & (lane_bit - 1)) == 0)
-                atomicAdd(&s_hist[cv[v]], (unsigned)__popcll(peers));
+            const LaneRuns r = lane_runs(cv[v], ok, __ballot(ok));
+            if ((r.starts & lane_bit) != 0)
+                atomicAdd(&s_hist[cv[v]], r.len);
         }
     }
     __syncthreads();
@@ -722,9 +737,9 @@ __global__ __launch_bounds__(kThreads) void level_count_kernel(const uint8_t *__
         const uint64_t any = __ballot(ok);
         if (any == 0)
             continue;  // no live sample in this wave's step
-        const uint64_t peers = match_peers(key, key_bits, any);
-        if (ok && (peers & (lane_bit - 1)) == 0)
-            atomicAdd(&s_hist[key], (unsigned)__popcll(peers));
+        const LaneRuns r = lane_runs(key, ok, any);
+        if ((r.starts & lane_bit) != 0)
+            atomicAdd(&s_hist[key], r.len);
     }
     __syncthreads();
     for (int k = threadIdx.x; k < num_keys; k += kThreads)
@@ -758,7 +773,6 @@ __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
     __shared__ unsigned s_base[kMaxSites];
     __shared__ unsigned s_pos[kWavesPerBlock][kMaxSites];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const uint64_t below = (1ull << lane) - 1;
     head_block_base(prefix, totals, num_blocks, num_sites, s_base);
     for (int k = threadIdx.x; k < num_sites; k += kThreads)
         for (int v = 0; v < kWavesPerBlock; ++v)
@@ -777,16 +791,16 @@ __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
             cs[step] += in[step] ? live.lvl[s] * live.heads : 0u;
     }
     __syncthreads();
-    // pass 1: this wave's count per head
+    // pass 1: this wave's count per head (run leaders)
 #pragma unroll
     for (int step = 0; step < kSteps; ++step) {
         const bool ok = in[step];
         const uint64_t any = __ballot(ok);
         if (LEVEL && any == 0)
             continue;
-        const uint64_t peers = match_peers(cs[step], site_bits, any);
-        if (ok && (peers & below) == 0)
-            s_pos[w][cs[step]] += (unsigned)__popcll(peers);
+        const LaneRuns r = lane_runs(cs[step], ok, any);
+        if ((r.starts >> lane) & 1ull)
+            atomicAdd(&s_pos[w][cs[step]], r.len);
     }
     __syncthreads();
     // counts -> each wave's first position per head
@@ -808,16 +822,18 @@ __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
         if (LEVEL && any == 0)
             continue;
         const unsigned c = cs[step];
-        const uint64_t peers = match_peers(c, site_bits, any);
-        const unsigned start = ok ? s_pos[w][c] : 0u;
+        // each run's leader reserves the run's positions; its lanes follow it
+        const LaneRuns r = lane_runs(c, ok, any);
+        unsigned start = 0;
+        if ((r.starts >> lane) & 1ull)
+            start = atomicAdd(&s_pos[w][c], r.len);
+        start = __shfl(start, r.first);
         if (ok) {
-            const unsigned pos = start + (unsigned)__popcll(peers & below);
+            const unsigned pos = start + (unsigned)(lane - r.first);
             if (pos < num_samples)  // always true when the counts are consistent
                 bucket[pos] = s;
             if (empty.test(MODE == kLevelCell ? c % live.heads : c))
                 sr[s] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-            if ((peers & below) == 0)
-                s_pos[w][c] = start + (unsigned)__popcll(peers);
         }
     }
 }
@@ -882,7 +898,6 @@ __global__ __launch_bounds__(kThreads) void level_compact_kernel(
     if ((unsigned long long)blockIdx.x * kBucketBlock >= end - begin)
         return;  // (block-uniform) past the level's entries
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const uint64_t below = (1ull << lane) - 1;
     for (int k = lane; k < heads; k += 64)
         s_pos[w][k] = 0;
     const unsigned wbase = begin + blockIdx.x * (unsigned)kBucketBlock + w * (kSteps * 64);
@@ -902,15 +917,15 @@ __global__ __launch_bounds__(kThreads) void level_compact_kernel(
         ok[step] = in && lvl[sid[step]] == level;
     }
     __syncthreads();
-    // pass 1: this wave's live entries per head
+    // pass 1: this wave's live entries per head (run leaders)
 #pragma unroll
     for (int step = 0; step < kSteps; ++step) {
         const uint64_t any = __ballot(ok[step]);
         if (any == 0)
             continue;
-        const uint64_t peers = match_peers(cs[step], head_bits, any);
-        if (ok[step] && (peers & below) == 0)
-            s_pos[w][cs[step]] += (unsigned)__popcll(peers);
+        const LaneRuns r = lane_runs(cs[step], ok[step], any);
+        if ((r.starts >> lane) & 1ull)
+            atomicAdd(&s_pos[w][cs[step]], r.len);
     }
     __syncthreads();
     // reserve each head's positions
@@ -926,16 +941,17 @@ __global__ __launch_bounds__(kThreads) void level_compact_kernel(
         if (any == 0)
             continue;
         const unsigned c = cs[step];
-        const uint64_t peers = match_peers(c, head_bits, any);
+        const LaneRuns r = lane_runs(c, ok[step], any);
+        unsigned start = 0;
+        if ((r.starts >> lane) & 1ull)
+            start = atomicAdd(&s_pos[w][c], r.len);
+        start = __shfl(start, r.first);
         if (ok[step]) {
-            const unsigned start = s_pos[w][c];
-            const unsigned pos = offsets[level * heads + c] + start + (unsigned)__popcll(peers & below);
+            const unsigned rank = start + (unsigned)(lane - r.first);
+            const unsigned pos = offsets[level * heads + c] + rank;
             // within the head's stretch whenever the totals are consistent
-            if (start + (unsigned)__popcll(peers & below) < totals[level * heads + c] &&
-                pos < num_samples)
+            if (rank < totals[level * heads + c] && pos < num_samples)
                 bucket[pos] = sid[step];
-            if ((peers & below) == 0)
-                s_pos[w][c] = start + (unsigned)__popcll(peers);
         }
     }
 }

@@ -176,11 +176,11 @@ __device__ __forceinline__ void encode(const float x[3], int g, float *f)
         f[e] = 0.0f;
 }
 
-// Persistent workgroups; wave w of workgroup b takes the 64-sample blocks
-// b kGateWaves + w + j gridDim.x kGateWaves.  Each lane draws the depth of
-// one sample of the block (the generator runs once per sample); the network
-// then runs twice, on the block's first and second 32 samples, with the
-// positions exchanged between the lane halves.  packed: the layout above,
+// Persistent workgroups; wave w of workgroup b takes the 256-sample
+// stretches b kGateWaves + w + j gridDim.x kGateWaves, in blocks of 64.  Each
+// lane computes the depth of one sample of a block; the network then runs
+// twice, on the block's first and second 32 samples, with the positions
+// exchanged between the lane halves.  packed: the layout above,
 // staged in LDS.  Writes each sample's depth to t and its gated head to cell
 // (and to out_cell, int32, when given).
 template <int L, int H>
@@ -279,41 +279,76 @@ __global__ __launch_bounds__(kGateThreads) void gate_kernel(RenderGeometry g,
         return bk < num_sites ? bk : num_sites - 1;
     };
 
-    const unsigned blocks = (unsigned)(((unsigned long long)g.num_samples + 63) / 64);
-    for (unsigned blk = blockIdx.x * kGateWaves + wave; blk < blocks;
-         blk += gridDim.x * kGateWaves) {
-        const unsigned s = blk * 64 + lane;
-        const bool valid = s < g.num_samples;
-        // s -> (ray, index within the ray); the float64 quotient is at most
-        // one below the true one
-        const unsigned sc = valid ? s : 0u;
-        unsigned ray = (unsigned)((double)sc * g.inv_n), i = sc - ray * g.n;
-        if (i >= g.n) {
-            ++ray;
-            i -= g.n;
+    // A wave takes 256 samples at a time, in four blocks of 64.  The jitter
+    // of samples 4 j .. 4 j + 3 of a ray is one Philox block (its four
+    // words); when the sample count per ray is a multiple of 4, those
+    // quadruples never straddle two rays, so lane l draws the block of the
+    // quadruple 4 l .. 4 l + 3 of the 256 once, and each sample reads its
+    // word from that lane.  Otherwise every lane draws its own sample's.
+    const bool quads = g.perturb && g.n % 4u == 0;
+    const unsigned long long NS = g.num_samples;
+    const unsigned supers = (unsigned)((NS + 255) / 256);
+    for (unsigned sb = blockIdx.x * kGateWaves + wave; sb < supers;
+         sb += gridDim.x * kGateWaves) {
+        uint4 blk4 = make_uint4(0u, 0u, 0u, 0u);
+        if (quads) {
+            const unsigned long long s4 = (unsigned long long)sb * 256 + 4 * lane;
+            const unsigned sc = s4 < NS ? (unsigned)s4 : 0u;
+            unsigned ray = (unsigned)((double)sc * g.inv_n), i = sc - ray * g.n;
+            if (i >= g.n) {
+                ++ray;
+                i -= g.n;
+            }
+            const uint64_t rg = g.ray_offset + ray;
+            blk4 = philox4x32_10(make_uint4(i >> 2, (unsigned)rg, (unsigned)(rg >> 32), 0u), key);
         }
-        const float xi = g.perturb ? jitter(key, g.ray_offset + ray, i, 0u) : 0.5f;
-        const float ts = fmaf(g.step, (float)i + xi, g.near_t);
-        float x[3], xa[3], xb[3];
+#pragma unroll 1
+        for (int w = 0; w < 4; ++w) {
+            const unsigned long long s64 = (unsigned long long)sb * 256 + 64 * w + lane;
+            const bool valid = s64 < NS;
+            const unsigned s = (unsigned)s64;
+            // s -> (ray, index within the ray); the float64 quotient is at
+            // most one below the true one
+            const unsigned sc = valid ? s : 0u;
+            unsigned ray = (unsigned)((double)sc * g.inv_n), i = sc - ray * g.n;
+            if (i >= g.n) {
+                ++ray;
+                i -= g.n;
+            }
+            float xi = 0.5f;
+            if (quads) {
+                // word i % 4 (= lane % 4) of the block drawn by lane 16 w + lane / 4
+                const int src = 16 * w + (lane >> 2);
+                const unsigned w0 = __shfl(blk4.x, src), w1 = __shfl(blk4.y, src);
+                const unsigned w2 = __shfl(blk4.z, src), w3 = __shfl(blk4.w, src);
+                const int e = lane & 3;
+                const unsigned word = e == 0 ? w0 : e == 1 ? w1 : e == 2 ? w2 : w3;
+                xi = (float)(word >> 8) * 0x1.0p-24f;
+            } else if (g.perturb) {
+                xi = jitter(key, g.ray_offset + ray, i, 0u);
+            }
+            const float ts = fmaf(g.step, (float)i + xi, g.near_t);
+            float x[3], xa[3], xb[3];
 #pragma unroll
-        for (int c = 0; c < 3; ++c) {
-            x[c] = fmaf(ts, g.rays_d[3 * (size_t)ray + c], g.rays_o[3 * (size_t)ray + c]);
-            // lane n holds sample n of the block, lane n + 32 sample n + 32:
-            // the first pass takes samples 0..31 on both halves, the second
-            // samples 32..63
-            const float other = __shfl_xor(x[c], 32);
-            xa[c] = lg ? other : x[c];
-            xb[c] = lg ? x[c] : other;
-        }
-        if (valid)
-            t[s] = ts;
-        const int ka = decide(xa);
-        const int kb = decide(xb);
-        if (valid) {
-            const int k = lg ? kb : ka;
-            cell[s] = (uint8_t)k;
-            if (out_cell)
-                out_cell[s] = k;
+            for (int c = 0; c < 3; ++c) {
+                x[c] = fmaf(ts, g.rays_d[3 * (size_t)ray + c], g.rays_o[3 * (size_t)ray + c]);
+                // lane n holds sample n of the block, lane n + 32 sample n +
+                // 32: the first pass takes samples 0..31 on both halves, the
+                // second samples 32..63
+                const float other = __shfl_xor(x[c], 32);
+                xa[c] = lg ? other : x[c];
+                xb[c] = lg ? x[c] : other;
+            }
+            if (valid)
+                t[s] = ts;
+            const int ka = decide(xa);
+            const int kb = decide(xb);
+            if (valid) {
+                const int k = lg ? kb : ka;
+                cell[s] = (uint8_t)k;
+                if (out_cell)
+                    out_cell[s] = k;
+            }
         }
     }
 }
@@ -340,8 +375,8 @@ hipError_t launch_gate_lh(const RenderGeometry &g, const unsigned char *packed, 
     // as many resident workgroups per CU as the LDS allows, at most 4
     const unsigned fit = (unsigned)(160u * 1024u / (lds + 1024));
     const unsigned per_cu = fit < 1 ? 1 : (fit > 4 ? 4 : fit);
-    const unsigned blocks = (unsigned)(((unsigned long long)g.num_samples + 63) / 64);
-    const unsigned want = (blocks + kGateWaves - 1) / kGateWaves;
+    const unsigned supers = (unsigned)(((unsigned long long)g.num_samples + 255) / 256);
+    const unsigned want = (supers + kGateWaves - 1) / kGateWaves;
     const unsigned cap = (unsigned)cus * per_cu;
     const unsigned grid = want < cap ? want : cap;
     gate_kernel<L, H><<<grid, kGateThreads, lds, s>>>(g, packed, (unsigned)lay.bytes, num_sites, t,

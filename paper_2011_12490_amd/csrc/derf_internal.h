@@ -71,6 +71,8 @@ hipError_t launch_gate(const RenderGeometry &g, const unsigned char *packed, int
                        hipStream_t s);
 
 // ---- sampling, assignment and bucketing (kernels_sample.hip) -------------
+// p[0 .. count) = v (a kernel: no memset node in a captured stream)
+hipError_t launch_fill_u32(unsigned *p, unsigned count, unsigned v, hipStream_t s);
 hipError_t launch_ray_encode(const RenderGeometry &g, void *dirbuf, bool bf16, hipStream_t s);
 // Walk every ray of g through the cells on [near, far] (one lane per ray).
 hipError_t launch_ray_walk(const RenderGeometry &g, const float4 *sites, int num_sites,

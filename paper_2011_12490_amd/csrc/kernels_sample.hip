@@ -1156,9 +1156,25 @@ __global__ __launch_bounds__(kThreads) void debug_expand_kernel(
     }
 }
 
+__global__ __launch_bounds__(kThreads) void fill_u32_kernel(unsigned *__restrict__ p, unsigned count,
+                                                          unsigned v)
+{
+    const unsigned i = blockIdx.x * kThreads + threadIdx.x;
+    if (i < count)
+        p[i] = v;
+}
+
 inline unsigned blocks_for(size_t items, unsigned per) { return (unsigned)((items + per - 1) / per); }
 
 }  // namespace
+
+hipError_t launch_fill_u32(unsigned *p, unsigned count, unsigned v, hipStream_t s)
+{
+    if (count == 0)
+        return hipSuccess;
+    fill_u32_kernel<<<blocks_for(count, kThreads), kThreads, 0, s>>>(p, count, v);
+    return hipGetLastError();
+}
 
 hipError_t launch_ray_encode(const RenderGeometry &g, void *dirbuf, bool bf16, hipStream_t s)
 {

@@ -8,7 +8,7 @@ sides.  Bars: rays that evaluate the same samples on both sides match within
 max-abs 1e-4 (fp32) / 2e-2 (bf16) and make up at least 99 % (fp32) / 95 %
 (bf16) of the rays; every ray is within that tolerance plus the culling bound
 (eps in colour and opacity, eps * far in depth) of the oracle's full render.
-One level (or eps = 0) reproduces derf_render.
+One level (or eps = 0) runs derf_render itself.
 """
 import os
 
@@ -178,10 +178,9 @@ def test_culled_ragged_sample_counts_fp32(n):
 
 
 def test_one_level_or_zero_eps_is_the_plain_render():
-    """levels = 1: derf_render bitwise (the same buckets, MLP tiles and
-    integration); eps = 0 with several levels: the same samples, merged level
-    by level (rounding of the merge only).  Also for heads of mixed
-    capacities (one grouped-MLP launch per architecture per level)."""
+    """levels = 1, or eps = 0 with several levels (no transmittance is below
+    0, so no ray can stop): the call runs derf_render's single pass, bitwise,
+    and counts every sample evaluated.  Also for heads of mixed capacities."""
     derf = _derf()
     sc = _dense_tiny()
     cfg = sc.cfg
@@ -201,10 +200,34 @@ def test_one_level_or_zero_eps_is_the_plain_render():
         for a, b in zip(plain, one[:3]):
             assert torch.equal(a, b), label
         for a, b in zip(plain, zero[:3]):
-            assert (a - b).abs().max().item() <= 1e-5, label
+            assert torch.equal(a, b), label
         assert (one[3] == cfg.n_coarse).all() and (zero[3] == cfg.n_coarse).all()
-        print("%s: one level bitwise, eps=0 max|d|=%.3g" % (
-            label, max((a - b).abs().max().item() for a, b in zip(plain, zero[:3]))), flush=True)
+        print("%s: one level and eps = 0 bitwise" % label, flush=True)
+
+
+def test_levels_that_stop_no_ray_match_the_plain_render():
+    """Several levels with an eps below every ray's final transmittance: no
+    ray stops, every sample is evaluated level by level, and the merge of
+    the levels equals the single pass up to the rounding of the merge."""
+    derf = _derf()
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], num_sites=8, sigma_bias=0.0)
+    sc = scenes.make_scene(cfg)
+    o, d = _rays(sc)
+    r = derf.Renderer(sc.sites, cfg.arch, sc.weights, "fp32")
+    plain = [x.cpu() for x in r.render(o, d, cfg.near, cfg.far, cfg.n_coarse, 0,
+                                       scenes.SEED_RENDER)]
+    eps = 0.5 * float((1.0 - plain[2]).min())
+    assert eps > 0.0
+    for levels, piece in ((4, 0), (8, 5)):
+        culled = [x.cpu() for x in r.render_culled(o, d, cfg.near, cfg.far, cfg.n_coarse, eps,
+                                                   levels, seed=scenes.SEED_RENDER,
+                                                   piece=piece)]
+        assert (culled[3] == cfg.n_coarse).all()
+        err = max((a - b).abs().max().item() for a, b in zip(plain, culled[:3]))
+        print("levels %d piece %d eps %.3g: max|d| vs plain %.3g" % (levels, piece, eps, err),
+              flush=True)
+        assert err <= 1e-5
+    r.close()
 
 
 def test_single_head_has_one_level_only():

@@ -1079,19 +1079,19 @@ hipError_t launch_mlp(const unsigned *bucket, const unsigned *totals, const unsi
                       const unsigned char *streams, const float *blocks, float4 *sr,
                       unsigned *queue, int cus, bool soft, const HeadMask &empty, hipStream_t s)
 {
-    static bool configured = false;
-    if (!configured) {
-        // raises the dynamic LDS limit where the runtime keeps one; a runtime
-        // without the limit may refuse the call, and the launch below reports
-        // any real problem
+    // raises the dynamic LDS limit where the runtime keeps one, once per
+    // variant (thread-safe); a runtime without the limit may refuse the
+    // call, and the launch below reports any real problem
+    static const bool raised = [] {
         for (const void *k : {(const void *)mlp_kernel<C, false, false>,
                               (const void *)mlp_kernel<C, true, false>,
                               (const void *)mlp_kernel<C, false, true>})
             if (hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES) !=
                 hipSuccess)
                 (void)hipGetLastError();
-        configured = true;
-    }
+        return true;
+    }();
+    (void)raised;
     if (soft)
         mlp_kernel<C, true, false><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(
             bucket, totals, nullptr, num_sites, g, t, dirbuf, streams, blocks, sr, queue, empty);

@@ -129,18 +129,23 @@ def test_culled_dense_headline_frame_bf16():
            "culled dense_k16 bf16")
 
 
-@pytest.mark.parametrize("piece,levels,n", [(5, 6, 32), (1, 32, 32), (3, 32, 7), (7, 12, 300),
-                                            (70, 6, 600)])
-def test_culled_pieces_fp32(piece, levels, n):
+@pytest.mark.parametrize("piece,levels,n,K", [(5, 6, 32, 8), (1, 32, 32, 8), (3, 32, 7, 8),
+                                              (7, 12, 300, 8), (48, 6, 300, 8), (70, 6, 600, 8),
+                                              (6, 8, 96, 64)])
+def test_culled_pieces_fp32(piece, levels, n, K):
     """Segments cut into pieces of at most `piece` samples (levels count
     pieces): piece ends inside and across the 64-sample steps of the level
-    bounds and the 256-sample staging chunks of the level composite."""
-    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], num_sites=8, sigma_bias=4.0, n_coarse=n)
+    bounds and the 256-sample staging chunks of the level composite; level
+    composites of 8 and 16 lanes per ray (pieces of at most 32 and 64) and
+    of a wave per ray (70); the one-pass (level, head) bucketing up to its
+    256 keys (32 levels x 8 heads) and the per-level passes beyond (8 levels
+    x 64 heads)."""
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], num_sites=K, sigma_bias=4.0, n_coarse=n)
     sc = scenes.make_scene(cfg)
     gpu = _gpu_culled(sc, "fp32", 1e-3, levels, piece=piece)
     ids = np.arange(0, cfg.num_rays, 1 if n <= 32 else 4)
-    _check(gpu, sc, ids, 1e-3, levels, "fp32", "culled tiny n=%d piece=%d L=%d"
-           % (n, piece, levels), piece=piece)
+    _check(gpu, sc, ids, 1e-3, levels, "fp32", "culled tiny n=%d piece=%d L=%d K=%d"
+           % (n, piece, levels, K), piece=piece)
 
 
 def test_culled_pieces_single_head_fp32():

@@ -121,9 +121,14 @@ def test_gated_256_heads_and_empty_heads_fp32():
     assert len(np.unique(cell)) > 128
 
 
-@pytest.mark.parametrize("n", [1, 2])
-def test_gated_one_or_two_samples_fp32(n):
-    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], num_sites=8, sigma_bias=1.0, n_coarse=n)
+@pytest.mark.parametrize("n", [1, 2, 12])
+def test_gated_sample_counts_fp32(n):
+    """1 and 2 samples per ray (each lane draws its own jitter), and 12 (four
+    samples share a Philox block, drawn once per four lanes), on 31 x 33
+    rays, so that with 12 samples the last 256-sample stretch of the gate is
+    partial."""
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], num_sites=8, sigma_bias=1.0, n_coarse=n,
+                              width=31, height=33)
     sc = scenes.make_scene(cfg)
     gw = random_gate(8, 6, 32, 41, scale=6.0)
     _run(sc, "fp32", 6, 32, gw, np.arange(0, cfg.num_rays, 4), "gated n=%d" % n)

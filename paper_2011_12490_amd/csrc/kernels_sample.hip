@@ -224,9 +224,15 @@ __global__ __launch_bounds__(kThreads) void ray_walk_kernel(RenderGeometry g,
                                                             unsigned char *__restrict__ nseg)
 {
     static_assert(L == 1 || L == 2 || L == 4 || L == 8 || L == 16, "group size");
-    __shared__ float4 s_sites[kMaxSites];
-    for (int k = threadIdx.x; k < num_sites; k += kThreads)
-        s_sites[k] = sites[k];
+    // the sites in float64 with their squared norms: |x - phi|^2 = |x|^2 +
+    // q(x, phi), q = |phi|^2 - 2 x.phi, so differences of squared distances
+    // at one x are differences of q (three fused multiply-adds per site)
+    __shared__ double4 s_sites[kMaxSites];
+    for (int k = threadIdx.x; k < num_sites; k += kThreads) {
+        const float4 p = sites[k];
+        const double px = p.x, py = p.y, pz = p.z;
+        s_sites[k] = make_double4(px, py, pz, px * px + py * py + pz * pz);
+    }
     __syncthreads();
     const size_t r = ((size_t)blockIdx.x * kThreads + threadIdx.x) / L;
     if (r >= g.num_rays)
@@ -236,10 +242,13 @@ __global__ __launch_bounds__(kThreads) void ray_walk_kernel(RenderGeometry g,
     const int j0 = min(gl * per, num_sites), j1 = min(j0 + per, num_sites);
     const double ox = g.rays_o[3 * r], oy = g.rays_o[3 * r + 1], oz = g.rays_o[3 * r + 2];
     const double dx = g.rays_d[3 * r], dy = g.rays_d[3 * r + 1], dz = g.rays_d[3 * r + 2];
-    auto d2 = [&](double x, double y, double z, int k) {
-        const float4 p = s_sites[k];
-        const double ex = x - p.x, ey = y - p.y, ez = z - p.z;
-        return ex * ex + ey * ey + ez * ez;
+    auto q = [&](double x, double y, double z, int k) {
+        const double4 p = s_sites[k];
+        return fma(-2.0, fma(x, p.x, fma(y, p.y, z * p.z)), p.w);
+    };
+    auto dproj = [&](int k) {  // d.phi_k
+        const double4 p = s_sites[k];
+        return fma(dx, p.x, fma(dy, p.y, dz * p.z));
     };
     double t0 = g.near_t;
     double x0 = ox + t0 * dx, y0 = oy + t0 * dy, z0 = oz + t0 * dz;
@@ -247,7 +256,7 @@ __global__ __launch_bounds__(kThreads) void ray_walk_kernel(RenderGeometry g,
     {
         double best = INFINITY;
         for (int k = j0; k < j1; ++k) {
-            const double v = d2(x0, y0, z0, k);
+            const double v = q(x0, y0, z0, k);
             if (v < best) {
                 best = v;
                 c = k;
@@ -259,19 +268,17 @@ __global__ __launch_bounds__(kThreads) void ray_walk_kernel(RenderGeometry g,
     int ns = 0;
     bool ok = true;
     for (;;) {
-        const float4 pc = s_sites[c];
-        const double dc0 = d2(x0, y0, z0, c);
-        // the first crossing: smallest f_j(t0) / (-slope_j) over slope_j < 0
+        const double qc0 = q(x0, y0, z0, c), bc = dproj(c);
+        // the first crossing: smallest f_j(t0) / (-slope_j) over slope_j < 0,
+        // f_j = q_j - q_c, slope_j = 2 d.(phi_c - phi_j)
         double bf = 0.0, bb = 0.0;
         int nextc = 0x7FFFFFFF;
         for (int j = j0; j < j1; ++j) {
             if (j == c)
                 continue;
-            const float4 pj = s_sites[j];
-            const double b = 2.0 * (dx * ((double)pc.x - pj.x) + dy * ((double)pc.y - pj.y) +
-                                    dz * ((double)pc.z - pj.z));
+            const double b = 2.0 * (bc - dproj(j));
             if (b < 0.0) {
-                const double f0 = fmax(d2(x0, y0, z0, j) - dc0, 0.0);
+                const double f0 = fmax(q(x0, y0, z0, j) - qc0, 0.0);
                 if (nextc == 0x7FFFFFFF || f0 * -bb < bf * -b) {
                     bf = f0;
                     bb = b;
@@ -279,15 +286,17 @@ __global__ __launch_bounds__(kThreads) void ray_walk_kernel(RenderGeometry g,
                 }
             }
         }
-        double q = nextc == 0x7FFFFFFF ? INFINITY : bf / -bb;
-        group_argmin<L>(q, nextc);
+        double tq = nextc == 0x7FFFFFFF ? INFINITY : bf / -bb;
+        group_argmin<L>(tq, nextc);
         double t1 = g.far_t;
-        if (nextc != 0x7FFFFFFF && t0 + q < t1)
-            t1 = t0 + q;
+        if (nextc != 0x7FFFFFFF && t0 + tq < t1)
+            t1 = t0 + tq;
         else
             nextc = -1;
         const double x1 = ox + t1 * dx, y1 = oy + t1 * dy, z1 = oz + t1 * dz;
-        const double dc1 = d2(x1, y1, z1, c);
+        const double qc1 = q(x1, y1, z1, c);
+        const double dc0 = fma(x0, x0, fma(y0, y0, z0 * z0)) + qc0;
+        const double dc1 = fma(x1, x1, fma(y1, y1, z1 * z1)) + qc1;
         const double tau = 1e-4 * (1.0 + fmax(dc0, dc1));
         // this lane's candidates, ascending, as a byte string (at most 12 kept)
         unsigned long long lo = 0, hi = 0;
@@ -295,7 +304,7 @@ __global__ __launch_bounds__(kThreads) void ray_walk_kernel(RenderGeometry g,
         for (int j = j0; j < j1; ++j) {
             bool take = j == c;
             if (!take)
-                take = fmin(d2(x0, y0, z0, j) - dc0, d2(x1, y1, z1, j) - dc1) <= tau;
+                take = fmin(q(x0, y0, z0, j) - qc0, q(x1, y1, z1, j) - qc1) <= tau;
             if (take) {
                 if (cl < 8)
                     lo |= (unsigned long long)j << (8 * cl);

@@ -257,6 +257,10 @@ def main():
     ap.add_argument("--mfma-ceiling", action="store_true",
                     help="also run the matrix-core throughput probe (operand patterns x vector "
                          "instructions per MFMA) and report it under mfma_ceiling")
+    ap.add_argument("--encoding", choices=["fused", "stored"], default="fused",
+                    help="where gamma(x) is formed: inside the MLP (fused, the default) or by "
+                         "its own pass into a table the MLP reads back (stored; heads without "
+                         "a skip layer)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (to scale HBM counters)")
     args = ap.parse_args()
@@ -301,6 +305,8 @@ def main():
             r = derf.Renderer(sc.sites, cfg.arch, sc.weights, precision)
         if empty_heads:
             r.set_empty_heads([k in empty_heads for k in range(cfg.num_sites)])
+        if args.encoding == "stored":
+            r.set_encoding(True)
         stream = torch.cuda.current_stream()
 
         def step():
@@ -536,7 +542,7 @@ def main():
         "data": "synthetic (seeded scene, Glorot-uniform random heads)",
         "config": {"workload": workload_text(cfg, precision), "rays": R,
                    "samples_per_ray": cfg.n_coarse + cfg.n_fine, "heads": cfg.num_sites,
-                   "samples": S},
+                   "samples": S, "encoding": args.encoding},
         "evaluated_samples": evaluated,
         "roofline": {"bound": "mfma", "kernel": "mlp_kernel (grouped per-head MLP)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",

@@ -26,6 +26,11 @@
  *                 it is nearly opaque                       (Sec. 3.3)
  *   derf_set_gate / derf_render_gated  the MLP-gating decomposition:
  *                 a small network picks each sample's head      (Sec. 4)
+ *   derf_weights_count  size of one head's packed weights: NeRF's
+ *                 network, scaled per head                       (Sec. 4)
+ *   derf_set_encoding  gamma(x) fused into the MLP or stored by its
+ *                 own pass (the ablation of the fusion)          (Sec. 4)
+ *   derf_render_noalloc  derf_render for callers that cannot allocate
  *
  * All functions return a derf_status (0 on success, negative on error),
  * never abort and never print.  derf_last_error() returns a thread-local
@@ -103,8 +108,10 @@ typedef struct {
     unsigned long long ray_offset;
 } derf_sampling;
 
-/* Number of floats of one head's packed weights for this architecture, or
- * -1 for invalid values.  Per head, in this order: for each hidden layer l,
+/* Number of floats of one head's packed weights for this architecture (a
+ * NeRF network of Sec. 4: ReLU layers over gamma(x) with an optional skip
+ * input, density from the last hidden layer, colour from it and gamma(d)),
+ * or -1 for invalid values.  Per head, in this order: for each hidden layer l,
  * W_l [width][in_l] row-major (out x in) then b_l [width], with in_0 =
  * 3 + 6 pos_freqs and in_skip = (3 + 6 pos_freqs) + width (input order
  * [gamma(x); h]); then w_sigma [width], b_sigma [1]; then, if rgb_hidden > 0,
@@ -180,7 +187,9 @@ int derf_render_noalloc(derf_handle *h, const float *rays_o, const float *rays_d
                         float *out_rgb, float *out_depth, float *out_opacity, void *hip_stream);
 
 /* Optional per-sample outputs of derf_render_debug: device pointers, any may
- * be NULL.  N = n_coarse + n_fine samples per ray, in depth order (with
+ * be NULL.  They are the quantities the integration of Sec. 3.1 (Eq. 1-2)
+ * consumes: each sample's depth, its owning site under the nearest-site
+ * partition (Sec. 3.3) and that head's density and colour.  N = n_coarse + n_fine samples per ray, in depth order (with
  * hierarchical sampling: the merged coarse and fine samples); sample i of
  * ray r is at index r * N + i. */
 typedef struct {
@@ -296,6 +305,26 @@ int derf_render_gated(derf_handle *h, const float *rays_o, const float *rays_d,
                       float *out_rgb, float *out_depth, float *out_opacity, int *out_cell,
                       void *hip_stream);
 
+/* Where gamma(x), the positional encoding of each sample (Sec. 4, the
+ * encoding the heads take as input), is formed.
+ *   DERF_ENCODING_FUSED   (default) inside the grouped MLP, per tile, from
+ *                         the sample's depth and ray: no table in HBM.
+ *   DERF_ENCODING_STORED  a separate pass after the assignment writes every
+ *                         sample's gamma(x) to a table in the workspace
+ *                         (128 B per sample in bf16 at L = 10, 256 B in
+ *                         fp32) and the MLP reads it back.  The outputs are
+ *                         the fused form's bit for bit; the form exists to
+ *                         measure what the fusion saves.
+ * STORED needs head architectures without a skip layer, all with the same
+ * pos_freqs (DERF_ERR_UNSUPPORTED otherwise, the setting unchanged); while
+ * it is set, derf_render, derf_render_debug and derf_render_noalloc use it
+ * (both passes of hierarchical sampling; the table counts towards the
+ * no-allocation render's limit) and derf_render_soft, derf_render_culled
+ * and derf_render_gated return DERF_ERR_UNSUPPORTED.  Other modes:
+ * DERF_ERR_INVALID_ARG.  Applies to renders issued after the call. */
+enum { DERF_ENCODING_FUSED = 0, DERF_ENCODING_STORED = 1 };
+int derf_set_encoding(derf_handle *h, int mode);
+
 /* Per-stage GPU time, recorded with HIP events on the render's stream when
  * timing is on (derf_set_timing); accumulated over renders since the last
  * derf_reset_stats.  With hierarchical sampling a stage's time is the sum of
@@ -308,7 +337,8 @@ int derf_render_gated(derf_handle *h, const float *rays_o, const float *rays_d,
  * assigned by the search over all sites instead (same cells, more work).
  * walk_rays is 0 when the render searched all sites for every sample. */
 enum {
-    DERF_STAGE_SAMPLE = 0,         /* sample + encode + assign (given depths: assign) */
+    DERF_STAGE_SAMPLE = 0,         /* sample + encode + assign (given depths: assign);
+                                      the stored gamma(x) pass                        */
     DERF_STAGE_BUCKET_SCAN = 1,    /* per-head counts -> offsets                     */
     DERF_STAGE_BUCKET_SCATTER = 2, /* sample ids into per-head buckets               */
     DERF_STAGE_MLP = 3,            /* grouped per-head MLP                           */

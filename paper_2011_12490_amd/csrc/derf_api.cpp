@@ -179,6 +179,9 @@ struct derf_handle {
     unsigned char *gate_w = nullptr;
     int gate_freqs = 0;
     int gate_hidden = 0;
+    // derf_set_encoding: gamma(x) stored in a table by a separate pass
+    // (bytes per sample of the table), or 0: encoded inside the MLP
+    size_t gx_bytes = 0;
 };
 
 namespace {
@@ -219,10 +222,11 @@ struct Buffers {
     unsigned *mlp_queue;
     SegRec *walk_seg;            // [R][kMaxSeg] (heads >= kWalkSites)
     unsigned char *walk_nseg;    // [R]
+    void *gxtab;                 // [max(S, Sf)] rows of gx_bytes (stored encoding), or null
 };
 
 size_t layout(char *base, unsigned S, unsigned Sf, unsigned R, unsigned nblk, int K, bool bf16,
-              Buffers *b)
+              size_t gx_bytes, Buffers *b)
 {
     char *p = base;
     Buffers x;
@@ -241,6 +245,7 @@ size_t layout(char *base, unsigned S, unsigned Sf, unsigned R, unsigned nblk, in
     const bool walk = K >= kWalkSites;
     x.walk_seg = walk ? carve<SegRec>(p, (size_t)R * kMaxSeg) : nullptr;
     x.walk_nseg = walk ? carve<unsigned char>(p, R) : nullptr;
+    x.gxtab = gx_bytes ? carve<char>(p, (size_t)(S > Sf ? S : Sf) * gx_bytes) : nullptr;
     if (b)
         *b = x;
     return (size_t)(p - base);
@@ -272,20 +277,24 @@ namespace {
 
 // The grouped MLP over every head: one launch per architecture group, each
 // skipping the other groups' heads and the 0-capacity ones, with its own
-// tile counters.
+// tile counters.  gxtab: the stored gamma(x) table of g's samples (the
+// stored-encoding forms run), or null.
 hipError_t launch_groups(const derf_handle *h, const unsigned *bucket, const unsigned *totals,
                          const RenderGeometry &g, const float *t, const void *dirbuf, float4 *sr,
                          unsigned *queue, bool soft, hipStream_t s,
-                         const unsigned *offsets = nullptr)
+                         const unsigned *offsets = nullptr, const void *gxtab = nullptr)
 {
     for (int gi = 0; gi < h->num_groups; ++gi) {
         const derf_handle::HeadGroup &grp = h->groups[gi];
+        const MlpVariant *v = gxtab ? grp.mlp->stored : grp.mlp;
+        if (!v)
+            return hipErrorInvalidValue;
         HeadMask skip;
         for (int w = 0; w < kMaxSites / 32; ++w)
             skip.w[w] = ~grp.members.w[w] | h->empty.w[w];
         const hipError_t e =
-            grp.mlp->launch(bucket, totals, offsets, h->num_sites, g, t, dirbuf, grp.streams,
-                            grp.blocks, sr, queue + kMlpQueues * gi, h->mlp_grid, soft, skip, s);
+            v->launch(bucket, totals, offsets, h->num_sites, g, t, dirbuf, gxtab, grp.streams,
+                      grp.blocks, sr, queue + kMlpQueues * gi, h->mlp_grid, soft, skip, s);
         if (e != hipSuccess)
             return e;
     }
@@ -433,7 +442,8 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
     const unsigned nblk = blocks_of(S);
     const unsigned nblk_f = blocks_of(Sf);
     const unsigned nblk_max = nblk > nblk_f ? nblk : nblk_f;
-    const size_t need = layout(nullptr, S, Sf, R, nblk_max, h->num_sites, h->bf16, nullptr);
+    const size_t need =
+        layout(nullptr, S, Sf, R, nblk_max, h->num_sites, h->bf16, h->gx_bytes, nullptr);
     int rc = DERF_OK;
     if (fixed_ws) {
         if (need > fixed_bytes)
@@ -452,7 +462,7 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
     }
     Buffers b;
     layout(reinterpret_cast<char *>(fixed_ws ? fixed_ws : h->ws.mem), S, Sf, R, nblk_max,
-           h->num_sites, h->bf16, &b);
+           h->num_sites, h->bf16, h->gx_bytes, &b);
 
     RenderGeometry g;
     g.rays_o = rays_o;
@@ -489,7 +499,8 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
                 "bucket_scatter launch");
         HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCATTER, 1), "hipEventRecord");
         HIP_TRY(mark(pass, DERF_STAGE_MLP, 0), "hipEventRecord");
-        HIP_TRY(launch_groups(h, b.bucket, totals, gp, t, b.dirbuf, sr, b.mlp_queue, false, s),
+        HIP_TRY(launch_groups(h, b.bucket, totals, gp, t, b.dirbuf, sr, b.mlp_queue, false, s,
+                              nullptr, b.gxtab),
                 "mlp launch");
         HIP_TRY(mark(pass, DERF_STAGE_MLP, 1), "hipEventRecord");
         return DERF_OK;
@@ -505,6 +516,9 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
     HIP_TRY(launch_sample_assign(g, h->sites, h->num_sites, h->site_bits, walk, b.t, b.cell,
                                  b.counts, nblk, s),
             "sample_assign launch");
+    if (b.gxtab)
+        HIP_TRY(h->groups[0].mlp->stored->encode(g, b.t, b.gxtab, h->mlp_grid, s),
+                "gx_encode launch");
     HIP_TRY(mark(0, DERF_STAGE_SAMPLE, 1), "hipEventRecord");
     rc = bucket_and_mlp(0, g, b.t, b.cell, nblk, b.totals, b.sr);
     if (rc != DERF_OK)
@@ -533,6 +547,9 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
         HIP_TRY(launch_assign_given(gf, h->sites, h->num_sites, h->site_bits, walk, b.t_fine,
                                     b.cell_fine, b.counts, nblk_f, s),
                 "assign launch");
+        if (b.gxtab)
+            HIP_TRY(h->groups[0].mlp->stored->encode(gf, b.t_fine, b.gxtab, h->mlp_grid, s),
+                    "gx_encode launch");
         HIP_TRY(mark(1, DERF_STAGE_SAMPLE, 1), "hipEventRecord");
         rc = bucket_and_mlp(1, gf, b.t_fine, b.cell_fine, nblk_f, b.totals_fine, b.sr_fine);
         if (rc != DERF_OK)
@@ -579,6 +596,8 @@ int render_soft_impl(derf_handle *h, const float *rays_o, const float *rays_d,
         return fail(DERF_ERR_INVALID_ARG, "need 1 <= n_coarse <= 1024, n_fine >= 0");
     if (samp->n_fine != 0)
         return fail(DERF_ERR_UNSUPPORTED, "the soft render has no hierarchical sampling");
+    if (h->gx_bytes)
+        return fail(DERF_ERR_UNSUPPORTED, "the soft render has no stored encoding");
     if (num_rays == 0)
         return DERF_OK;
     if (!rays_o || !rays_d || !out_rgb || !out_depth || !out_opacity)
@@ -679,7 +698,7 @@ inline bool one_pass_levels(unsigned levels, int K, unsigned piece)
 size_t layout_culled(char *base, unsigned S, unsigned R, unsigned nblk, int K, bool bf16,
                      unsigned levels, unsigned piece, Buffers *b, CullBuffers *c)
 {
-    char *p = base + layout(base, S, 0, R, nblk, K, bf16, b);
+    char *p = base + layout(base, S, 0, R, nblk, K, bf16, 0, b);
     CullBuffers x;
     x.lb = carve<unsigned>(p, (size_t)R * (levels + 1));
     x.lvl = carve<uint8_t>(p, S);
@@ -724,6 +743,8 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
         return fail(DERF_ERR_INVALID_ARG, "need 1 <= n_coarse <= 1024, n_fine >= 0");
     if (samp->n_fine != 0)
         return fail(DERF_ERR_UNSUPPORTED, "the culled render has no hierarchical sampling");
+    if (h->gx_bytes)
+        return fail(DERF_ERR_UNSUPPORTED, "the culled and gated renders have no stored encoding");
     if (num_rays == 0)
         return DERF_OK;
     if (!rays_o || !rays_d || !out_rgb || !out_depth || !out_opacity)
@@ -1169,6 +1190,36 @@ int derf_set_empty_heads(derf_handle *h, const int *flags)
             if (flags[k])
                 m.w[k >> 5] |= 1u << (k & 31);
     h->empty = m;
+    return DERF_OK;
+}
+
+int derf_set_encoding(derf_handle *h, int mode)
+{
+    if (!h)
+        return fail(DERF_ERR_INVALID_ARG, "null handle");
+    if (mode == DERF_ENCODING_FUSED) {
+        h->gx_bytes = 0;
+        return DERF_OK;
+    }
+    if (mode != DERF_ENCODING_STORED)
+        return fail(DERF_ERR_INVALID_ARG, "unknown encoding mode %d", mode);
+    // every group needs a stored form, and all of them one table layout
+    const MlpVariant *first = nullptr;
+    for (int gi = 0; gi < h->num_groups; ++gi) {
+        const MlpVariant *v = h->groups[gi].mlp->stored;
+        if (!v)
+            return fail(DERF_ERR_UNSUPPORTED,
+                        "stored encoding: no stored form for a head architecture with a skip "
+                        "layer");
+        if (first && (v->gx_bytes != first->gx_bytes || v->pos_freqs != first->pos_freqs))
+            return fail(DERF_ERR_UNSUPPORTED,
+                        "stored encoding: the heads' position encodings differ");
+        if (!first)
+            first = v;
+    }
+    if (!first)
+        return fail(DERF_ERR_UNSUPPORTED, "stored encoding: no heads");
+    h->gx_bytes = first->gx_bytes;
     return DERF_OK;
 }
 

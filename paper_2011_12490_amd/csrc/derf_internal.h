@@ -140,12 +140,24 @@ struct MlpVariant {
     // takes every sample (bucket = 0 .. S-1, totals[k] = S) and writes its
     // outputs to sr[k * S + sample]; otherwise sr[sample].  offsets: null
     // (head k's entries follow head k - 1's), or where each head's totals[k]
-    // entries start in bucket (not soft).
+    // entries start in bucket (not soft).  gxtab: null, or for the
+    // stored-encoding form (which needs it, and takes no soft launch) the
+    // table its encode wrote for the same samples.
     hipError_t (*launch)(const unsigned *bucket, const unsigned *totals, const unsigned *offsets,
                          int num_sites,
                          const RenderGeometry &g, const float *t, const void *dirbuf,
-                         const unsigned char *streams, const float *blocks, float4 *sr,
-                         unsigned *queue, int grid, bool soft, const HeadMask &empty,
+                         const void *gxtab, const unsigned char *streams, const float *blocks,
+                         float4 *sr, unsigned *queue, int grid, bool soft, const HeadMask &empty,
+                         hipStream_t s);
+    // The stored-encoding form of this architecture (same packed weights;
+    // gamma(x) read from a table instead of encoded per tile), or null.
+    const MlpVariant *stored;
+    // stored-encoding form only: table bytes per sample, the number of
+    // position frequencies, and the kernel that fills the table from the
+    // depths t of g's samples (one row per sample)
+    size_t gx_bytes;
+    int pos_freqs;
+    hipError_t (*encode)(const RenderGeometry &g, const float *t, void *gxtab, int cus,
                          hipStream_t s);
 };
 

@@ -81,10 +81,14 @@ enum { K_HID = 0, K_RGBH = 1, K_OUT = 2 };
 // step F (the F-th fragment of a tile) the wave reads fragment F + kPrefetch.
 constexpr int kPrefetch = 3;
 
-template <bool BF16_, int W_, int D_, int SKIP_, int RH_, int LP_>
+// GX_: the stored-encoding form, which reads each sample's gamma(x) entries
+// from a table in HBM (gx_encode_kernel) instead of encoding them in the
+// tile prologue; kept to measure what the fusion saves.
+template <bool BF16_, int W_, int D_, int SKIP_, int RH_, int LP_, bool GX_ = false>
 struct Cfg {
     static constexpr bool BF16 = BF16_;
     static constexpr int W = W_, D = D_, SKIP = SKIP_, RH = RH_, LP = LP_;
+    static constexpr bool GX = GX_;
     static constexpr int E = BF16 ? 8 : 1;     // k-entries per lane per MFMA
     static constexpr int CPU = BF16 ? 1 : 4;   // MFMA k-chunks per 1 KB unit
     static constexpr int NB = BF16 ? 2 : 1;    // 32-sample column blocks per wave
@@ -111,6 +115,7 @@ struct Cfg {
     static constexpr int LA = 6;               // weight loads issued this many stages ahead
     static constexpr int NT = D * MT + MTR + 1;
     static_assert(LP % 2 == 0, "pos_freqs must be even");
+    static_assert(!GX || SKIP < 0, "the stored encoding has no skip-layer re-encode");
     static_assert(W % 64 == 0, "width");
 
     static constexpr int t_kind(int T) { return T < D * MT ? K_HID : (T < D * MT + MTR ? K_RGBH : K_OUT); }
@@ -204,10 +209,11 @@ struct Cfg {
     // The next tile's sample records are prefetched into LDS during this one:
     // its bucket ids at group start S_PA (NPA loads per wave), then, once the
     // group wait of S_PB has covered those, its depths and ray origins and
-    // directions (NPB loads per wave).  The last tile re-reads its own, so
-    // that the wait counts do not depend on whether a next tile exists.
+    // directions (NPB loads per wave; none in the stored-encoding form, whose
+    // gamma(x) rows are read at the tile start).  The last tile re-reads its
+    // own, so that the wait counts do not depend on whether a next tile exists.
     static constexpr int S_PA = 0, S_PB = LA;
-    static constexpr int NPA = 1, NPB = 7;
+    static constexpr int NPA = 1, NPB = GX ? 0 : 7;
 
     // Barrier groups: stages [a, a + G) of a tile share one barrier.  At a
     // group start a the wave issues the weight loads of stages a + LA ..
@@ -594,11 +600,13 @@ constexpr unsigned kNoTile = 0xFFFFFFFFu;
 
 // SOFT: every head takes every sample (see MlpVariant::launch).  OFFS: each
 // head's entries start at offsets[k] (not SOFT).
+// gxtab (stored-encoding form only): gamma(x) rows of gx_encode_kernel.
 template <class C, bool SOFT, bool OFFS>
 __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
     const unsigned *__restrict__ bucket, const unsigned *__restrict__ totals,
     const unsigned *__restrict__ offsets, int num_sites, RenderGeometry geo,
     const float *__restrict__ tbuf, const void *__restrict__ dirbuf,
+    const Chunk<C> *__restrict__ gxtab,
     const unsigned char *__restrict__ streams, const float *__restrict__ blocks,
     float4 *__restrict__ sr, unsigned *__restrict__ queue, HeadMask empty)
 {
@@ -750,6 +758,8 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
         load_lds4(bucket + min(row - base, geo.num_samples - 1), pf_wave);
     };
     auto prefetch_rays = [&]() {
+        if constexpr (C::GX)
+            return;
         // depths, ray origins and directions of the ids in LDS
         const unsigned sn = min(pf[lane], geo.num_samples - 1);
         unsigned r = (unsigned)((double)sn * geo.inv_n);
@@ -822,6 +832,22 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
             if (sid[nb] - r * geo.n >= geo.n)
                 ++r;
             ray[nb] = r;
+            if constexpr (C::GX) {
+                // this lane group's entries of the sample's row, as stored
+                const Chunk<C> *src = gxtab + ((size_t)sid[nb] * 2 + g) * C::EXC;
+                if constexpr (C::BF16) {
+#pragma unroll
+                    for (int ch = 0; ch < C::EXC; ++ch)
+                        gx[nb][ch] = src[ch];
+                } else {
+#pragma unroll
+                    for (int e = 0; e < C::EX; e += 4) {
+                        const f32x4 v = *reinterpret_cast<const f32x4 *>(src + e);
+                        gx[nb][e] = v[0]; gx[nb][e + 1] = v[1]; gx[nb][e + 2] = v[2]; gx[nb][e + 3] = v[3];
+                    }
+                }
+                continue;
+            }
             const float t = __uint_as_float(pf[64 + q]);
             float x[3];
 #pragma unroll
@@ -1072,19 +1098,93 @@ __global__ __launch_bounds__(C::THREADS, C::WG_PER_CU) void mlp_kernel(
     wait_vmcnt<0>();
 }
 
+// gamma(x) of every sample into the table the stored-encoding form reads:
+// row s holds lane group 0's EX entries, then lane group 1's, exactly as the
+// tile prologue would hold them (the same encode_x and rounding), so both
+// forms give the same outputs bit for bit.  One lane per (sample, group)
+// encodes its entries into LDS; the block then writes its 256 rows out as
+// one contiguous stretch, each store 16 contiguous bytes per lane.
+template <class C>
+__global__ __launch_bounds__(256) void gx_encode_kernel(RenderGeometry geo,
+                                                        const float *__restrict__ tbuf,
+                                                        Chunk<C> *__restrict__ out)
+{
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+    constexpr int U = C::EX * (C::BF16 ? 2 : 4) / 16;  // 16-byte units per row
+    __shared__ u32x4 stage[256 * U];
+    const unsigned long long rows = 2ull * geo.num_samples;
+    u32x4 *const dst_all = reinterpret_cast<u32x4 *>(out);
+    for (unsigned long long base = (unsigned long long)blockIdx.x * 256; base < rows;
+         base += (unsigned long long)gridDim.x * 256) {
+        const unsigned long long i = base + threadIdx.x;
+        if (i < rows) {
+            const unsigned sn = (unsigned)(i >> 1);
+            const int g = (int)(i & 1);
+            unsigned r = (unsigned)((double)sn * geo.inv_n);
+            if (sn - r * geo.n >= geo.n)
+                ++r;
+            const float t = tbuf[sn];
+            float x[3];
+#pragma unroll
+            for (int c = 0; c < 3; ++c)
+                x[c] = fmaf(t, geo.rays_d[3 * (size_t)r + c], geo.rays_o[3 * (size_t)r + c]);
+            float f[C::EX];
+            encode_x<C>(x, g, f);
+            u32x4 *mine = stage + threadIdx.x * U;
+            if constexpr (C::BF16) {
+#pragma unroll
+                for (int ch = 0; ch < C::EXC; ++ch)
+                    mine[ch] = __builtin_bit_cast(u32x4, to_bf16x8(f + 8 * ch));
+            } else {
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    mine[u] = u32x4{__float_as_uint(f[4 * u]), __float_as_uint(f[4 * u + 1]),
+                                    __float_as_uint(f[4 * u + 2]), __float_as_uint(f[4 * u + 3])};
+            }
+        }
+        __syncthreads();
+        const unsigned long long left = rows - base;
+        const unsigned units = (unsigned)(left < 256 ? left : 256) * U;
+        u32x4 *dst = dst_all + base * U;
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const unsigned idx = k * 256 + threadIdx.x;
+            if (idx < units)
+                dst[idx] = stage[idx];
+        }
+        __syncthreads();  // the stage is rewritten by the next stretch
+    }
+}
+
+template <class C>
+hipError_t launch_gx_encode(const RenderGeometry &g, const float *t, void *gxtab, int cus,
+                            hipStream_t s)
+{
+    if (g.num_samples == 0)
+        return hipSuccess;
+    const unsigned long long lanes = 2ull * g.num_samples;
+    const unsigned long long want = (lanes + 255) / 256, cap = (unsigned long long)cus * 64;
+    gx_encode_kernel<C><<<(unsigned)(want < cap ? want : cap), 256, 0, s>>>(
+        g, t, reinterpret_cast<Chunk<C> *>(gxtab));
+    return hipGetLastError();
+}
+
 template <class C>
 hipError_t launch_mlp(const unsigned *bucket, const unsigned *totals, const unsigned *offsets,
                       int num_sites,
                       const RenderGeometry &g, const float *t, const void *dirbuf,
-                      const unsigned char *streams, const float *blocks, float4 *sr,
-                      unsigned *queue, int cus, bool soft, const HeadMask &empty, hipStream_t s)
+                      const void *gxtab, const unsigned char *streams, const float *blocks,
+                      float4 *sr, unsigned *queue, int cus, bool soft, const HeadMask &empty,
+                      hipStream_t s)
 {
+    if (C::GX ? (soft || !gxtab) : gxtab != nullptr)
+        return hipErrorInvalidValue;
     // raises the dynamic LDS limit where the runtime keeps one, once per
     // variant (thread-safe); a runtime without the limit may refuse the
     // call, and the launch below reports any real problem
     static const bool raised = [] {
         for (const void *k : {(const void *)mlp_kernel<C, false, false>,
-                              (const void *)mlp_kernel<C, true, false>,
+                              (const void *)mlp_kernel<C, !C::GX, false>,
                               (const void *)mlp_kernel<C, false, true>})
             if (hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES) !=
                 hipSuccess)
@@ -1092,23 +1192,48 @@ hipError_t launch_mlp(const unsigned *bucket, const unsigned *totals, const unsi
         return true;
     }();
     (void)raised;
-    if (soft)
-        mlp_kernel<C, true, false><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(
-            bucket, totals, nullptr, num_sites, g, t, dirbuf, streams, blocks, sr, queue, empty);
-    else if (offsets)
-        mlp_kernel<C, false, true><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(
-            bucket, totals, offsets, num_sites, g, t, dirbuf, streams, blocks, sr, queue, empty);
+    const Chunk<C> *gx = reinterpret_cast<const Chunk<C> *>(gxtab);
+    const dim3 grid(cus * C::WG_PER_CU), block(C::THREADS);
+    if constexpr (!C::GX) {
+        if (soft) {
+            mlp_kernel<C, true, false><<<grid, block, C::LDS_BYTES, s>>>(
+                bucket, totals, nullptr, num_sites, g, t, dirbuf, gx, streams, blocks, sr, queue,
+                empty);
+            return hipGetLastError();
+        }
+    }
+    if (offsets)
+        mlp_kernel<C, false, true><<<grid, block, C::LDS_BYTES, s>>>(
+            bucket, totals, offsets, num_sites, g, t, dirbuf, gx, streams, blocks, sr, queue, empty);
     else
-        mlp_kernel<C, false, false><<<cus * C::WG_PER_CU, C::THREADS, C::LDS_BYTES, s>>>(
-            bucket, totals, nullptr, num_sites, g, t, dirbuf, streams, blocks, sr, queue, empty);
+        mlp_kernel<C, false, false><<<grid, block, C::LDS_BYTES, s>>>(
+            bucket, totals, nullptr, num_sites, g, t, dirbuf, gx, streams, blocks, sr, queue, empty);
     return hipGetLastError();
 }
+
+// The stored-encoding form of an architecture without a skip layer.
+template <class C>
+using StoredForm = Cfg<C::BF16, C::W, C::D, C::SKIP, C::RH, C::LP, true>;
 
 template <class C>
 const MlpVariant *variant()
 {
-    static const MlpVariant v = {(size_t)C::STREAM_UNITS * 1024, (size_t)C::BLOCK_FLOATS * 4,
-                                 C::TILE, &Packer<C>::pack, &launch_mlp<C>};
+    const MlpVariant *stored = nullptr;
+    if constexpr (C::SKIP < 0 && !C::GX) {
+        static_assert(StoredForm<C>::STREAM_UNITS == C::STREAM_UNITS &&
+                          StoredForm<C>::BLOCK_FLOATS == C::BLOCK_FLOATS,
+                      "both forms take the same packed weights");
+        stored = variant<StoredForm<C>>();
+    }
+    static const MlpVariant v = {(size_t)C::STREAM_UNITS * 1024,
+                                 (size_t)C::BLOCK_FLOATS * 4,
+                                 C::TILE,
+                                 &Packer<C>::pack,
+                                 &launch_mlp<C>,
+                                 stored,
+                                 C::GX ? (size_t)2 * C::EX * (C::BF16 ? 2 : 4) : 0,
+                                 C::LP,
+                                 C::GX ? &launch_gx_encode<C> : nullptr};
     return &v;
 }
 

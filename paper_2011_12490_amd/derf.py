@@ -57,7 +57,8 @@ class derf_stats(ctypes.Structure):
 EXPORTS = ("derf_weights_count", "derf_create", "derf_create_mixed", "derf_render",
            "derf_render_debug", "derf_render_noalloc",
            "derf_render_soft", "derf_render_culled", "derf_set_empty_heads", "derf_set_gate",
-           "derf_gate_weights_count", "derf_render_gated", "derf_set_timing", "derf_get_stats",
+           "derf_gate_weights_count", "derf_render_gated", "derf_set_encoding", "derf_set_timing",
+           "derf_get_stats",
            "derf_reset_stats", "derf_destroy",
            "derf_status_string", "derf_last_error")
 
@@ -113,6 +114,8 @@ def lib() -> ctypes.CDLL:
                                         ctypes.c_float, ctypes.POINTER(derf_sampling), P, P, P, P,
                                         P]
         L.derf_render_gated.restype = ctypes.c_int
+        L.derf_set_encoding.argtypes = [P, ctypes.c_int]
+        L.derf_set_encoding.restype = ctypes.c_int
         L.derf_set_timing.argtypes = [P, ctypes.c_int]
         L.derf_set_timing.restype = ctypes.c_int
         L.derf_get_stats.argtypes = [P, ctypes.POINTER(derf_stats)]
@@ -361,6 +364,14 @@ def derf_render_gated(h, rays_o: torch.Tensor, rays_d: torch.Tensor, near: float
            "derf_render_gated")
 
 
+DERF_ENCODING_FUSED = 0
+DERF_ENCODING_STORED = 1
+
+
+def derf_set_encoding(h, mode: int):
+    _check(lib().derf_set_encoding(h, int(mode)), "derf_set_encoding")
+
+
 def derf_set_timing(h, on: bool):
     _check(lib().derf_set_timing(h, int(on)), "derf_set_timing")
 
@@ -451,6 +462,11 @@ class Renderer:
         derf_render_gated(self.handle, rays_o, rays_d, near, far, samp, rgb, depth, opac, cell,
                           stream)
         return (rgb, depth, opac, cell) if cells else (rgb, depth, opac)
+
+    def set_encoding(self, stored: bool):
+        """gamma(x) encoded inside the MLP (False, the default) or written to a
+        table by its own pass and read back (True; heads without a skip layer)."""
+        derf_set_encoding(self.handle, DERF_ENCODING_STORED if stored else DERF_ENCODING_FUSED)
 
     def set_empty_heads(self, flags):
         """Mark 0-capacity heads (K flags; None clears)."""

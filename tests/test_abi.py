@@ -159,6 +159,7 @@ def test_mixed_create_soft_culled_render_and_empty_heads_reject_bad_arguments_wi
     assert L.derf_render_culled(None, None, None, 1, 2.0, 6.0, ctypes.byref(samp), 1e-3, 4, 0,
                                 None, None, None, None, None) == derf.DERF_ERR_INVALID_ARG
     assert L.derf_set_gate(None, 6, 16, None) == derf.DERF_ERR_INVALID_ARG
+    assert L.derf_set_encoding(None, derf.DERF_ENCODING_STORED) == derf.DERF_ERR_INVALID_ARG
     assert L.derf_render_gated(None, None, None, 1, 2.0, 6.0, ctypes.byref(samp), None, None,
                                None, None, None) == derf.DERF_ERR_INVALID_ARG
     assert L.derf_gate_weights_count(4, 6, 16) == 16 * 39 + 16 + 4 * 16 + 4

@@ -249,9 +249,9 @@ int derf_render_soft(derf_handle *h, const float *rays_o, const float *rays_d, l
  * associative; cutting only adds places where a ray can stop, which matters
  * when a ray crosses few cells).  The result is the Painter's merge of the evaluated segments: colour
  * and opacity within eps of derf_render's (colours lie in [0, 1]), depth
- * within eps * far.  With levels = 1 or eps = 0 nothing can be skipped: the
- * call runs derf_render's single pass, and the outputs equal derf_render's
- * bitwise.
+ * within eps * far.  With levels = 1, eps = 0, or a single head in whole
+ * segments (every ray is one segment) nothing can be skipped: the call runs
+ * derf_render's single pass, and the outputs equal derf_render's bitwise.
  *   eps            finite, >= 0: the transmittance below which a ray stops
  *   levels         1 .. 32: levels (one bucketing, MLP and integration pass
  *                  each)

@@ -756,10 +756,12 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     HIP_TRY(hipSetDevice(h->device), "hipSetDevice");
     const unsigned R = (unsigned)num_rays, N = (unsigned)samp->n_coarse, S = R * N;
     const unsigned L = (unsigned)levels, nblk = blocks_of(S);
-    if (!gated && (L == 1 || eps == 0.0f)) {
-        // Nothing can stop a ray (one level, or eps = 0, which every
-        // transmittance passes): the single pass, derf_render's outputs
-        // bitwise, every sample evaluated.
+    if (!gated && (L == 1 || eps == 0.0f ||
+                   (h->num_sites == 1 && (piece == 0 || (unsigned)piece >= N)))) {
+        // Nothing can stop a ray (one level; eps = 0, which every
+        // transmittance passes; or one head in whole segments, where level 0
+        // is the whole ray): the single pass, derf_render's outputs bitwise,
+        // every sample evaluated.
         const int rc = render_impl(h, rays_o, rays_d, num_rays, near_t, far_t, samp, out_rgb,
                                    out_depth, out_opacity, nullptr, stream);
         if (rc != DERF_OK)

@@ -1083,9 +1083,11 @@ __global__ __launch_bounds__(kThreads) void composite_kernel(
     }
 }
 
-// Level composite for a level whose ranges are single pieces of at most a
-// few dozen samples (every level but the last of a render cut into pieces):
-// G lanes per ray, 64 / G rays per wave.  Lane gl of a ray's group
+// Level composite for every level but the last: of a render cut into pieces
+// (ranges of at most a few dozen samples) or in whole segments (a wave per
+// ray for one segment spent most of its time in the dependent loads of the
+// bounds and range, not in the integration).  G lanes per ray, 64 / G rays
+// per wave.  Lane gl of a ray's group
 // integrates the consecutive samples [a + gl c, a + (gl + 1) c) of its range
 // [a, b), c = ceil((b - a) / G), straight from memory, and the group merges
 // its lanes in order.  State, outputs and closing marks as
@@ -1344,6 +1346,15 @@ hipError_t launch_level_composite(const RenderGeometry &g, const float *t, const
                                   float *rgb, float *depth, float *opacity, hipStream_t s)
 {
     const LevelState st{lv.lb, lv.lvl, lv.trans, lv.evaluated, lv.levels, lv.level, lv.eps};
+    // Whole segments (no length bound) below the last level: 16 lanes per ray
+    // too, whatever the range's length; the last level, which holds every
+    // later segment, keeps a wave per ray.
+    if (max_len == 0 && lv.level + 1 < lv.levels) {
+        level_composite_short_kernel<16><<<blocks_for((size_t)g.num_rays * 16, kThreads), kThreads,
+                                           0, s>>>(t, cell, sr, g.n, g.num_rays, g.near_t, g.far_t,
+                                                   st, rgb, depth, opacity);
+        return hipGetLastError();
+    }
     if (max_len > 0 && max_len <= 32) {
         level_composite_short_kernel<8><<<blocks_for((size_t)g.num_rays * 8, kThreads), kThreads, 0,
                                           s>>>(t, cell, sr, g.n, g.num_rays, g.near_t, g.far_t, st,

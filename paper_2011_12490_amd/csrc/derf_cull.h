@@ -63,7 +63,8 @@ hipError_t launch_level_scatter(const RenderGeometry &g, const uint8_t *cell,
 // integrates each open ray's samples of the level behind its state in
 // rgb / depth / trans (level 0: from the empty state) and sets opacity.
 // max_len: a bound on every ray's sample count at this level (the piece
-// length), or 0 for none; short levels take a few lanes per ray.
+// length), or 0 for none; levels of at most 32 samples take 8 lanes per ray,
+// the others 16.
 hipError_t launch_level_composite(const RenderGeometry &g, const float *t, const uint8_t *cell,
                                   const float4 *sr, const CullLevel &lv, unsigned max_len,
                                   float *rgb, float *depth, float *opacity, hipStream_t s);

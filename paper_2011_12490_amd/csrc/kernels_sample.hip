@@ -973,12 +973,52 @@ __global__ __launch_bounds__(kThreads) void level_compact_kernel(
 // runs (integrate_runs), and the 64 lane results are merged in lane order;
 // the chunk results are merged in chunk order.  A segment cut by a lane or
 // chunk boundary is integrated in pieces merged by "over", which is exact.
-// LEVEL: only the ray's samples of one culling level, [lb[l], lb[l + 1]),
-// are integrated (the depths of the whole chunk are staged for the interval
-// ends), and the result is merged behind the ray's state from the earlier
-// levels: rgb, depth and the transmittance trans; a ray whose transmittance
-// is below eps is left as it is.
 constexpr int kChunk = 256;
+
+__global__ __launch_bounds__(kThreads) void composite_kernel(
+    const float *__restrict__ t, const uint8_t *__restrict__ cell, const float4 *__restrict__ sr,
+    unsigned n, unsigned num_rays, float near_t, float far_t, float *__restrict__ out_rgb,
+    float *__restrict__ out_depth, float *__restrict__ out_opacity)
+{
+    __shared__ float4 s_sr[kThreads / 64][kChunk];
+    __shared__ float s_t[kThreads / 64][kChunk + 2];  // [0]: sample before the chunk, [len + 1]: after
+    __shared__ uint8_t s_c[kThreads / 64][kChunk];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const unsigned ray = blockIdx.x * (kThreads / 64) + wv;
+    // every wave runs every barrier; waves past the last ray stage ray 0 and store nothing
+    const bool live = ray < num_rays;
+    const size_t base = (size_t)(live ? ray : 0u) * n;
+    Over acc{0.f, 0.f, 0.f, 0.f, 1.f};
+    for (unsigned c0 = 0; c0 < n; c0 += kChunk) {
+        const unsigned len = min((unsigned)kChunk, n - c0);
+        for (unsigned k = lane; k < len; k += 64) {
+            s_sr[wv][k] = sr[base + c0 + k];
+            s_t[wv][k + 1] = t[base + c0 + k];
+            s_c[wv][k] = cell[base + c0 + k];
+        }
+        if (lane == 0)
+            s_t[wv][0] = c0 > 0 ? t[base + c0 - 1] : 0.0f;
+        if (lane == 1)
+            s_t[wv][len + 1] = c0 + len < n ? t[base + c0 + len] : 0.0f;
+        __syncthreads();
+        const unsigned cl = (len + 63) / 64;
+        const unsigned i0 = min(lane * cl, len), i1 = min(i0 + cl, len);
+        Over part = integrate_runs(
+            c0 + i0, c0 + i1, n, near_t, far_t, [&](unsigned i) { return s_t[wv][i - c0 + 1]; },
+            [&](unsigned i) { return (unsigned)s_c[wv][i - c0]; },
+            [&](unsigned i) { return s_sr[wv][i - c0]; });
+        part = wave_over(part, lane);
+        acc = over(acc, part);  // meaningful in lane 0
+        __syncthreads();
+    }
+    if (live && lane == 0) {
+        out_rgb[3 * ray] = acc.r;
+        out_rgb[3 * ray + 1] = acc.g;
+        out_rgb[3 * ray + 2] = acc.b;
+        out_depth[ray] = acc.d;
+        out_opacity[ray] = 1.0f - acc.t;
+    }
+}
 
 // The state the levels of a culled render carry from one to the next.
 struct LevelState {
@@ -990,121 +1030,37 @@ struct LevelState {
     float eps;
 };
 
-template <bool LEVEL>
-__global__ __launch_bounds__(kThreads) void composite_kernel(
-    const float *__restrict__ t, const uint8_t *__restrict__ cell, const float4 *__restrict__ sr,
-    unsigned n, unsigned num_rays, float near_t, float far_t, LevelState lv,
-    float *__restrict__ out_rgb, float *__restrict__ out_depth, float *__restrict__ out_opacity)
-{
-    __shared__ float4 s_sr[kThreads / 64][kChunk];
-    __shared__ float s_t[kThreads / 64][kChunk + 2];  // [0]: sample before the chunk, [len + 1]: after
-    __shared__ uint8_t s_c[kThreads / 64][kChunk];
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const unsigned ray = blockIdx.x * (kThreads / 64) + wv;
-    // every wave runs every barrier; waves past the last ray stage ray 0 and store nothing
-    const bool live = ray < num_rays;
-    const size_t base = (size_t)(live ? ray : 0u) * n;
-    Over acc{0.f, 0.f, 0.f, 0.f, 1.f};
-    unsigned a = 0, b = n;  // the samples integrated
-    bool go = live;
-    if constexpr (LEVEL) {
-        if (live) {
-            const unsigned *r_lb = lv.lb + (size_t)ray * (lv.levels + 1) + lv.level;
-            a = r_lb[0];
-            b = r_lb[1];
-            if (lv.level > 0) {
-                acc = Over{out_rgb[3 * ray], out_rgb[3 * ray + 1], out_rgb[3 * ray + 2],
-                           out_depth[ray], lv.trans[ray]};
-                go = acc.t >= lv.eps;
-            }
-        }
-        if (!go)
-            a = b = 0;
-    }
-    for (unsigned c0 = 0; c0 < n; c0 += kChunk) {
-        const unsigned len = min((unsigned)kChunk, n - c0);
-        // this chunk's part of [a, b), relative to c0
-        const unsigned ca = min(max(a, c0), c0 + len) - c0;
-        const unsigned cb = max(min(b, c0 + len), c0 + ca) - c0;
-        if (ca < cb) {
-            if constexpr (!LEVEL) {
-                for (unsigned k = lane; k < len; k += 64) {
-                    s_sr[wv][k] = sr[base + c0 + k];
-                    s_t[wv][k + 1] = t[base + c0 + k];
-                    s_c[wv][k] = cell[base + c0 + k];
-                }
-            } else {
-                // the depths of the range and of one sample on each side
-                for (unsigned k = (ca > 0 ? ca - 1 : 0) + lane; k < min(cb + 1, len); k += 64)
-                    s_t[wv][k + 1] = t[base + c0 + k];
-                for (unsigned k = ca + lane; k < cb; k += 64) {
-                    s_sr[wv][k] = sr[base + c0 + k];
-                    s_c[wv][k] = cell[base + c0 + k];
-                }
-            }
-            if (lane == 0)
-                s_t[wv][0] = c0 > 0 ? t[base + c0 - 1] : 0.0f;
-            if (lane == 1)
-                s_t[wv][len + 1] = c0 + len < n ? t[base + c0 + len] : 0.0f;
-        }
-        __syncthreads();
-        // (wave-uniform) an empty range merges the identity: nothing to do
-        if (ca < cb) {
-            const unsigned cl = (cb - ca + 63) / 64;
-            const unsigned i0 = min(ca + lane * cl, cb), i1 = min(i0 + cl, cb);
-            Over part = integrate_runs(
-                c0 + i0, c0 + i1, n, near_t, far_t,
-                [&](unsigned i) { return s_t[wv][i - c0 + 1]; },
-                [&](unsigned i) { return (unsigned)s_c[wv][i - c0]; },
-                [&](unsigned i) { return s_sr[wv][i - c0]; });
-            part = wave_over(part, lane);
-            acc = over(acc, part);  // meaningful in lane 0
-        }
-        __syncthreads();
-    }
-    if (go && lane == 0) {
-        out_rgb[3 * ray] = acc.r;
-        out_rgb[3 * ray + 1] = acc.g;
-        out_rgb[3 * ray + 2] = acc.b;
-        out_depth[ray] = acc.d;
-        out_opacity[ray] = 1.0f - acc.t;
-        if constexpr (LEVEL) {
-            lv.trans[ray] = acc.t;
-            if (lv.evaluated)
-                lv.evaluated[ray] = (lv.level > 0 ? lv.evaluated[ray] : 0u) + (b - a);
-        }
-    }
-    if constexpr (LEVEL) {
-        // a ray that closes here takes no part in later levels
-        const float tr = __shfl(acc.t, 0);
-        if (go && tr < lv.eps && lv.level + 1 < lv.levels)
-            for (unsigned i = b + lane; i < n; i += 64)
-                lv.lvl[base + i] = kDeadLevel;
-    }
-}
-
-// Level composite for every level but the last: of a render cut into pieces
-// (ranges of at most a few dozen samples) or in whole segments (a wave per
-// ray for one segment spent most of its time in the dependent loads of the
-// bounds and range, not in the integration).  G lanes per ray, 64 / G rays
-// per wave.  Lane gl of a ray's group
-// integrates the consecutive samples [a + gl c, a + (gl + 1) c) of its range
-// [a, b), c = ceil((b - a) / G), straight from memory, and the group merges
-// its lanes in order.  State, outputs and closing marks as
-// composite_kernel<true>; the rounding differs from it only in how the range
-// is split over lanes.
+// Integration of one culling level: only the ray's samples of the level,
+// [lb[l], lb[l + 1]), are integrated, and the result is merged behind the
+// ray's state from the earlier levels (rgb, depth and the transmittance
+// trans); a ray whose transmittance is below eps is left as it is, and the
+// level that takes a ray below eps marks its later samples dead.
+//
+// G lanes per ray, 64 / G rays per wave, each wave on its own LDS rows (no
+// block barrier: the waves of a block run different numbers of chunks).  A
+// ray's range goes in chunks of 4 G samples, staged with consecutive lanes
+// on consecutive samples (one load instruction covers 16 G contiguous bytes
+// of colours per ray; lanes each reading a stretch of their own from memory
+// touched a cache line per lane, and 4x the L2 requests); lane gl then
+// integrates the chunk's samples [4 gl, 4 gl + 4) from LDS, the group merges
+// its lanes in order (the first log2 G steps of the wave merge), and the
+// chunks are merged front to back.
 template <int G>
-__global__ __launch_bounds__(kThreads) void level_composite_short_kernel(
+__global__ __launch_bounds__(kThreads) void level_composite_kernel(
     const float *__restrict__ t, const uint8_t *__restrict__ cell, const float4 *__restrict__ sr,
     unsigned n, unsigned num_rays, float near_t, float far_t, LevelState lv,
     float *__restrict__ out_rgb, float *__restrict__ out_depth, float *__restrict__ out_opacity)
 {
-    const int lane = threadIdx.x & 63, gl = lane & (G - 1);
+    constexpr int CH = 4 * G, RPW = 64 / G;  // samples per chunk, rays per wave
+    __shared__ float4 s_sr[kThreads / 64][RPW][CH];
+    __shared__ float s_t[kThreads / 64][RPW][CH + 2];  // [0]: before the chunk, [len + 1]: after
+    __shared__ uint8_t s_c[kThreads / 64][RPW][CH];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, gl = lane & (G - 1), gr = lane / G;
     const unsigned ray = (blockIdx.x * kThreads + threadIdx.x) / G;
-    // groups past the last ray read ray 0's samples and store nothing
+    // groups past the last ray stage nothing and store nothing
     const bool live = ray < num_rays;
     const size_t base = (size_t)(live ? ray : 0u) * n;
-    Over st{0.f, 0.f, 0.f, 0.f, 1.f};
+    Over acc{0.f, 0.f, 0.f, 0.f, 1.f};  // meaningful in the group's first lane
     unsigned a = 0, b = 0;
     bool go = live;
     if (live) {
@@ -1112,21 +1068,47 @@ __global__ __launch_bounds__(kThreads) void level_composite_short_kernel(
         a = r_lb[0];
         b = r_lb[1];
         if (lv.level > 0) {
-            st = Over{out_rgb[3 * ray], out_rgb[3 * ray + 1], out_rgb[3 * ray + 2], out_depth[ray],
-                      lv.trans[ray]};
-            go = st.t >= lv.eps;
+            acc = Over{out_rgb[3 * ray], out_rgb[3 * ray + 1], out_rgb[3 * ray + 2], out_depth[ray],
+                       lv.trans[ray]};
+            go = acc.t >= lv.eps;
         }
     }
     if (!go)
         a = b = 0;
-    const unsigned c = (b - a + G - 1) / G;
-    const unsigned i0 = min(a + gl * c, b), i1 = min(i0 + c, b);
-    Over part = integrate_runs(
-        i0, i1, n, near_t, far_t, [&](unsigned i) { return t[base + i]; },
-        [&](unsigned i) { return (unsigned)cell[base + i]; },
-        [&](unsigned i) { return sr[base + i]; });
-    part = group_over<G>(part, gl);
-    const Over acc = over(st, part);  // meaningful in the group's first lane
+    float4 *const gsr = s_sr[wv][gr];
+    float *const gt = s_t[wv][gr];
+    uint8_t *const gc = s_c[wv][gr];
+    // LDS written by some lanes of the wave and read by others
+    auto wave_sync = [] {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    };
+    // (wave-uniform) until every group of the wave has passed its range's end
+    for (unsigned c0 = a; __ballot(c0 < b) != 0; c0 += CH) {
+        const unsigned len = c0 < b ? min((unsigned)CH, b - c0) : 0u;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const unsigned j = gl + G * k;
+            if (j < len) {
+                gsr[j] = sr[base + c0 + j];
+                gc[j] = cell[base + c0 + j];
+                gt[j + 1] = t[base + c0 + j];
+            }
+        }
+        if (len > 0 && gl == 0)
+            gt[0] = c0 > 0 ? t[base + c0 - 1] : 0.0f;
+        if (len > 0 && gl == 1)
+            gt[len + 1] = c0 + len < n ? t[base + c0 + len] : 0.0f;
+        wave_sync();
+        const unsigned i0 = min(4u * gl, len), i1 = min(i0 + 4u, len);
+        Over part = integrate_runs(
+            c0 + i0, c0 + i1, n, near_t, far_t, [&](unsigned i) { return gt[i - c0 + 1]; },
+            [&](unsigned i) { return (unsigned)gc[i - c0]; }, [&](unsigned i) { return gsr[i - c0]; });
+        part = group_over<G>(part, gl);
+        acc = over(acc, part);
+        wave_sync();  // the rows are rewritten by the next chunk
+    }
     if (go && gl == 0) {
         out_rgb[3 * ray] = acc.r;
         out_rgb[3 * ray + 1] = acc.g;
@@ -1266,8 +1248,8 @@ hipError_t launch_composite(const RenderGeometry &g, const float *t, const uint8
                             hipStream_t s)
 {
     const unsigned grid = blocks_for(g.num_rays, kThreads / 64);
-    composite_kernel<false><<<grid, kThreads, 0, s>>>(t, cell, sr, g.n, g.num_rays, g.near_t,
-                                                      g.far_t, LevelState{}, rgb, depth, opacity);
+    composite_kernel<<<grid, kThreads, 0, s>>>(t, cell, sr, g.n, g.num_rays, g.near_t, g.far_t, rgb,
+                                               depth, opacity);
     return hipGetLastError();
 }
 
@@ -1346,30 +1328,15 @@ hipError_t launch_level_composite(const RenderGeometry &g, const float *t, const
                                   float *rgb, float *depth, float *opacity, hipStream_t s)
 {
     const LevelState st{lv.lb, lv.lvl, lv.trans, lv.evaluated, lv.levels, lv.level, lv.eps};
-    // Whole segments (no length bound) below the last level: 16 lanes per ray
-    // too, whatever the range's length; the last level, which holds every
-    // later segment, keeps a wave per ray.
-    if (max_len == 0 && lv.level + 1 < lv.levels) {
-        level_composite_short_kernel<16><<<blocks_for((size_t)g.num_rays * 16, kThreads), kThreads,
-                                           0, s>>>(t, cell, sr, g.n, g.num_rays, g.near_t, g.far_t,
-                                                   st, rgb, depth, opacity);
-        return hipGetLastError();
-    }
-    if (max_len > 0 && max_len <= 32) {
-        level_composite_short_kernel<8><<<blocks_for((size_t)g.num_rays * 8, kThreads), kThreads, 0,
-                                          s>>>(t, cell, sr, g.n, g.num_rays, g.near_t, g.far_t, st,
-                                               rgb, depth, opacity);
-        return hipGetLastError();
-    }
-    if (max_len > 0 && max_len <= 64) {
-        level_composite_short_kernel<16><<<blocks_for((size_t)g.num_rays * 16, kThreads), kThreads,
-                                           0, s>>>(t, cell, sr, g.n, g.num_rays, g.near_t, g.far_t,
-                                                   st, rgb, depth, opacity);
-        return hipGetLastError();
-    }
-    const unsigned grid = blocks_for(g.num_rays, kThreads / 64);
-    composite_kernel<true><<<grid, kThreads, 0, s>>>(t, cell, sr, g.n, g.num_rays, g.near_t,
-                                                     g.far_t, st, rgb, depth, opacity);
+    // pieces of at most 32 samples: one chunk of 8 lanes per ray; otherwise
+    // 16 lanes, in as many chunks of 64 as the range needs
+    if (max_len > 0 && max_len <= 32)
+        level_composite_kernel<8><<<blocks_for((size_t)g.num_rays * 8, kThreads), kThreads, 0, s>>>(
+            t, cell, sr, g.n, g.num_rays, g.near_t, g.far_t, st, rgb, depth, opacity);
+    else
+        level_composite_kernel<16><<<blocks_for((size_t)g.num_rays * 16, kThreads), kThreads, 0,
+                                     s>>>(t, cell, sr, g.n, g.num_rays, g.near_t, g.far_t, st, rgb,
+                                          depth, opacity);
     return hipGetLastError();
 }
 

@@ -135,11 +135,11 @@ def test_culled_dense_headline_frame_bf16():
 def test_culled_pieces_fp32(piece, levels, n, K):
     """Segments cut into pieces of at most `piece` samples (levels count
     pieces): piece ends inside and across the 64-sample steps of the level
-    bounds and the 256-sample staging chunks of the level composite; level
-    composites of 8 and 16 lanes per ray (pieces of at most 32 and 64) and
-    of a wave per ray (70); the one-pass (level, head) bucketing up to its
-    256 keys (32 levels x 8 heads) and the per-level passes beyond (8 levels
-    x 64 heads)."""
+    bounds; level composites of 8 lanes per ray (pieces of at most 32, one
+    32-sample staging chunk) and of 16 lanes (pieces of 48 and 70 and the
+    last levels, ranges over one or several 64-sample chunks); the one-pass
+    (level, head) bucketing up to its 256 keys (32 levels x 8 heads) and the
+    per-level passes beyond (8 levels x 64 heads)."""
     cfg = scenes.with_changes(scenes.CONFIGS["tiny"], num_sites=K, sigma_bias=4.0, n_coarse=n)
     sc = scenes.make_scene(cfg)
     gpu = _gpu_culled(sc, "fp32", 1e-3, levels, piece=piece)

@@ -155,10 +155,26 @@ static void fault_injection()
                DERF_OK,
            "gated render");
     expect(hipDeviceSynchronize() == hipSuccess, "gated render completed");
+    // the stored encoding: its larger workspace fails cleanly too (the old
+    // one is released first), and its outputs are the fused form's
+    expect(derf_set_encoding(h, DERF_ENCODING_STORED) == DERF_OK, "stored encoding");
+    const long with_ws2 = derf_debug_live_allocations();
+    derf_debug_fail_alloc(0);
+    expect(derf_render(h, o, d, f.R, 2.0f, 6.0f, &samp, rgb2, dep, op, nullptr) == DERF_ERR_OOM,
+           "a stored-encoding render whose workspace cannot be allocated returns DERF_ERR_OOM");
+    derf_debug_fail_alloc(-1);
+    expect(derf_debug_live_allocations() == with_ws2 - 1, "the failed render holds no workspace");
+    expect(derf_render(h, o, d, f.R, 2.0f, 6.0f, &samp, rgb2, dep, op, nullptr) == DERF_OK,
+           "stored-encoding render after the failure");
+    expect(hipDeviceSynchronize() == hipSuccess, "stored-encoding render completed");
+    (void)hipMemcpy(b.data(), rgb2, sizeof(float) * 3 * R, hipMemcpyDeviceToHost);
+    expect(a == b, "the stored encoding renders the fused form's pixels");
+    expect(derf_set_encoding(h, 2) == DERF_ERR_INVALID_ARG, "unknown encoding mode");
+    expect(derf_set_encoding(h, DERF_ENCODING_FUSED) == DERF_OK, "fused encoding");
     derf_destroy(h);
     (void)hipFree(dev);
     expect(derf_debug_live_allocations() == base, "everything released at the end");
-    printf("fault injection: render workspace and gate failures handled\n");
+    printf("fault injection: render workspace, gate and stored-encoding failures handled\n");
 }
 
 int main()
@@ -237,6 +253,8 @@ int main()
     expect(derf_set_empty_heads(nullptr, nullptr) == DERF_ERR_INVALID_ARG,
            "empty heads without a handle");
     expect(derf_set_timing(nullptr, 1) == DERF_ERR_INVALID_ARG, "timing without a handle");
+    expect(derf_set_encoding(nullptr, DERF_ENCODING_STORED) == DERF_ERR_INVALID_ARG,
+           "encoding without a handle");
     expect(derf_reset_stats(nullptr) == DERF_ERR_INVALID_ARG, "reset without a handle");
     derf_stats st;
     expect(derf_get_stats(nullptr, &st) == DERF_ERR_INVALID_ARG, "stats without a handle");

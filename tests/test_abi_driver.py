@@ -47,4 +47,4 @@ def test_allocation_failures_on_the_gpu():
     r = _run(DRIVER)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "abi driver: 0 failure(s)" in r.stdout
-    assert "render workspace and gate failures handled" in r.stdout
+    assert "render workspace, gate and stored-encoding failures handled" in r.stdout

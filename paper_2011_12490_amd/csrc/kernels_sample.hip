@@ -119,6 +119,35 @@ __device__ __forceinline__ LaneRuns lane_runs(unsigned key, bool ok, uint64_t va
     return r;
 }
 
+// out[step] = p[wbase + 64 step + lane], or 0 from index n on: a wave's
+// 64 STEPS consecutive bytes, read as dwords four to a lane (a quarter of
+// the load instructions of one byte per lane, which kept the texture-data
+// path busy) and handed to their lanes by lane permutes.  p + wbase must be
+// 4-byte aligned, and a dword that starts below n must lie in p's
+// allocation (byte buffers are allocated in whole 256-byte units).
+template <int STEPS>
+__device__ __forceinline__ void wave_bytes(const uint8_t *__restrict__ p, unsigned wbase,
+                                           unsigned n, unsigned (&out)[STEPS])
+{
+    static_assert(STEPS % 4 == 0, "whole dwords per lane");
+    const int lane = (int)(threadIdx.x & 63);
+    unsigned word[STEPS / 4];
+#pragma unroll
+    for (int q = 0; q < STEPS / 4; ++q) {
+        const unsigned first = wbase + 256 * q + 4 * lane;
+        word[q] = first < n ? *reinterpret_cast<const unsigned *>(p + first) : 0u;
+    }
+#pragma unroll
+    for (int q = 0; q < STEPS / 4; ++q)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            // byte 256 q + 64 j + lane lies in the dword of lane 16 j + lane / 4
+            const unsigned v = (unsigned)__shfl((int)word[q], 16 * j + (lane >> 2));
+            const unsigned idx = wbase + 256 * q + 64 * j + lane;
+            out[4 * q + j] = idx < n ? (v >> (8 * (lane & 3))) & 0xFFu : 0u;
+        }
+}
+
 // ---------------------------------------------------------------------------
 // Cross-lane helpers over the aligned group of L lanes (L = 1, 2, 4, 8, 16)
 // holding this lane: DPP quad permutes (lane ^ 1, lane ^ 2) and the 8- and
@@ -760,8 +789,9 @@ __global__ __launch_bounds__(kThreads) void level_count_kernel(const uint8_t *__
 // within it samples keep increasing sample-id order, so each ray's run
 // through cell k stays contiguous.  Block b's samples are its 4096 of the
 // counting pass; wave w takes the 1024 consecutive ones from 1024 w, in 16
-// steps of 64 (all 16 cells loaded up front).  Pass 1 counts each wave's
-// samples per head (equal-cell ballots, wave-private counters); after one
+// steps of 64 (all 16 cells loaded up front, four to a lane: wave_bytes).
+// Pass 1 counts each wave's samples per head (equal-cell runs, wave-private
+// counters); after one
 // barrier every wave knows its first position per head (the block's base
 // plus the earlier waves' counts); pass 2 ranks each step's samples of one
 // head by ballot and advances the wave's own counters.  A sample owned by a
@@ -789,15 +819,17 @@ __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
     const unsigned wbase = blockIdx.x * (unsigned)kBucketBlock + w * (kSteps * 64);
     unsigned cs[kSteps];
     bool in[kSteps];  // the sample exists (LEVEL: and is live at this level)
+    wave_bytes(cell, wbase, num_samples, cs);
+    unsigned lv[MODE == kCellKey ? 1 : kSteps];
+    if constexpr (MODE != kCellKey)
+        wave_bytes(live.lvl, wbase, num_samples, lv);
 #pragma unroll
     for (int step = 0; step < kSteps; ++step) {
-        const unsigned s = wbase + step * 64 + lane;
-        in[step] = s < num_samples;
-        cs[step] = in[step] ? cell[s] : 0u;  // not gated on liveness: loads overlap
+        in[step] = wbase + step * 64 + lane < num_samples;
         if constexpr (LEVEL)
-            in[step] = in[step] && live(s);
+            in[step] = in[step] && lv[step] == live.level;
         if constexpr (MODE == kLevelCell)
-            cs[step] += in[step] ? live.lvl[s] * live.heads : 0u;
+            cs[step] += in[step] ? lv[step] * live.heads : 0u;
     }
     __syncthreads();
     // pass 1: this wave's count per head (run leaders)

@@ -179,7 +179,8 @@ def parity_record(sc, precision, out, ids, ref, nthreads):
 def mfma_ceiling(iters=12000):
     """Throughput of back-to-back 32x32x16 bf16 MFMAs on every SIMD (two waves
     each, four independent accumulator chains per wave) for operand patterns
-    random / constant / zero and 0, 2 or 4 bf16-pack + packed-max vector
+    random / constant / zero / random A with equal B columns (samples alike)
+    and 0, 2 or 4 bf16-pack + packed-max vector
     instructions beside each MFMA (the head MLP's epilogue mix): the clock-
     and power-limited ceiling against which the MLP's fraction of the
     nominal 2.5 PFLOP/s is read.  Timed with events on torch's stream, which
@@ -199,7 +200,7 @@ def mfma_ceiling(iters=12000):
     out = torch.empty(grid * 256, device="cuda")
     stream = torch.cuda.current_stream()
     res = []
-    for mode, name in ((0, "random"), (1, "constant"), (2, "zero")):
+    for mode, name in ((0, "random"), (1, "constant"), (2, "zero"), (3, "random, equal columns")):
         for valu in (0, 2, 4):
             def launch():
                 rc = L.derf_probe_mfma(grid, iters, 1234, mode, valu, ctypes.c_void_p(out.data_ptr()),

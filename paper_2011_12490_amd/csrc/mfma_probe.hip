@@ -34,7 +34,8 @@ __device__ __forceinline__ uint32_t mix(uint32_t x)
 
 // One operand register set (8 bf16 values) for pattern `mode`:
 // 0 random values in [-1, 1) (every bit toggles between operands),
-// 1 one constant value, 2 zeros.
+// 1 one constant value, 2 zeros.  (Mode 3 of the kernel, random A and a B
+// whose 32 columns are equal, draws both with mode 0.)
 __device__ bf16x8 operand(uint32_t seed, int mode)
 {
     bf16x8 v;
@@ -57,12 +58,16 @@ __global__ __launch_bounds__(256, 2) void mfma_probe_kernel(int iters, uint32_t 
                                                             float *out)
 {
     const uint32_t lane_seed = seed ^ (blockIdx.x * 256u + threadIdx.x);
+    // mode 3: B lane n + 32 g holds column n's k-entries of group g; one seed
+    // per half-wave makes the 32 columns (the samples) equal, A stays random
+    const uint32_t col_seed = seed ^ (blockIdx.x * 256u + (threadIdx.x & ~31u));
+    const int draw = mode == 3 ? 0 : mode;
     bf16x8 a[kChains], b[kChains];
     f32x16 acc[kChains];
 #pragma unroll
     for (int k = 0; k < kChains; ++k) {
-        a[k] = operand(lane_seed * 131u + (uint32_t)k, mode);
-        b[k] = operand(lane_seed * 137u + (uint32_t)k + 7u, mode);
+        a[k] = operand(lane_seed * 131u + (uint32_t)k, draw);
+        b[k] = operand((mode == 3 ? col_seed : lane_seed) * 137u + (uint32_t)k + 7u, draw);
         for (int i = 0; i < 16; ++i)
             acc[k][i] = 0.0f;
     }
@@ -103,13 +108,14 @@ extern "C" {
 
 // Launch the probe: grid workgroups of 256 threads (two per CU fill the
 // chip's SIMDs with two waves each), `iters` rounds of kChains MFMAs per
-// wave.  out: device float [grid * 256].  valu: 0, 2 or 4.  Returns the HIP
+// wave.  mode: 0 random, 1 constant, 2 zero operands, 3 random A with the
+// 32 columns of B equal.  out: device float [grid * 256].  valu: 0, 2 or 4.  Returns the HIP
 // status of the launch; MFMAs per launch = grid * 4 * iters * kChains.
 int derf_probe_mfma(int grid, int iters, unsigned seed, int mode, int valu, float *out,
                     void *stream)
 {
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    if (grid < 1 || iters < 1 || mode < 0 || mode > 2 || !out)
+    if (grid < 1 || iters < 1 || mode < 0 || mode > 3 || !out)
         return (int)hipErrorInvalidValue;
     switch (valu) {
     case 0:

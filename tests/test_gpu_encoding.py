@@ -156,3 +156,44 @@ def test_stored_encoding_refused_where_it_has_no_form():
     assert e.value.status == derf.DERF_ERR_UNSUPPORTED
     torch.cuda.synchronize()
     r.close()
+
+
+def test_stored_encoding_in_the_no_allocation_render():
+    """The table lives in the no-allocation render's fixed scratch array too:
+    a small frame renders there bit for bit as with the fused form, and a
+    frame whose table no longer fits is refused where the fused form's
+    workspace still fits."""
+    derf = _derf()
+    cfg = scenes.with_changes(_skew_small(), width=32, height=32, n_coarse=32)
+    sc = scenes.make_scene(cfg)
+    o = torch.from_numpy(sc.rays_o).cuda()
+    d = torch.from_numpy(sc.rays_d).cuda()
+    R = o.shape[0]
+    r = derf.Renderer(sc.sites, cfg.arch, sc.weights, "bf16")
+    samp = derf.derf_sampling(cfg.n_coarse, 0, scenes.SEED_RENDER, 1, 0)
+
+    def outs(n):
+        return (torch.empty((n, 3), device="cuda"), torch.empty((n,), device="cuda"),
+                torch.empty((n,), device="cuda"))
+
+    fused, stored = outs(R), outs(R)
+    r.set_encoding(False)
+    derf.derf_render_noalloc(r.handle, o, d, cfg.near, cfg.far, samp, *fused)
+    r.set_encoding(True)
+    derf.derf_render_noalloc(r.handle, o, d, cfg.near, cfg.far, samp, *stored)
+    torch.cuda.synchronize()
+    for a, b in zip(fused, stored):
+        assert torch.equal(a, b)
+    # 49,152 rays x 32 samples: the fused form's 30 B or so per sample fit
+    # the 64 MiB array, with the table's 128 B more they do not
+    big_o = o.repeat(48, 1)
+    big_d = d.repeat(48, 1)
+    big = outs(big_o.shape[0])
+    big_samp = derf.derf_sampling(32, 0, scenes.SEED_RENDER, 1, 0)
+    with pytest.raises(derf.DerfError) as e:
+        derf.derf_render_noalloc(r.handle, big_o, big_d, cfg.near, cfg.far, big_samp, *big)
+    assert e.value.status == derf.DERF_ERR_INVALID_ARG
+    r.set_encoding(False)
+    derf.derf_render_noalloc(r.handle, big_o, big_d, cfg.near, cfg.far, big_samp, *big)
+    torch.cuda.synchronize()
+    r.close()

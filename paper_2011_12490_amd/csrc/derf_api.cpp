@@ -141,7 +141,6 @@ inline int ev_index(int pass, int stage, int end) { return 2 * (pass * DERF_NUM_
 struct derf_handle {
     int device = 0;
     int num_sites = 0;
-    int site_bits = 0;
     bool bf16 = false;
     int mlp_grid = 0;
     float4 *sites = nullptr;
@@ -495,7 +494,7 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
         HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCAN, 1), "hipEventRecord");
         HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCATTER, 0), "hipEventRecord");
         HIP_TRY(launch_bucket_scatter(cell, b.counts, totals, gp.num_samples, nb, h->num_sites,
-                                      h->site_bits, h->empty, b.bucket, sr, s),
+                                      h->empty, b.bucket, sr, s),
                 "bucket_scatter launch");
         HIP_TRY(mark(pass, DERF_STAGE_BUCKET_SCATTER, 1), "hipEventRecord");
         HIP_TRY(mark(pass, DERF_STAGE_MLP, 0), "hipEventRecord");
@@ -513,7 +512,7 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
     if (walk.seg)
         HIP_TRY(launch_ray_walk(g, h->sites, h->num_sites, b.walk_seg, b.walk_nseg, s),
                 "ray_walk launch");
-    HIP_TRY(launch_sample_assign(g, h->sites, h->num_sites, h->site_bits, walk, b.t, b.cell,
+    HIP_TRY(launch_sample_assign(g, h->sites, h->num_sites, walk, b.t, b.cell,
                                  b.counts, nblk, s),
             "sample_assign launch");
     if (b.gxtab)
@@ -544,7 +543,7 @@ int render_impl(derf_handle *h, const float *rays_o, const float *rays_d, long l
         gf.num_samples = Sf;
         gf.inv_n = 1.0 / (double)NF;
         HIP_TRY(mark(1, DERF_STAGE_SAMPLE, 0), "hipEventRecord");
-        HIP_TRY(launch_assign_given(gf, h->sites, h->num_sites, h->site_bits, walk, b.t_fine,
+        HIP_TRY(launch_assign_given(gf, h->sites, h->num_sites, walk, b.t_fine,
                                     b.cell_fine, b.counts, nblk_f, s),
                 "assign launch");
         if (b.gxtab)
@@ -645,7 +644,7 @@ int render_soft_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     // stratified depths (the owning cells it also writes are not used)
     HIP_TRY(mark(DERF_STAGE_SAMPLE, 0), "hipEventRecord");
     HIP_TRY(launch_ray_encode(g, b.dirbuf, h->bf16, s), "ray_encode launch");
-    HIP_TRY(launch_sample_assign(g, h->sites, h->num_sites, h->site_bits, WalkTable{nullptr, nullptr},
+    HIP_TRY(launch_sample_assign(g, h->sites, h->num_sites, WalkTable{nullptr, nullptr},
                                  b.t, b.cell, b.counts, nblk, s),
             "sample_assign launch");
     HIP_TRY(launch_soft_setup(S, h->num_sites, b.bucket, b.totals, b.mlp_queue, s),
@@ -819,7 +818,7 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
         if (walk.seg)
             HIP_TRY(launch_ray_walk(g, h->sites, K, b.walk_seg, b.walk_nseg, s),
                     "ray_walk launch");
-        HIP_TRY(launch_sample_assign(g, h->sites, K, h->site_bits, walk, b.t, b.cell, b.counts,
+        HIP_TRY(launch_sample_assign(g, h->sites, K, walk, b.t, b.cell, b.counts,
                                      nblk, s),
                 "sample_assign launch");
     }
@@ -831,10 +830,7 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
     // live samples.
     const bool one_pass = one_pass_levels(L, K, P);
     if (one_pass) {
-        int key_bits = 0;
-        while ((1u << key_bits) < L * (unsigned)K)
-            ++key_bits;
-        HIP_TRY(launch_level_head_order(g, L, K, key_bits, c.lvl, b.cell, h->empty, c.key_counts,
+        HIP_TRY(launch_level_head_order(g, L, K, c.lvl, b.cell, h->empty, c.key_counts,
                                         nblk, c.key_totals, c.order, c.key_offsets,
                                         c.level_totals, b.sr, b.mlp_queue, s),
                 "level_head_order launch");
@@ -851,7 +847,7 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
                 const unsigned lblk =
                     P > 0 && l + 1 < L ? std::min(nblk, blocks_of_ll((unsigned long long)R * P))
                                        : nblk;
-                HIP_TRY(launch_level_compact(g, l, L, K, h->site_bits, c.order, c.key_offsets,
+                HIP_TRY(launch_level_compact(g, l, L, K, c.order, c.key_offsets,
                                              c.key_totals, c.lvl, b.cell, lblk, tot, b.bucket,
                                              b.mlp_queue, s),
                         "level_compact launch");
@@ -861,11 +857,11 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
                                   c.key_offsets + (size_t)l * K),
                     "mlp launch");
         } else {
-            HIP_TRY(launch_level_count(g, b.cell, K, h->site_bits, lv, b.counts, nblk, s),
+            HIP_TRY(launch_level_count(g, b.cell, K, lv, b.counts, nblk, s),
                     "level_count launch");
             HIP_TRY(launch_bucket_scan(b.counts, nblk, K, tot, b.mlp_queue, s),
                     "bucket_scan launch");
-            HIP_TRY(launch_level_scatter(g, b.cell, b.counts, tot, nblk, K, h->site_bits, h->empty,
+            HIP_TRY(launch_level_scatter(g, b.cell, b.counts, tot, nblk, K, h->empty,
                                          lv, b.bucket, b.sr, s),
                     "level_scatter launch");
             HIP_TRY(launch_groups(h, b.bucket, tot, g, b.t, b.dirbuf, b.sr, b.mlp_queue, false, s),
@@ -952,9 +948,6 @@ int create_body(derf_handle **out, int num_sites, const float *sites_xyz,
             return cleanup(rc);
     }
     h->num_sites = num_sites;
-    h->site_bits = 0;
-    while ((1 << h->site_bits) < num_sites)
-        ++h->site_bits;
     h->bf16 = bf16;
     h->mlp_grid = cus;
     std::vector<int> head_group(num_sites);

@@ -30,16 +30,16 @@ hipError_t launch_level_bounds(const uint8_t *cell, unsigned n, unsigned num_ray
 // per-block head counts of the samples live at the level (the layout of the
 // assignment's counts)
 hipError_t launch_level_count(const RenderGeometry &g, const uint8_t *cell, int num_sites,
-                              int site_bits, const CullLevel &lv, unsigned *counts,
+                              const CullLevel &lv, unsigned *counts,
                               unsigned num_blocks, hipStream_t s);
-// One-pass bucketing of every level at once (levels K <= 256 keys of
-// key_bits bits): order [S] receives the sample ids sorted by (level, head),
+// One-pass bucketing of every level at once (levels K <= 256 keys): order
+// [S] receives the sample ids sorted by (level, head),
 // stably; totals [levels K] the samples per key and offsets [levels K] where
 // each key's stretch starts; live [levels][K] the level-0 counts (zeros
 // after).  Samples of 0-capacity heads get zero density and colour in sr.
 // counts: [levels K][num_blocks] scratch.  Clears the MLP's tile counters.
 hipError_t launch_level_head_order(const RenderGeometry &g, unsigned levels, int heads,
-                                   int key_bits, const uint8_t *lvl, const uint8_t *cell,
+                                   const uint8_t *lvl, const uint8_t *cell,
                                    const HeadMask &empty, unsigned *counts, unsigned num_blocks,
                                    unsigned *totals, unsigned *order, unsigned *offsets,
                                    unsigned *live, float4 *sr, unsigned *mlp_queue, hipStream_t s);
@@ -49,7 +49,7 @@ hipError_t launch_level_head_order(const RenderGeometry &g, unsigned levels, int
 // entry).  num_blocks blocks of 4096 entries must cover the level.  Clears
 // the MLP's tile counters.
 hipError_t launch_level_compact(const RenderGeometry &g, unsigned level, unsigned levels,
-                                int heads, int head_bits, const unsigned *order,
+                                int heads, const unsigned *order,
                                 const unsigned *offsets, const unsigned *totals,
                                 const uint8_t *lvl, const uint8_t *cell, unsigned num_blocks,
                                 unsigned *live, unsigned *bucket, unsigned *mlp_queue,
@@ -57,7 +57,7 @@ hipError_t launch_level_compact(const RenderGeometry &g, unsigned level, unsigne
 // bucket_scatter over the samples live at the level
 hipError_t launch_level_scatter(const RenderGeometry &g, const uint8_t *cell,
                                 const unsigned *counts, const unsigned *totals,
-                                unsigned num_blocks, int num_sites, int site_bits,
+                                unsigned num_blocks, int num_sites,
                                 const HeadMask &empty, const CullLevel &lv, unsigned *bucket,
                                 float4 *sr, hipStream_t s);
 // integrates each open ray's samples of the level behind its state in

@@ -79,11 +79,11 @@ hipError_t launch_ray_walk(const RenderGeometry &g, const float4 *sites, int num
                            SegRec *seg, unsigned char *nseg, hipStream_t s);
 // walk: the table of launch_ray_walk for the same rays, or {nullptr, nullptr}
 hipError_t launch_sample_assign(const RenderGeometry &g, const float4 *sites, int num_sites,
-                                int site_bits, const WalkTable &walk, float *t, uint8_t *cell,
+                                const WalkTable &walk, float *t, uint8_t *cell,
                                 unsigned *counts, unsigned num_blocks, hipStream_t s);
 // same, for given depths t (read only): no sampling
 hipError_t launch_assign_given(const RenderGeometry &g, const float4 *sites, int num_sites,
-                               int site_bits, const WalkTable &walk, const float *t,
+                               const WalkTable &walk, const float *t,
                                uint8_t *cell, unsigned *counts, unsigned num_blocks,
                                hipStream_t s);
 // also clears the kMlpQueues tile counters of the MLP launch that follows
@@ -92,7 +92,7 @@ hipError_t launch_bucket_scan(unsigned *counts, unsigned num_blocks, int num_sit
 // Samples of 0-capacity heads also get sr = 0 here (the MLP skips those heads).
 hipError_t launch_bucket_scatter(const uint8_t *cell, const unsigned *counts,
                                  const unsigned *totals, unsigned num_samples,
-                                 unsigned num_blocks, int num_sites, int site_bits,
+                                 unsigned num_blocks, int num_sites,
                                  const HeadMask &empty, unsigned *bucket, float4 *sr,
                                  hipStream_t s);
 // Soft decomposition: bucket[i] = i (i < S), totals[k] = S, queue cleared.

@@ -428,7 +428,7 @@ __device__ __forceinline__ unsigned nearest_site(const float4 *s_sites, int num_
 // as the search over all sites.
 template <bool FROM_T, bool WALK>
 __global__ __launch_bounds__(kThreads) void sample_assign_kernel(
-    RenderGeometry g, const float4 *__restrict__ sites, int num_sites, int site_bits,
+    RenderGeometry g, const float4 *__restrict__ sites, int num_sites,
     WalkTable walk, float *__restrict__ t_out, uint8_t *__restrict__ cell_out,
     unsigned *__restrict__ counts, unsigned num_blocks)
 {
@@ -742,14 +742,14 @@ __global__ __launch_bounds__(kThreads) void level_bounds_kernel(const uint8_t *_
 }
 
 // Per-block key histograms (the layout of the assignment's counts:
-// counts[key * num_blocks + b]; num_keys keys of key_bits bits), MODE
+// counts[key * num_blocks + b]; num_keys keys), MODE
 // kCellAtLevel or kLevelCell.  Thread t takes samples t + 256 q of the block
 // (q < 16); all 16 level bytes and cells are loaded up front, so the loads
 // are in flight together.
 template <int MODE>
 __global__ __launch_bounds__(kThreads) void level_count_kernel(const uint8_t *__restrict__ cell,
                                                               unsigned num_samples, int num_keys,
-                                                              int key_bits, LevelLive live,
+                                                              LevelLive live,
                                                               unsigned *__restrict__ counts,
                                                               unsigned num_blocks)
 {
@@ -798,12 +798,12 @@ __global__ __launch_bounds__(kThreads) void level_count_kernel(const uint8_t *__
 // 0-capacity head keeps its bucket slot (the offsets are the same) but gets
 // zero density and colour in sr: the MLP does not evaluate that head.
 // MODE: the key (kCellKey, kCellAtLevel, kLevelCell); num_sites counts the
-// keys, site_bits their bits.
+// keys.
 template <int MODE>
 __global__ __launch_bounds__(kThreads) void bucket_scatter_kernel(
     const uint8_t *__restrict__ cell, const unsigned *__restrict__ prefix,
     const unsigned *__restrict__ totals, unsigned num_samples, unsigned num_blocks,
-    int num_sites, int site_bits, HeadMask empty, LevelLive live, unsigned *__restrict__ bucket,
+    int num_sites, HeadMask empty, LevelLive live, unsigned *__restrict__ bucket,
     float4 *__restrict__ sr)
 {
     constexpr bool LEVEL = MODE == kCellAtLevel;
@@ -925,7 +925,7 @@ __global__ __launch_bounds__(kThreads) void level_head_init_kernel(
 __global__ __launch_bounds__(kThreads) void level_compact_kernel(
     const unsigned *__restrict__ order, const unsigned *__restrict__ offsets,
     const unsigned *__restrict__ totals, const uint8_t *__restrict__ lvl,
-    const uint8_t *__restrict__ cell, unsigned level, unsigned levels, int heads, int head_bits,
+    const uint8_t *__restrict__ cell, unsigned level, unsigned levels, int heads,
     unsigned num_samples, unsigned *__restrict__ live, unsigned *__restrict__ bucket,
     unsigned *__restrict__ mlp_queue)
 {
@@ -1229,30 +1229,30 @@ hipError_t launch_ray_walk(const RenderGeometry &g, const float4 *sites, int num
 }
 
 hipError_t launch_sample_assign(const RenderGeometry &g, const float4 *sites, int num_sites,
-                                int site_bits, const WalkTable &walk, float *t, uint8_t *cell,
+                                const WalkTable &walk, float *t, uint8_t *cell,
                                 unsigned *counts, unsigned num_blocks, hipStream_t s)
 {
     if (walk.seg)
         sample_assign_kernel<false, true><<<num_blocks, kThreads, 0, s>>>(
-            g, sites, num_sites, site_bits, walk, t, cell, counts, num_blocks);
+            g, sites, num_sites, walk, t, cell, counts, num_blocks);
     else
         sample_assign_kernel<false, false><<<num_blocks, kThreads, 0, s>>>(
-            g, sites, num_sites, site_bits, walk, t, cell, counts, num_blocks);
+            g, sites, num_sites, walk, t, cell, counts, num_blocks);
     return hipGetLastError();
 }
 
 hipError_t launch_assign_given(const RenderGeometry &g, const float4 *sites, int num_sites,
-                               int site_bits, const WalkTable &walk, const float *t,
+                               const WalkTable &walk, const float *t,
                                uint8_t *cell, unsigned *counts, unsigned num_blocks,
                                hipStream_t s)
 {
     // t is only read in these instantiations
     if (walk.seg)
         sample_assign_kernel<true, true><<<num_blocks, kThreads, 0, s>>>(
-            g, sites, num_sites, site_bits, walk, const_cast<float *>(t), cell, counts, num_blocks);
+            g, sites, num_sites, walk, const_cast<float *>(t), cell, counts, num_blocks);
     else
         sample_assign_kernel<true, false><<<num_blocks, kThreads, 0, s>>>(
-            g, sites, num_sites, site_bits, walk, const_cast<float *>(t), cell, counts, num_blocks);
+            g, sites, num_sites, walk, const_cast<float *>(t), cell, counts, num_blocks);
     return hipGetLastError();
 }
 
@@ -1265,12 +1265,12 @@ hipError_t launch_bucket_scan(unsigned *counts, unsigned num_blocks, int num_sit
 
 hipError_t launch_bucket_scatter(const uint8_t *cell, const unsigned *counts,
                                  const unsigned *totals, unsigned num_samples,
-                                 unsigned num_blocks, int num_sites, int site_bits,
+                                 unsigned num_blocks, int num_sites,
                                  const HeadMask &empty, unsigned *bucket, float4 *sr,
                                  hipStream_t s)
 {
     bucket_scatter_kernel<kCellKey><<<num_blocks, kThreads, 0, s>>>(
-        cell, counts, totals, num_samples, num_blocks, num_sites, site_bits, empty, LevelLive{},
+        cell, counts, totals, num_samples, num_blocks, num_sites, empty, LevelLive{},
         bucket, sr);
     return hipGetLastError();
 }
@@ -1297,16 +1297,16 @@ hipError_t launch_level_bounds(const uint8_t *cell, unsigned n, unsigned num_ray
 static LevelLive level_live(const CullLevel &lv) { return LevelLive{lv.lvl, lv.level, 0u}; }
 
 hipError_t launch_level_count(const RenderGeometry &g, const uint8_t *cell, int num_sites,
-                              int site_bits, const CullLevel &lv, unsigned *counts,
+                              const CullLevel &lv, unsigned *counts,
                               unsigned num_blocks, hipStream_t s)
 {
     level_count_kernel<kCellAtLevel><<<num_blocks, kThreads, 0, s>>>(
-        cell, g.num_samples, num_sites, site_bits, level_live(lv), counts, num_blocks);
+        cell, g.num_samples, num_sites, level_live(lv), counts, num_blocks);
     return hipGetLastError();
 }
 
 hipError_t launch_level_head_order(const RenderGeometry &g, unsigned levels, int heads,
-                                   int key_bits, const uint8_t *lvl, const uint8_t *cell,
+                                   const uint8_t *lvl, const uint8_t *cell,
                                    const HeadMask &empty, unsigned *counts, unsigned num_blocks,
                                    unsigned *totals, unsigned *order, unsigned *offsets,
                                    unsigned *live, float4 *sr, unsigned *mlp_queue, hipStream_t s)
@@ -1314,7 +1314,7 @@ hipError_t launch_level_head_order(const RenderGeometry &g, unsigned levels, int
     const int keys = (int)levels * heads;
     const LevelLive lk{lvl, 0u, (unsigned)heads};
     level_count_kernel<kLevelCell><<<num_blocks, kThreads, 0, s>>>(cell, g.num_samples, keys,
-                                                                   key_bits, lk, counts, num_blocks);
+                                                                   lk, counts, num_blocks);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
@@ -1322,7 +1322,7 @@ hipError_t launch_level_head_order(const RenderGeometry &g, unsigned levels, int
     if (e != hipSuccess)
         return e;
     bucket_scatter_kernel<kLevelCell><<<num_blocks, kThreads, 0, s>>>(
-        cell, counts, totals, g.num_samples, num_blocks, keys, key_bits, empty, lk, order, sr);
+        cell, counts, totals, g.num_samples, num_blocks, keys, empty, lk, order, sr);
     e = hipGetLastError();
     if (e != hipSuccess)
         return e;
@@ -1331,26 +1331,26 @@ hipError_t launch_level_head_order(const RenderGeometry &g, unsigned levels, int
 }
 
 hipError_t launch_level_compact(const RenderGeometry &g, unsigned level, unsigned levels,
-                                int heads, int head_bits, const unsigned *order,
+                                int heads, const unsigned *order,
                                 const unsigned *offsets, const unsigned *totals,
                                 const uint8_t *lvl, const uint8_t *cell, unsigned num_blocks,
                                 unsigned *live, unsigned *bucket, unsigned *mlp_queue,
                                 hipStream_t s)
 {
     level_compact_kernel<<<num_blocks, kThreads, 0, s>>>(order, offsets, totals, lvl, cell, level,
-                                                         levels, heads, head_bits, g.num_samples,
+                                                         levels, heads, g.num_samples,
                                                          live, bucket, mlp_queue);
     return hipGetLastError();
 }
 
 hipError_t launch_level_scatter(const RenderGeometry &g, const uint8_t *cell,
                                 const unsigned *counts, const unsigned *totals,
-                                unsigned num_blocks, int num_sites, int site_bits,
+                                unsigned num_blocks, int num_sites,
                                 const HeadMask &empty, const CullLevel &lv, unsigned *bucket,
                                 float4 *sr, hipStream_t s)
 {
     bucket_scatter_kernel<kCellAtLevel><<<num_blocks, kThreads, 0, s>>>(
-        cell, counts, totals, g.num_samples, num_blocks, num_sites, site_bits, empty,
+        cell, counts, totals, g.num_samples, num_blocks, num_sites, empty,
         level_live(lv), bucket, sr);
     return hipGetLastError();
 }

@@ -784,6 +784,34 @@ __global__ __launch_bounds__(kThreads) void level_count_kernel(const uint8_t *__
         counts[(size_t)k * num_blocks + blockIdx.x] = s_hist[k];
 }
 
+// The same counts for a level below the last, ray by ray: such a level is
+// one piece of each ray (between two consecutive openings), so all of a
+// ray's samples there lie in one cell.  A ray still open (level 0, or its
+// transmittance after the previous level at least eps: exactly the rays whose
+// level bytes the earlier level composites left live) adds its range's
+// length to that cell's count of each block the range touches.  counts
+// must be zero on entry.  One thread per ray.
+__global__ __launch_bounds__(kThreads) void level_ray_count_kernel(
+    const uint8_t *__restrict__ cell, const unsigned *__restrict__ lb,
+    const float *__restrict__ trans, unsigned n, unsigned num_rays, unsigned level,
+    unsigned levels, float eps, unsigned *__restrict__ counts, unsigned num_blocks)
+{
+    const unsigned ray = blockIdx.x * kThreads + threadIdx.x;
+    if (ray >= num_rays)
+        return;
+    const unsigned *r_lb = lb + (size_t)ray * (levels + 1) + level;
+    const unsigned a = r_lb[0], b = r_lb[1];
+    if (a >= b || (level > 0 && !(trans[ray] >= eps)))
+        return;
+    const unsigned long long s0 = (unsigned long long)ray * n + a, s1 = (unsigned long long)ray * n + b;
+    unsigned *row = counts + (size_t)cell[s0] * num_blocks;
+    for (unsigned long long blk = s0 / kBucketBlock; blk * kBucketBlock < s1; ++blk) {
+        const unsigned long long lo = blk * kBucketBlock > s0 ? blk * kBucketBlock : s0;
+        const unsigned long long hi = (blk + 1) * kBucketBlock < s1 ? (blk + 1) * kBucketBlock : s1;
+        atomicAdd(row + blk, (unsigned)(hi - lo));
+    }
+}
+
 // Stable scatter of sample ids into per-head buckets.  Bucket k occupies
 // [offset_k, offset_k + total_k) with offset_k = sum of totals below k;
 // within it samples keep increasing sample-id order, so each ray's run
@@ -1300,6 +1328,16 @@ hipError_t launch_level_count(const RenderGeometry &g, const uint8_t *cell, int 
                               const CullLevel &lv, unsigned *counts,
                               unsigned num_blocks, hipStream_t s)
 {
+    if (lv.level + 1 < lv.levels) {
+        // one cell per ray at this level: count ray by ray
+        const hipError_t e = launch_fill_u32(counts, (unsigned)num_sites * num_blocks, 0u, s);
+        if (e != hipSuccess)
+            return e;
+        level_ray_count_kernel<<<blocks_for(g.num_rays, kThreads), kThreads, 0, s>>>(
+            cell, lv.lb, lv.trans, g.n, g.num_rays, lv.level, lv.levels, lv.eps, counts,
+            num_blocks);
+        return hipGetLastError();
+    }
     level_count_kernel<kCellAtLevel><<<num_blocks, kThreads, 0, s>>>(
         cell, g.num_samples, num_sites, level_live(lv), counts, num_blocks);
     return hipGetLastError();

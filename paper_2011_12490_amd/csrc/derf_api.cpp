@@ -856,6 +856,13 @@ int render_culled_impl(derf_handle *h, const float *rays_o, const float *rays_d,
             HIP_TRY(launch_groups(h, src, tot, g, b.t, b.dirbuf, b.sr, b.mlp_queue, false, s,
                                   c.key_offsets + (size_t)l * K),
                     "mlp launch");
+        } else if (l + 1 < L) {
+            // one run of one cell per open ray: bucketed ray by ray
+            HIP_TRY(launch_level_ray_bucket(g, b.cell, K, h->empty, lv, b.counts, nblk, tot,
+                                            b.totals, b.bucket, b.sr, b.mlp_queue, s),
+                    "level_ray_bucket launch");
+            HIP_TRY(launch_groups(h, b.bucket, tot, g, b.t, b.dirbuf, b.sr, b.mlp_queue, false, s),
+                    "mlp launch");
         } else {
             HIP_TRY(launch_level_count(g, b.cell, K, lv, b.counts, nblk, s),
                     "level_count launch");

@@ -54,6 +54,19 @@ hipError_t launch_level_compact(const RenderGeometry &g, unsigned level, unsigne
                                 const uint8_t *lvl, const uint8_t *cell, unsigned num_blocks,
                                 unsigned *live, unsigned *bucket, unsigned *mlp_queue,
                                 hipStream_t s);
+// A level below the last, bucketed ray by ray (each open ray's samples at
+// such a level are one run of one cell, touching at most two blocks): the
+// runs are counted into counts [K][num_blocks] (the per-sample counts'
+// layout), scanned by bucket_scan into per-block prefixes and totals [K],
+// and written to bucket at head_off [K] (K words of scratch: the exclusive
+// scan of the totals) plus a position reserved from the prefix of their
+// block (runs of one block in no fixed order).  sr gets zeros for
+// 0-capacity heads.  Clears the MLP's tile counters.
+hipError_t launch_level_ray_bucket(const RenderGeometry &g, const uint8_t *cell, int num_sites,
+                                   const HeadMask &empty, const CullLevel &lv, unsigned *counts,
+                                   unsigned num_blocks, unsigned *totals, unsigned *head_off,
+                                   unsigned *bucket, float4 *sr, unsigned *mlp_queue,
+                                   hipStream_t s);
 // bucket_scatter over the samples live at the level
 hipError_t launch_level_scatter(const RenderGeometry &g, const uint8_t *cell,
                                 const unsigned *counts, const unsigned *totals,

@@ -784,31 +784,132 @@ __global__ __launch_bounds__(kThreads) void level_count_kernel(const uint8_t *__
         counts[(size_t)k * num_blocks + blockIdx.x] = s_hist[k];
 }
 
-// The same counts for a level below the last, ray by ray: such a level is
-// one piece of each ray (between two consecutive openings), so all of a
-// ray's samples there lie in one cell.  A ray still open (level 0, or its
-// transmittance after the previous level at least eps: exactly the rays whose
-// level bytes the earlier level composites left live) adds its range's
-// length to that cell's count of each block the range touches.  counts
-// must be zero on entry.  One thread per ray.
+// Bucketing of a level below the last, ray by ray.  Such a level is one
+// piece of each ray (between two consecutive openings), so a ray's samples
+// there form one run of one cell.  A ray takes part while it is open: level
+// 0, or its transmittance after the previous level at least eps (exactly the
+// rays whose level bytes the earlier level composites left live).  The
+// order of the runs within a head's bucket is not fixed (each sample's MLP
+// outputs do not depend on it), so positions are reserved by atomics,
+// aggregated over the lanes of a wave that share a cell.
+struct RayRun {
+    bool on;
+    unsigned k, len;
+    unsigned long long s0;  // first sample of the run
+};
+__device__ __forceinline__ RayRun level_ray_run(const uint8_t *__restrict__ cell,
+                                                const unsigned *__restrict__ lb,
+                                                const float *__restrict__ trans, unsigned n,
+                                                unsigned num_rays, unsigned level,
+                                                unsigned levels, float eps)
+{
+    RayRun r{false, 0u, 0u, 0ull};
+    const unsigned ray = blockIdx.x * kThreads + threadIdx.x;
+    if (ray >= num_rays)
+        return r;
+    const unsigned *r_lb = lb + (size_t)ray * (levels + 1) + level;
+    const unsigned a = r_lb[0], b = r_lb[1];
+    if (a >= b || (level > 0 && !(trans[ray] >= eps)))
+        return r;
+    r.on = true;
+    r.s0 = (unsigned long long)ray * n + a;
+    r.len = b - a;
+    r.k = cell[r.s0];
+    return r;
+}
+
+// counts[k * num_blocks + b] += the samples of each open ray's run in block
+// b (zero on entry; the layout of the per-sample counts, so bucket_scan
+// turns them into per-block prefixes).  A run is shorter than a block, so it
+// touches at most two.  One thread per ray.
 __global__ __launch_bounds__(kThreads) void level_ray_count_kernel(
     const uint8_t *__restrict__ cell, const unsigned *__restrict__ lb,
     const float *__restrict__ trans, unsigned n, unsigned num_rays, unsigned level,
     unsigned levels, float eps, unsigned *__restrict__ counts, unsigned num_blocks)
 {
-    const unsigned ray = blockIdx.x * kThreads + threadIdx.x;
-    if (ray >= num_rays)
+    const RayRun r = level_ray_run(cell, lb, trans, n, num_rays, level, levels, eps);
+    if (!r.on)
         return;
-    const unsigned *r_lb = lb + (size_t)ray * (levels + 1) + level;
-    const unsigned a = r_lb[0], b = r_lb[1];
-    if (a >= b || (level > 0 && !(trans[ray] >= eps)))
-        return;
-    const unsigned long long s0 = (unsigned long long)ray * n + a, s1 = (unsigned long long)ray * n + b;
-    unsigned *row = counts + (size_t)cell[s0] * num_blocks;
-    for (unsigned long long blk = s0 / kBucketBlock; blk * kBucketBlock < s1; ++blk) {
-        const unsigned long long lo = blk * kBucketBlock > s0 ? blk * kBucketBlock : s0;
-        const unsigned long long hi = (blk + 1) * kBucketBlock < s1 ? (blk + 1) * kBucketBlock : s1;
-        atomicAdd(row + blk, (unsigned)(hi - lo));
+    const unsigned long long s1 = r.s0 + r.len;
+    const unsigned long long b0 = r.s0 / kBucketBlock, split = (b0 + 1) * kBucketBlock;
+    unsigned *row = counts + (size_t)r.k * num_blocks;
+    atomicAdd(row + b0, (unsigned)((s1 < split ? s1 : split) - r.s0));
+    if (s1 > split)
+        atomicAdd(row + b0 + 1, (unsigned)(s1 - split));
+}
+
+// head_off[k] = sum of totals below k (where head k's stretch starts).  One
+// block, K <= 256.
+__global__ __launch_bounds__(kThreads) void head_offsets_kernel(const unsigned *__restrict__ totals,
+                                                                int num_sites,
+                                                                unsigned *__restrict__ head_off)
+{
+    __shared__ unsigned s_v[kThreads];
+    const int t = threadIdx.x;
+    const unsigned v = t < num_sites ? totals[t] : 0u;
+    s_v[t] = v;
+    __syncthreads();
+    for (int o = 1; o < kThreads; o <<= 1) {
+        const unsigned y = t >= o ? s_v[t - o] : 0u;
+        __syncthreads();
+        s_v[t] += y;
+        __syncthreads();
+    }
+    if (t < num_sites)
+        head_off[t] = s_v[t] - v;
+}
+
+// Each open ray's run (in at most two block pieces) goes to head k's
+// stretch at head_off[k] plus a position reserved from the block's prefix
+// prefix[k * num_blocks + b] (the scanned counts: rays of one block and
+// head share a counter, so reservations rarely contend).  The wave then
+// writes its pieces one after another with all its lanes (coalesced).
+// Samples of 0-capacity heads get zero density and colour in sr, as in the
+// per-sample scatter.
+__global__ __launch_bounds__(kThreads) void level_ray_scatter_kernel(
+    const uint8_t *__restrict__ cell, const unsigned *__restrict__ lb,
+    const float *__restrict__ trans, unsigned n, unsigned num_rays, unsigned num_samples,
+    unsigned level, unsigned levels, float eps, HeadMask empty,
+    const unsigned *__restrict__ head_off, unsigned *__restrict__ prefix, unsigned num_blocks,
+    unsigned *__restrict__ bucket, float4 *__restrict__ sr)
+{
+    const RayRun r = level_ray_run(cell, lb, trans, n, num_rays, level, levels, eps);
+    const int lane = (int)(threadIdx.x & 63);
+    unsigned pos[2] = {0u, 0u}, len[2] = {0u, 0u};
+    if (r.on) {
+        const unsigned long long s1 = r.s0 + r.len;
+        const unsigned long long b0 = r.s0 / kBucketBlock, split = (b0 + 1) * kBucketBlock;
+        unsigned *row = prefix + (size_t)r.k * num_blocks;
+        const unsigned base = head_off[r.k];
+        len[0] = (unsigned)((s1 < split ? s1 : split) - r.s0);
+        pos[0] = base + atomicAdd(row + b0, len[0]);
+        if (s1 > split) {
+            len[1] = (unsigned)(s1 - split);
+            pos[1] = base + atomicAdd(row + b0 + 1, len[1]);
+        }
+    }
+#pragma unroll
+    for (int part = 0; part < 2; ++part) {
+        uint64_t todo = __ballot(len[part] > 0);
+        while (todo) {
+            const int q = __builtin_ctzll(todo);
+            todo &= todo - 1;
+            const unsigned qpos = (unsigned)__shfl((int)pos[part], q);
+            const unsigned qlen = (unsigned)__shfl((int)len[part], q);
+            const unsigned qk = (unsigned)__shfl((int)r.k, q);
+            const unsigned long long s_first = r.s0 + (part ? len[0] : 0u);
+            const unsigned lo = (unsigned)__shfl((int)(unsigned)s_first, q);
+            const unsigned hi = (unsigned)__shfl((int)(unsigned)(s_first >> 32), q);
+            const unsigned long long qs = ((unsigned long long)hi << 32) | lo;
+            const bool zero = empty.test((int)qk);
+            for (unsigned j = lane; j < qlen; j += 64) {
+                // within the bucket whenever the counts are consistent
+                if (qpos + j < num_samples)
+                    bucket[qpos + j] = (unsigned)(qs + j);
+                if (zero)
+                    sr[qs + j] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            }
+        }
     }
 }
 
@@ -1324,20 +1425,42 @@ hipError_t launch_level_bounds(const uint8_t *cell, unsigned n, unsigned num_ray
 
 static LevelLive level_live(const CullLevel &lv) { return LevelLive{lv.lvl, lv.level, 0u}; }
 
+hipError_t launch_level_ray_bucket(const RenderGeometry &g, const uint8_t *cell, int num_sites,
+                                   const HeadMask &empty, const CullLevel &lv, unsigned *counts,
+                                   unsigned num_blocks, unsigned *totals, unsigned *head_off,
+                                   unsigned *bucket, float4 *sr, unsigned *mlp_queue,
+                                   hipStream_t s)
+{
+    if (lv.level + 1 >= lv.levels || num_sites < 1 || num_sites > kMaxSites)
+        return hipErrorInvalidValue;
+    hipError_t e = launch_fill_u32(counts, (unsigned)num_sites * num_blocks, 0u, s);
+    if (e != hipSuccess)
+        return e;
+    const unsigned grid = blocks_for(g.num_rays, kThreads);
+    if (grid > 0) {
+        level_ray_count_kernel<<<grid, kThreads, 0, s>>>(cell, lv.lb, lv.trans, g.n, g.num_rays,
+                                                         lv.level, lv.levels, lv.eps, counts,
+                                                         num_blocks);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+    }
+    if ((e = launch_bucket_scan(counts, num_blocks, num_sites, totals, mlp_queue, s)) !=
+        hipSuccess)
+        return e;
+    head_offsets_kernel<<<1, kThreads, 0, s>>>(totals, num_sites, head_off);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    if (grid > 0)
+        level_ray_scatter_kernel<<<grid, kThreads, 0, s>>>(
+            cell, lv.lb, lv.trans, g.n, g.num_rays, g.num_samples, lv.level, lv.levels, lv.eps,
+            empty, head_off, counts, num_blocks, bucket, sr);
+    return hipGetLastError();
+}
+
 hipError_t launch_level_count(const RenderGeometry &g, const uint8_t *cell, int num_sites,
                               const CullLevel &lv, unsigned *counts,
                               unsigned num_blocks, hipStream_t s)
 {
-    if (lv.level + 1 < lv.levels) {
-        // one cell per ray at this level: count ray by ray
-        const hipError_t e = launch_fill_u32(counts, (unsigned)num_sites * num_blocks, 0u, s);
-        if (e != hipSuccess)
-            return e;
-        level_ray_count_kernel<<<blocks_for(g.num_rays, kThreads), kThreads, 0, s>>>(
-            cell, lv.lb, lv.trans, g.n, g.num_rays, lv.level, lv.levels, lv.eps, counts,
-            num_blocks);
-        return hipGetLastError();
-    }
     level_count_kernel<kCellAtLevel><<<num_blocks, kThreads, 0, s>>>(
         cell, g.num_samples, num_sites, level_live(lv), counts, num_blocks);
     return hipGetLastError();

@@ -174,8 +174,10 @@ def test_culled_pieces_no_cut_and_zero_eps():
 
 @pytest.mark.parametrize("n", [1, 7, 65, 300, 600])
 def test_culled_ragged_sample_counts_fp32(n):
-    """Sample counts off the 64-lane steps, and past the 256-sample staging
-    chunk of the level composite (a level's range then spans chunks)."""
+    """Sample counts off the 64-lane steps; level ranges past the 64-sample
+    staging chunks of the level composite; and, with n not dividing 4096,
+    rays whose run at a level below the last straddles two bucketing blocks
+    (those levels are bucketed ray by ray)."""
     cfg = scenes.with_changes(scenes.CONFIGS["tiny"], num_sites=8, sigma_bias=4.0, n_coarse=n)
     sc = scenes.make_scene(cfg)
     gpu = _gpu_culled(sc, "fp32", 1e-3, 5)

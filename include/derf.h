@@ -331,7 +331,7 @@ int derf_set_encoding(derf_handle *h, int mode);
  * its coarse and fine passes; stage_launches counts the renders that ran the
  * stage.  head_samples counts head evaluations of both passes.
  * walk_rays and walk_fallback_rays describe the last render's assignment
- * (Sec. 3.3: a ray crosses each convex cell in one segment): from 28 heads
+ * (Sec. 3.3: a ray crosses each convex cell in one segment): from 17 heads
  * every ray is first walked through its cells; a ray that crosses more than
  * 32 cells, or has a segment with more than 11 near-tied candidate sites, is
  * assigned by the search over all sites instead (same cells, more work).

@@ -35,7 +35,7 @@ struct alignas(16) SegRec {
 };
 // Heads from which the assignment uses the walk instead of all sites (below,
 // the search over all sites costs less than the walk and its table lookups).
-constexpr int kWalkSites = 28;
+constexpr int kWalkSites = 17;
 struct WalkTable {
     const SegRec *seg;           // [R][kMaxSeg]
     const unsigned char *nseg;   // [R]; 0: the ray takes the search over all sites

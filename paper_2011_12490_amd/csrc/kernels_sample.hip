@@ -425,17 +425,21 @@ __device__ __forceinline__ unsigned nearest_site(const float4 *s_sites, int num_
 // FROM_T the depths are given (t is read, not written): the assignment of
 // the inverse-CDF samples of hierarchical sampling.  WALK: the owning cell
 // comes from the ray's walk table (nearest_site), which gives the same cell
-// as the search over all sites.
+// as the search over all sites.  The lookup waits on its table reads, so
+// WALK asks for 8 waves per SIMD (at most 64 registers, no spills; the
+// staging below keeps 8 blocks within the CU's LDS).
 template <bool FROM_T, bool WALK>
-__global__ __launch_bounds__(kThreads) void sample_assign_kernel(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(WALK ? 8 : 1)))
+void sample_assign_kernel(
     RenderGeometry g, const float4 *__restrict__ sites, int num_sites,
     WalkTable walk, float *__restrict__ t_out, uint8_t *__restrict__ cell_out,
     unsigned *__restrict__ counts, unsigned num_blocks)
 {
     __shared__ float4 s_sites[kMaxSites];
     __shared__ unsigned s_hist[kMaxSites];
-    // walk tables of the block's rays, when they are few enough (n >= ~108)
-    constexpr int kStageRays = 40;
+    // walk tables of the block's rays, when they are few enough (n >= ~152):
+    // 14 KB, so that 8 blocks fit in 160 KB of LDS with the sites
+    constexpr int kStageRays = 28;
     __shared__ SegRec s_seg[WALK ? kStageRays * kMaxSeg : 1];
     __shared__ unsigned char s_nseg[WALK ? kStageRays : 1];
     for (int k = threadIdx.x; k < num_sites; k += kThreads) {
@@ -466,18 +470,20 @@ __global__ __launch_bounds__(kThreads) void sample_assign_kernel(
         }
     }
     __syncthreads();
-    // walk table and segment count of ray r (count 0: search all sites)
-    auto table_of = [&](unsigned r, unsigned &ns) -> const SegRec * {
+    // owning cell of a sample of ray r: through its walk table (segment count
+    // 0: search all sites).  The staged and the global table are separate
+    // calls so that each keeps its address space: a pointer that may be
+    // either would turn the table reads into generic loads, which go through
+    // the texture path even when they hit LDS.
+    auto cell_of = [&](unsigned r, float t, float x, float y, float z) -> unsigned {
         if constexpr (WALK) {
-            if (staged) {
-                ns = s_nseg[r - r_first];
-                return s_seg + (r - r_first) * kMaxSeg;
-            }
-            ns = walk.nseg[r];
-            return walk.seg + (size_t)r * kMaxSeg;
+            if (staged)
+                return nearest_site(s_sites, num_sites, s_seg + (r - r_first) * kMaxSeg,
+                                    s_nseg[r - r_first], t, x, y, z);
+            return nearest_site(s_sites, num_sites, walk.seg + (size_t)r * kMaxSeg,
+                                walk.nseg[r], t, x, y, z);
         } else {
-            ns = 0;
-            return nullptr;
+            return nearest_site(s_sites, num_sites, nullptr, 0u, t, x, y, z);
         }
     };
 
@@ -532,9 +538,7 @@ __global__ __launch_bounds__(kThreads) void sample_assign_kernel(
                 }
                 const float x = fmaf(t, dx, ox), y = fmaf(t, dy, oy), z = fmaf(t, dz, oz);
                 tv[v] = t;
-                unsigned ns;
-                const SegRec *tab = table_of(r, ns);
-                cv[v] = nearest_site(s_sites, num_sites, tab, ns, t, x, y, z);
+                cv[v] = cell_of(r, t, x, y, z);
             }
             // next sample of the same thread
             if (++i == g.n) {

@@ -260,7 +260,31 @@ def test_many_sites_and_empty_heads():
     _check_pixels(gpu, ref, ids, TOL["fp32"], "tiny K=256")
 
 
-@pytest.mark.parametrize("sites", [28, 33, 64, 100, 256])
+@pytest.mark.parametrize("sites", [16, 17])
+def test_walk_threshold(sites):
+    """The assignment switches from the search over all sites to the cell walk
+    at 17 heads: 16 heads walk no ray, 17 heads walk every ray, and the cells
+    are the oracle's either way (the headline frame's shape, cut to 96 x 64
+    rays, k-means sites)."""
+    derf = _derf()
+    cfg = scenes.with_changes(scenes.CONFIGS["tiny"], width=96, height=64, num_sites=sites,
+                              sites="gmm_kmeans")
+    sc = scenes.make_scene(cfg)
+    R, n = cfg.num_rays, cfg.n_coarse
+    o = torch.from_numpy(sc.rays_o).cuda()
+    d = torch.from_numpy(sc.rays_d).cuda()
+    r = derf.Renderer(sc.sites, cfg.arch, sc.weights, "fp32")
+    out = r.render(o, d, cfg.near, cfg.far, n, 0, scenes.SEED_RENDER, debug=True)
+    torch.cuda.synchronize()
+    st = derf.derf_get_stats(r.handle)
+    r.close()
+    print("K=%d: walked rays %d of %d" % (sites, st.walk_rays, R), flush=True)
+    assert st.walk_rays == (R if sites >= 17 else 0)
+    dbg = {k: v.cpu().numpy() for k, v in out[3].items()}
+    _check_cells(sc, dbg["t"], dbg["cell"], n, "threshold K=%d" % sites)
+
+
+@pytest.mark.parametrize("sites", [17, 28, 33, 64, 100, 256])
 @pytest.mark.parametrize("layout", ["uniform", "gmm_kmeans"])
 def test_walk_site_counts(sites, layout):
     """Cells from the per-ray walk tables (4 lanes per ray on this frame, site

@@ -246,11 +246,14 @@ __device__ __forceinline__ unsigned group_exclusive_sum(unsigned x, int gl)
 // all sites, whatever crossing ends the segment.  A ray with more than
 // kMaxSeg segments, or a segment with more than kMaxCand candidates, is
 // marked (nseg = 0) for the search over all sites.
+//
+// One lane per ray (the largest frames) asks for 8 waves per SIMD: 64
+// registers without spills, against 96 and 5 waves by default, to cover the
+// lanes' differing walk lengths.  The grouped forms would spill at 64.
 template <int L>
-__global__ __launch_bounds__(kThreads) void ray_walk_kernel(RenderGeometry g,
-                                                            const float4 *__restrict__ sites,
-                                                            int num_sites, SegRec *__restrict__ seg,
-                                                            unsigned char *__restrict__ nseg)
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(L == 1 ? 8 : 1)))
+void ray_walk_kernel(RenderGeometry g, const float4 *__restrict__ sites, int num_sites,
+                     SegRec *__restrict__ seg, unsigned char *__restrict__ nseg)
 {
     static_assert(L == 1 || L == 2 || L == 4 || L == 8 || L == 16, "group size");
     // the sites in float64 with their squared norms: |x - phi|^2 = |x|^2 +

@@ -706,24 +706,33 @@ constexpr int kCellKey = 0, kCellAtLevel = 1, kLevelCell = 2;
 // min(ordinal, levels - 1), goes to lvl, and lane j (1 <= j < levels) records
 // where the j-th opening is (the start of piece j), taking the (j - seen)-th
 // set bit of the step's opening ballot.
+//
+// WORDS (n a multiple of 4, both byte arrays 4-byte aligned): the wave moves
+// its ray's cells and level bytes through LDS 256 at a time, as one dword per
+// lane each way.  One byte per lane and step, as the other form does, keeps
+// the texture path busy four times as long for the same bytes.
+template <bool WORDS>
 __global__ __launch_bounds__(kThreads) void level_bounds_kernel(const uint8_t *__restrict__ cell,
                                                                unsigned n, unsigned num_rays,
                                                                unsigned levels, unsigned piece,
                                                                unsigned *__restrict__ lb,
                                                                uint8_t *__restrict__ lvl)
 {
+    __shared__ uint32_t s_in[WORDS ? kThreads : 1], s_out[WORDS ? kThreads : 1];
     const unsigned lane = threadIdx.x & 63;
     const unsigned ray = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
     if (ray >= num_rays)
-        return;
+        return;  // a whole wave: the LDS rows are per wave, with no block barrier
     const size_t base = (size_t)ray * n;
     const uint64_t upto = ~0ull >> (63 - lane);  // lanes 0 .. lane
     unsigned mine = n;  // start of level `lane`
     unsigned seen = 0;  // openings before this step (wave-uniform)
     unsigned seg0 = 0;  // start of the segment open at the step's first sample (wave-uniform)
-    for (unsigned c0 = 0; c0 < n; c0 += 64) {
+    // the step of samples c0 .. c0 + 63: cur and prv are the cells of sample
+    // i = c0 + lane and of i - 1 (read when 0 < i < n); returns i's level
+    auto step = [&](unsigned c0, unsigned cur, unsigned prv) -> unsigned {
         const unsigned i = c0 + lane;
-        const bool change = i > 0 && i < n && cell[base + i] != cell[base + i - 1];
+        const bool change = i > 0 && i < n && cur != prv;
         uint64_t m = __ballot(change);
         if (piece > 0) {
             const uint64_t before = m & upto;
@@ -740,9 +749,50 @@ __global__ __launch_bounds__(kThreads) void level_bounds_kernel(const uint8_t *_
                 mm &= mm - 1;
             mine = c0 + (unsigned)__builtin_ctzll(mm);
         }
-        if (i < n)
-            lvl[base + i] = (uint8_t)min(seen + (unsigned)__popcll(m & upto), levels - 1);
+        const unsigned v = min(seen + (unsigned)__popcll(m & upto), levels - 1);
         seen += cnt;
+        return v;
+    };
+    if constexpr (!WORDS) {
+        for (unsigned c0 = 0; c0 < n; c0 += 64) {
+            const unsigned i = c0 + lane;
+            const unsigned cur = i < n ? cell[base + i] : 0u;
+            const unsigned prv = i > 0 && i < n ? cell[base + i - 1] : 0u;
+            const unsigned v = step(c0, cur, prv);
+            if (i < n)
+                lvl[base + i] = (uint8_t)v;
+        }
+    } else {
+        // LDS written by some lanes of the wave and read by others
+        auto wave_sync = [] {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        };
+        uint32_t *const w_in = s_in + (threadIdx.x & ~63u);
+        uint32_t *const w_out = s_out + (threadIdx.x & ~63u);
+        const uint8_t *const b_in = reinterpret_cast<const uint8_t *>(w_in);
+        uint8_t *const b_out = reinterpret_cast<uint8_t *>(w_out);
+        unsigned last = 0;  // cell of the sample before the chunk
+        for (unsigned a = 0; a < n; a += 256) {
+            const unsigned len = min(256u, n - a);  // a multiple of 4
+            if (4 * lane < len)
+                w_in[lane] = *reinterpret_cast<const uint32_t *>(cell + base + a + 4 * lane);
+            wave_sync();
+            for (unsigned q = 0; q < len; q += 64) {
+                const unsigned k = q + lane;  // within the chunk
+                const unsigned cur = k < len ? b_in[k] : 0u;
+                const unsigned prv = k == 0 ? last : k < len ? b_in[k - 1] : 0u;
+                const unsigned v = step(a + q, cur, prv);
+                if (k < len)
+                    b_out[k] = (uint8_t)v;
+            }
+            last = b_in[len - 1];
+            wave_sync();
+            if (4 * lane < len)
+                *reinterpret_cast<uint32_t *>(lvl + base + a + 4 * lane) = w_out[lane];
+            wave_sync();  // the next chunk's writes come after these reads
+        }
     }
     if (lane <= levels)
         lb[(size_t)ray * (levels + 1) + lane] = lane == 0 ? 0u : mine;
@@ -1425,8 +1475,13 @@ hipError_t launch_level_bounds(const uint8_t *cell, unsigned n, unsigned num_ray
                                unsigned levels, unsigned piece, unsigned *lb, uint8_t *lvl,
                                hipStream_t s)
 {
-    level_bounds_kernel<<<blocks_for(num_rays, kThreads / 64), kThreads, 0, s>>>(
-        cell, n, num_rays, levels, piece, lb, lvl);
+    const unsigned grid = blocks_for(num_rays, kThreads / 64);
+    if (n % 4 == 0 && ((uintptr_t)cell | (uintptr_t)lvl) % 4 == 0)
+        level_bounds_kernel<true><<<grid, kThreads, 0, s>>>(cell, n, num_rays, levels, piece, lb,
+                                                            lvl);
+    else
+        level_bounds_kernel<false><<<grid, kThreads, 0, s>>>(cell, n, num_rays, levels, piece, lb,
+                                                             lvl);
     return hipGetLastError();
 }
 

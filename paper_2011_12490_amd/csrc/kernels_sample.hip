@@ -579,26 +579,56 @@ void sample_assign_kernel(
 // ---------------------------------------------------------------------------
 // Exclusive prefix over blocks of each head's counts (one block per head),
 // in place; the head's total goes to totals[head].  Block 0 also clears the
-// tile counters of the MLP launch that follows on the stream.
+// tile counters of the MLP launch that follows on the stream.  The column
+// goes through LDS 8192 counts at a time (coalesced loads and stores, the
+// next chunk's loads in flight during the current chunk's scan); each thread
+// scans 8 consecutive counts, and the block scans the threads' sums.
+// (One count per thread and round took 64 rounds of four barriers for a
+// column of 65,536 blocks.)  LDS rows are padded by one word per 32 so that
+// the threads' strided reads hit distinct banks.
 __global__ __launch_bounds__(1024) void bucket_scan_kernel(unsigned *__restrict__ counts,
                                                            unsigned num_blocks,
                                                            unsigned *__restrict__ totals,
                                                            unsigned *__restrict__ mlp_queue)
 {
+    constexpr unsigned kItems = 8, kChunk = 1024 * kItems;
     if (blockIdx.x == 0 && threadIdx.x < (unsigned)(kMlpQueues * kMaxHeadGroups))
         mlp_queue[threadIdx.x] = 0;
+    __shared__ unsigned s_v[kChunk + kChunk / 32];
     __shared__ unsigned s_wave[16];
     __shared__ unsigned s_carry;
+    auto at = [](unsigned i) { return i + (i >> 5); };
     unsigned *col = counts + (size_t)blockIdx.x * num_blocks;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    if (threadIdx.x == 0)
+    const unsigned tid = threadIdx.x;
+    const int lane = tid & 63, w = tid >> 6;
+    if (tid == 0)
         s_carry = 0;
-    __syncthreads();
-    for (unsigned base = 0; base < num_blocks; base += 1024) {
-        const unsigned idx = base + threadIdx.x;
-        const unsigned v = idx < num_blocks ? col[idx] : 0u;
-        // inclusive scan within the wave
-        unsigned x = v;
+    // the next chunk's counts, loaded while the current one is scanned
+    unsigned nxt[kItems];
+    auto load = [&](unsigned b0) {
+#pragma unroll
+        for (unsigned j = 0; j < kItems; ++j) {
+            const unsigned i = b0 + j * 1024 + tid;
+            nxt[j] = i < num_blocks ? col[i] : 0u;
+        }
+    };
+    load(0);
+    for (unsigned base = 0; base < num_blocks; base += kChunk) {
+        const unsigned len = min(kChunk, num_blocks - base);
+#pragma unroll
+        for (unsigned j = 0; j < kItems; ++j)
+            s_v[at(j * 1024 + tid)] = nxt[j];
+        if (base + kChunk < num_blocks)
+            load(base + kChunk);  // counts not yet overwritten: the stores below are this chunk's
+        __syncthreads();
+        unsigned loc[kItems], sum = 0;
+#pragma unroll
+        for (unsigned j = 0; j < kItems; ++j) {
+            loc[j] = s_v[at(kItems * tid + j)];
+            sum += loc[j];
+        }
+        // inclusive scan of the threads' sums within the wave
+        unsigned x = sum;
 #pragma unroll
         for (int off = 1; off < 64; off <<= 1) {
             const unsigned y = __shfl_up(x, off);
@@ -621,11 +651,20 @@ __global__ __launch_bounds__(1024) void bucket_scan_kernel(unsigned *__restrict_
         }
         __syncthreads();
         const unsigned carry = s_carry;
-        const unsigned before = (w > 0 ? s_wave[w - 1] : 0u) + x - v;
-        if (idx < num_blocks)
-            col[idx] = carry + before;
+        unsigned run = carry + (w > 0 ? s_wave[w - 1] : 0u) + x - sum;  // before this thread
+#pragma unroll
+        for (unsigned j = 0; j < kItems; ++j) {
+            s_v[at(kItems * tid + j)] = run;
+            run += loc[j];
+        }
         __syncthreads();
-        if (threadIdx.x == 0)
+#pragma unroll
+        for (unsigned j = 0; j < kItems; ++j) {
+            const unsigned i = j * 1024 + tid;
+            if (i < len)
+                col[base + i] = s_v[at(i)];
+        }
+        if (tid == 0)
             s_carry = carry + s_wave[15];
         __syncthreads();
     }
